@@ -1,0 +1,273 @@
+"""EntQuant CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow C implementation (``eq_oracle.c``) of what the decode path
+computes, with ctypes wrappers.  Only the test suite, the package smoke check
+and the CPU-baseline leg of the benchmark may import this module; the product
+library never uses it.  ``build()`` compiles ``liboracle.so`` with gcc.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+OK, EINVAL, EFORMAT, ECORRUPT, ENOMEM = 0, -1, -2, -4, -5
+
+_u8p = ctypes.c_void_p
+_vp = ctypes.c_void_p
+
+
+class Info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint32) for n in
+                ("rows", "cols", "chunk_syms", "n_chunks", "lanes", "prob_bits", "n_syms",
+                 "base_format")] + \
+               [(n, ctypes.c_uint64) for n in
+                ("total_words", "padded_words", "seed", "file_bytes")] + \
+               [(n, ctypes.c_float) for n in ("alpha", "target_bits", "entropy_bits")] + \
+               [(n, ctypes.c_uint64) for n in
+                ("off_scale", "off_sym", "off_freq", "off_chunk_off", "off_chunk_state",
+                 "off_words")]
+
+
+def build() -> str:
+    """Compile liboracle.so (always recompiles)."""
+    cmd = ["gcc", "-O2", "-std=c99", "-D_GNU_SOURCE", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", os.path.join(_HERE, "eq_oracle.c"), "-o", _LIB_PATH + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        sig = {
+            "or_e4m3_value": (ctypes.c_double, [ctypes.c_uint8]),
+            "or_e4m3_round": (ctypes.c_uint8, [ctypes.c_float]),
+            "or_bf16_value": (ctypes.c_double, [ctypes.c_uint16]),
+            "or_bf16_round": (ctypes.c_uint16, [ctypes.c_double]),
+            "or_entropy_counts": (ctypes.c_double, [_vp, ctypes.c_uint32]),
+            "or_entropy_codes": (ctypes.c_double, [_vp, ctypes.c_uint64]),
+            "or_sparsity_entropy": (ctypes.c_double, [ctypes.c_double, ctypes.c_double]),
+            "or_row_scales": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float, _vp]),
+            "or_quantize": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, _vp]),
+            "or_dequant": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, _vp]),
+            "or_alpha_search": (ctypes.c_float, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                                 ctypes.c_double, ctypes.POINTER(ctypes.c_double)]),
+            "or_freq_table": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, _vp,
+                                             ctypes.POINTER(ctypes.c_uint32)]),
+            "or_rans_encode": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                              ctypes.c_uint32, _vp, _vp, ctypes.c_uint32, _vp,
+                                              ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint32),
+                                              _vp]),
+            "or_rans_decode": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32,
+                                              ctypes.c_uint32, ctypes.c_uint32, _vp, _vp,
+                                              ctypes.c_uint32, _vp]),
+            "or_container_build": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                                  ctypes.c_float, ctypes.c_uint32,
+                                                  ctypes.c_uint32, ctypes.c_uint32,
+                                                  ctypes.c_uint64, ctypes.c_float,
+                                                  ctypes.POINTER(ctypes.c_void_p),
+                                                  ctypes.POINTER(ctypes.c_uint64)]),
+            "or_free": (None, [_vp]),
+            "or_container_info": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.POINTER(Info)]),
+            "or_container_decode_chunk": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.c_uint32,
+                                                         _vp]),
+            "or_container_decode": (ctypes.c_int, [_vp, ctypes.c_uint64, _vp]),
+            "or_gemv": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp,
+                               _vp]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data
+
+
+# ---- number formats ----
+def e4m3_value(code: int) -> float:
+    return lib().or_e4m3_value(code)
+
+
+def e4m3_round(v: float) -> int:
+    return lib().or_e4m3_round(v)
+
+
+def bf16_value(bits: int) -> float:
+    return lib().or_bf16_value(bits)
+
+
+def bf16_round(v: float) -> int:
+    return lib().or_bf16_round(v)
+
+
+# ---- entropy ----
+def entropy_counts(counts) -> float:
+    c = np.ascontiguousarray(counts, dtype=np.uint64)
+    return lib().or_entropy_counts(_ptr(c), c.size)
+
+
+def entropy_codes(q: np.ndarray) -> float:
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    return lib().or_entropy_codes(_ptr(q), q.size)
+
+
+def sparsity_entropy(s: float, h_nz: float) -> float:
+    return lib().or_sparsity_entropy(s, h_nz)
+
+
+# ---- quantiser ----
+def row_scales(w: np.ndarray, alpha: float) -> np.ndarray:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M, N = w.shape
+    out = np.empty(M, dtype=np.uint16)
+    lib().or_row_scales(_ptr(w), M, N, alpha, _ptr(out))
+    return out
+
+
+def quantize(w: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    scale = np.ascontiguousarray(scale, dtype=np.uint16)
+    M, N = w.shape
+    out = np.empty((M, N), dtype=np.uint8)
+    lib().or_quantize(_ptr(w), M, N, _ptr(scale), _ptr(out))
+    return out
+
+
+def dequant(q: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    scale = np.ascontiguousarray(scale, dtype=np.uint16)
+    M, N = q.shape
+    out = np.empty((M, N), dtype=np.uint16)
+    lib().or_dequant(_ptr(q), M, N, _ptr(scale), _ptr(out))
+    return out
+
+
+def alpha_search(w: np.ndarray, target_bits: float):
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M, N = w.shape
+    h = ctypes.c_double()
+    a = lib().or_alpha_search(_ptr(w), M, N, target_bits, ctypes.byref(h))
+    return a, h.value
+
+
+# ---- frequency table / coder ----
+def freq_table(counts, P: int):
+    c = np.ascontiguousarray(counts, dtype=np.uint64)
+    assert c.size == 256
+    sym = np.zeros(256, dtype=np.uint8)
+    freq = np.zeros(256, dtype=np.uint16)
+    K = ctypes.c_uint32()
+    rc = lib().or_freq_table(_ptr(c), P, _ptr(sym), _ptr(freq), ctypes.byref(K))
+    if rc != OK:
+        raise ValueError(f"or_freq_table: {rc}")
+    return sym[:K.value].copy(), freq[:K.value].copy()
+
+
+def rans_encode(q: np.ndarray, lanes: int, P: int, sym: np.ndarray, freq: np.ndarray):
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    sym = np.ascontiguousarray(sym, dtype=np.uint8)
+    freq = np.ascontiguousarray(freq, dtype=np.uint16)
+    words = np.zeros(max(q.size, 1), dtype=np.uint16)
+    states = np.zeros(lanes, dtype=np.uint32)
+    nw = ctypes.c_uint32()
+    rc = lib().or_rans_encode(_ptr(q), q.size, lanes, P, _ptr(sym), _ptr(freq), sym.size,
+                              _ptr(words), words.size, ctypes.byref(nw), _ptr(states))
+    if rc != OK:
+        raise ValueError(f"or_rans_encode: {rc}")
+    return words[:nw.value].copy(), states
+
+
+def rans_decode(words: np.ndarray, states: np.ndarray, n: int, lanes: int, P: int,
+                sym: np.ndarray, freq: np.ndarray):
+    words = np.ascontiguousarray(words, dtype=np.uint16)
+    states = np.ascontiguousarray(states, dtype=np.uint32)
+    sym = np.ascontiguousarray(sym, dtype=np.uint8)
+    freq = np.ascontiguousarray(freq, dtype=np.uint16)
+    q = np.zeros(max(n, 1), dtype=np.uint8)
+    w = words if words.size else np.zeros(1, dtype=np.uint16)
+    rc = lib().or_rans_decode(_ptr(w), words.size, _ptr(states), n, lanes, P, _ptr(sym),
+                              _ptr(freq), sym.size, _ptr(q))
+    return rc, q[:n]
+
+
+# ---- container ----
+def container_build(w: np.ndarray, alpha: float, P: int, chunk_syms: int, lanes: int,
+                    seed: int = 0, target_bits: float = 0.0) -> np.ndarray:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M, N = w.shape
+    p = ctypes.c_void_p()
+    nb = ctypes.c_uint64()
+    rc = lib().or_container_build(_ptr(w), M, N, alpha, P, chunk_syms, lanes, seed, target_bits,
+                                  ctypes.byref(p), ctypes.byref(nb))
+    if rc != OK:
+        raise ValueError(f"or_container_build: {rc}")
+    try:
+        out = np.frombuffer(ctypes.string_at(p.value, nb.value), dtype=np.uint8).copy()
+    finally:
+        lib().or_free(p)
+    return out
+
+
+def container_info(blob: np.ndarray) -> Info:
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = Info()
+    rc = lib().or_container_info(_ptr(blob), blob.size, ctypes.byref(info))
+    if rc != OK:
+        raise ValueError(f"or_container_info: {rc}")
+    return info
+
+
+def container_decode_chunk(blob: np.ndarray, c: int):
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = container_info(blob)
+    n = info.rows * info.cols
+    nc = min(info.chunk_syms, n - c * info.chunk_syms)
+    q = np.zeros(info.chunk_syms, dtype=np.uint8)
+    rc = lib().or_container_decode_chunk(_ptr(blob), blob.size, c, _ptr(q))
+    return rc, q[:nc]
+
+
+def container_decode(blob: np.ndarray):
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = container_info(blob)
+    q = np.zeros(info.n_chunks * info.chunk_syms, dtype=np.uint8)
+    rc = lib().or_container_decode(_ptr(blob), blob.size, _ptr(q))
+    return rc, q[:info.rows * info.cols].reshape(info.rows, info.cols)
+
+
+def container_scales(blob: np.ndarray) -> np.ndarray:
+    info = container_info(blob)
+    return np.frombuffer(blob[info.off_scale:info.off_scale + 2 * info.rows].tobytes(),
+                         dtype=np.uint16).copy()
+
+
+# ---- linear layer ----
+def gemv(w_hat: np.ndarray, x: np.ndarray, bias: np.ndarray | None = None) -> np.ndarray:
+    w_hat = np.ascontiguousarray(w_hat, dtype=np.uint16)
+    x = np.ascontiguousarray(np.atleast_2d(x), dtype=np.uint16)
+    M, N = w_hat.shape
+    B = x.shape[0]
+    assert x.shape[1] == N
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=np.uint16)
+    y = np.empty((B, M), dtype=np.float64)
+    lib().or_gemv(_ptr(w_hat), M, N, _ptr(x), B, _ptr(bias), _ptr(y))
+    return y

@@ -1,0 +1,110 @@
+/*
+ * EntQuant CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, scalar C implementation of what the decode path computes,
+ * used to check the GPU library.  Only the test suite, the package smoke
+ * check and the CPU-baseline leg of the benchmark may load it; the product
+ * library never links, calls or falls back to it.  It shares no code with
+ * the product library.
+ *
+ * Paper: "Float8@2bits: Entropy Coding Enables Data-Free Model
+ * Compression" (EntQuant, arXiv 2601.22787).
+ *   Sec. 2.1  quantiser Q (round to nearest representable value of the
+ *             base format, clamp to +-Qmax), AbsMax scale, dequantiser
+ *             W_hat = s * W_q, channel-wise scales (one per output row),
+ *             linear layer y = x W_hat^T + b.
+ *   Sec. 2.2  empirical entropy (eq. emp_entropy); Alg. 1 (AbsMax init,
+ *             scale choice, quantise, vec, ANS encode); Alg. 2 (ANS decode,
+ *             view, QMatMul + bias).
+ *   App. A.1  Float8 E4M3 base format, signed zeros resolved, byte-level
+ *             ANS in fixed-size chunks.
+ *   App. B.1  closed-form entropy of a sparse mixture, Tab. sparsity_entropy.
+ *
+ * The paper's ANS coder is a closed library whose format it does not give.
+ * The coder here is interleaved rANS (Duda 2014; Giesen 2014 for the
+ * interleaving), with these parameters, all recorded in the container:
+ *   P      probability precision, M = 2^P, 1 <= P <= 12
+ *   W      lanes: independent coder states per chunk (multiple of 64)
+ *   state  32-bit, normalised interval [2^16, 2^32), 16-bit stream words
+ * Symbol k of a chunk belongs to lane k mod W at step k div W.
+ *
+ * Every floating-point reading the paper leaves open is fixed here:
+ *   E4M3FN (OCP), Qmax = 448, ties to even, clamp before rounding, one
+ *   fp32 division W/s, -0 stored as +0, BF16 scales
+ *   s = bf16(fp64(alpha * absmax / 448)) (all-zero row: s = 1),
+ *   dequantised weight = bf16(s * v(q)) rounded once from the exact product.
+ *
+ * Parity pins for every function are in the test suite; none is unpinned.
+ */
+#ifndef EQ_ORACLE_H
+#define EQ_ORACLE_H
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OR_OK 0
+#define OR_EINVAL (-1)
+#define OR_EFORMAT (-2)
+#define OR_ECORRUPT (-4)
+#define OR_ENOMEM (-5)
+
+/* ---- number formats (Sec. 2.1, App. A.1) ---- */
+double or_e4m3_value(uint8_t code);   /* NaN for 0x7F / 0xFF */
+uint8_t or_e4m3_round(float v);       /* nearest E4M3FN code, ties to even */
+double or_bf16_value(uint16_t bits);
+uint16_t or_bf16_round(double v);     /* nearest BF16, ties to even */
+
+/* ---- entropy (eq. emp_entropy; App. B.1) ---- */
+double or_entropy_counts(const uint64_t *counts, uint32_t n_bins);
+double or_entropy_codes(const uint8_t *q, uint64_t n);
+double or_sparsity_entropy(double s, double h_nz);
+
+/* ---- quantiser / dequantiser (Sec. 2.1) ---- */
+void or_row_scales(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint16_t *scale);
+void or_quantize(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale, uint8_t *q);
+void or_dequant(const uint8_t *q, uint32_t M, uint32_t N, const uint16_t *scale, uint16_t *w_hat);
+/* Bisection on log2(alpha) in [-4, 24] for the alpha whose entropy is
+ * closest to target (the stand-in for the paper's lambda optimisation). */
+float or_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, double target_bits,
+                      double *h_out);
+
+/* ---- frequency table (ANS metadata) ---- */
+int or_freq_table(const uint64_t counts[256], uint32_t P, uint8_t *sym, uint16_t *freq,
+                  uint32_t *K);
+
+/* ---- one chunk of interleaved rANS ---- */
+int or_rans_encode(const uint8_t *q, uint32_t n, uint32_t lanes, uint32_t P,
+                   const uint8_t *sym, const uint16_t *freq, uint32_t K,
+                   uint16_t *words, uint32_t max_words, uint32_t *n_words, uint32_t *states);
+int or_rans_decode(const uint16_t *words, uint32_t n_words, const uint32_t *states,
+                   uint32_t n, uint32_t lanes, uint32_t P, const uint8_t *sym,
+                   const uint16_t *freq, uint32_t K, uint8_t *q);
+
+/* ---- container (all sections of one compressed layer) ---- */
+typedef struct or_info {
+  uint32_t rows, cols, chunk_syms, n_chunks, lanes, prob_bits, n_syms, base_format;
+  uint64_t total_words, padded_words, seed, file_bytes;
+  float alpha, target_bits, entropy_bits;
+  uint64_t off_scale, off_sym, off_freq, off_chunk_off, off_chunk_state, off_words;
+} or_info;
+
+int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t P,
+                       uint32_t chunk_syms, uint32_t lanes, uint64_t seed, float target_bits,
+                       uint8_t **blob, uint64_t *blob_bytes);
+void or_free(void *p);
+int or_container_info(const uint8_t *blob, uint64_t blob_bytes, or_info *info);
+int or_container_decode_chunk(const uint8_t *blob, uint64_t blob_bytes, uint32_t chunk,
+                              uint8_t *q);
+int or_container_decode(const uint8_t *blob, uint64_t blob_bytes, uint8_t *q);
+
+/* ---- linear layer (Sec. 2.1): y[b][i] = sum_j w_hat[i][j] x[b][j] + bias[i] in fp64 ---- */
+void or_gemv(const uint16_t *w_hat, uint32_t M, uint32_t N, const uint16_t *x, uint32_t B,
+             const uint16_t *bias, double *y);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,142 @@
+/*
+ * libeq -- EntQuant inference-time decoding on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Float8@2bits: Entropy Coding Enables Data-Free Model Compression"
+ * (EntQuant, arXiv 2601.22787).  The weights of a linear layer stay in VRAM
+ * as an entropy-coded bitstream z with BF16 per-output-row scales S and ANS
+ * metadata M (Sec. 2.2, "Weight encoding"); Alg. 2 decodes them on the fly:
+ *   w   <- ANS^-1(z, M)            entropy decoding        (eq_decode_codes)
+ *   W_q <- view(w)                 row-major [M rows, N cols]
+ *   W_hat = s_i * W_q              dequantiser, Sec. 2.1   (eq_decode_bf16)
+ *   y   <- QMatMul(W_q, S, x) + b  y = x W_hat^T + b       (eq_decode_gemv)
+ * The decode+GEMV entry point fuses all three steps and never materialises
+ * the weights.
+ *
+ * Container (".eqc", one compressed layer; little-endian; every section
+ * 256-byte aligned).  Header, 256 bytes:
+ *   0 "EQC1"  4 version=1  8 header_bytes=256  12 base_format (1 = E4M3FN)
+ *   16 rows M  20 cols N  24 chunk_syms C  28 n_chunks = ceil(M*N/C)
+ *   32 lanes W  36 prob_bits P  40 n_syms K  44 flags=0
+ *   48 total_words (u64)  56 padded_words (u64)  64 seed (u64)
+ *   72 alpha (f32)  76 target_bits (f32)  80 entropy_bits (f32)
+ *   88.. u64 byte offsets of the sections scale, sym, freq, chunk_off,
+ *   chunk_state, words; 136 file_bytes (u64).
+ * Sections:
+ *   scale       u16[M]       BF16 bit patterns, one scale per output row
+ *   sym         u8[K]        E4M3FN codes present, strictly ascending
+ *   freq        u16[K]       frequencies, >= 1, summing to 2^P
+ *   chunk_off   u32[n+1]     first stream word of each chunk; [n] = total_words
+ *   chunk_state u32[n*W]     initial decoder state of every lane of every chunk
+ *   words       u16[padded_words]  all chunks' streams, then >= 1024 zero words
+ * Coder (the paper's ANS library is closed; this is interleaved rANS after
+ * Duda 2014 with Giesen's interleaving): symbol k of chunk c is element
+ * c*C + k of the row-major code matrix and belongs to lane k mod W at step
+ * k div W.  A step first decodes every active lane
+ *   slot = x mod 2^P;  symbol s with cum_s <= slot < cum_s + f_s;
+ *   x = f_s * (x >> P) + slot - cum_s
+ * then, in ascending lane order, each active lane with x < 2^16 takes the
+ * next word: x = (x << 16) | word.  After the last step every lane is at
+ * 2^16 and the chunk's words are used up exactly.
+ *
+ * Conventions for every entry point below:
+ *  - Device pointers are allocated and owned by the caller; the library never
+ *    allocates, frees or synchronises (except eq_get_status, which waits on
+ *    the given stream).
+ *  - Calls are asynchronous on `stream` and reentrant; different layers or
+ *    outputs may be processed on several streams at once.
+ *  - Return codes: EQ_OK, EQ_EINVAL (null pointer, size or range),
+ *    EQ_EFORMAT (container header or sections inconsistent), EQ_EHIP (a HIP
+ *    launch or runtime call failed).  Stream corruption found while decoding
+ *    on the device is recorded in the layer's status word (EQ_ECORRUPT via
+ *    eq_get_status); outputs of a corrupted chunk are then unspecified, but
+ *    no access ever leaves the container or the output buffers.
+ */
+#ifndef EQ_H
+#define EQ_H
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EQ_OK 0
+#define EQ_EINVAL (-1)
+#define EQ_EFORMAT (-2)
+#define EQ_EHIP (-3)
+#define EQ_ECORRUPT (-4)
+
+/* A validated view of one container in device memory (filled by eq_layer_init). */
+typedef struct eq_layer {
+  uint32_t rows, cols;       /* M output rows, N input columns                    */
+  uint32_t chunk_syms;       /* C                                                  */
+  uint32_t n_chunks;
+  uint32_t lanes;            /* W: 64, 128 or 256                                  */
+  uint32_t prob_bits;        /* P: 1..12                                           */
+  uint32_t n_syms;           /* K: 1..256                                          */
+  uint32_t reserved;
+  uint64_t total_words, padded_words;
+  const uint16_t *scale;     /* device: the container's sections                   */
+  const uint8_t *sym;
+  const uint16_t *freq;
+  const uint32_t *chunk_off;
+  const uint32_t *chunk_state;
+  const uint16_t *words;
+  uint32_t *lut;             /* device scratch, eq_lut_bytes() bytes, caller-owned */
+  int32_t *status;           /* device int32, caller-owned                         */
+} eq_layer;
+
+/* Bytes of device scratch the decode tables of a layer need. */
+size_t eq_lut_bytes(void);
+
+/* Validate the container `host_blob` (blob_bytes long, host memory) and fill
+ * *L with pointers into `dev_blob`, a device copy of the same bytes.  The
+ * host copy is read only during the call.  `dev_lut` (eq_lut_bytes() bytes)
+ * and `dev_status` (one int32) are device scratch owned by the caller and
+ * tied to this layer.  Checks: magic/version/base format, sizes and
+ * section bounds, ascending symbols, frequencies >= 1 summing to 2^P,
+ * monotone chunk offsets ending at total_words, padding >= 1024 words,
+ * initial states in [2^16, 2^32), scales finite with magnitude in
+ * [2^-117, 2^120) (so every dequantised product is exact in fp32).
+ * Returns EQ_OK, EQ_EINVAL or EQ_EFORMAT. */
+int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t blob_bytes, const void *dev_blob,
+                  void *dev_lut, int32_t *dev_status);
+
+/* Build the layer's decode tables on the device (slot -> symbol/frequency/
+ * offset, symbol -> E4M3 value; Sec. 2.2 metadata M) and clear its status
+ * word.  Must run (on the same stream, or be complete) before any decode. */
+int eq_layer_prepare(const eq_layer *L, hipStream_t stream);
+
+/* Alg. 2 lines 1-2: entropy-decode every chunk; codes[k] is the E4M3FN code of
+ * element k of the row-major M x N matrix (M*N bytes, device). */
+int eq_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t stream);
+
+/* Alg. 2 lines 1-2 plus the dequantiser of Sec. 2.1: w[i*N + j] =
+ * bf16(s_i * v(q_ij)), the exact product rounded once to nearest-even
+ * (M*N BF16 bit patterns, device). */
+int eq_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t stream);
+
+/* Workspace bytes eq_decode_gemv needs for batch B (1..8). */
+size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B);
+
+/* Alg. 2 fused: y[b][i] = s_i * sum_j v(q_ij) x[b][j] + bias[i] for
+ * b < B <= 8, without materialising the weights.  x is [B][N] BF16 (device),
+ * bias is [M] BF16 or NULL, y is [B][M] fp32 (device).  The row sum is
+ * accumulated in fp32 and scaled by s_i once, as QMatMul(W_q, S, x) does.
+ * ws/ws_bytes: device workspace of at least eq_gemv_workspace_bytes(L, B). */
+int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
+                   float *y, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Wait for `stream`, then report EQ_ECORRUPT if any decode since the last
+ * eq_layer_prepare found a chunk whose stream or terminal states did not
+ * check out, else EQ_OK (or EQ_EHIP). */
+int eq_get_status(const eq_layer *L, hipStream_t stream);
+
+/* Static description of a return code. */
+const char *eq_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,279 @@
+"""EntQuant inference-time decoding on MI355X: thin ctypes binding of libeq.
+
+Every function here has the name of the C entry point it wraps (include/eq.h,
+include/eq_encode.h) and only marshals arguments: torch supplies device memory
+and streams, all decoding runs in libeq's gfx950 kernels.  There is no CPU
+fallback: if libeq.so is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from ._build import LIB as _LIB_PATH
+from ._build import build as _build_lib
+
+EQ_OK, EQ_EINVAL, EQ_EFORMAT, EQ_EHIP, EQ_ECORRUPT = 0, -1, -2, -3, -4
+
+_lib = None
+_vp = ctypes.c_void_p
+
+
+class EqError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn}: {eq_strerror(code)} ({code})")
+        self.code = code
+
+
+class eq_layer(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_uint32), ("cols", ctypes.c_uint32),
+                ("chunk_syms", ctypes.c_uint32), ("n_chunks", ctypes.c_uint32),
+                ("lanes", ctypes.c_uint32), ("prob_bits", ctypes.c_uint32),
+                ("n_syms", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("total_words", ctypes.c_uint64), ("padded_words", ctypes.c_uint64),
+                ("scale", _vp), ("sym", _vp), ("freq", _vp), ("chunk_off", _vp),
+                ("chunk_state", _vp), ("words", _vp), ("lut", _vp), ("status", _vp)]
+
+
+class eqe_params(ctypes.Structure):
+    _fields_ = [("prob_bits", ctypes.c_uint32), ("chunk_syms", ctypes.c_uint32),
+                ("lanes", ctypes.c_uint32), ("threads", ctypes.c_uint32),
+                ("seed", ctypes.c_uint64), ("target_bits", ctypes.c_float)]
+
+
+# name -> (restype, argtypes): every symbol the public headers declare
+SIGNATURES = {
+    "eq_lut_bytes": (ctypes.c_size_t, []),
+    "eq_layer_init": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint64, _vp, _vp,
+                                     _vp]),
+    "eq_layer_prepare": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp]),
+    "eq_decode_codes": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, _vp]),
+    "eq_decode_bf16": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, _vp]),
+    "eq_gemv_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer), ctypes.c_uint32]),
+    "eq_decode_gemv": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp, _vp,
+                                      _vp, ctypes.c_size_t, _vp]),
+    "eq_get_status": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp]),
+    "eq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "eqe_alpha_search": (ctypes.c_float, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_double,
+                                          ctypes.c_uint32, ctypes.c_uint32,
+                                          ctypes.POINTER(ctypes.c_double)]),
+    "eqe_encode": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float,
+                                  ctypes.POINTER(eqe_params), ctypes.POINTER(ctypes.c_void_p),
+                                  ctypes.POINTER(ctypes.c_uint64)]),
+    "eqe_free": (None, [_vp]),
+}
+
+
+def build() -> str:
+    """Compile libeq.so (gfx950) in place and reload it."""
+    global _lib
+    path = _build_lib()
+    _lib = None
+    return path
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, rc: int) -> None:
+    if rc != EQ_OK:
+        raise EqError(fn, rc)
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dptr(t, dtype=None, numel=None):
+    """Device pointer of a contiguous CUDA tensor, with optional checks."""
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"expected dtype {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"tensor too small: {t.numel()} < {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+# ---------------------------------------------------------------- decode ABI
+def eq_strerror(code: int) -> str:
+    return lib().eq_strerror(code).decode()
+
+
+def eq_lut_bytes() -> int:
+    return lib().eq_lut_bytes()
+
+
+def eq_layer_init(host_blob: np.ndarray, dev_blob, dev_lut, dev_status) -> eq_layer:
+    host_blob = np.ascontiguousarray(host_blob, dtype=np.uint8)
+    L = eq_layer()
+    rc = lib().eq_layer_init(ctypes.byref(L), host_blob.ctypes.data, host_blob.size,
+                             _dptr(dev_blob, numel=host_blob.size),
+                             _dptr(dev_lut, numel=None), _dptr(dev_status))
+    _check("eq_layer_init", rc)
+    return L
+
+
+def eq_layer_prepare(L, stream=None) -> None:
+    _check("eq_layer_prepare", lib().eq_layer_prepare(ctypes.byref(_raw(L)), _stream(stream)))
+
+
+def eq_decode_codes(L, codes, stream=None) -> None:
+    import torch
+    r = _raw(L)
+    p = _dptr(codes, torch.uint8, r.rows * r.cols)
+    _check("eq_decode_codes", lib().eq_decode_codes(ctypes.byref(r), p, _stream(stream)))
+
+
+def eq_decode_bf16(L, w, stream=None) -> None:
+    import torch
+    r = _raw(L)
+    if w.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError("w must hold 16-bit BF16 patterns")
+    p = _dptr(w, None, r.rows * r.cols)
+    _check("eq_decode_bf16", lib().eq_decode_bf16(ctypes.byref(r), p, _stream(stream)))
+
+
+def eq_gemv_workspace_bytes(L, B: int) -> int:
+    return lib().eq_gemv_workspace_bytes(ctypes.byref(_raw(L)), B)
+
+
+def eq_decode_gemv(L, x, B: int, bias, y, ws, stream=None) -> None:
+    import torch
+    r = _raw(L)
+    if x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError("x must hold 16-bit BF16 patterns")
+    px = _dptr(x, None, B * r.cols)
+    pb = _dptr(bias, None, r.rows) if bias is not None else None
+    py = _dptr(y, torch.float32, B * r.rows)
+    pw = _dptr(ws)
+    nbytes = ws.numel() * ws.element_size()
+    _check("eq_decode_gemv", lib().eq_decode_gemv(ctypes.byref(r), px, B, pb, py, pw, nbytes,
+                                                  _stream(stream)))
+
+
+def eq_get_status(L, stream=None) -> int:
+    return lib().eq_get_status(ctypes.byref(_raw(L)), _stream(stream))
+
+
+# ---------------------------------------------------------------- encoder ABI
+def eqe_alpha_search(w: np.ndarray, target_bits: float, sample_rows: int = 0,
+                     threads: int = 0):
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    h = ctypes.c_double()
+    a = lib().eqe_alpha_search(w.ctypes.data, w.shape[0], w.shape[1], target_bits, sample_rows,
+                               threads, ctypes.byref(h))
+    if a <= 0:
+        raise EqError("eqe_alpha_search", EQ_EINVAL)
+    return a, h.value
+
+
+def eqe_encode(w: np.ndarray, alpha: float, *, prob_bits: int = 12, chunk_syms: int,
+               lanes: int, threads: int = 0, seed: int = 0,
+               target_bits: float = 0.0) -> np.ndarray:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    prm = eqe_params(prob_bits, chunk_syms, lanes, threads, seed, target_bits)
+    p = ctypes.c_void_p()
+    nb = ctypes.c_uint64()
+    rc = lib().eqe_encode(w.ctypes.data, w.shape[0], w.shape[1], alpha, ctypes.byref(prm),
+                          ctypes.byref(p), ctypes.byref(nb))
+    _check("eqe_encode", rc)
+    try:
+        out = np.empty(nb.value, dtype=np.uint8)
+        ctypes.memmove(out.ctypes.data, p.value, nb.value)
+    finally:
+        lib().eqe_free(p)
+    return out
+
+
+# ---------------------------------------------------------------- layer object
+class Layer:
+    """One compressed layer resident on the device: the container bytes, the
+    decode-table scratch and the status word, with its validated eq_layer."""
+
+    def __init__(self, blob: np.ndarray, device="cuda", stream=None):
+        import torch
+        self.blob = np.ascontiguousarray(blob, dtype=np.uint8)
+        self.dev_blob = torch.from_numpy(self.blob).to(device)
+        self.lut = torch.empty(eq_lut_bytes(), dtype=torch.uint8, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        self.raw = eq_layer_init(self.blob, self.dev_blob, self.lut, self.status)
+        eq_layer_prepare(self, stream)
+
+    @property
+    def rows(self) -> int:
+        return self.raw.rows
+
+    @property
+    def cols(self) -> int:
+        return self.raw.cols
+
+    def workspace(self, B: int):
+        import torch
+        return torch.empty(eq_gemv_workspace_bytes(self, B), dtype=torch.uint8,
+                           device=self.dev_blob.device)
+
+
+def _raw(L) -> eq_layer:
+    return L.raw if isinstance(L, Layer) else L
+
+
+def smoke() -> None:
+    """One small decode (codes, BF16) and fused GEMV (B = 1, 3) on cuda:0,
+    checked against the CPU oracle."""
+    import sys
+
+    import torch
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    import oracle
+    import synth
+    from synth.configs import small_spec
+
+    spec = small_spec(96, 320, bits=2.5, chunk=1024, lanes=64, seed=77)
+    w = synth.weights(spec)
+    alpha, _ = eqe_alpha_search(w, spec.target_bits)
+    blob = eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes)
+    dev = torch.device("cuda:0")
+    L = Layer(blob, dev)
+    codes = torch.empty(spec.params, dtype=torch.uint8, device=dev)
+    eq_decode_codes(L, codes)
+    wb = torch.empty(spec.params, dtype=torch.int16, device=dev)
+    eq_decode_bf16(L, wb)
+    B = 3
+    x = torch.from_numpy(synth.activations(spec, B).view(np.int16)).to(dev)
+    y = torch.empty(B, spec.rows, dtype=torch.float32, device=dev)
+    ws = L.workspace(B)
+    eq_decode_gemv(L, x, B, None, y, ws)
+    _check("eq_get_status", eq_get_status(L))
+
+    rc, q_ref = oracle.container_decode(blob)
+    assert rc == oracle.OK
+    assert np.array_equal(codes.cpu().numpy().reshape(q_ref.shape), q_ref), "codes differ"
+    w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
+    assert np.array_equal(wb.cpu().numpy().view(np.uint16).reshape(w_ref.shape), w_ref), \
+        "bf16 differs"
+    y_ref = oracle.gemv(w_ref, synth.activations(spec, B))
+    err = np.abs(y.cpu().numpy() - y_ref).max(axis=1) / np.abs(y_ref).max(axis=1)
+    assert (err <= 1e-2).all(), f"gemv error {err}"
+    print(f"smoke ok: codes/bf16 bit-exact, gemv max rel err {err.max():.2e}")

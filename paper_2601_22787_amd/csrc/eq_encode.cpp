@@ -1,0 +1,363 @@
+// Host encoder for the compressed-layer container (declared in eq_encode.h).
+//
+// Alg. 1 of the paper (Sec. 2.2): AbsMax-based per-row scales (eq. absmax,
+// channel-wise as in Sec. 2.1), Float8 E4M3FN quantisation Q, row-major vec,
+// ANS entropy coding per chunk (App. A.1).  The coder is interleaved rANS
+// with a 32-bit state in [2^16, 2^32), 16-bit stream words and W lanes per
+// chunk; symbol k of a chunk is coded by lane k mod W at step k div W.
+#include "eq_encode.h"
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+namespace {
+
+constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
+constexpr uint64_t kHeaderBytes = 256;
+
+// Default worker count: one per hardware thread, at most 16.
+unsigned worker_count(uint32_t requested) {
+  if (requested) return requested;
+  unsigned n = std::thread::hardware_concurrency();
+  return n ? std::min(n, 16u) : 1;
+}
+
+// Run fn(i) for i in [0, n) on up to `threads` workers (dynamic schedule).
+template <class Fn>
+void parallel_for(uint64_t n, unsigned threads, Fn fn) {
+  threads = static_cast<unsigned>(std::min<uint64_t>(threads, n));
+  if (threads <= 1) {
+    for (uint64_t i = 0; i < n; ++i) fn(i);
+    return;
+  }
+  std::atomic<uint64_t> next{0};
+  auto body = [&] {
+    for (uint64_t i; (i = next.fetch_add(1)) < n;) fn(i);
+  };
+  std::vector<std::thread> pool;
+  pool.reserve(threads - 1);
+  for (unsigned t = 1; t < threads; ++t) pool.emplace_back(body);
+  body();
+  for (auto &t : pool) t.join();
+}
+
+inline float bf16_to_float(uint16_t b) {
+  uint32_t u = static_cast<uint32_t>(b) << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+// Nearest BF16 of a double (ties to even): scale the binade to an integer
+// significand of 8 bits and round it with the current (nearest-even) mode.
+uint16_t double_to_bf16(double v) {
+  if (v == 0.0) return std::signbit(v) ? 0x8000 : 0;
+  int e;
+  double m = std::frexp(v, &e);
+  int shift = 8;
+  if (e - 1 < -126) shift = 8 - (-126 - (e - 1));  // BF16 subnormal range
+  double r = std::nearbyint(std::ldexp(m, shift));
+  float f = static_cast<float>(std::ldexp(r, e - shift));
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// E4M3FN code of v: clamp |v| to 448, round to nearest (ties to even) on the
+// E4M3 grid, -0 -> +0.  Normal range: round the fp32 significand from 23 to
+// 3 bits in place (a carry moves into the exponent); subnormal range
+// (|v| < 2^-6): the grid is k * 2^-9, so round |v| * 2^9 to an integer.
+uint8_t quantize_e4m3(float v) {
+  float a = std::fabs(v);
+  if (a > 448.0f) a = 448.0f;
+  uint32_t mag;
+  if (a < 0.015625f) {
+    mag = static_cast<uint32_t>(std::nearbyint(a * 512.0f));  // exact scaling
+  } else {
+    uint32_t b;
+    std::memcpy(&b, &a, 4);
+    uint32_t r = (b + 0x7FFFFu + ((b >> 20) & 1u)) >> 20;  // exponent:8 | mantissa:3
+    mag = r - ((127u - 7u) << 3);
+  }
+  if (mag == 0) return 0;
+  return static_cast<uint8_t>(mag | (std::signbit(v) ? 0x80u : 0u));
+}
+
+struct Quantized {
+  std::vector<uint16_t> scale;
+  std::vector<uint8_t> codes;
+  uint64_t hist[256] = {};
+};
+
+uint16_t row_scale(const uint16_t *row, uint32_t N, float alpha) {
+  float amax = 0.0f;
+  for (uint32_t j = 0; j < N; ++j) amax = std::max(amax, std::fabs(bf16_to_float(row[j])));
+  if (amax == 0.0f) return 0x3F80;
+  return double_to_bf16(static_cast<double>(alpha) * static_cast<double>(amax) / 448.0);
+}
+
+// Quantise the listed rows; codes are written only if `codes` is non-null.
+void quantize_rows(const uint16_t *w, uint32_t N, float alpha, const std::vector<uint32_t> &rows,
+                   unsigned threads, uint16_t *scale, uint8_t *codes, uint64_t hist[256]) {
+  const uint64_t n_rows = rows.size();
+  const uint64_t per = 16;  // rows per task
+  const uint64_t tasks = (n_rows + per - 1) / per;
+  std::vector<std::vector<uint64_t>> part(tasks, std::vector<uint64_t>(256, 0));
+  parallel_for(tasks, threads, [&](uint64_t t) {
+    uint64_t *h = part[t].data();
+    for (uint64_t r = t * per; r < std::min(n_rows, (t + 1) * per); ++r) {
+      const uint32_t i = rows[r];
+      const uint16_t *src = w + static_cast<uint64_t>(i) * N;
+      uint16_t s = row_scale(src, N, alpha);
+      if (scale) scale[i] = s;
+      const float sf = bf16_to_float(s);
+      uint8_t *dst = codes ? codes + static_cast<uint64_t>(i) * N : nullptr;
+      for (uint32_t j = 0; j < N; ++j) {
+        uint8_t q = quantize_e4m3(bf16_to_float(src[j]) / sf);
+        ++h[q];
+        if (dst) dst[j] = q;
+      }
+    }
+  });
+  for (int c = 0; c < 256; ++c) {
+    uint64_t acc = 0;
+    for (auto &p : part) acc += p[c];
+    hist[c] = acc;
+  }
+}
+
+// eq. emp_entropy over a 256-bin histogram, summed in ascending code order.
+double entropy_bits(const uint64_t hist[256]) {
+  uint64_t n = 0;
+  for (int c = 0; c < 256; ++c) n += hist[c];
+  if (!n) return 0.0;
+  double h = 0.0;
+  for (int c = 0; c < 256; ++c) {
+    if (!hist[c]) continue;
+    double p = static_cast<double>(hist[c]) / static_cast<double>(n);
+    h -= p * std::log2(p);
+  }
+  return h;
+}
+
+// ANS metadata: frequencies summing to 2^P over the present symbols (ascending
+// code): f = max(1, floor(n_k 2^P / n)); surplus units by largest remainder
+// (ties: lower code), cycling; excess units removed one at a time from the
+// largest f > 1 (ties: lower code).
+bool normalise(const uint64_t hist[256], uint32_t P, std::vector<uint8_t> &sym,
+               std::vector<uint16_t> &freq) {
+  const int64_t M = int64_t(1) << P;
+  uint64_t n = 0;
+  sym.clear();
+  for (int c = 0; c < 256; ++c)
+    if (hist[c]) {
+      sym.push_back(static_cast<uint8_t>(c));
+      n += hist[c];
+    }
+  const size_t K = sym.size();
+  if (K == 0 || static_cast<int64_t>(K) > M) return false;
+  std::vector<int64_t> f(K);
+  std::vector<uint64_t> rem(K);
+  if (K == 1) {
+    freq.assign(1, static_cast<uint16_t>(M));
+    return true;
+  }
+  int64_t sum = 0;
+  for (size_t k = 0; k < K; ++k) {
+    uint64_t num = hist[sym[k]] * static_cast<uint64_t>(M);
+    f[k] = std::max<int64_t>(1, static_cast<int64_t>(num / n));
+    rem[k] = num % n;
+    sum += f[k];
+  }
+  int64_t deficit = M - sum;
+  if (deficit > 0) {
+    std::vector<size_t> order(K);
+    for (size_t k = 0; k < K; ++k) order[k] = k;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](size_t a, size_t b) { return rem[a] > rem[b]; });
+    for (size_t i = 0; deficit > 0; i = (i + 1) % K, --deficit) ++f[order[i]];
+  }
+  while (deficit < 0) {
+    size_t best = K;
+    for (size_t k = 0; k < K; ++k)
+      if (f[k] > 1 && (best == K || f[k] > f[best])) best = k;
+    if (best == K) return false;
+    --f[best];
+    ++deficit;
+  }
+  freq.resize(K);
+  for (size_t k = 0; k < K; ++k) freq[k] = static_cast<uint16_t>(f[k]);
+  return true;
+}
+
+struct SymbolCoder {
+  uint32_t freq = 0, cum = 0;
+  uint64_t push_at = 0;  // push a word first when x >= freq * 2^(32-P)
+};
+
+// Encode one chunk of n symbols.  Words are produced back to front into
+// `out` (capacity n), so the decoder reads them front to back; returns the
+// number of words, which end at out + n.
+uint32_t encode_chunk(const uint8_t *q, uint32_t n, uint32_t W, uint32_t P,
+                      const SymbolCoder *coder, uint16_t *out_end, uint32_t *states) {
+  std::vector<uint64_t> x(W, kStateLow);
+  uint16_t *w = out_end;
+  const uint32_t T = (n + W - 1) / W;
+  for (uint32_t t = T; t-- > 0;) {
+    const uint32_t base = t * W;
+    const uint32_t last = std::min(W, n - base);
+    for (uint32_t l = last; l-- > 0;) {
+      const SymbolCoder &c = coder[q[base + l]];
+      uint64_t s = x[l];
+      if (s >= c.push_at) {
+        *--w = static_cast<uint16_t>(s & 0xFFFF);
+        s >>= 16;
+      }
+      x[l] = ((s / c.freq) << P) + (s % c.freq) + c.cum;
+    }
+  }
+  for (uint32_t l = 0; l < W; ++l) states[l] = static_cast<uint32_t>(x[l]);
+  return static_cast<uint32_t>(out_end - w);
+}
+
+template <class T>
+void put(uint8_t *b, uint64_t off, T v) {
+  std::memcpy(b + off, &v, sizeof v);  // little-endian host
+}
+
+uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+extern "C" float eqe_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, double target_bits,
+                                  uint32_t sample_rows, uint32_t threads, double *h_out) {
+  if (!w || !M || !N) return -1.0f;
+  std::vector<uint32_t> rows;
+  if (sample_rows && sample_rows < M) {
+    for (uint32_t r = 0; r < sample_rows; ++r)
+      rows.push_back(static_cast<uint32_t>(static_cast<uint64_t>(r) * M / sample_rows));
+  } else {
+    for (uint32_t r = 0; r < M; ++r) rows.push_back(r);
+  }
+  const unsigned nt = worker_count(threads);
+  double lo = -4.0, hi = 24.0, best_err = INFINITY, best_h = 0.0;
+  float best = 1.0f;
+  for (int it = 0; it < 40; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    const float alpha = static_cast<float>(std::exp2(mid));
+    uint64_t hist[256];
+    quantize_rows(w, N, alpha, rows, nt, nullptr, nullptr, hist);
+    const double h = entropy_bits(hist);
+    if (std::fabs(h - target_bits) < best_err) {
+      best_err = std::fabs(h - target_bits);
+      best = alpha;
+      best_h = h;
+    }
+    (h > target_bits ? lo : hi) = mid;
+  }
+  if (h_out) *h_out = best_h;
+  return best;
+}
+
+extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
+                          const eqe_params *p, uint8_t **blob_out, uint64_t *bytes_out) {
+  if (!w || !p || !blob_out || !bytes_out || !M || !N) return -1;
+  const uint64_t n = static_cast<uint64_t>(M) * N;
+  const uint32_t W = p->lanes, C = p->chunk_syms, P = p->prob_bits;
+  if (n >= (uint64_t(1) << 32) || (W != 64 && W != 128 && W != 256) || C == 0 || C % W ||
+      P < 1 || P > 12 || !(alpha > 0.0f))
+    return -1;
+  const unsigned nt = worker_count(p->threads);
+  try {
+    std::vector<uint16_t> scale(M);
+    std::vector<uint8_t> codes(n);
+    std::vector<uint32_t> rows(M);
+    for (uint32_t i = 0; i < M; ++i) rows[i] = i;
+    uint64_t hist[256];
+    quantize_rows(w, N, alpha, rows, nt, scale.data(), codes.data(), hist);
+
+    std::vector<uint8_t> sym;
+    std::vector<uint16_t> freq;
+    if (!normalise(hist, P, sym, freq)) return -1;
+    SymbolCoder coder[256];
+    uint32_t cum = 0;
+    for (size_t k = 0; k < sym.size(); ++k) {
+      coder[sym[k]].freq = freq[k];
+      coder[sym[k]].cum = cum;
+      coder[sym[k]].push_at = static_cast<uint64_t>(freq[k]) << (32 - P);
+      cum += freq[k];
+    }
+
+    const uint32_t n_chunks = static_cast<uint32_t>((n + C - 1) / C);
+    std::vector<uint16_t> scratch(static_cast<uint64_t>(n_chunks) * C);
+    std::vector<uint32_t> count(n_chunks);
+    std::vector<uint32_t> states(static_cast<uint64_t>(n_chunks) * W);
+    parallel_for(n_chunks, nt, [&](uint64_t c) {
+      const uint64_t k0 = c * C;
+      const uint32_t nc = static_cast<uint32_t>(std::min<uint64_t>(C, n - k0));
+      count[c] = encode_chunk(codes.data() + k0, nc, W, P, coder, scratch.data() + k0 + C,
+                              states.data() + c * W);
+    });
+    std::vector<uint32_t> off(n_chunks + 1, 0);
+    for (uint32_t c = 0; c < n_chunks; ++c) off[c + 1] = off[c] + count[c];
+    const uint64_t total = off[n_chunks];
+    const uint64_t padded = round_up(total + 1024, 128);
+    const uint32_t K = static_cast<uint32_t>(sym.size());
+
+    const uint64_t o_scale = kHeaderBytes;
+    const uint64_t o_sym = round_up(o_scale + 2ull * M, 256);
+    const uint64_t o_freq = round_up(o_sym + K, 256);
+    const uint64_t o_off = round_up(o_freq + 2ull * K, 256);
+    const uint64_t o_state = round_up(o_off + 4ull * (n_chunks + 1), 256);
+    const uint64_t o_words = round_up(o_state + 4ull * n_chunks * W, 256);
+    const uint64_t bytes = round_up(o_words + 2 * padded, 256);
+    uint8_t *b = static_cast<uint8_t *>(std::calloc(1, bytes));
+    if (!b) return -5;
+    std::memcpy(b, "EQC1", 4);
+    put<uint32_t>(b, 4, 1);                  // version
+    put<uint32_t>(b, 8, kHeaderBytes);
+    put<uint32_t>(b, 12, 1);                 // base format: E4M3FN
+    put<uint32_t>(b, 16, M);
+    put<uint32_t>(b, 20, N);
+    put<uint32_t>(b, 24, C);
+    put<uint32_t>(b, 28, n_chunks);
+    put<uint32_t>(b, 32, W);
+    put<uint32_t>(b, 36, P);
+    put<uint32_t>(b, 40, K);
+    put<uint32_t>(b, 44, 0);                 // flags
+    put<uint64_t>(b, 48, total);
+    put<uint64_t>(b, 56, padded);
+    put<uint64_t>(b, 64, p->seed);
+    put<float>(b, 72, alpha);
+    put<float>(b, 76, p->target_bits);
+    put<float>(b, 80, static_cast<float>(entropy_bits(hist)));
+    put<uint64_t>(b, 88, o_scale);
+    put<uint64_t>(b, 96, o_sym);
+    put<uint64_t>(b, 104, o_freq);
+    put<uint64_t>(b, 112, o_off);
+    put<uint64_t>(b, 120, o_state);
+    put<uint64_t>(b, 128, o_words);
+    put<uint64_t>(b, 136, bytes);
+    std::memcpy(b + o_scale, scale.data(), 2ull * M);
+    std::memcpy(b + o_sym, sym.data(), K);
+    std::memcpy(b + o_freq, freq.data(), 2ull * K);
+    std::memcpy(b + o_off, off.data(), 4ull * (n_chunks + 1));
+    std::memcpy(b + o_state, states.data(), 4ull * n_chunks * W);
+    parallel_for(n_chunks, nt, [&](uint64_t c) {
+      const uint64_t end = c * C + C;
+      std::memcpy(b + o_words + 2ull * off[c], scratch.data() + end - count[c], 2ull * count[c]);
+    });
+    *blob_out = b;
+    *bytes_out = bytes;
+    return 0;
+  } catch (const std::bad_alloc &) {
+    return -5;
+  }
+}
+
+extern "C" void eqe_free(void *ptr) { std::free(ptr); }

@@ -1,0 +1,120 @@
+// Host side of libeq: container validation (eq_layer_init), error strings.
+// The container layout and the checks are documented in eq.h.
+#include <cmath>
+#include <cstring>
+
+#include "eq.h"
+#include "eq_internal.h"
+
+namespace {
+
+template <class T>
+T rd(const uint8_t *b, uint64_t off) {
+  T v;
+  std::memcpy(&v, b + off, sizeof v);  // little-endian host
+  return v;
+}
+
+bool section_ok(uint64_t off, uint64_t len, uint64_t file_bytes) {
+  return off % 256 == 0 && off >= 256 && off <= file_bytes && len <= file_bytes - off;
+}
+
+// BF16 scale usable by the dequantiser: finite, normal, 2^-117 <= |s| < 2^120,
+// so s * v(q) is an exact fp32 product for every E4M3 value v(q).
+bool scale_ok(uint16_t s) {
+  const int e = (s >> 7) & 0xFF;
+  return e >= 127 - 117 && e <= 127 + 119;
+}
+
+}  // namespace
+
+extern "C" size_t eq_lut_bytes(void) { return eq_detail::kLutBytes; }
+
+extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
+                             const void *dev_blob, void *dev_lut, int32_t *dev_status) {
+  if (!L || !host_blob || !dev_blob || !dev_lut || !dev_status) return EQ_EINVAL;
+  const uint8_t *b = static_cast<const uint8_t *>(host_blob);
+  if (bytes < 256 || std::memcmp(b, "EQC1", 4) != 0) return EQ_EFORMAT;
+  if (rd<uint32_t>(b, 4) != 1 || rd<uint32_t>(b, 8) != 256 || rd<uint32_t>(b, 12) != 1)
+    return EQ_EFORMAT;
+  const uint32_t M = rd<uint32_t>(b, 16), N = rd<uint32_t>(b, 20), C = rd<uint32_t>(b, 24);
+  const uint32_t n_chunks = rd<uint32_t>(b, 28), W = rd<uint32_t>(b, 32);
+  const uint32_t P = rd<uint32_t>(b, 36), K = rd<uint32_t>(b, 40);
+  const uint64_t total = rd<uint64_t>(b, 48), padded = rd<uint64_t>(b, 56);
+  const uint64_t o_scale = rd<uint64_t>(b, 88), o_sym = rd<uint64_t>(b, 96);
+  const uint64_t o_freq = rd<uint64_t>(b, 104), o_off = rd<uint64_t>(b, 112);
+  const uint64_t o_state = rd<uint64_t>(b, 120), o_words = rd<uint64_t>(b, 128);
+  const uint64_t file_bytes = rd<uint64_t>(b, 136);
+  const uint64_t n = static_cast<uint64_t>(M) * N;
+  if (file_bytes > bytes || n == 0 || n >= (uint64_t(1) << 32)) return EQ_EFORMAT;
+  if ((W != 64 && W != 128 && W != 256) || C == 0 || C % W != 0) return EQ_EFORMAT;
+  if (n_chunks != (n + C - 1) / C || P < eq_detail::kMinProbBits || P > 12 || K < 1 || K > 256 ||
+      K > (1u << P))
+    return EQ_EFORMAT;
+  // word indices (including a chunk's worth of overrun on a corrupt stream)
+  // stay below 2^32
+  if (padded < total + 1024 || padded % 128 != 0 || padded + C >= (uint64_t(1) << 32))
+    return EQ_EFORMAT;
+  if (!section_ok(o_scale, 2ull * M, file_bytes) || !section_ok(o_sym, K, file_bytes) ||
+      !section_ok(o_freq, 2ull * K, file_bytes) ||
+      !section_ok(o_off, 4ull * (n_chunks + 1), file_bytes) ||
+      !section_ok(o_state, 4ull * n_chunks * W, file_bytes) ||
+      !section_ok(o_words, 2 * padded, file_bytes))
+    return EQ_EFORMAT;
+
+  uint32_t fsum = 0;
+  for (uint32_t k = 0; k < K; ++k) {
+    const uint8_t s = b[o_sym + k];
+    if ((s & 0x7F) == 0x7F) return EQ_EFORMAT;          // NaN code
+    if (k && s <= b[o_sym + k - 1]) return EQ_EFORMAT;  // strictly ascending
+    const uint16_t f = rd<uint16_t>(b, o_freq + 2ull * k);
+    if (f == 0) return EQ_EFORMAT;
+    fsum += f;
+  }
+  if (fsum != (1u << P)) return EQ_EFORMAT;
+  uint32_t prev = 0;
+  for (uint32_t c = 0; c <= n_chunks; ++c) {
+    const uint32_t o = rd<uint32_t>(b, o_off + 4ull * c);
+    if ((c == 0 && o != 0) || o < prev) return EQ_EFORMAT;
+    prev = o;
+  }
+  if (prev != total) return EQ_EFORMAT;
+  for (uint64_t s = 0; s < static_cast<uint64_t>(n_chunks) * W; ++s)
+    if (rd<uint32_t>(b, o_state + 4 * s) < (1u << 16)) return EQ_EFORMAT;
+  for (uint32_t i = 0; i < M; ++i)
+    if (!scale_ok(rd<uint16_t>(b, o_scale + 2ull * i))) return EQ_EFORMAT;
+
+  const uint8_t *d = static_cast<const uint8_t *>(dev_blob);
+  eq_layer v;
+  std::memset(&v, 0, sizeof v);
+  v.rows = M;
+  v.cols = N;
+  v.chunk_syms = C;
+  v.n_chunks = n_chunks;
+  v.lanes = W;
+  v.prob_bits = P;
+  v.n_syms = K;
+  v.total_words = total;
+  v.padded_words = padded;
+  v.scale = reinterpret_cast<const uint16_t *>(d + o_scale);
+  v.sym = d + o_sym;
+  v.freq = reinterpret_cast<const uint16_t *>(d + o_freq);
+  v.chunk_off = reinterpret_cast<const uint32_t *>(d + o_off);
+  v.chunk_state = reinterpret_cast<const uint32_t *>(d + o_state);
+  v.words = reinterpret_cast<const uint16_t *>(d + o_words);
+  v.lut = static_cast<uint32_t *>(dev_lut);
+  v.status = dev_status;
+  *L = v;
+  return EQ_OK;
+}
+
+extern "C" const char *eq_strerror(int code) {
+  switch (code) {
+    case EQ_OK: return "ok";
+    case EQ_EINVAL: return "invalid argument (null pointer, size or range)";
+    case EQ_EFORMAT: return "container header or sections inconsistent";
+    case EQ_EHIP: return "HIP launch or runtime call failed";
+    case EQ_ECORRUPT: return "entropy-coded stream failed its end-of-chunk check";
+    default: return "unknown error code";
+  }
+}

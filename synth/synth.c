@@ -96,9 +96,9 @@ int eqs_weights(const eqs_weight_spec *spec, uint64_t seed, uint32_t M,
   if (!spec || !w || M == 0 || N == 0) return -1;
   if (spec->kind == EQS_STUDENT_T && (spec->nu < 1 || spec->nu > 7)) return -1;
   if (spec->kind != EQS_STUDENT_T && spec->kind != EQS_GAUSS_OUTLIER) return -1;
-  if (nthreads <= 0) {
+  if (nthreads <= 0) { /* one per online CPU, at most 16 */
     long n = sysconf(_SC_NPROCESSORS_ONLN);
-    nthreads = n > 0 ? (int)n : 1;
+    nthreads = n > 16 ? 16 : (n > 0 ? (int)n : 1);
   }
   if (nthreads > 64) nthreads = 64;
   if ((uint32_t)nthreads > M) nthreads = (int)M;

@@ -55,7 +55,8 @@ typedef struct eqs_weight_spec {
 
 /* Fill w[M*N] (row-major BF16 bit patterns) with
  * W_ij = bf16(r_i * e_ij).  Returns 0, or -1 on bad arguments.
- * nthreads <= 0 uses one thread per online CPU (at most 64). */
+ * nthreads <= 0 uses one thread per online CPU, at most 16 (at most 64
+ * threads in any case). */
 int eqs_weights(const eqs_weight_spec *spec, uint64_t seed, uint32_t M,
                 uint32_t N, uint16_t *w, int nthreads);
 

@@ -1,0 +1,117 @@
+"""The C-ABI library: loads without a GPU, exports every declared symbol, and
+validates containers on the host (no device access in these calls)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2601_22787_amd as eq
+import synth
+from synth.configs import small_spec
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in ("eq.h", "eq_encode.h"):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(eqe?_\w+)\s*\(", text))
+    return names
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert {"eq_layer_init", "eq_layer_prepare", "eq_decode_codes", "eq_decode_bf16",
+            "eq_decode_gemv", "eq_gemv_workspace_bytes", "eq_get_status", "eq_strerror",
+            "eq_lut_bytes", "eqe_encode", "eqe_alpha_search", "eqe_free"} <= names
+    L = ctypes.CDLL(eq._LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    assert names == set(eq.SIGNATURES)
+
+
+def test_strerror():
+    assert eq.eq_strerror(0) == "ok"
+    for code in (-1, -2, -3, -4):
+        assert eq.eq_strerror(code) and eq.eq_strerror(code) != "unknown error code"
+    assert eq.eq_strerror(7) == "unknown error code"
+
+
+@pytest.fixture(scope="module")
+def blob():
+    w = synth.weights(small_spec(40, 512, seed=21))
+    return eq.eqe_encode(w, 300.0, chunk_syms=2048, lanes=128)
+
+
+def _init(b):
+    b = np.ascontiguousarray(b, dtype=np.uint8)
+    fake = np.zeros(64, dtype=np.uint8)  # stand-in device pointers: never dereferenced
+    L = eq.eq_layer()
+    rc = eq.lib().eq_layer_init(ctypes.byref(L), b.ctypes.data, b.size, fake.ctypes.data,
+                                fake.ctypes.data, fake.ctypes.data)
+    return rc, L
+
+
+def test_layer_init_accepts_valid(blob):
+    rc, L = _init(blob)
+    assert rc == eq.EQ_OK
+    info = oracle.container_info(blob)
+    assert (L.rows, L.cols, L.chunk_syms, L.n_chunks, L.lanes, L.prob_bits, L.n_syms) == \
+        (info.rows, info.cols, info.chunk_syms, info.n_chunks, info.lanes, info.prob_bits,
+         info.n_syms)
+    assert L.total_words == info.total_words
+
+
+def _patch(b, off, value, dtype):
+    b = b.copy()
+    b[off:off + np.dtype(dtype).itemsize] = np.frombuffer(np.array([value], dtype=dtype).tobytes(),
+                                                          dtype=np.uint8)
+    return b
+
+
+def test_layer_init_rejects_bad_containers(blob):
+    info = oracle.container_info(blob)
+    bad = {
+        "magic": _patch(blob, 0, 0x31435158, np.uint32),
+        "version": _patch(blob, 4, 2, np.uint32),
+        "format": _patch(blob, 12, 2, np.uint32),
+        "lanes": _patch(blob, 32, 96, np.uint32),
+        "chunks": _patch(blob, 28, info.n_chunks + 1, np.uint32),
+        "prob_bits_small": _patch(blob, 36, 7, np.uint32),
+        "freq_sum": _patch(blob, info.off_freq, 1 + int(blob[info.off_freq]), np.uint8),
+        "sym_order": _patch(blob, info.off_sym, 0xFE, np.uint8),
+        "offset_order": _patch(blob, info.off_chunk_off + 4, 0xFFFFFFF, np.uint32),
+        "state_low": _patch(blob, info.off_chunk_state + 8, 5, np.uint32),
+        "scale_zero": _patch(blob, info.off_scale + 6, 0, np.uint16),
+        "scale_inf": _patch(blob, info.off_scale + 6, 0x7F80, np.uint16),
+        "padding": _patch(blob, 56, info.total_words + 8, np.uint64),
+        "section": _patch(blob, 128, 1 << 40, np.uint64),
+    }
+    for name, b in bad.items():
+        rc, _ = _init(b)
+        assert rc == eq.EQ_EFORMAT, name
+    rc, _ = _init(blob[:300])
+    assert rc == eq.EQ_EFORMAT
+    L = eq.eq_layer()
+    assert eq.lib().eq_layer_init(ctypes.byref(L), None, 0, None, None, None) == eq.EQ_EINVAL
+
+
+def test_workspace_size_and_argument_checks(blob):
+    rc, L = _init(blob)
+    assert rc == eq.EQ_OK
+    assert eq.lib().eq_gemv_workspace_bytes(ctypes.byref(L), 0) == 0
+    assert eq.lib().eq_gemv_workspace_bytes(ctypes.byref(L), 9) == 0
+    assert eq.lib().eq_gemv_workspace_bytes(ctypes.byref(L), 8) >= 2 * L.n_chunks * 8 * 4
+    # null outputs are rejected on the host, before any launch
+    assert eq.lib().eq_decode_codes(ctypes.byref(L), None, None) == eq.EQ_EINVAL
+    assert eq.lib().eq_decode_bf16(ctypes.byref(L), None, None) == eq.EQ_EINVAL
+    fake = np.zeros(16, dtype=np.uint8)
+    assert eq.lib().eq_decode_gemv(ctypes.byref(L), fake.ctypes.data, 9, None, fake.ctypes.data,
+                                   fake.ctypes.data, 1 << 20, None) == eq.EQ_EINVAL
+    assert eq.lib().eq_decode_gemv(ctypes.byref(L), fake.ctypes.data, 2, None, fake.ctypes.data,
+                                   fake.ctypes.data, 4, None) == eq.EQ_EINVAL

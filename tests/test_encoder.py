@@ -1,0 +1,89 @@
+"""The product's host encoder against the oracle.
+
+Both implement the same container definition independently; given the same
+weights and alpha they must produce byte-identical containers.  The scale
+search must land on the target entropy (measured by the oracle).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2601_22787_amd as eq
+import synth
+from synth.configs import config_matrices, small_spec
+
+
+def test_c1_container_identical_to_oracle(c1_container):
+    spec, w, alpha, blob_ref = c1_container
+    blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes, seed=spec.seed,
+                         target_bits=spec.target_bits)
+    assert blob.size == blob_ref.size
+    assert (blob == blob_ref).all()
+
+
+@pytest.mark.parametrize("M,N,C,lanes,alpha,outliers", [
+    (5, 77, 128, 64, 300.0, False), (1, 1, 64, 64, 1.0, False), (33, 1000, 1024, 256, 1e4, False),
+    (64, 256, 4096, 128, 2.0, True), (17, 640, 640, 64, 7e5, False), (9, 4160, 8192, 256, 50.0, True)])
+def test_small_containers_identical_to_oracle(M, N, C, lanes, alpha, outliers):
+    w = synth.weights(small_spec(M, N, seed=M + N, outliers=outliers))
+    a = eq.eqe_encode(w, alpha, chunk_syms=C, lanes=lanes, threads=3)
+    b = oracle.container_build(w, alpha, 12, C, lanes)
+    assert (a == b).all()
+
+
+def test_zero_matrix_and_thread_independence():
+    w = np.zeros((8, 128), dtype=np.uint16)
+    assert (eq.eqe_encode(w, 1.0, chunk_syms=256, lanes=64) ==
+            oracle.container_build(w, 1.0, 12, 256, 64)).all()
+    w = synth.weights(small_spec(300, 512, seed=4))
+    a = eq.eqe_encode(w, 999.0, chunk_syms=4096, lanes=64, threads=1)
+    b = eq.eqe_encode(w, 999.0, chunk_syms=4096, lanes=64, threads=8)
+    assert (a == b).all()
+
+
+def test_rejects_bad_arguments():
+    w = np.zeros((4, 64), dtype=np.uint16)
+    for kw in (dict(chunk_syms=100, lanes=64), dict(chunk_syms=256, lanes=96),
+               dict(chunk_syms=256, lanes=64, prob_bits=13), dict(chunk_syms=0, lanes=64)):
+        with pytest.raises(eq.EqError):
+            eq.eqe_encode(w, 1.0, **kw)
+    with pytest.raises(eq.EqError):
+        eq.eqe_encode(w, -1.0, chunk_syms=256, lanes=64)
+
+
+@pytest.mark.parametrize("bits", [2.0, 3.0, 4.0])
+def test_alpha_search_hits_target(c1_weights, bits):
+    spec, w = c1_weights
+    alpha, h = eq.eqe_alpha_search(w, bits)
+    assert abs(h - bits) <= 0.05
+    q = oracle.quantize(w, oracle.row_scales(w, alpha))
+    assert oracle.entropy_codes(q) == pytest.approx(h, abs=1e-9)
+
+
+def test_alpha_search_on_row_sample(c1_weights):
+    spec, w = c1_weights
+    alpha, h_sample = eq.eqe_alpha_search(w, 2.0, sample_rows=128)
+    q = oracle.quantize(w, oracle.row_scales(w, alpha))
+    assert abs(oracle.entropy_codes(q) - 2.0) <= 0.05
+
+
+def test_c3_gate_full_size_matches_oracle_quantiser():
+    """Full-size config-3 matrix: the product container's codes (decoded by
+    the oracle on sampled chunks) equal the oracle's quantiser applied to the
+    generated weights with the container's alpha."""
+    spec = config_matrices(3)[0]
+    w = synth.weights(spec)
+    alpha, h = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=1024)
+    blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes)
+    info = oracle.container_info(blob)
+    assert abs(info.entropy_bits - spec.target_bits) <= 0.05
+    scale = oracle.container_scales(blob)
+    r = np.random.default_rng(0)
+    for c in sorted(r.choice(info.n_chunks, 6, replace=False)) + [info.n_chunks - 1]:
+        rc, q = oracle.container_decode_chunk(blob, int(c))
+        assert rc == oracle.OK
+        k0 = int(c) * info.chunk_syms
+        rows = range(k0 // spec.cols, (k0 + q.size - 1) // spec.cols + 1)
+        ref = oracle.quantize(w[rows.start:rows.stop], scale[rows.start:rows.stop]).ravel()
+        off = k0 - rows.start * spec.cols
+        assert (ref[off:off + q.size] == q).all()

@@ -1,0 +1,265 @@
+"""GPU parity: libeq's gfx950 kernels against the CPU oracle.
+
+Codes and dequantised BF16 weights must be bit-exact; the fused GEMV must be
+within max|y - y_ref| / max|y_ref| <= 1e-2 per batch row against the oracle's
+fp64 GEMV on the decoded BF16 weights (the bar stated for this path; the
+kernel's own error is fp32 accumulation plus the BF16 rounding of W_hat that
+it skips, about 1e-3 of the row norm at worst).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import config_matrices, small_spec
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def eq():
+    import paper_2601_22787_amd as m
+    m.lib()  # fails loudly if the library is not built
+    assert torch.cuda.is_available()
+    return m
+
+
+def _dev():
+    return torch.device("cuda:0")
+
+
+def gpu_codes(eq, L):
+    out = torch.empty(L.rows * L.cols, dtype=torch.uint8, device=_dev())
+    eq.eq_decode_codes(L, out)
+    return out.cpu().numpy().reshape(L.rows, L.cols)
+
+
+def gpu_bf16(eq, L):
+    out = torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev())
+    eq.eq_decode_bf16(L, out)
+    return out.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)
+
+
+def gpu_gemv(eq, L, x_bits, bias_bits=None, stream=None):
+    B = x_bits.shape[0]
+    x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+    bias = None if bias_bits is None else torch.from_numpy(bias_bits.view(np.int16)).to(_dev())
+    y = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+    eq.eq_decode_gemv(L, x, B, bias, y, L.workspace(B), stream)
+    return y.cpu().numpy()
+
+
+def rel_err(y, y_ref):
+    return np.abs(y - y_ref).max(axis=1) / np.maximum(np.abs(y_ref).max(axis=1), 1e-30)
+
+
+def check_full(eq, blob, spec_like, batches=(1,), with_bias=True):
+    """Whole-matrix comparison (sizes the oracle finishes in seconds)."""
+    L = eq.Layer(blob, _dev())
+    rc, q_ref = oracle.container_decode(blob)
+    assert rc == oracle.OK
+    q = gpu_codes(eq, L)
+    assert np.array_equal(q, q_ref), "codes differ"
+    w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
+    w = gpu_bf16(eq, L)
+    assert np.array_equal(w, w_ref), "bf16 differs"
+    for B in batches:
+        x = synth.activations(spec_like, B)
+        bias = synth.bias(spec_like) if with_bias else None
+        y = gpu_gemv(eq, L, x, bias)
+        y_ref = oracle.gemv(w_ref, x, bias)
+        err = rel_err(y, y_ref)
+        assert np.isfinite(y).all() and (err <= TOL).all(), (B, err)
+    assert eq.eq_get_status(L) == eq.EQ_OK
+    return L
+
+
+EDGE = [
+    # M, N, C, lanes, bits, outliers
+    (1, 64, 64, 64, 2.0, False),       # a single full step
+    (1, 1, 64, 64, 2.0, False),        # one symbol, one partial step
+    (3, 77, 128, 64, 3.0, False),      # ragged N, partial last chunk
+    (5, 100, 256, 256, 2.0, False),    # N < W: steps span several rows
+    (40, 640, 1024, 64, 2.0, False),   # rows split between chunks
+    (6, 8192, 4096, 64, 2.5, False),   # rows longer than chunks
+    (64, 512, 4096, 128, 4.0, True),   # W = 128, outliers
+    (37, 1280, 65536, 256, 2.0, False),  # W = 256, single partial chunk
+    (16, 4160, 8192, 256, 3.0, False), # ragged at W = 256; B = 8 reads x from global memory
+    (24, 1024, 2048, 128, 6.0, False), # near-flat distribution (many symbols)
+]
+
+
+@pytest.mark.parametrize("M,N,C,lanes,bits,outliers", EDGE)
+def test_edge_shapes(eq, M, N, C, lanes, bits, outliers):
+    say("edge", M, N, C, lanes, bits)
+    spec = small_spec(M, N, bits=bits, chunk=C, lanes=lanes, seed=1000 + M * 7 + N,
+                      outliers=outliers)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, bits)
+    blob = eq.eqe_encode(w, alpha, chunk_syms=C, lanes=lanes)
+    check_full(eq, blob, spec, batches=(1, 3, 8))
+
+
+def test_single_symbol_layer(eq):
+    say("single symbol")
+    spec = small_spec(8, 128, chunk=256, lanes=64)
+    w = np.zeros((8, 128), dtype=np.uint16)
+    blob = eq.eqe_encode(w, 1.0, chunk_syms=256, lanes=64)
+    assert oracle.container_info(blob).n_syms == 1
+    check_full(eq, blob, spec, batches=(1, 2))
+
+
+def test_oracle_built_container(eq, c1_container):
+    """A container written by the oracle's own encoder decodes identically."""
+    say("oracle-built c1")
+    spec, w, alpha, blob = c1_container
+    check_full(eq, blob, spec, batches=(1, 8))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_config_full(eq, cfg):
+    for spec in config_matrices(cfg):
+        say("config", cfg, spec.name, spec.rows, spec.cols)
+        w = synth.weights(spec)
+        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=1024)
+        blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
+                             seed=spec.seed, target_bits=spec.target_bits)
+        info = oracle.container_info(blob)
+        assert abs(info.entropy_bits - spec.target_bits) <= 0.05
+        check_full(eq, blob, spec, batches=(1, 8) if cfg < 3 else (1,))
+
+
+def test_one_hot_and_zero_inputs(eq):
+    say("one-hot")
+    spec = small_spec(48, 1024, bits=3.0, chunk=4096, lanes=64, seed=5)
+    w = synth.weights(spec)
+    blob = eq.eqe_encode(w, eq.eqe_alpha_search(w, 3.0)[0], chunk_syms=4096, lanes=64)
+    L = eq.Layer(blob, _dev())
+    _, q_ref = oracle.container_decode(blob)
+    scale = oracle.container_scales(blob)
+    w_ref = oracle.dequant(q_ref, scale)
+    cols = [0, 1, 63, 64, 511, 1023]
+    x = np.zeros((len(cols), 1024), dtype=np.uint16)
+    for b, j in enumerate(cols):
+        x[b, j] = 0x3F80  # 1.0
+    y = gpu_gemv(eq, L, x)
+    for b, j in enumerate(cols):
+        exact = synth.bf16_to_f32(scale).astype(np.float64) * \
+            np.array([oracle.e4m3_value(int(c)) for c in q_ref[:, j]])
+        assert np.array_equal(y[b].astype(np.float64), exact)   # s_i * v(q_ij), exact in fp32
+        back = torch.from_numpy(y[b]).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(back, w_ref[:, j])
+    bias = synth.bias(spec)
+    y0 = gpu_gemv(eq, L, np.zeros((2, 1024), dtype=np.uint16), bias)
+    assert np.array_equal(y0, np.stack([synth.bf16_to_f32(bias)] * 2))
+
+
+def test_deterministic_and_streams(eq):
+    say("determinism")
+    spec = small_spec(256, 2048, bits=2.0, chunk=16384, lanes=64, seed=8)
+    w = synth.weights(spec)
+    blob = eq.eqe_encode(w, eq.eqe_alpha_search(w, 2.0)[0], chunk_syms=16384, lanes=64)
+    L = eq.Layer(blob, _dev())
+    x = synth.activations(spec, 2)
+    y0 = gpu_gemv(eq, L, x)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y1 = gpu_gemv(eq, L, x, stream=s)
+    torch.cuda.synchronize()
+    y2 = gpu_gemv(eq, L, x)
+    assert np.array_equal(y0, y1) and np.array_equal(y0, y2)
+
+
+def test_corrupted_stream_flagged(eq):
+    """A flipped stream bit: the GPU must reach the oracle's verdict, and
+    when the oracle still decodes cleanly the codes must agree."""
+    say("corruption")
+    spec = small_spec(32, 1024, bits=2.0, chunk=4096, lanes=64, seed=9)
+    w = synth.weights(spec)
+    blob = eq.eqe_encode(w, eq.eqe_alpha_search(w, 2.0)[0], chunk_syms=4096, lanes=64)
+    info = oracle.container_info(blob)
+    r = np.random.default_rng(3)
+    flagged = 0
+    for trial in range(6):
+        bad = blob.copy()
+        word = int(r.integers(info.total_words))
+        bad[info.off_words + 2 * word + int(r.integers(2))] ^= np.uint8(1 << int(r.integers(8)))
+        L = eq.Layer(bad, _dev())
+        q = gpu_codes(eq, L)
+        rc_gpu = eq.eq_get_status(L)
+        rc_ref, q_ref = oracle.container_decode(bad)
+        if rc_ref == oracle.ECORRUPT:
+            assert rc_gpu == eq.EQ_ECORRUPT
+            flagged += 1
+        else:
+            assert rc_gpu == eq.EQ_OK and np.array_equal(q, q_ref)
+        eq.eq_layer_prepare(L)  # clears the status word
+        assert eq.eq_get_status(L) == eq.EQ_OK
+    assert flagged >= 1
+
+
+@pytest.fixture(scope="module")
+def c4_layers(eq):
+    out = []
+    for spec in config_matrices(4):
+        say("config 4 build", spec.name)
+        w = synth.weights(spec)
+        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
+        blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
+                             seed=spec.seed, target_bits=spec.target_bits)
+        out.append((spec, w, alpha, blob, eq.Layer(blob, _dev())))
+    return out
+
+
+def _chunk_rows(info, c):
+    k0 = c * info.chunk_syms
+    n = min(info.chunk_syms, info.rows * info.cols - k0)
+    return k0, n
+
+
+def test_config4_full_size_sampled(eq, c4_layers):
+    """Full 8192x28672 and 28672x8192 layers in the launch configuration the
+    benchmark times: sampled chunks bit-exact (codes, BF16), sampled rows of
+    the fused GEMV at B = 1 and 8 against the oracle."""
+    r = np.random.default_rng(44)
+    for spec, w, alpha, blob, L in c4_layers:
+        say("config 4 parity", spec.name)
+        info = oracle.container_info(blob)
+        assert abs(info.entropy_bits - spec.target_bits) <= 0.05
+        scale = oracle.container_scales(blob)
+        q = gpu_codes(eq, L).ravel()
+        wb = gpu_bf16(eq, L).ravel()
+        assert eq.eq_get_status(L) == eq.EQ_OK
+        chunks = sorted(set(r.choice(info.n_chunks, 10, replace=False).tolist()) |
+                        {0, info.n_chunks - 1})
+        for c in chunks:
+            rc, q_ref = oracle.container_decode_chunk(blob, c)
+            assert rc == oracle.OK
+            k0, n = _chunk_rows(info, c)
+            assert np.array_equal(q[k0:k0 + n], q_ref), c
+            r0, r1 = k0 // spec.cols, (k0 + n - 1) // spec.cols + 1
+            # the oracle quantiser on the generated weights gives the same codes
+            q_rows = oracle.quantize(w[r0:r1], scale[r0:r1]).ravel()
+            assert np.array_equal(q_rows[k0 - r0 * spec.cols:][:n], q_ref)
+            w_rows = oracle.dequant(q_rows.reshape(r1 - r0, spec.cols), scale[r0:r1]).ravel()
+            assert np.array_equal(wb[k0:k0 + n], w_rows[k0 - r0 * spec.cols:][:n])
+        rows = sorted(set(r.choice(spec.rows, 6, replace=False).tolist()) | {0, spec.rows - 1})
+        w_rows = oracle.dequant(oracle.quantize(w[rows], scale[rows]), scale[rows])
+        for B in (1, 8):
+            x = synth.activations(spec, B)
+            y = gpu_gemv(eq, L, x)
+            y_ref = oracle.gemv(w_rows, x)
+            # normwise over the sampled rows
+            err = rel_err(y[:, rows], y_ref)
+            assert (err <= TOL).all(), (spec.name, B, err)
+            assert np.isfinite(y).all()

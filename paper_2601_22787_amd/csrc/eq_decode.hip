@@ -20,16 +20,17 @@ namespace {
 using namespace eq_detail;
 
 constexpr int kWave = 64;
-constexpr int kBlock = 512;              // 8 wavefronts, one chunk each
-constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kMaxWaves = 16;                 // wavefronts per block (one chunk each at a time)
+constexpr int kMaxBlock = kWave * kMaxWaves;
 constexpr int kMaxBatch = 8;
-constexpr uint32_t kHalf = 512;          // stream words per window half (1 KiB)
-constexpr uint32_t kWin = 2 * kHalf;     // per-wave LDS window of stream words
+constexpr uint32_t kHalf = 512;               // stream words per window half (1 KiB)
+constexpr uint32_t kWin = 2 * kHalf;          // per-wave LDS window of stream words
+constexpr int32_t kBufferFlags = 0x00020000;  // buffer resource word 3 (gfx9 family)
 
 enum Mode { kCodes = 0, kBf16 = 1, kGemv = 2 };
 
 struct Args {
-  const uint32_t *lut;          // slot table (2 x u32 per slot), then E4M3 value table
+  const uint32_t *lut;          // slot table, f32 value table, bf16 value table
   const uint16_t *scale;
   const uint32_t *chunk_off;
   const uint32_t *chunk_state;
@@ -47,12 +48,21 @@ struct Args {
   float *ws;
 };
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-// Round a finite fp32 value to nearest-even BF16.
-__device__ inline uint16_t f32_to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+// Two fp32 values to two nearest-even BF16 (low half: a).
+__device__ inline uint32_t pack_bf16(float a, float b) {
+  const float2v v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// acc + lo16(a) * lo16(b) + hi16(a) * hi16(b), operands as BF16 pairs.
+__device__ inline float dot2_bf16(uint32_t a, uint32_t b, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
+                                        __builtin_bit_cast(bf16x2, b), acc, false);
 }
 
 // E4M3FN value of a code: sign | exponent (bias 7) | 3-bit mantissa;
@@ -74,6 +84,19 @@ __device__ inline float wave_sum(float v) {
 
 __device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Value-table entry of the code in bits 24..31 of a slot entry.  Bits 13..23
+// of the entry are zero (f <= 2^12), so e >> 22 is already the byte offset.
+__device__ inline uint32_t code_value(const uint32_t *val_s, uint32_t e) {
+  return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(val_s) + (e >> 22));
+}
+
+// BF16 element i of an array in device memory, read as the containing
+// aligned dword so that a wave-uniform index becomes a scalar load.
+__device__ inline float bf16_at(const uint16_t *base, uint32_t i) {
+  const uint32_t w = reinterpret_cast<const uint32_t *>(base)[i >> 1];
+  return __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
+}
+
 // 16 stream words starting at word index i (a multiple of 8), clamped to the
 // padded section so that a read ahead never leaves the container.
 __device__ inline uint4 load_words(const uint16_t *words, uint32_t i, uint32_t last8) {
@@ -83,57 +106,58 @@ __device__ inline uint4 load_words(const uint16_t *words, uint32_t i, uint32_t l
 // Decode tables.  Slot s of symbol k (cum_k <= s < cum_k + f_k):
 //   lut[2s]   = f_k | code_k << 24     (low 24 bits feed a 24-bit multiply-add)
 //   lut[2s+1] = s - cum_k
-// then lut[2 * kMaxSlots + c] = bits of the E4M3 value of code c.
-__global__ void prepare_kernel(const uint8_t *sym, const uint16_t *freq, uint32_t K,
-                               uint32_t *lut, int32_t *status) {
+// then lut[2 kMaxSlots + c] = fp32 bits of the E4M3 value of code c and
+// lut[2 kMaxSlots + 256 + c] = its BF16 bits (exact), zero-extended.
+__global__ __launch_bounds__(1024) void prepare_kernel(const uint8_t *sym, const uint16_t *freq,
+                                                       uint32_t K, uint32_t nslots, uint32_t *lut,
+                                                       int32_t *status) {
+  __shared__ uint32_t cum_s[257];
   const uint32_t t = threadIdx.x;
-  if (t < K) {
-    uint32_t cum = 0;
-    for (uint32_t k = 0; k < t; ++k) cum += freq[k];
-    const uint32_t f = freq[t];
-    for (uint32_t s = 0; s < f; ++s) {
-      lut[2 * (cum + s)] = f | (uint32_t(sym[t]) << 24);
-      lut[2 * (cum + s) + 1] = s;
+  if (t == 0) {
+    uint32_t c = 0;
+    for (uint32_t k = 0; k < K; ++k) {
+      cum_s[k] = c;
+      c += freq[k];
     }
+    cum_s[K] = c;
   }
-  lut[2 * kMaxSlots + t] = __float_as_uint(e4m3_value(t));
+  __syncthreads();
+  for (uint32_t s = t; s < nslots; s += blockDim.x) {
+    uint32_t lo = 0, hi = K - 1;  // largest k with cum_k <= s
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) / 2;
+      if (cum_s[mid] <= s) lo = mid;
+      else hi = mid - 1;
+    }
+    lut[2 * s] = uint32_t(freq[lo]) | (uint32_t(sym[lo]) << 24);
+    lut[2 * s + 1] = s - cum_s[lo];
+  }
+  if (t < 256) {
+    const uint32_t bits = __float_as_uint(e4m3_value(t));
+    lut[2 * kMaxSlots + t] = bits;
+    lut[2 * kMaxSlots + 256 + t] = bits >> 16;
+  }
   if (t == 0) *status = 0;
 }
 
 // One wavefront decodes one chunk.  G = W / 64 coder states per lane (state
 // g * 64 + lane); MODE selects what is done with each decoded symbol;
 // UNIFORM means every step of W symbols lies inside one matrix row (N is a
-// multiple of W); XLDS means the activations are staged in LDS.
-template <int G, int MODE, bool UNIFORM, bool XLDS>
-__global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
-  extern __shared__ uint16_t x_s[];  // [batch][cols] BF16 when XLDS
-  __shared__ uint2 slot_s[kMaxSlots];
-  __shared__ float val_s[256];
-  __shared__ uint4 win_s[kWavesPerBlock][kWin / 8];
-  const uint32_t nslots = 1u << a.prob_bits;
-  const uint32_t N = a.cols;
-  {
-    const uint2 *src = reinterpret_cast<const uint2 *>(a.lut);
-    for (uint32_t i = threadIdx.x; i < nslots; i += kBlock) slot_s[i] = src[i];
-    if (threadIdx.x < 256) val_s[threadIdx.x] = __uint_as_float(a.lut[2 * kMaxSlots + threadIdx.x]);
-    if (XLDS) {
-      const uint32_t nx = a.batch * N;
-      for (uint32_t i = threadIdx.x; i < nx; i += kBlock) x_s[i] = a.x[i];
-    }
-  }
-  __syncthreads();
-
-  const uint32_t lane = threadIdx.x & (kWave - 1);
-  const uint32_t wave = uniform(threadIdx.x / kWave);
-  const uint32_t c = uniform(blockIdx.x * kWavesPerBlock + wave);
-  if (c >= a.n_chunks) return;
-
+// multiple of W); XLDS means the activations are staged in LDS; NB is the
+// GEMV batch when fixed at compile time (0: the runtime batch, up to 8).
+template <int G, int MODE, bool UNIFORM, bool XLDS, int NB>
+__device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t lane,
+                                             const uint2 *slot_s, const uint32_t *val_s,
+                                             uint4 *win4, const uint16_t *x_s) {
   constexpr uint32_t W = G * kWave;
+  const uint32_t N = a.cols;
   const uint32_t k0 = c * a.chunk_syms;
   const uint32_t nc = min(a.chunk_syms, a.n - k0);
-  const uint32_t mask = nslots - 1;
   const uint32_t P = a.prob_bits;
+  const uint32_t mask = (1u << P) - 1;
   const uint32_t last8 = a.padded_words - 8;
+  const uint16_t *win = reinterpret_cast<const uint16_t *>(win4);
+  const int nb = NB ? NB : static_cast<int>(a.batch);  // GEMV batch
 
   uint32_t x[G];
 #pragma unroll
@@ -145,23 +169,31 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
   // half is in flight in registers.  A step reads at most W words and the
   // window slides by a half whenever p passes its middle, so every word a
   // step can read is in LDS.
-  const uint16_t *win = reinterpret_cast<const uint16_t *>(win_s[wave]);
   uint32_t wb = p & ~7u;
   {
     const uint4 h0 = load_words(a.words, wb + 8 * lane, last8);
     const uint4 h1 = load_words(a.words, wb + kHalf + 8 * lane, last8);
-    win_s[wave][lane] = h0;
-    win_s[wave][kHalf / 8 + lane] = h1;
+    win4[lane] = h0;
+    win4[kHalf / 8 + lane] = h1;
   }
   __builtin_amdgcn_s_waitcnt(0);  // states, offsets and window are in
   uint4 next = load_words(a.words, wb + kWin + 8 * lane, last8);
+
+  // Outputs of this chunk through buffer resources: the address is the
+  // chunk's base plus a scalar step offset plus the lane's offset.  Stores
+  // of the partial last step are predicated per lane.
+  __amdgpu_buffer_rsrc_t out_rsrc;
+  if (MODE == kCodes)
+    out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + k0, 0, int(nc), kBufferFlags);
+  if (MODE == kBf16)
+    out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.wout + k0, 0, int(2 * nc), kBufferFlags);
 
   // uniform-row bookkeeping (every step lies inside one row)
   uint32_t row = k0 / N;
   const uint32_t first_row = row;
   uint32_t row_end = (row + 1) * N;  // <= n < 2^32
   float srow = 0.0f;
-  if (MODE == kBf16 && UNIFORM) srow = bf16_to_f32(a.scale[row]);
+  if (MODE == kBf16 && UNIFORM) srow = bf16_at(a.scale, row);
   // per-state row/column (general shapes)
   uint32_t prow[G], pcol[G];
   if (!UNIFORM) {
@@ -181,17 +213,17 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
 #pragma unroll
   for (int g = 0; g < G; ++g) pending[g] = false;
 
-  auto xval = [&](uint32_t b, uint32_t col) -> float {
-    return bf16_to_f32(XLDS ? x_s[b * N + col] : a.x[b * N + col]);
+  auto xbits = [&](uint32_t b, uint32_t col) -> uint32_t {
+    return XLDS ? x_s[b * N + col] : a.x[b * N + col];
   };
 
   auto flush_uniform = [&](uint32_t r) {
     const bool owned = r * N >= k0 && (r + 1) * N <= k0 + nc;
-    const float s = bf16_to_f32(a.scale[r]);
-    const float bb = a.bias ? bf16_to_f32(a.bias[r]) : 0.0f;
+    const float s = bf16_at(a.scale, r);
+    const float bb = a.bias ? bf16_at(a.bias, r) : 0.0f;
 #pragma unroll
     for (int b = 0; b < kMaxBatch; ++b) {
-      if (b < (int)a.batch) {
+      if (b < nb) {
         const float sum = wave_sum(acc[0][b]);
         if (lane == 0) {
           if (owned) a.y[b * a.rows + r] = s * sum + bb;
@@ -206,9 +238,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
   auto step = [&](auto tail_tag, uint32_t t) {
     constexpr bool TAIL = decltype(tail_tag)::value;
     if (p - wb >= kHalf) {  // slide the window by one half
-      const uint4 keep = win_s[wave][kHalf / 8 + lane];
-      win_s[wave][lane] = keep;
-      win_s[wave][kHalf / 8 + lane] = next;
+      const uint4 keep = win4[kHalf / 8 + lane];
+      win4[lane] = keep;
+      win4[kHalf / 8 + lane] = next;
       wb += kHalf;
       next = load_words(a.words, wb + kWin + 8 * lane, last8);
     }
@@ -217,39 +249,73 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
       if (MODE == kGemv) flush_uniform(row);
       ++row;
       row_end += N;
-      if (MODE == kBf16) srow = bf16_to_f32(a.scale[row]);
+      if (MODE == kBf16) srow = bf16_at(a.scale, row);
     }
+    bool act[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) act[g] = !TAIL || kk + g * kWave + lane < nc;
+
     // decode every active state of the step
+    uint32_t e0[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const uint32_t pos = kk + g * kWave + lane;
-      if (!TAIL || pos < nc) {
+      if (act[g]) {
         const uint2 e = slot_s[x[g] & mask];
         x[g] = __umul24(e.x, x[g] >> P) + e.y;
-        if (MODE == kCodes) {
-          uint8_t *out = a.codes + (k0 + kk + g * kWave);
-          out[lane] = static_cast<uint8_t>(e.x >> 24);
-        } else if (MODE == kBf16) {
-          const float s = UNIFORM ? srow : bf16_to_f32(a.scale[prow[g]]);
-          uint16_t *out = a.wout + (k0 + kk + g * kWave);
-          out[lane] = f32_to_bf16(s * val_s[e.x >> 24]);
-        } else {
-          const float v = val_s[e.x >> 24];
-          const uint32_t col = UNIFORM ? (k0 + kk + N - row_end) + g * kWave + lane : pcol[g];
-#pragma unroll
-          for (int b = 0; b < kMaxBatch; ++b)
-            if (b < (int)a.batch) acc[UNIFORM ? 0 : g][b] += v * xval(b, col);
-          if (!UNIFORM) pending[g] = true;
-        }
+        e0[g] = e.x;
+      } else {
+        e0[g] = 0;
       }
-      if (!UNIFORM && MODE != kCodes) {
+    }
+
+    // use the symbols
+    if (MODE == kCodes) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (!TAIL || act[g])
+          __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(e0[g] >> 24), out_rsrc, lane,
+                                               kk + g * kWave, 0);
+    } else if (MODE == kBf16) {
+#pragma unroll
+      for (int g = 0; g < G; g += 2) {
+        const float s0 = UNIFORM ? srow : bf16_at(a.scale, prow[g]);
+        const float v0 = s0 * __uint_as_float(code_value(val_s, e0[g]));
+        float v1 = 0.0f;
+        if (g + 1 < G) {
+          const float s1 = UNIFORM ? srow : bf16_at(a.scale, prow[g + 1]);
+          v1 = s1 * __uint_as_float(code_value(val_s, e0[g + 1]));
+        }
+        const uint32_t h = pack_bf16(v0, v1);  // exact products, rounded once
+        if (!TAIL || act[g])
+          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h), out_rsrc, 2 * lane,
+                                                2 * (kk + g * kWave), 0);
+        if (g + 1 < G && (!TAIL || act[g + 1]))
+          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h >> 16), out_rsrc,
+                                                2 * lane, 2 * (kk + (g + 1) * kWave), 0);
+      }
+    } else {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        if (!act[g]) continue;
+        const uint32_t v = code_value(val_s, e0[g]);  // BF16 value in the low half
+        const uint32_t col = UNIFORM ? (k0 + kk + N - row_end) + g * kWave + lane : pcol[g];
+#pragma unroll
+        for (int b = 0; b < kMaxBatch; ++b)
+          if (b < nb)
+            acc[UNIFORM ? 0 : g][b] = dot2_bf16(v, xbits(b, col), acc[UNIFORM ? 0 : g][b]);
+        if (!UNIFORM) pending[g] = true;
+      }
+    }
+    if (!UNIFORM && MODE != kCodes) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
         // advance this state's position by one step (W symbols)
         pcol[g] += W;
         if (pcol[g] >= N) {
           if (MODE == kGemv && pending[g]) {
 #pragma unroll
             for (int b = 0; b < kMaxBatch; ++b) {
-              if (b < (int)a.batch) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
+              if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
               acc[g][b] = 0.0f;
             }
             pending[g] = false;
@@ -259,17 +325,25 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
         }
       }
     }
-    // renormalise in ascending state order: state g*64 + lane
+
+    // renormalise in ascending state order (state g*64 + lane): all reads of
+    // the step are issued before any is used
+    bool need[G];
+    uint32_t word[G];
+    uint32_t rel = p - wb;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const bool need = (!TAIL || kk + g * kWave + lane < nc) && x[g] < kStateLow;
-      const uint64_t m = __builtin_amdgcn_ballot_w64(need);
+      need[g] = act[g] && x[g] < kStateLow;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(need[g]);
       const uint32_t below = __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32),
                                                        __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
-      const uint16_t *wp = win + (p - wb);
-      if (need) x[g] = (x[g] << 16) | wp[below];
-      p += static_cast<uint32_t>(__popcll(m));
+      word[g] = win[rel + below];
+      rel += static_cast<uint32_t>(__popcll(m));
     }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (need[g]) x[g] = (x[g] << 16) | word[g];
+    p = wb + rel;
   };
 
   const uint32_t full = nc / W;
@@ -285,7 +359,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
         if (pending[g])
 #pragma unroll
           for (int b = 0; b < kMaxBatch; ++b)
-            if (b < (int)a.batch) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
+            if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
     }
   }
 
@@ -294,6 +368,48 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Args a) {
 #pragma unroll
   for (int g = 0; g < G; ++g) bad |= x[g] != kStateLow;
   if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
+}
+
+// LDS of a decode block.  The value table comes first so that its byte
+// offsets fit the 16-bit immediate of LDS instructions.
+struct DecodeLds {
+  uint32_t val[256];
+  uint2 slot[kMaxSlots];
+  uint4 win[kMaxWaves][kWin / 8];
+};
+
+template <int G, int MODE, bool UNIFORM, bool XLDS, int NB>
+__global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
+  extern __shared__ uint4 x_dyn[];  // [batch][cols] BF16 when XLDS
+  __shared__ DecodeLds sm;
+  const uint32_t nthreads = blockDim.x;
+  const uint32_t nslots = 1u << a.prob_bits;
+  {
+    const uint4 *src = reinterpret_cast<const uint4 *>(a.lut);
+    uint4 *dst = reinterpret_cast<uint4 *>(sm.slot);
+    for (uint32_t i = threadIdx.x; i < nslots / 2; i += nthreads) dst[i] = src[i];
+    const uint32_t *vsrc = a.lut + 2 * kMaxSlots + (MODE == kGemv ? 256 : 0);
+    for (uint32_t i = threadIdx.x; i < 256; i += nthreads) sm.val[i] = vsrc[i];
+    if (XLDS) {
+      const uint32_t nx = a.batch * a.cols;
+      uint16_t *xs = reinterpret_cast<uint16_t *>(x_dyn);
+      if (nx % 8 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0) {
+        const uint4 *xv = reinterpret_cast<const uint4 *>(a.x);
+        for (uint32_t i = threadIdx.x; i < nx / 8; i += nthreads) x_dyn[i] = xv[i];
+      } else {
+        for (uint32_t i = threadIdx.x; i < nx; i += nthreads) xs[i] = a.x[i];
+      }
+    }
+  }
+  __syncthreads();
+
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave = uniform(threadIdx.x / kWave);
+  const uint32_t waves = uniform(nthreads / kWave);
+  for (uint32_t c = uniform(blockIdx.x * waves + wave); c < a.n_chunks;
+       c += gridDim.x * waves)
+    decode_chunk<G, MODE, UNIFORM, XLDS, NB>(a, c, lane, sm.slot, sm.val, sm.win[wave],
+                                         reinterpret_cast<const uint16_t *>(x_dyn));
 }
 
 // Rows split between chunks (whole-row steps): y = s * (sum of the chunks'
@@ -361,52 +477,87 @@ bool layer_ok(const eq_layer *L) {
 }
 
 constexpr uint32_t kMaxXLdsBytes = 64 * 1024;
-constexpr size_t kStaticLds =
-    kMaxSlots * sizeof(uint2) + 256 * sizeof(float) + kWavesPerBlock * kWin * sizeof(uint16_t);
+constexpr size_t kStaticLds = sizeof(DecodeLds);
 
-// LDS bytes one workgroup may use on the current device (cached per device).
-size_t lds_per_block() {
-  static std::atomic<int> cache[64];
+struct DeviceFacts {
+  int lds_per_block = 64 * 1024;
+  int cus = 256;
+};
+
+// Per-device limits, queried once per device.
+DeviceFacts device_facts() {
+  static std::atomic<int> lds[64], cus[64];
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 64 * 1024;
-  int v = cache[dev].load(std::memory_order_relaxed);
-  if (v == 0) {
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
-        v <= 0)
-      v = 64 * 1024;
-    cache[dev].store(v, std::memory_order_relaxed);
+  DeviceFacts f;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return f;
+  int l = lds[dev].load(std::memory_order_relaxed), c = cus[dev].load(std::memory_order_relaxed);
+  if (l == 0) {
+    if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+        l <= 0)
+      l = f.lds_per_block;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c <= 0)
+      c = f.cus;
+    lds[dev].store(l, std::memory_order_relaxed);
+    cus[dev].store(c, std::memory_order_relaxed);
   }
-  return static_cast<size_t>(v);
+  f.lds_per_block = l;
+  f.cus = c;
+  return f;
 }
 
-template <int MODE, bool UNIFORM, bool XLDS>
-void launch_mode(const Args &a, hipStream_t s) {
-  const dim3 grid((a.n_chunks + kWavesPerBlock - 1) / kWavesPerBlock), block(kBlock);
+// Blocks of up to 16 wavefronts, one chunk per wavefront at a time.  With
+// fewer chunks than wavefront slots, the chunks are spread evenly over the
+// compute units (one block each); otherwise each wavefront loops over chunks.
+void launch_shape(uint32_t n_chunks, int cus, dim3 &grid, dim3 &block) {
+  uint32_t waves = (n_chunks + cus - 1) / cus;
+  waves = waves < 1 ? 1 : (waves > kMaxWaves ? kMaxWaves : waves);
+  uint32_t blocks = (n_chunks + waves - 1) / waves;
+  if (blocks > uint32_t(cus) * 4) blocks = uint32_t(cus) * 4;
+  grid = dim3(blocks);
+  block = dim3(waves * kWave);
+}
+
+template <int MODE, bool UNIFORM, bool XLDS, int NB>
+void launch_mode(const Args &a, hipStream_t s, const DeviceFacts &f) {
+  dim3 grid, block;
+  launch_shape(a.n_chunks, f.cus, grid, block);
   const size_t shm = XLDS ? size_t(a.batch) * a.cols * sizeof(uint16_t) : 0;
   switch (a.lanes) {
     case 64:
-      hipLaunchKernelGGL((decode_kernel<1, MODE, UNIFORM, XLDS>), grid, block, shm, s, a);
+      hipLaunchKernelGGL((decode_kernel<1, MODE, UNIFORM, XLDS, NB>), grid, block, shm, s, a);
       break;
     case 128:
-      hipLaunchKernelGGL((decode_kernel<2, MODE, UNIFORM, XLDS>), grid, block, shm, s, a);
+      hipLaunchKernelGGL((decode_kernel<2, MODE, UNIFORM, XLDS, NB>), grid, block, shm, s, a);
       break;
     default:
-      hipLaunchKernelGGL((decode_kernel<4, MODE, UNIFORM, XLDS>), grid, block, shm, s, a);
+      hipLaunchKernelGGL((decode_kernel<4, MODE, UNIFORM, XLDS, NB>), grid, block, shm, s, a);
       break;
   }
+}
+
+template <int MODE, bool UNIFORM, bool XLDS>
+void launch_batch(const Args &a, hipStream_t s, const DeviceFacts &f) {
+  if (MODE != kGemv || a.batch == 1) launch_mode<MODE, UNIFORM, XLDS, 1>(a, s, f);
+  else launch_mode<MODE, UNIFORM, XLDS, 0>(a, s, f);
 }
 
 template <int MODE>
 int launch_decode(const Args &a, hipStream_t s) {
+  const DeviceFacts f = device_facts();
   const bool uniform = a.cols % a.lanes == 0;
   const size_t xbytes = size_t(a.batch) * a.cols * sizeof(uint16_t);
-  const bool xlds = MODE == kGemv && xbytes <= kMaxXLdsBytes && kStaticLds + xbytes <= lds_per_block();
-  if (uniform) {
-    if (xlds) launch_mode<MODE, true, true>(a, s);
-    else launch_mode<MODE, true, false>(a, s);
+  const bool xlds = MODE == kGemv && xbytes <= kMaxXLdsBytes &&
+                    kStaticLds + xbytes <= size_t(f.lds_per_block);
+  if (MODE != kGemv) {
+    if (uniform) launch_batch<MODE, true, false>(a, s, f);
+    else launch_batch<MODE, false, false>(a, s, f);
+  } else if (uniform) {
+    if (xlds) launch_batch<MODE, true, true>(a, s, f);
+    else launch_batch<MODE, true, false>(a, s, f);
   } else {
-    if (xlds) launch_mode<MODE, false, true>(a, s);
-    else launch_mode<MODE, false, false>(a, s);
+    if (xlds) launch_batch<MODE, false, true>(a, s, f);
+    else launch_batch<MODE, false, false>(a, s, f);
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
@@ -415,8 +566,8 @@ int launch_decode(const Args &a, hipStream_t s) {
 
 extern "C" int eq_layer_prepare(const eq_layer *L, hipStream_t stream) {
   if (!layer_ok(L) || !L->sym || !L->freq || L->n_syms < 1 || L->n_syms > 256) return EQ_EINVAL;
-  hipLaunchKernelGGL(prepare_kernel, dim3(1), dim3(256), 0, stream, L->sym, L->freq, L->n_syms,
-                     L->lut, L->status);
+  hipLaunchKernelGGL(prepare_kernel, dim3(1), dim3(1024), 0, stream, L->sym, L->freq, L->n_syms,
+                     1u << L->prob_bits, L->lut, L->status);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 

@@ -3,10 +3,10 @@
 // Alg. 2 of the paper: ANS decoding of the per-layer bitstream, view as the
 // row-major weight matrix, and the product with the per-row-scaled weights
 // (Sec. 2.1 dequantiser and linear layer).  One wavefront owns one chunk:
-// each of its 64 lanes holds W/64 interleaved coder states, the slot and
-// value tables sit in LDS, and the stream words of a step are handed out
-// with a wavefront ballot and a masked bit count, which reproduces the
-// coder's ascending-lane read order exactly.
+// each of its 64 lanes holds W/64 interleaved coder states, the slot table
+// sits in LDS, and the stream words of a step are handed out with a
+// wavefront ballot and a masked bit count, which reproduces the coder's
+// ascending-lane read order exactly.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -26,8 +26,18 @@ constexpr int kMaxBatch = 8;
 constexpr uint32_t kHalf = 512;               // stream words per window half (1 KiB)
 constexpr uint32_t kWin = 2 * kHalf;          // per-wave LDS window of stream words
 constexpr int32_t kBufferFlags = 0x00020000;  // buffer resource word 3 (gfx9 family)
+constexpr uint32_t kMaxXLdsBytes = 64 * 1024; // activations staged whole up to this size
+constexpr uint32_t kTileBytes = 32 * 1024;    // one activation tile (two are in LDS)
+constexpr uint32_t kStageRegs = 4;            // 16-byte registers per thread to stage a tile
 
 enum Mode { kCodes = 0, kBf16 = 1, kGemv = 2 };
+
+// Where the GEMV reads activations from.
+enum XSrc {
+  kXGlobal = 0,  // device memory, [batch][cols]
+  kXLds = 1,     // whole in LDS (column pairs when W >= 128 and rows are whole steps)
+  kXTile = 2     // tiles shared by a block of same-column chunks (see gemv_tiled_kernel)
+};
 
 struct Args {
   const uint32_t *lut;          // slot table, f32 value table, bf16 value table
@@ -45,7 +55,10 @@ struct Args {
   uint32_t batch;
   const uint16_t *bias;
   float *y;
-  float *ws;
+  float *ws;                    // row partials (uniform) or row sums (general shapes)
+  const uint32_t *xp;           // activations in column-pair layout (tiled GEMV)
+  uint32_t ncls;                // chunk classes sharing a start column (tiled GEMV)
+  uint32_t tile_steps;          // steps per activation tile (tiled GEMV)
 };
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -84,17 +97,29 @@ __device__ inline float wave_sum(float v) {
 
 __device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Read-only inputs seen through the constant address space, so that loads
+// at wave-uniform addresses become scalar (SMEM) loads and never wait on the
+// vector memory counter.
+typedef const __attribute__((address_space(4))) uint32_t const_u32;
+
+__device__ inline const_u32 *as_const(const void *p) { return (const_u32 *)(p); }
+
+// BF16 element i of a read-only array (i wave-uniform), via its aligned dword.
+__device__ inline float bf16_at(const uint16_t *base, uint32_t i) {
+  const uint32_t w = as_const(base)[i >> 1];
+  return __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
+}
+
+// Two E4M3FN codes (bytes 0 and 1 of c) to the BF16 pair of their values
+// (exact: every E4M3 value is a BF16 value).
+__device__ inline uint32_t e4m3x2_to_bf16x2(uint32_t c) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c, 1.0f, false));
+}
+
 // Value-table entry of the code in bits 24..31 of a slot entry.  Bits 13..23
 // of the entry are zero (f <= 2^12), so e >> 22 is already the byte offset.
 __device__ inline uint32_t code_value(const uint32_t *val_s, uint32_t e) {
   return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(val_s) + (e >> 22));
-}
-
-// BF16 element i of an array in device memory, read as the containing
-// aligned dword so that a wave-uniform index becomes a scalar load.
-__device__ inline float bf16_at(const uint16_t *base, uint32_t i) {
-  const uint32_t w = reinterpret_cast<const uint32_t *>(base)[i >> 1];
-  return __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
 }
 
 // 16 stream words starting at word index i (a multiple of 8), clamped to the
@@ -140,84 +165,146 @@ __global__ __launch_bounds__(1024) void prepare_kernel(const uint8_t *sym, const
   if (t == 0) *status = 0;
 }
 
-// One wavefront decodes one chunk.  G = W / 64 coder states per lane (state
-// g * 64 + lane); MODE selects what is done with each decoded symbol;
+// Column-pair layout of the activations (whole-row steps, W >= 128, so N is
+// a multiple of 128).  A pair is (x[b][128 m + l], x[b][128 m + 64 + l]) as
+// two BF16; batch rows go in groups of bw = 4 (bw = 1 when B = 1), padded
+// with zeros, and u32 entry ((m * BG + bg) * 64 + l) * bw + bb holds the pair
+// of batch row b = bg * bw + bb.  One lane then reads the pairs of four batch
+// rows with one 16-byte load.
+__host__ __device__ inline uint32_t pair_width(uint32_t B) { return B == 1 ? 1u : 4u; }
+__host__ __device__ inline uint32_t pair_groups(uint32_t B) {
+  return (B + pair_width(B) - 1) / pair_width(B);
+}
+__host__ __device__ inline size_t pair_bytes(uint32_t B, uint32_t N) {
+  return size_t(N / 2) * pair_groups(B) * pair_width(B) * sizeof(uint32_t);
+}
+
+__device__ inline uint32_t pair_entry(const uint16_t *x, uint32_t N, uint32_t B, uint32_t i) {
+  const uint32_t bw = pair_width(B), BG = pair_groups(B);
+  const uint32_t bb = i % bw, l = (i / bw) % 64, bg = (i / (bw * 64)) % BG;
+  const uint32_t m = i / (bw * 64 * BG), b = bg * bw + bb;
+  if (b >= B) return 0;
+  const uint16_t *row = x + size_t(b) * N + 128 * m + l;
+  return uint32_t(row[0]) | (uint32_t(row[64]) << 16);
+}
+
+__global__ void pair_layout_kernel(const uint16_t *x, uint32_t N, uint32_t B, uint32_t *xp) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < pair_bytes(B, N) / sizeof(uint32_t)) xp[i] = pair_entry(x, N, B, i);
+}
+
+// LDS of a decode block.  The value table comes first so that its byte
+// offsets fit the 16-bit immediate of LDS instructions.
+struct DecodeLds {
+  uint32_t val[256];
+  uint2 slot[kMaxSlots];
+  uint4 win[kMaxWaves][kWin / 8];
+};
+
+// Stage the decode tables (and nothing else) into LDS.
+template <int MODE>
+__device__ inline void stage_tables(const Args &a, DecodeLds &sm) {
+  const uint32_t nthreads = blockDim.x;
+  const uint32_t nslots = 1u << a.prob_bits;
+  const uint4 *src = reinterpret_cast<const uint4 *>(a.lut);
+  uint4 *dst = reinterpret_cast<uint4 *>(sm.slot);
+  for (uint32_t i = threadIdx.x; i < nslots / 2; i += nthreads) dst[i] = src[i];
+  const uint32_t *vsrc = a.lut + 2 * kMaxSlots + (MODE == kGemv ? 256 : 0);
+  for (uint32_t i = threadIdx.x; i < 256; i += nthreads) sm.val[i] = vsrc[i];
+}
+
+// Decoder of one chunk by one wavefront.  G = W / 64 coder states per lane
+// (state g * 64 + lane); MODE selects what is done with each decoded symbol;
 // UNIFORM means every step of W symbols lies inside one matrix row (N is a
-// multiple of W); XLDS means the activations are staged in LDS; NB is the
-// GEMV batch when fixed at compile time (0: the runtime batch, up to 8).
-template <int G, int MODE, bool UNIFORM, bool XLDS, int NB>
-__device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t lane,
-                                             const uint2 *slot_s, const uint32_t *val_s,
-                                             uint4 *win4, const uint16_t *x_s) {
-  constexpr uint32_t W = G * kWave;
-  const uint32_t N = a.cols;
-  const uint32_t k0 = c * a.chunk_syms;
-  const uint32_t nc = min(a.chunk_syms, a.n - k0);
-  const uint32_t P = a.prob_bits;
-  const uint32_t mask = (1u << P) - 1;
-  const uint32_t last8 = a.padded_words - 8;
-  const uint16_t *win = reinterpret_cast<const uint16_t *>(win4);
-  const int nb = NB ? NB : static_cast<int>(a.batch);  // GEMV batch
+// multiple of W); XS says where the GEMV reads activations; NB is the GEMV
+// batch when fixed at compile time (0: the runtime batch, up to 8).
+template <int G, int MODE, bool UNIFORM, int XS, int NB>
+struct Decoder {
+  static constexpr uint32_t W = G * kWave;
+  // GEMV on pairs of states (2q, 2q+1) of a lane: columns j and j + 64
+  static constexpr bool PAIR = MODE == kGemv && UNIFORM && G >= 2 && XS != kXGlobal;
 
+  const Args &a;
+  const uint2 *slot;
+  const uint32_t *val;
+  uint4 *win4;
+  const uint16_t *win;
+  const void *xl;  // activations in LDS (kXLds)
+  uint32_t lane, c, N, k0, nc, P, mask, last8, full;
+  int nb;
   uint32_t x[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) x[g] = a.chunk_state[c * W + g * kWave + lane];
-  uint32_t p = a.chunk_off[c];
-  const uint32_t p_end = a.chunk_off[c + 1];
-
-  // Stream words [wb, wb + kWin) live in this wave's LDS window and the next
-  // half is in flight in registers.  A step reads at most W words and the
-  // window slides by a half whenever p passes its middle, so every word a
-  // step can read is in LDS.
-  uint32_t wb = p & ~7u;
-  {
-    const uint4 h0 = load_words(a.words, wb + 8 * lane, last8);
-    const uint4 h1 = load_words(a.words, wb + kHalf + 8 * lane, last8);
-    win4[lane] = h0;
-    win4[kHalf / 8 + lane] = h1;
-  }
-  __builtin_amdgcn_s_waitcnt(0);  // states, offsets and window are in
-  uint4 next = load_words(a.words, wb + kWin + 8 * lane, last8);
-
-  // Outputs of this chunk through buffer resources: the address is the
-  // chunk's base plus a scalar step offset plus the lane's offset.  Stores
-  // of the partial last step are predicated per lane.
+  uint32_t p, p_end, wb;
+  uint4 next;
   __amdgpu_buffer_rsrc_t out_rsrc;
-  if (MODE == kCodes)
-    out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + k0, 0, int(nc), kBufferFlags);
-  if (MODE == kBf16)
-    out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.wout + k0, 0, int(2 * nc), kBufferFlags);
-
-  // uniform-row bookkeeping (every step lies inside one row)
-  uint32_t row = k0 / N;
-  const uint32_t first_row = row;
-  uint32_t row_end = (row + 1) * N;  // <= n < 2^32
-  float srow = 0.0f;
-  if (MODE == kBf16 && UNIFORM) srow = bf16_at(a.scale, row);
-  // per-state row/column (general shapes)
+  uint32_t row, first_row, row_end;
+  float srow;
   uint32_t prow[G], pcol[G];
-  if (!UNIFORM) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const uint32_t pos = k0 + g * kWave + lane;
-      prow[g] = pos / N;
-      pcol[g] = pos - prow[g] * N;
-    }
-  }
   float acc[UNIFORM ? 1 : G][kMaxBatch];
-#pragma unroll
-  for (int g = 0; g < (UNIFORM ? 1 : G); ++g)
-#pragma unroll
-    for (int b = 0; b < kMaxBatch; ++b) acc[g][b] = 0.0f;
   bool pending[G];
+
+  __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
+                                     const DecodeLds &sm, uint4 *win4_, const void *xl_)
+      : a(a_), slot(sm.slot), val(sm.val), win4(win4_),
+        win(reinterpret_cast<const uint16_t *>(win4_)), xl(xl_), lane(lane_), c(c_) {
+    N = a.cols;
+    k0 = c * a.chunk_syms;
+    nc = min(a.chunk_syms, a.n - k0);
+    P = a.prob_bits;
+    mask = (1u << P) - 1;
+    last8 = a.padded_words - 8;
+    full = nc / W;
+    nb = NB ? NB : static_cast<int>(a.batch);
 #pragma unroll
-  for (int g = 0; g < G; ++g) pending[g] = false;
+    for (int g = 0; g < G; ++g) x[g] = a.chunk_state[c * W + g * kWave + lane];
+    p = as_const(a.chunk_off)[c];
+    p_end = as_const(a.chunk_off)[c + 1];
+    // Stream words [wb, wb + kWin) live in this wave's LDS window and the
+    // next half is in flight in registers.  A step reads at most W words and
+    // the window slides by a half whenever p passes its middle, so every word
+    // a step can read is in LDS.
+    wb = p & ~7u;
+    {
+      const uint4 h0 = load_words(a.words, wb + 8 * lane, last8);
+      const uint4 h1 = load_words(a.words, wb + kHalf + 8 * lane, last8);
+      win4[lane] = h0;
+      win4[kHalf / 8 + lane] = h1;
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // states, offsets and window are in
+    next = load_words(a.words, wb + kWin + 8 * lane, last8);
+    // Outputs of this chunk go through buffer resources: the address is the
+    // chunk's base plus a scalar step offset plus the lane's offset.  Stores
+    // of the partial last step are predicated per lane.
+    if (MODE == kCodes)
+      out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + k0, 0, int(nc), kBufferFlags);
+    if (MODE == kBf16)
+      out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.wout + k0, 0, int(2 * nc), kBufferFlags);
+    row = k0 / N;
+    first_row = row;
+    row_end = (row + 1) * N;  // <= n < 2^32
+    srow = (MODE == kBf16 && UNIFORM) ? bf16_at(a.scale, row) : 0.0f;
+    if (!UNIFORM) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const uint32_t pos = k0 + g * kWave + lane;
+        prow[g] = pos / N;
+        pcol[g] = pos - prow[g] * N;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < (UNIFORM ? 1 : G); ++g)
+#pragma unroll
+      for (int b = 0; b < kMaxBatch; ++b) acc[g][b] = 0.0f;
+#pragma unroll
+    for (int g = 0; g < G; ++g) pending[g] = false;
+  }
 
-  auto xbits = [&](uint32_t b, uint32_t col) -> uint32_t {
-    return XLDS ? x_s[b * N + col] : a.x[b * N + col];
-  };
+  __device__ __forceinline__ uint32_t xbits(uint32_t b, uint32_t col) const {
+    return XS == kXLds ? reinterpret_cast<const uint16_t *>(xl)[b * N + col] : a.x[b * N + col];
+  }
 
-  auto flush_uniform = [&](uint32_t r) {
+  // Finished row r of a uniform chunk: y directly if the chunk holds the whole
+  // row, else the partial sum (slot 0: first row, slot 1: last row).
+  __device__ __forceinline__ void flush_uniform(uint32_t r) {
     const bool owned = r * N >= k0 && (r + 1) * N <= k0 + nc;
     const float s = bf16_at(a.scale, r);
     const float bb = a.bias ? bf16_at(a.bias, r) : 0.0f;
@@ -232,11 +319,13 @@ __device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t
       }
       acc[0][b] = 0.0f;
     }
-  };
+  }
 
   // One step: W symbols at chunk offset t * W.  TAIL: the last, partial step.
-  auto step = [&](auto tail_tag, uint32_t t) {
-    constexpr bool TAIL = decltype(tail_tag)::value;
+  // xt: this step's activation pairs in LDS (kXTile only), in column-pair
+  // layout starting at the step's first 128-column block.
+  template <bool TAIL>
+  __device__ __forceinline__ void step(uint32_t t, const uint32_t *xt) {
     if (p - wb >= kHalf) {  // slide the window by one half
       const uint4 keep = win4[kHalf / 8 + lane];
       win4[lane] = keep;
@@ -260,11 +349,11 @@ __device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       if (act[g]) {
-        const uint2 e = slot_s[x[g] & mask];
+        const uint2 e = slot[x[g] & mask];
         x[g] = __umul24(e.x, x[g] >> P) + e.y;
         e0[g] = e.x;
       } else {
-        e0[g] = 0;
+        e0[g] = 0;  // code 0: value +0
       }
     }
 
@@ -279,11 +368,11 @@ __device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t
 #pragma unroll
       for (int g = 0; g < G; g += 2) {
         const float s0 = UNIFORM ? srow : bf16_at(a.scale, prow[g]);
-        const float v0 = s0 * __uint_as_float(code_value(val_s, e0[g]));
+        const float v0 = s0 * __builtin_amdgcn_cvt_f32_fp8(e0[g], 3);
         float v1 = 0.0f;
         if (g + 1 < G) {
           const float s1 = UNIFORM ? srow : bf16_at(a.scale, prow[g + 1]);
-          v1 = s1 * __uint_as_float(code_value(val_s, e0[g + 1]));
+          v1 = s1 * __builtin_amdgcn_cvt_f32_fp8(e0[g + 1], 3);
         }
         const uint32_t h = pack_bf16(v0, v1);  // exact products, rounded once
         if (!TAIL || act[g])
@@ -293,11 +382,42 @@ __device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t
           __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h >> 16), out_rsrc,
                                                 2 * lane, 2 * (kk + (g + 1) * kWave), 0);
       }
+    } else if (PAIR) {
+      // pairs of this step's 128-column blocks: xq + (q * BG + bg) * 64 * bw
+      constexpr uint32_t bw = NB == 1 ? 1 : 4;
+      const uint32_t BG = NB == 1 ? 1 : (nb + 3) / 4;
+      const uint32_t *xq;
+      if (XS == kXTile) {
+        xq = xt + lane * bw;
+      } else {
+        const uint32_t blk = (k0 + kk + N - row_end) >> 7;  // first 128-column block
+        xq = reinterpret_cast<const uint32_t *>(xl) + (blk * BG * kWave + lane) * bw;
+      }
+#pragma unroll
+      for (int q = 0; q < G / 2; ++q) {
+        const uint32_t w2 = e4m3x2_to_bf16x2(__builtin_amdgcn_perm(e0[2 * q + 1], e0[2 * q],
+                                                                  0x0c0c0703u));
+        if (NB == 1) {
+          acc[0][0] = dot2_bf16(w2, xq[q * kWave], acc[0][0]);
+        } else {
+#pragma unroll
+          for (uint32_t bg = 0; bg < 2; ++bg) {
+            if (bg < BG) {
+              const uint4 xv =
+                  *reinterpret_cast<const uint4 *>(xq + (q * BG + bg) * kWave * bw);
+              acc[0][4 * bg + 0] = dot2_bf16(w2, xv.x, acc[0][4 * bg + 0]);
+              acc[0][4 * bg + 1] = dot2_bf16(w2, xv.y, acc[0][4 * bg + 1]);
+              acc[0][4 * bg + 2] = dot2_bf16(w2, xv.z, acc[0][4 * bg + 2]);
+              acc[0][4 * bg + 3] = dot2_bf16(w2, xv.w, acc[0][4 * bg + 3]);
+            }
+          }
+        }
+      }
     } else {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         if (!act[g]) continue;
-        const uint32_t v = code_value(val_s, e0[g]);  // BF16 value in the low half
+        const uint32_t v = code_value(val, e0[g]);  // BF16 value in the low half
         const uint32_t col = UNIFORM ? (k0 + kk + N - row_end) + g * kWave + lane : pcol[g];
 #pragma unroll
         for (int b = 0; b < kMaxBatch; ++b)
@@ -344,72 +464,150 @@ __device__ __forceinline__ void decode_chunk(const Args &a, uint32_t c, uint32_t
     for (int g = 0; g < G; ++g)
       if (need[g]) x[g] = (x[g] << 16) | word[g];
     p = wb + rel;
-  };
-
-  const uint32_t full = nc / W;
-  for (uint32_t t = 0; t < full; ++t) step(std::false_type{}, t);
-  if (nc % W) step(std::true_type{}, full);
-
-  if (MODE == kGemv) {
-    if (UNIFORM) {
-      flush_uniform(row);
-    } else {
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-        if (pending[g])
-#pragma unroll
-          for (int b = 0; b < kMaxBatch; ++b)
-            if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
-    }
   }
 
-  // end-of-chunk check: every state back at 2^16, stream used up exactly
-  bool bad = p != p_end;
+  // Close the chunk: last row sums, end-of-chunk check (every state back at
+  // 2^16, stream used up exactly).
+  __device__ __forceinline__ void finish() {
+    if (MODE == kGemv) {
+      if (UNIFORM) {
+        flush_uniform(row);
+      } else {
 #pragma unroll
-  for (int g = 0; g < G; ++g) bad |= x[g] != kStateLow;
-  if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
-}
+        for (int g = 0; g < G; ++g)
+          if (pending[g])
+#pragma unroll
+            for (int b = 0; b < kMaxBatch; ++b)
+              if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
+      }
+    }
+    bool bad = p != p_end;
+#pragma unroll
+    for (int g = 0; g < G; ++g) bad |= x[g] != kStateLow;
+    if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
+  }
 
-// LDS of a decode block.  The value table comes first so that its byte
-// offsets fit the 16-bit immediate of LDS instructions.
-struct DecodeLds {
-  uint32_t val[256];
-  uint2 slot[kMaxSlots];
-  uint4 win[kMaxWaves][kWin / 8];
+  __device__ __forceinline__ void run() {
+    for (uint32_t t = 0; t < full; ++t) step<false>(t, nullptr);
+    if (nc % W) step<true>(full, nullptr);
+    finish();
+  }
 };
 
-template <int G, int MODE, bool UNIFORM, bool XLDS, int NB>
+// Each wavefront decodes chunks blockIdx.x * waves + wave, + gridDim.x * waves, ...
+template <int G, int MODE, bool UNIFORM, int XS, int NB>
 __global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
-  extern __shared__ uint4 x_dyn[];  // [batch][cols] BF16 when XLDS
+  extern __shared__ uint4 x_dyn[];  // activations when XS == kXLds
   __shared__ DecodeLds sm;
-  const uint32_t nthreads = blockDim.x;
-  const uint32_t nslots = 1u << a.prob_bits;
-  {
-    const uint4 *src = reinterpret_cast<const uint4 *>(a.lut);
-    uint4 *dst = reinterpret_cast<uint4 *>(sm.slot);
-    for (uint32_t i = threadIdx.x; i < nslots / 2; i += nthreads) dst[i] = src[i];
-    const uint32_t *vsrc = a.lut + 2 * kMaxSlots + (MODE == kGemv ? 256 : 0);
-    for (uint32_t i = threadIdx.x; i < 256; i += nthreads) sm.val[i] = vsrc[i];
-    if (XLDS) {
-      const uint32_t nx = a.batch * a.cols;
+  stage_tables<MODE>(a, sm);
+  if (XS == kXLds) {
+    const uint32_t nthreads = blockDim.x;
+    const uint32_t nx = a.batch * a.cols;
+    if (Decoder<G, MODE, UNIFORM, XS, NB>::PAIR) {
+      uint32_t *xp = reinterpret_cast<uint32_t *>(x_dyn);
+      const uint32_t np = pair_bytes(a.batch, a.cols) / sizeof(uint32_t);
+      for (uint32_t i = threadIdx.x; i < np; i += nthreads) xp[i] = pair_entry(a.x, a.cols, a.batch, i);
+    } else if (nx % 8 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0) {
+      const uint4 *xv = reinterpret_cast<const uint4 *>(a.x);
+      for (uint32_t i = threadIdx.x; i < nx / 8; i += nthreads) x_dyn[i] = xv[i];
+    } else {
       uint16_t *xs = reinterpret_cast<uint16_t *>(x_dyn);
-      if (nx % 8 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0) {
-        const uint4 *xv = reinterpret_cast<const uint4 *>(a.x);
-        for (uint32_t i = threadIdx.x; i < nx / 8; i += nthreads) x_dyn[i] = xv[i];
-      } else {
-        for (uint32_t i = threadIdx.x; i < nx; i += nthreads) xs[i] = a.x[i];
-      }
+      for (uint32_t i = threadIdx.x; i < nx; i += nthreads) xs[i] = a.x[i];
     }
   }
   __syncthreads();
 
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint32_t wave = uniform(threadIdx.x / kWave);
+  const uint32_t waves = uniform(blockDim.x / kWave);
+  for (uint32_t c = uniform(blockIdx.x * waves + wave); c < a.n_chunks; c += gridDim.x * waves) {
+    Decoder<G, MODE, UNIFORM, XS, NB> d(a, c, lane, sm, sm.win[wave], x_dyn);
+    d.run();
+  }
+}
+
+// Fused GEMV for activations too large for LDS (whole-row steps, W >= 128).
+// Chunks c and c + ncls start at the same column (ncls = N / gcd(C, N)), so a
+// block of wavefronts holding chunks of one class walks the same columns in
+// lockstep: the block stages tiles of tile_steps steps of column-paired
+// activations (from a.xp) into LDS, double-buffered, with one barrier per
+// tile.  Block b serves class b % ncls, chunks of index (b / ncls) * waves +
+// wave within the class.
+template <int G, int NB>
+__global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
+  extern __shared__ uint4 tiles[];  // 2 x tile
+  __shared__ DecodeLds sm;
+  using Dec = Decoder<G, kGemv, true, kXTile, NB>;
+  constexpr uint32_t W = Dec::W;
+  stage_tables<kGemv>(a, sm);
+
+  const uint32_t nthreads = blockDim.x;
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave = uniform(threadIdx.x / kWave);
   const uint32_t waves = uniform(nthreads / kWave);
-  for (uint32_t c = uniform(blockIdx.x * waves + wave); c < a.n_chunks;
-       c += gridDim.x * waves)
-    decode_chunk<G, MODE, UNIFORM, XLDS, NB>(a, c, lane, sm.slot, sm.val, sm.win[wave],
-                                         reinterpret_cast<const uint16_t *>(x_dyn));
+  const uint32_t N = a.cols, B = a.batch, T = a.tile_steps;
+  (void)B;
+  const uint32_t cls = blockIdx.x % a.ncls;
+  const uint32_t c = cls + a.ncls * ((blockIdx.x / a.ncls) * waves + wave);
+  const bool has = c < a.n_chunks;
+  const uint32_t col0 = uint32_t((uint64_t(cls) * a.chunk_syms) % N);
+  const uint32_t nblk = N / 128;                      // 128-column blocks per row
+  const uint32_t blk_u4 = pair_groups(B) * pair_width(B) * kWave / 4;  // 16-byte units per block
+  const uint32_t step_u4 = (W / 128) * blk_u4;        // per step
+  const uint32_t tile_u4 = T * step_u4;
+  const uint32_t steps = a.chunk_syms / W;            // steps of a full chunk
+  const uint32_t ntiles = (steps + T - 1) / T;
+  const uint4 *src = reinterpret_cast<const uint4 *>(a.xp);
+
+  // tile k covers steps [k T, k T + T): 128-column blocks from col0/128 + k T W/128;
+  // each thread moves 16-byte units threadIdx.x + s * nthreads, s < kStageRegs
+  static_assert(kStageRegs == 4, "staging uses four registers");
+  auto fetch = [&](uint32_t k, uint32_t s) -> uint4 {
+    const uint32_t i = threadIdx.x + s * nthreads;
+    if (i >= tile_u4) return uint4{0, 0, 0, 0};
+    const uint32_t blk = (col0 / 128 + k * T * (W / 128) + i / blk_u4) % nblk;
+    return src[blk * blk_u4 + i % blk_u4];
+  };
+  auto store = [&](uint32_t buf, uint32_t s, const uint4 v) {
+    const uint32_t i = threadIdx.x + s * nthreads;
+    if (i < tile_u4) tiles[buf * tile_u4 + i] = v;
+  };
+
+  uint4 r0 = fetch(0, 0), r1 = fetch(0, 1), r2 = fetch(0, 2), r3 = fetch(0, 3);
+  store(0, 0, r0);
+  store(0, 1, r1);
+  store(0, 2, r2);
+  store(0, 3, r3);
+  __syncthreads();  // tables and the first tile are in
+
+  Dec d(a, has ? c : 0, lane, sm, sm.win[wave], nullptr);
+  for (uint32_t k = 0; k < ntiles; ++k) {
+    const bool more = k + 1 < ntiles;
+    if (more) {
+      r0 = fetch(k + 1, 0);
+      r1 = fetch(k + 1, 1);
+      r2 = fetch(k + 1, 2);
+      r3 = fetch(k + 1, 3);
+    }
+    if (has) {
+      const uint32_t *tile = reinterpret_cast<const uint32_t *>(tiles + (k & 1) * tile_u4);
+      for (uint32_t tt = 0; tt < T; ++tt) {
+        const uint32_t t = k * T + tt;
+        const uint32_t *xt = tile + tt * step_u4 * 4;
+        if (t < d.full) d.template step<false>(t, xt);
+        else if (t == d.full && d.nc % W) d.template step<true>(t, xt);
+      }
+    }
+    if (more) {
+      const uint32_t buf = (k + 1) & 1;
+      store(buf, 0, r0);
+      store(buf, 1, r1);
+      store(buf, 2, r2);
+      store(buf, 3, r3);
+    }
+    __syncthreads();
+  }
+  if (has) d.finish();
 }
 
 // Rows split between chunks (whole-row steps): y = s * (sum of the chunks'
@@ -472,11 +670,11 @@ Args make_args(const eq_layer *L) {
 
 bool layer_ok(const eq_layer *L) {
   return L && L->lut && L->status && L->words && L->chunk_off && L->chunk_state && L->scale &&
-         (L->lanes == 64 || L->lanes == 128 || L->lanes == 256) && L->prob_bits >= 8 &&
-         L->prob_bits <= 12 && L->n_chunks > 0 && L->cols > 0 && L->rows > 0;
+         (L->lanes == 64 || L->lanes == 128 || L->lanes == 256) &&
+         L->prob_bits >= kMinProbBits && L->prob_bits <= 12 && L->n_chunks > 0 && L->cols > 0 &&
+         L->rows > 0;
 }
 
-constexpr uint32_t kMaxXLdsBytes = 64 * 1024;
 constexpr size_t kStaticLds = sizeof(DecodeLds);
 
 struct DeviceFacts {
@@ -518,49 +716,103 @@ void launch_shape(uint32_t n_chunks, int cus, dim3 &grid, dim3 &block) {
   block = dim3(waves * kWave);
 }
 
-template <int MODE, bool UNIFORM, bool XLDS, int NB>
+uint32_t gcd_u32(uint32_t a, uint32_t b) {
+  while (b) {
+    const uint32_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+// LDS bytes of the activations staged whole (column pairs when usable).
+size_t xlds_bytes(const Args &a) {
+  const bool pairs = a.cols % a.lanes == 0 && a.lanes >= 128;
+  return pairs ? pair_bytes(a.batch, a.cols) : size_t(a.batch) * a.cols * sizeof(uint16_t);
+}
+
+// Activation placement of a GEMV launch.
+int gemv_xsrc(const Args &a, const DeviceFacts &f) {
+  const bool uniform = a.cols % a.lanes == 0;
+  const size_t xbytes = xlds_bytes(a);
+  if (xbytes <= kMaxXLdsBytes && kStaticLds + xbytes <= size_t(f.lds_per_block)) return kXLds;
+  if (uniform && a.lanes >= 128 && kStaticLds + 2 * kTileBytes <= size_t(f.lds_per_block))
+    return kXTile;
+  return kXGlobal;
+}
+
+template <int MODE, bool UNIFORM, int XS, int NB>
 void launch_mode(const Args &a, hipStream_t s, const DeviceFacts &f) {
   dim3 grid, block;
   launch_shape(a.n_chunks, f.cus, grid, block);
-  const size_t shm = XLDS ? size_t(a.batch) * a.cols * sizeof(uint16_t) : 0;
+  const size_t shm = XS == kXLds ? xlds_bytes(a) : 0;
   switch (a.lanes) {
     case 64:
-      hipLaunchKernelGGL((decode_kernel<1, MODE, UNIFORM, XLDS, NB>), grid, block, shm, s, a);
+      hipLaunchKernelGGL((decode_kernel<1, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
       break;
     case 128:
-      hipLaunchKernelGGL((decode_kernel<2, MODE, UNIFORM, XLDS, NB>), grid, block, shm, s, a);
+      hipLaunchKernelGGL((decode_kernel<2, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
       break;
     default:
-      hipLaunchKernelGGL((decode_kernel<4, MODE, UNIFORM, XLDS, NB>), grid, block, shm, s, a);
+      hipLaunchKernelGGL((decode_kernel<4, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
       break;
   }
 }
 
-template <int MODE, bool UNIFORM, bool XLDS>
+template <int MODE, bool UNIFORM, int XS>
 void launch_batch(const Args &a, hipStream_t s, const DeviceFacts &f) {
-  if (MODE != kGemv || a.batch == 1) launch_mode<MODE, UNIFORM, XLDS, 1>(a, s, f);
-  else launch_mode<MODE, UNIFORM, XLDS, 0>(a, s, f);
+  if (MODE != kGemv || a.batch == 1) launch_mode<MODE, UNIFORM, XS, 1>(a, s, f);
+  else launch_mode<MODE, UNIFORM, XS, 0>(a, s, f);
 }
 
 template <int MODE>
 int launch_decode(const Args &a, hipStream_t s) {
   const DeviceFacts f = device_facts();
   const bool uniform = a.cols % a.lanes == 0;
-  const size_t xbytes = size_t(a.batch) * a.cols * sizeof(uint16_t);
-  const bool xlds = MODE == kGemv && xbytes <= kMaxXLdsBytes &&
-                    kStaticLds + xbytes <= size_t(f.lds_per_block);
   if (MODE != kGemv) {
-    if (uniform) launch_batch<MODE, true, false>(a, s, f);
-    else launch_batch<MODE, false, false>(a, s, f);
-  } else if (uniform) {
-    if (xlds) launch_batch<MODE, true, true>(a, s, f);
-    else launch_batch<MODE, true, false>(a, s, f);
+    if (uniform) launch_batch<MODE, true, kXGlobal>(a, s, f);
+    else launch_batch<MODE, false, kXGlobal>(a, s, f);
+  } else if (gemv_xsrc(a, f) == kXLds) {
+    if (uniform) launch_batch<MODE, true, kXLds>(a, s, f);
+    else launch_batch<MODE, false, kXLds>(a, s, f);
   } else {
-    if (xlds) launch_batch<MODE, false, true>(a, s, f);
-    else launch_batch<MODE, false, false>(a, s, f);
+    if (uniform) launch_batch<MODE, true, kXGlobal>(a, s, f);
+    else launch_batch<MODE, false, kXGlobal>(a, s, f);
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
+
+// Tiled GEMV launch: the number of wavefronts per block is the smallest that
+// lets every block of every class run at once; tiles are as long as the
+// LDS budget and the staging registers allow.
+template <int NB>
+int launch_tiled(Args a, hipStream_t s, const DeviceFacts &f) {
+  const uint32_t W = a.lanes, C = a.chunk_syms, N = a.cols;
+  a.ncls = N / gcd_u32(C % N, N);  // gcd(0, N) = N: one class
+  const uint32_t per_cls = (a.n_chunks + a.ncls - 1) / a.ncls;
+  uint32_t waves = kMaxWaves;
+  for (uint32_t w = (a.n_chunks + f.cus - 1) / f.cus; w <= kMaxWaves; ++w) {
+    if (w == 0) continue;
+    if (a.ncls * ((per_cls + w - 1) / w) <= uint32_t(f.cus)) {
+      waves = w;
+      break;
+    }
+  }
+  const uint32_t step_bytes =
+      uint32_t(pair_bytes(a.batch, W));  // W columns of column-paired activations
+  uint32_t T = kTileBytes / step_bytes;
+  const uint32_t max_by_regs = kStageRegs * waves * kWave * 16 / step_bytes;
+  if (T > max_by_regs) T = max_by_regs;
+  if (T < 1) T = 1;
+  a.tile_steps = T;
+  const dim3 grid(a.ncls * ((per_cls + waves - 1) / waves)), block(waves * kWave);
+  const size_t shm = 2 * size_t(T) * step_bytes;
+  if (W == 128) hipLaunchKernelGGL((gemv_tiled_kernel<2, NB>), grid, block, shm, s, a);
+  else hipLaunchKernelGGL((gemv_tiled_kernel<4, NB>), grid, block, shm, s, a);
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
 }  // namespace
 
@@ -585,10 +837,13 @@ extern "C" int eq_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t stream
   return launch_decode<kBf16>(a, stream);
 }
 
+// Workspace: row partials (2 per chunk and batch row) or row sums (general
+// shapes), then room for the column-paired activations.
 extern "C" size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
   if (!layer_ok(L) || B < 1 || B > kMaxBatch) return 0;
-  size_t floats = (L->cols % L->lanes == 0) ? size_t(2) * L->n_chunks * B : size_t(L->rows) * B;
-  return (floats * sizeof(float) + 255) / 256 * 256;
+  const size_t floats =
+      (L->cols % L->lanes == 0) ? size_t(2) * L->n_chunks * B : size_t(L->rows) * B;
+  return round256(floats * sizeof(float)) + round256(pair_bytes(B, L->cols));
 }
 
 extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
@@ -605,11 +860,23 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
   a.y = y;
   a.ws = static_cast<float *>(ws);
   const bool uniform = L->cols % L->lanes == 0;
+  const size_t part_bytes =
+      round256((uniform ? size_t(2) * L->n_chunks * B : size_t(L->rows) * B) * sizeof(float));
+  a.xp = reinterpret_cast<const uint32_t *>(static_cast<char *>(ws) + part_bytes);
   if (!uniform) {
     const uint32_t n = L->rows * B;
     hipLaunchKernelGGL(fill_zero_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a.ws, n);
   }
-  int rc = launch_decode<kGemv>(a, stream);
+  const DeviceFacts f = device_facts();
+  int rc;
+  if (gemv_xsrc(a, f) == kXTile) {
+    const uint32_t np = uint32_t(pair_bytes(B, L->cols) / sizeof(uint32_t));
+    hipLaunchKernelGGL(pair_layout_kernel, dim3((np + 255) / 256), dim3(256), 0, stream, x,
+                       L->cols, B, const_cast<uint32_t *>(a.xp));
+    rc = (B == 1) ? launch_tiled<1>(a, stream, f) : launch_tiled<0>(a, stream, f);
+  } else {
+    rc = launch_decode<kGemv>(a, stream);
+  }
   if (rc != EQ_OK) return rc;
   if (uniform) {
     if (L->n_chunks > 1)

@@ -96,6 +96,10 @@ EDGE = [
     (37, 1280, 65536, 256, 2.0, False),  # W = 256, single partial chunk
     (16, 4160, 8192, 256, 3.0, False), # ragged at W = 256; B = 8 reads x from global memory
     (24, 1024, 2048, 128, 6.0, False), # near-flat distribution (many symbols)
+    # B = 8 of these does not fit LDS: tiled GEMV (17 start-column classes,
+    # partial last chunk; W = 128)
+    (24, 4352, 8192, 256, 2.0, False),
+    (32, 4224, 4096, 128, 3.0, True),
 ]
 
 
@@ -137,6 +141,37 @@ def test_config_full(eq, cfg):
         info = oracle.container_info(blob)
         assert abs(info.entropy_bits - spec.target_bits) <= 0.05
         check_full(eq, blob, spec, batches=(1, 8) if cfg < 3 else (1,))
+
+
+@pytest.mark.parametrize("lanes", [64, 256])
+def test_every_e4m3_code(eq, lanes):
+    """A layer whose codes are all 253 finite E4M3FN codes (rows hold s * v(q)
+    for every q, so AbsMax with alpha = 1 reproduces each code exactly):
+    decode, dequantisation and the GEMV's code-to-value conversion are
+    checked on every code."""
+    say("every code", lanes)
+    codes = [c for c in range(256) if (c & 0x7F) != 0x7F and c != 0x80]
+    vals = np.array([oracle.e4m3_value(c) for c in codes])
+    M, N = 6, 512
+    w = np.zeros((M, N), dtype=np.uint16)
+    for i in range(M):
+        row = np.resize(np.roll(vals, 37 * i), N) * (2.0 ** (i - 2))
+        w[i] = [synth.to_bf16(float(v)) for v in row]
+    blob = eq.eqe_encode(w, 1.0, chunk_syms=1024, lanes=lanes)
+    rc, q_ref = oracle.container_decode(blob)
+    assert rc == oracle.OK and len(np.unique(q_ref)) == len(codes)
+    spec = small_spec(M, N, chunk=1024, lanes=lanes, seed=3)
+    L = check_full(eq, blob, spec, batches=(1, 2))
+    # one-hot activations: y_i = s_i * v(q_ij) exactly, for every column
+    scale = synth.bf16_to_f32(oracle.container_scales(blob)).astype(np.float64)
+    for j0 in range(0, N, 8):
+        x = np.zeros((8, N), dtype=np.uint16)
+        for b in range(8):
+            x[b, j0 + b] = 0x3F80
+        y = gpu_gemv(eq, L, x)
+        for b in range(8):
+            exact = scale * np.array([oracle.e4m3_value(int(c)) for c in q_ref[:, j0 + b]])
+            assert np.array_equal(y[b].astype(np.float64), exact), (j0 + b)
 
 
 def test_one_hot_and_zero_inputs(eq):

@@ -591,12 +591,11 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
     }
     if (has) {
       const uint32_t *tile = reinterpret_cast<const uint32_t *>(tiles + (k & 1) * tile_u4);
-      for (uint32_t tt = 0; tt < T; ++tt) {
-        const uint32_t t = k * T + tt;
-        const uint32_t *xt = tile + tt * step_u4 * 4;
-        if (t < d.full) d.template step<false>(t, xt);
-        else if (t == d.full && d.nc % W) d.template step<true>(t, xt);
-      }
+      const uint32_t t0 = k * T, t1 = min(t0 + T, d.full);
+      for (uint32_t t = t0; t < t1; ++t) d.template step<false>(t, tile + (t - t0) * step_u4 * 4);
+      // the partial last step of the matrix's last chunk, while its tile is in LDS
+      if (d.nc % W && d.full >= t0 && d.full < t0 + T)
+        d.template step<true>(d.full, tile + (d.full - t0) * step_u4 * 4);
     }
     if (more) {
       const uint32_t buf = (k + 1) & 1;
@@ -762,6 +761,7 @@ void launch_mode(const Args &a, hipStream_t s, const DeviceFacts &f) {
 template <int MODE, bool UNIFORM, int XS>
 void launch_batch(const Args &a, hipStream_t s, const DeviceFacts &f) {
   if (MODE != kGemv || a.batch == 1) launch_mode<MODE, UNIFORM, XS, 1>(a, s, f);
+  else if (a.batch == kMaxBatch) launch_mode<MODE, UNIFORM, XS, kMaxBatch>(a, s, f);
   else launch_mode<MODE, UNIFORM, XS, 0>(a, s, f);
 }
 
@@ -873,7 +873,9 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
     const uint32_t np = uint32_t(pair_bytes(B, L->cols) / sizeof(uint32_t));
     hipLaunchKernelGGL(pair_layout_kernel, dim3((np + 255) / 256), dim3(256), 0, stream, x,
                        L->cols, B, const_cast<uint32_t *>(a.xp));
-    rc = (B == 1) ? launch_tiled<1>(a, stream, f) : launch_tiled<0>(a, stream, f);
+    rc = (B == 1) ? launch_tiled<1>(a, stream, f)
+                  : (B == kMaxBatch ? launch_tiled<kMaxBatch>(a, stream, f)
+                                    : launch_tiled<0>(a, stream, f));
   } else {
     rc = launch_decode<kGemv>(a, stream);
   }

@@ -256,6 +256,54 @@ def c4_layers(eq):
     return out
 
 
+def _check_sampled(eq, spec, w, blob, L, r, batches=(1,), n_chunks=6, n_rows=4):
+    """Sampled parity at full size: chunks bit-exact (codes against the
+    oracle's decode and quantiser, BF16 against the oracle's dequantiser),
+    GEMV rows within the bar."""
+    info = oracle.container_info(blob)
+    scale = oracle.container_scales(blob)
+    q = gpu_codes(eq, L).ravel()
+    wb = gpu_bf16(eq, L).ravel()
+    assert eq.eq_get_status(L) == eq.EQ_OK
+    chunks = sorted(set(r.choice(info.n_chunks, min(n_chunks, info.n_chunks),
+                                 replace=False).tolist()) | {0, info.n_chunks - 1})
+    for c in chunks:
+        rc, q_ref = oracle.container_decode_chunk(blob, c)
+        assert rc == oracle.OK
+        k0, n = _chunk_rows(info, c)
+        assert np.array_equal(q[k0:k0 + n], q_ref), (spec.name, c)
+        r0, r1 = k0 // spec.cols, (k0 + n - 1) // spec.cols + 1
+        q_rows = oracle.quantize(w[r0:r1], scale[r0:r1]).ravel()
+        assert np.array_equal(q_rows[k0 - r0 * spec.cols:][:n], q_ref)
+        w_rows = oracle.dequant(q_rows.reshape(r1 - r0, spec.cols), scale[r0:r1]).ravel()
+        assert np.array_equal(wb[k0:k0 + n], w_rows[k0 - r0 * spec.cols:][:n])
+    rows = sorted(set(r.choice(spec.rows, n_rows, replace=False).tolist()) | {0, spec.rows - 1})
+    w_rows = oracle.dequant(oracle.quantize(w[rows], scale[rows]), scale[rows])
+    for B in batches:
+        x = synth.activations(spec, B)
+        y = gpu_gemv(eq, L, x)
+        err = rel_err(y[:, rows], oracle.gemv(w_rows, x))
+        assert np.isfinite(y).all() and (err <= TOL).all(), (spec.name, B, err)
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2])
+def test_config5_layer_per_entropy_class(eq, layer):
+    """The 80-layer 70B-shaped stack: one full layer of each entropy class
+    (layer l targets (2, 3, 4)[l mod 3] bits), all seven matrices at full size
+    in the benchmark's launch configuration."""
+    r = np.random.default_rng(500 + layer)
+    for spec in config_matrices(5, layers=[layer]):
+        say("config 5", spec.name, spec.rows, spec.cols, spec.target_bits)
+        w = synth.weights(spec)
+        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
+        blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
+                             seed=spec.seed, target_bits=spec.target_bits)
+        assert abs(oracle.container_info(blob).entropy_bits - spec.target_bits) <= 0.05
+        L = eq.Layer(blob, _dev())
+        _check_sampled(eq, spec, w, blob, L, r)
+        del L
+
+
 def _chunk_rows(info, c):
     k0 = c * info.chunk_syms
     n = min(info.chunk_syms, info.rows * info.cols - k0)

@@ -97,6 +97,7 @@ __device__ inline float wave_sum(float v) {
 
 __device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+
 // Read-only inputs seen through the constant address space, so that loads
 // at wave-uniform addresses become scalar (SMEM) loads and never wait on the
 // vector memory counter.
@@ -321,25 +322,37 @@ struct Decoder {
     }
   }
 
-  // One step: W symbols at chunk offset t * W.  TAIL: the last, partial step.
-  // xt: this step's activation pairs in LDS (kXTile only), in column-pair
-  // layout starting at the step's first 128-column block.
-  template <bool TAIL>
-  __device__ __forceinline__ void step(uint32_t t, const uint32_t *xt) {
-    if (p - wb >= kHalf) {  // slide the window by one half
+  // Whole-row steps: move to the next row when step t starts it.
+  __device__ __forceinline__ void row_check(uint32_t t) {
+    if (UNIFORM && MODE != kCodes && k0 + t * W >= row_end) {
+      if (MODE == kGemv) flush_uniform(row);
+      ++row;
+      row_end += N;
+      if (MODE == kBf16) srow = bf16_at(a.scale, row);
+    }
+  }
+
+  // Slide the stream window by one half once p has passed its middle.
+  __device__ __forceinline__ void slide() {
+    if (p - wb >= kHalf) {
       const uint4 keep = win4[kHalf / 8 + lane];
       win4[lane] = keep;
       win4[kHalf / 8 + lane] = next;
       wb += kHalf;
       next = load_words(a.words, wb + kWin + 8 * lane, last8);
     }
+  }
+
+  // One step: W symbols at chunk offset t * W, inside the current row (for
+  // whole-row steps the caller has done row_check).  TAIL: the last,
+  // partial step.  SLIDE: check the window first (a step reads at most W
+  // words, so two steps fit between checks).  xt: this step's activation
+  // pairs in LDS (kXTile only), in column-pair layout starting at the step's
+  // first 128-column block.
+  template <bool TAIL, bool SLIDE = true>
+  __device__ __forceinline__ void step(uint32_t t, const uint32_t *xt) {
+    if (SLIDE) slide();
     const uint32_t kk = t * W;  // offset of this step inside the chunk
-    if (UNIFORM && MODE != kCodes && k0 + kk >= row_end) {
-      if (MODE == kGemv) flush_uniform(row);
-      ++row;
-      row_end += N;
-      if (MODE == kBf16) srow = bf16_at(a.scale, row);
-    }
     bool act[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) act[g] = !TAIL || kk + g * kWave + lane < nc;
@@ -487,9 +500,41 @@ struct Decoder {
     if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
   }
 
+  // Full steps [t, t_end), a row segment at a time, two steps per iteration
+  // with one window check.  Step t's activation tile is xt + (t - t_first) *
+  // xs (kXTile).
+  __device__ __forceinline__ void run_steps(uint32_t t, uint32_t t_end, const uint32_t *xt,
+                                            uint32_t xs) {
+    static_assert(2 * W <= kWin - kHalf, "two steps must fit the window");
+    while (t < t_end) {
+      uint32_t seg_end = t_end;
+      if (UNIFORM && MODE != kCodes) {
+        row_check(t);
+        seg_end = min(t_end, (row_end - k0) / W);  // first step of the next row
+      }
+      for (; t + 1 < seg_end; t += 2, xt += 2 * xs) {
+        step<false, true>(t, xt);
+        step<false, false>(t + 1, xt + xs);
+      }
+      if (t < seg_end) {
+        step<false, true>(t, xt);
+        ++t;
+        xt += xs;
+      }
+    }
+  }
+
+  // The partial last step of a chunk, if any.
+  __device__ __forceinline__ void tail(const uint32_t *xt) {
+    if (nc % W) {
+      row_check(full);
+      step<true>(full, xt);
+    }
+  }
+
   __device__ __forceinline__ void run() {
-    for (uint32_t t = 0; t < full; ++t) step<false>(t, nullptr);
-    if (nc % W) step<true>(full, nullptr);
+    run_steps(0, full, nullptr, 0);
+    tail(nullptr);
     finish();
   }
 };
@@ -592,10 +637,9 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
     if (has) {
       const uint32_t *tile = reinterpret_cast<const uint32_t *>(tiles + (k & 1) * tile_u4);
       const uint32_t t0 = k * T, t1 = min(t0 + T, d.full);
-      for (uint32_t t = t0; t < t1; ++t) d.template step<false>(t, tile + (t - t0) * step_u4 * 4);
+      if (t0 < t1) d.run_steps(t0, t1, tile, step_u4 * 4);
       // the partial last step of the matrix's last chunk, while its tile is in LDS
-      if (d.nc % W && d.full >= t0 && d.full < t0 + T)
-        d.template step<true>(d.full, tile + (d.full - t0) * step_u4 * 4);
+      if (d.full >= t0 && d.full < t0 + T) d.tail(tile + (d.full - t0) * step_u4 * 4);
     }
     if (more) {
       const uint32_t buf = (k + 1) & 1;

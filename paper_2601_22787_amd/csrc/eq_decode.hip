@@ -97,6 +97,37 @@ __device__ inline float wave_sum(float v) {
 
 __device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// LDS pointers as 32-bit byte addresses, so that wave-uniform positions can
+// live in scalar registers and be advanced by scalar arithmetic.
+typedef __attribute__((address_space(3))) const uint16_t lds_u16;
+__device__ inline uint32_t lds_addr(const void *p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
+}
+__device__ inline uint32_t lds_read_u16(uint32_t addr) { return *(lds_u16 *)(addr); }
+
+// Byte address of the row-table entry of the code in bits 24..31 of a slot
+// entry e (bits 13..23 of e are zero, so e >> 23 is twice the code); tab is
+// the table's address over 512.
+__device__ inline uint32_t rowtab_addr(uint32_t tab, uint32_t e) {
+  return __builtin_amdgcn_alignbit(tab, e, 23);
+}
+
+// a + 2 * b on the scalar unit in one instruction (both wave-uniform)
+__device__ inline uint32_t add_twice(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("s_lshl1_add_u32 %0, %1, %2" : "=s"(r) : "s"(b), "s"(a));
+  return r;
+}
+
+// Per-lane select by a wave mask (bit l of m picks b for lane l), as one
+// v_cndmask.  Written out so that the compiler keeps it branch-free and does
+// not sink the loads feeding b into a branch.
+__device__ inline uint32_t select_by_mask(uint64_t m, uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "s"(m));
+  return r;
+}
 
 // Read-only inputs seen through the constant address space, so that loads
 // at wave-uniform addresses become scalar (SMEM) loads and never wait on the
@@ -196,7 +227,11 @@ __global__ void pair_layout_kernel(const uint16_t *x, uint32_t N, uint32_t B, ui
 
 // LDS of a decode block.  The value table comes first so that its byte
 // offsets fit the 16-bit immediate of LDS instructions.
-struct DecodeLds {
+// rowtab[w] holds, for wavefront w decoding to BF16, the dequantised value
+// of every code in its current row; 512-byte aligned, so that the byte
+// address of an entry is (w << 9) | (2 * code).
+struct alignas(512) DecodeLds {
+  uint16_t rowtab[kMaxWaves][256];
   uint32_t val[256];
   uint2 slot[kMaxSlots];
   uint4 win[kMaxWaves][kWin / 8];
@@ -234,19 +269,23 @@ struct Decoder {
   uint32_t lane, c, N, k0, nc, P, mask, last8, full;
   int nb;
   uint32_t x[G];
-  uint32_t p, p_end, wb;
+  // Stream position: wb is the word index of the window's first word, ra
+  // the LDS byte address of the next unread word (wa: of the window start).
+  uint32_t p_end, wb, wa, ra;
   uint4 next;
   __amdgpu_buffer_rsrc_t out_rsrc;
   uint32_t row, first_row, row_end;
-  float srow;
+  uint16_t *rowtab;  // this wavefront's row table (BF16 output, uniform rows)
+  uint32_t tab;      // its LDS address over 512
   uint32_t prow[G], pcol[G];
   float acc[UNIFORM ? 1 : G][kMaxBatch];
   bool pending[G];
 
   __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
-                                     const DecodeLds &sm, uint4 *win4_, const void *xl_)
-      : a(a_), slot(sm.slot), val(sm.val), win4(win4_),
-        win(reinterpret_cast<const uint16_t *>(win4_)), xl(xl_), lane(lane_), c(c_) {
+                                     DecodeLds &sm, uint32_t wave, const void *xl_)
+      : a(a_), slot(sm.slot), val(sm.val), win4(sm.win[wave]),
+        win(reinterpret_cast<const uint16_t *>(sm.win[wave])), xl(xl_), lane(lane_), c(c_),
+        rowtab(sm.rowtab[wave]) {
     N = a.cols;
     k0 = c * a.chunk_syms;
     nc = min(a.chunk_syms, a.n - k0);
@@ -257,13 +296,15 @@ struct Decoder {
     nb = NB ? NB : static_cast<int>(a.batch);
 #pragma unroll
     for (int g = 0; g < G; ++g) x[g] = a.chunk_state[c * W + g * kWave + lane];
-    p = as_const(a.chunk_off)[c];
+    const uint32_t p = as_const(a.chunk_off)[c];
     p_end = as_const(a.chunk_off)[c + 1];
     // Stream words [wb, wb + kWin) live in this wave's LDS window and the
     // next half is in flight in registers.  A step reads at most W words and
     // the window slides by a half whenever p passes its middle, so every word
     // a step can read is in LDS.
     wb = p & ~7u;
+    wa = uniform(lds_addr(win));
+    ra = wa + 2 * (p - wb);
     {
       const uint4 h0 = load_words(a.words, wb + 8 * lane, last8);
       const uint4 h1 = load_words(a.words, wb + kHalf + 8 * lane, last8);
@@ -282,7 +323,10 @@ struct Decoder {
     row = k0 / N;
     first_row = row;
     row_end = (row + 1) * N;  // <= n < 2^32
-    srow = (MODE == kBf16 && UNIFORM) ? bf16_at(a.scale, row) : 0.0f;
+    if (MODE == kBf16 && UNIFORM) {
+      tab = uniform(lds_addr(rowtab) >> 9);
+      fill_rowtab(row);
+    }
     if (!UNIFORM) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
@@ -322,23 +366,37 @@ struct Decoder {
     }
   }
 
+  // Row table of row r: bf16(s_r * v(code)) for every code, the exact
+  // product rounded once (NaN codes never occur in a valid container).
+  __device__ __forceinline__ void fill_rowtab(uint32_t r) {
+    const float s = bf16_at(a.scale, r);
+    const uint32_t c = 4 * lane;
+    const uint32_t lo = pack_bf16(s * __builtin_amdgcn_cvt_f32_fp8(c, 0),
+                                  s * __builtin_amdgcn_cvt_f32_fp8(c + 1, 0));
+    const uint32_t hi = pack_bf16(s * __builtin_amdgcn_cvt_f32_fp8(c + 2, 0),
+                                  s * __builtin_amdgcn_cvt_f32_fp8(c + 3, 0));
+    reinterpret_cast<uint2 *>(rowtab)[lane] = make_uint2(lo, hi);
+  }
+
   // Whole-row steps: move to the next row when step t starts it.
   __device__ __forceinline__ void row_check(uint32_t t) {
     if (UNIFORM && MODE != kCodes && k0 + t * W >= row_end) {
       if (MODE == kGemv) flush_uniform(row);
       ++row;
       row_end += N;
-      if (MODE == kBf16) srow = bf16_at(a.scale, row);
+      if (MODE == kBf16) fill_rowtab(row);
     }
   }
 
-  // Slide the stream window by one half once p has passed its middle.
+  // Slide the stream window by one half once the position has passed its
+  // middle.
   __device__ __forceinline__ void slide() {
-    if (p - wb >= kHalf) {
+    if (ra - wa >= 2 * kHalf) {
       const uint4 keep = win4[kHalf / 8 + lane];
       win4[lane] = keep;
       win4[kHalf / 8 + lane] = next;
       wb += kHalf;
+      ra -= 2 * kHalf;
       next = load_words(a.words, wb + kWin + 8 * lane, last8);
     }
   }
@@ -371,29 +429,35 @@ struct Decoder {
     }
 
     // use the symbols
+    uint32_t outv[G];
     if (MODE == kCodes) {
 #pragma unroll
       for (int g = 0; g < G; ++g)
         if (!TAIL || act[g])
-          __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(e0[g] >> 24), out_rsrc, lane,
-                                               kk + g * kWave, 0);
+          __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(e0[g] >> 24), out_rsrc,
+                                               lane + g * kWave, kk, 0);
+    } else if (MODE == kBf16 && UNIFORM) {
+      // one row-table read per symbol; stored once the renormalisation has
+      // been issued
+#pragma unroll
+      for (int g = 0; g < G; ++g) outv[g] = lds_read_u16(rowtab_addr(tab, e0[g]));
     } else if (MODE == kBf16) {
 #pragma unroll
       for (int g = 0; g < G; g += 2) {
-        const float s0 = UNIFORM ? srow : bf16_at(a.scale, prow[g]);
+        const float s0 = bf16_at(a.scale, prow[g]);
         const float v0 = s0 * __builtin_amdgcn_cvt_f32_fp8(e0[g], 3);
         float v1 = 0.0f;
         if (g + 1 < G) {
-          const float s1 = UNIFORM ? srow : bf16_at(a.scale, prow[g + 1]);
+          const float s1 = bf16_at(a.scale, prow[g + 1]);
           v1 = s1 * __builtin_amdgcn_cvt_f32_fp8(e0[g + 1], 3);
         }
         const uint32_t h = pack_bf16(v0, v1);  // exact products, rounded once
         if (!TAIL || act[g])
-          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h), out_rsrc, 2 * lane,
-                                                2 * (kk + g * kWave), 0);
+          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h), out_rsrc,
+                                                2 * (lane + g * kWave), 2 * kk, 0);
         if (g + 1 < G && (!TAIL || act[g + 1]))
           __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h >> 16), out_rsrc,
-                                                2 * lane, 2 * (kk + (g + 1) * kWave), 0);
+                                                2 * (lane + (g + 1) * kWave), 2 * kk, 0);
       }
     } else if (PAIR) {
       // pairs of this step's 128-column blocks: xq + (q * BG + bg) * 64 * bw
@@ -460,23 +524,30 @@ struct Decoder {
     }
 
     // renormalise in ascending state order (state g*64 + lane): all reads of
-    // the step are issued before any is used
-    bool need[G];
+    // the step are issued before any is used.  A lane's word follows those of
+    // the needing lanes below it.
+    uint64_t need[G];
     uint32_t word[G];
-    uint32_t rel = p - wb;
+    uint32_t r = ra;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      need[g] = act[g] && x[g] < kStateLow;
-      const uint64_t m = __builtin_amdgcn_ballot_w64(need[g]);
-      const uint32_t below = __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32),
-                                                       __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
-      word[g] = win[rel + below];
-      rel += static_cast<uint32_t>(__popcll(m));
+      need[g] = __builtin_amdgcn_ballot_w64(act[g] && x[g] < kStateLow);
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+          uint32_t(need[g] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(need[g]), 0u));
+      word[g] = lds_read_u16(r + 2 * below);
+      r = add_twice(r, static_cast<uint32_t>(__popcll(need[g])));
     }
 #pragma unroll
-    for (int g = 0; g < G; ++g)
-      if (need[g]) x[g] = (x[g] << 16) | word[g];
-    p = wb + rel;
+    for (int g = 0; g < G; ++g) x[g] = select_by_mask(need[g], x[g], (x[g] << 16) | word[g]);
+    ra = r;
+
+    if (MODE == kBf16 && UNIFORM) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (!TAIL || act[g])
+          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
+                                                2 * (lane + g * kWave), 2 * kk, 0);
+    }
   }
 
   // Close the chunk: last row sums, end-of-chunk check (every state back at
@@ -494,7 +565,7 @@ struct Decoder {
               if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
       }
     }
-    bool bad = p != p_end;
+    bool bad = wb + (ra - wa) / 2 != p_end;
 #pragma unroll
     for (int g = 0; g < G; ++g) bad |= x[g] != kStateLow;
     if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
@@ -566,7 +637,7 @@ __global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
   const uint32_t wave = uniform(threadIdx.x / kWave);
   const uint32_t waves = uniform(blockDim.x / kWave);
   for (uint32_t c = uniform(blockIdx.x * waves + wave); c < a.n_chunks; c += gridDim.x * waves) {
-    Decoder<G, MODE, UNIFORM, XS, NB> d(a, c, lane, sm, sm.win[wave], x_dyn);
+    Decoder<G, MODE, UNIFORM, XS, NB> d(a, c, lane, sm, wave, x_dyn);
     d.run();
   }
 }
@@ -625,7 +696,7 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
   store(0, 3, r3);
   __syncthreads();  // tables and the first tile are in
 
-  Dec d(a, has ? c : 0, lane, sm, sm.win[wave], nullptr);
+  Dec d(a, has ? c : 0, lane, sm, wave, nullptr);
   for (uint32_t k = 0; k < ntiles; ++k) {
     const bool more = k + 1 < ntiles;
     if (more) {

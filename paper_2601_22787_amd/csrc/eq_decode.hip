@@ -113,10 +113,11 @@ __device__ inline uint32_t rowtab_addr(uint32_t tab, uint32_t e) {
   return __builtin_amdgcn_alignbit(tab, e, 23);
 }
 
-// a + 2 * b on the scalar unit in one instruction (both wave-uniform)
+// a + 2 * b on the scalar unit in one instruction (both wave-uniform).  The
+// instruction writes SCC, which the compiler must not keep live across it.
 __device__ inline uint32_t add_twice(uint32_t a, uint32_t b) {
   uint32_t r;
-  asm("s_lshl1_add_u32 %0, %1, %2" : "=s"(r) : "s"(b), "s"(a));
+  asm("s_lshl1_add_u32 %0, %1, %2" : "=s"(r) : "s"(b), "s"(a) : "scc");
   return r;
 }
 
@@ -280,6 +281,23 @@ struct Decoder {
   uint32_t prow[G], pcol[G];
   float acc[UNIFORM ? 1 : G][kMaxBatch];
   bool pending[G];
+
+  // Software pipeline over the states of a lane (full steps, see prun): a
+  // state's slot entry is read while the states issued before it are
+  // processed, and its renormalisation word while later states are.
+  static constexpr bool PIPE =
+      G >= 2 && (MODE == kCodes || (UNIFORM && (MODE == kBf16 || PAIR)));
+  static constexpr int LAG = G / 2;  // processing trails issue by LAG states
+  uint2 ent[G];      // slot entries in flight
+  uint32_t qv[G];    // x >> P of the state whose entry is in flight
+  uint64_t nd[G];    // renormalisation masks of the last processed step
+  uint32_t wd[G];    // renormalisation words in flight
+  uint32_t sym[G];   // slot entry .x of the last processed step (code in bits 24..31)
+  uint32_t outv[G];  // BF16 values in flight, stored at step offset okk[g]
+  uint32_t okk[G];
+  uint32_t xv1[G / 2 > 0 ? G / 2 : 1];    // activation pairs of a state pair (batch 1)
+  uint4 xv8[G / 2 > 0 ? G / 2 : 1][2];     // (batch > 1), per 4-row batch group
+  uint32_t icol;     // column of the first symbol of the step being issued
 
   __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
                                      DecodeLds &sm, uint32_t wave, const void *xl_)
@@ -571,12 +589,136 @@ struct Decoder {
     if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
   }
 
+  // --- pipelined full steps -------------------------------------------------
+
+  // Activation pairs of state pair q for the step whose first column is col
+  // (kXLds) or whose tile is at xt (kXTile).
+  __device__ __forceinline__ void load_x(int q, uint32_t col, const uint32_t *xt) {
+    constexpr uint32_t bw = NB == 1 ? 1 : 4;
+    const uint32_t BG = NB == 1 ? 1 : (nb + 3) / 4;
+    const uint32_t *xq;
+    if (XS == kXTile) xq = xt + lane * bw;
+    else xq = reinterpret_cast<const uint32_t *>(xl) + ((col >> 7) * BG * kWave + lane) * bw;
+    if (NB == 1) {
+      xv1[q] = xq[q * kWave];
+    } else {
+#pragma unroll
+      for (uint32_t bg = 0; bg < 2; ++bg)
+        if (bg < BG) xv8[q][bg] = *reinterpret_cast<const uint4 *>(xq + (q * BG + bg) * kWave * bw);
+    }
+  }
+
+  // Issue state g of step t: finish its renormalisation from the previous
+  // step (unless FIRST), store its pending BF16 value, start its slot read.
+  template <bool FIRST>
+  __device__ __forceinline__ void pissue(int g, const uint32_t *xt) {
+    if (!FIRST) {
+      x[g] = select_by_mask(nd[g], x[g], (x[g] << 16) | wd[g]);
+      if (MODE == kBf16)
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
+                                              2 * (lane + g * kWave), 2 * okk[g], 0);
+    }
+    ent[g] = slot[x[g] & mask];
+    qv[g] = x[g] >> P;
+    if (PAIR && (g & 1)) load_x(g / 2, icol, xt);
+  }
+
+  // Process state h of step t (chunk offset kk): decode, start its
+  // renormalisation read, use the symbol.
+  __device__ __forceinline__ void pproc(int h, uint32_t kk) {
+    x[h] = __umul24(ent[h].x, qv[h]) + ent[h].y;
+    sym[h] = ent[h].x;
+    nd[h] = __builtin_amdgcn_ballot_w64(x[h] < kStateLow);
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi(uint32_t(nd[h] >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo(uint32_t(nd[h]), 0u));
+    wd[h] = lds_read_u16(ra + 2 * below);
+    ra = add_twice(ra, static_cast<uint32_t>(__popcll(nd[h])));
+    if (MODE == kCodes) {
+      __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(sym[h] >> 24), out_rsrc,
+                                           lane + h * kWave, kk, 0);
+    } else if (MODE == kBf16) {
+      outv[h] = lds_read_u16(rowtab_addr(tab, sym[h]));
+      okk[h] = kk;
+    } else if (h & 1) {
+      const int q = h / 2;
+      const uint32_t w2 =
+          e4m3x2_to_bf16x2(__builtin_amdgcn_perm(sym[h], sym[h - 1], 0x0c0c0703u));
+      if (NB == 1) {
+        acc[0][0] = dot2_bf16(w2, xv1[q], acc[0][0]);
+      } else {
+        const uint32_t BG = (nb + 3) / 4;
+#pragma unroll
+        for (uint32_t bg = 0; bg < 2; ++bg) {
+          if (bg < BG) {
+            const uint4 xv = xv8[q][bg];
+            acc[0][4 * bg + 0] = dot2_bf16(w2, xv.x, acc[0][4 * bg + 0]);
+            acc[0][4 * bg + 1] = dot2_bf16(w2, xv.y, acc[0][4 * bg + 1]);
+            acc[0][4 * bg + 2] = dot2_bf16(w2, xv.z, acc[0][4 * bg + 2]);
+            acc[0][4 * bg + 3] = dot2_bf16(w2, xv.w, acc[0][4 * bg + 3]);
+          }
+        }
+      }
+    }
+  }
+
+  // Full steps [t, t_end), software-pipelined: for each step t the states are
+  // issued in order g = 0..G-1, and after issuing g the wave processes state
+  // g - LAG (of step t, or of step t - 1 when g < LAG).  Processing stays in
+  // ascending state order, step by step, which is the order of the stream's
+  // words.  Rows change between the last state of step t - 1 and the first
+  // of step t.  xt: step t's activation tile (kXTile), stride xs per step.
+  __device__ __forceinline__ void prun(uint32_t t, uint32_t t_end, const uint32_t *xt,
+                                       uint32_t xs) {
+    static_assert(2 * W <= kWin - kHalf, "a step and a half must fit the window");
+    slide();
+    if (MODE != kCodes) {
+      row_check(t);
+      icol = k0 + t * W + N - row_end;
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) pissue<true>(g, xt);
+#pragma unroll
+    for (int h = 0; h < LAG; ++h) pproc(h, t * W);
+    for (++t; t < t_end; ++t) {
+      // words read since the last check: at most one step and a half
+      slide();
+      xt += xs;
+      if (MODE != kCodes) {
+        icol += W;
+        if (icol >= N) icol -= N;
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        pissue<false>(g, xt);
+        if (g < LAG) {
+          pproc(g + G - LAG, (t - 1) * W);
+        } else {
+          if (g == LAG) row_check(t);
+          pproc(g - LAG, t * W);
+        }
+      }
+    }
+#pragma unroll
+    for (int h = LAG; h < G; ++h) pproc(h, (t - 1) * W);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      x[g] = select_by_mask(nd[g], x[g], (x[g] << 16) | wd[g]);
+      if (MODE == kBf16)
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
+                                              2 * (lane + g * kWave), 2 * okk[g], 0);
+    }
+  }
+
   // Full steps [t, t_end), a row segment at a time, two steps per iteration
   // with one window check.  Step t's activation tile is xt + (t - t_first) *
   // xs (kXTile).
   __device__ __forceinline__ void run_steps(uint32_t t, uint32_t t_end, const uint32_t *xt,
                                             uint32_t xs) {
     static_assert(2 * W <= kWin - kHalf, "two steps must fit the window");
+    if constexpr (PIPE) {
+      if (t < t_end) prun(t, t_end, xt, xs);
+      return;
+    }
     while (t < t_end) {
       uint32_t seg_end = t_end;
       if (UNIFORM && MODE != kCodes) {

@@ -212,13 +212,31 @@ __host__ __device__ inline size_t pair_bytes(uint32_t B, uint32_t N) {
   return size_t(N / 2) * pair_groups(B) * pair_width(B) * sizeof(uint32_t);
 }
 
+// Entry i = ((m * BG + bg) * 64 + l) * bw + bb of the column-paired layout:
+// x[b][128 m + l] | x[b][128 m + l + 64] << 16 with b = bg * bw + bb (zero
+// beyond the batch).  bw is 1 or 4 and BG is 1 or 2 (B <= 8), so the index
+// splits with shifts.
 __device__ inline uint32_t pair_entry(const uint16_t *x, uint32_t N, uint32_t B, uint32_t i) {
-  const uint32_t bw = pair_width(B), BG = pair_groups(B);
-  const uint32_t bb = i % bw, l = (i / bw) % 64, bg = (i / (bw * 64)) % BG;
-  const uint32_t m = i / (bw * 64 * BG), b = bg * bw + bb;
+  const uint32_t lbw = B == 1 ? 0u : 2u;  // log2 bw
+  const uint32_t lbg = B > 4 ? 1u : 0u;   // log2 BG
+  const uint32_t bb = i & ((1u << lbw) - 1), l = (i >> lbw) & 63u;
+  const uint32_t bg = (i >> (lbw + 6)) & ((1u << lbg) - 1), m = i >> (lbw + 6 + lbg);
+  const uint32_t b = (bg << lbw) + bb;
   if (b >= B) return 0;
   const uint16_t *row = x + size_t(b) * N + 128 * m + l;
   return uint32_t(row[0]) | (uint32_t(row[64]) << 16);
+}
+
+// Batch 1: entries 4 j .. 4 j + 3 of the paired layout (N % 128 == 0, x
+// 8-byte aligned): two 8-byte loads and one 16-byte result.
+__device__ inline uint4 pair_entries4(const uint16_t *x, uint32_t j) {
+  const uint32_t m = j >> 4, l = (j & 15) * 4;
+  const uint2 lo = *reinterpret_cast<const uint2 *>(x + 128 * m + l);
+  const uint2 hi = *reinterpret_cast<const uint2 *>(x + 128 * m + l + 64);
+  return make_uint4(__builtin_amdgcn_perm(hi.x, lo.x, 0x05040100u),
+                    __builtin_amdgcn_perm(hi.x, lo.x, 0x07060302u),
+                    __builtin_amdgcn_perm(hi.y, lo.y, 0x05040100u),
+                    __builtin_amdgcn_perm(hi.y, lo.y, 0x07060302u));
 }
 
 __global__ void pair_layout_kernel(const uint16_t *x, uint32_t N, uint32_t B, uint32_t *xp) {
@@ -309,13 +327,15 @@ struct Decoder {
     nc = min(a.chunk_syms, a.n - k0);
     P = a.prob_bits;
     mask = (1u << P) - 1;
-    last8 = a.padded_words - 8;
     full = nc / W;
     nb = NB ? NB : static_cast<int>(a.batch);
 #pragma unroll
     for (int g = 0; g < G; ++g) x[g] = a.chunk_state[c * W + g * kWave + lane];
     const uint32_t p = as_const(a.chunk_off)[c];
     p_end = as_const(a.chunk_off)[c + 1];
+    // Window loads stop at the 8-word group holding the chunk's last word
+    // (words past it are never consumed); later groups repeat it from cache.
+    last8 = min(a.padded_words - 8, p_end & ~7u);
     // Stream words [wb, wb + kWin) live in this wave's LDS window and the
     // next half is in flight in registers.  A step reads at most W words and
     // the window slides by a half whenever p passes its middle, so every word
@@ -764,7 +784,11 @@ __global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
     if (Decoder<G, MODE, UNIFORM, XS, NB>::PAIR) {
       uint32_t *xp = reinterpret_cast<uint32_t *>(x_dyn);
       const uint32_t np = pair_bytes(a.batch, a.cols) / sizeof(uint32_t);
-      for (uint32_t i = threadIdx.x; i < np; i += nthreads) xp[i] = pair_entry(a.x, a.cols, a.batch, i);
+      if (a.batch == 1 && (reinterpret_cast<uintptr_t>(a.x) & 7) == 0) {
+        for (uint32_t j = threadIdx.x; j < np / 4; j += nthreads) x_dyn[j] = pair_entries4(a.x, j);
+      } else {
+        for (uint32_t i = threadIdx.x; i < np; i += nthreads) xp[i] = pair_entry(a.x, a.cols, a.batch, i);
+      }
     } else if (nx % 8 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0) {
       const uint4 *xv = reinterpret_cast<const uint4 *>(a.x);
       for (uint32_t i = threadIdx.x; i < nx / 8; i += nthreads) x_dyn[i] = xv[i];

@@ -128,6 +128,36 @@ size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B);
 int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
                    float *y, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Block-wise decompression (Sec. 2.2, paragraph "Block-Wise Decompression
+ * Pipeline": all compressed matrices of a transformer block are decoded
+ * together, ahead of the block's forward pass).  Decodes layers L[0..n-1]
+ * (host array of n views, 1 <= n <= 8) to BF16: layer i to w[i] (device, its
+ * M*N BF16 values), as eq_decode_bf16 does, with identical results.  Layers
+ * whose rows are whole steps (N a multiple of W) and that share one lane
+ * count are decoded by one launch, which keeps more chunks in flight per
+ * compute unit; otherwise each layer gets its own launch, in order. */
+int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
+                         hipStream_t stream);
+
+/* Workspace bytes eq_decode_gemv_multi needs: the sum of the layers'
+ * eq_gemv_workspace_bytes(L[i], B); 0 if an argument is invalid. */
+size_t eq_gemv_multi_workspace_bytes(const eq_layer *const *L, uint32_t n, uint32_t B);
+
+/* Fused decode-GEMV of n layers (1 <= n <= 8) that read the same input, such
+ * as the query/key/value or gate/up projections of a block (Alg. 2 for each
+ * layer, decoded block-wise as in Sec. 2.2): y[i][b][r] = s_r * sum_j
+ * v(q_rj) x[b][j] + bias[i][r] for layer i.  All layers must have the same
+ * N; x is [B][N] BF16 (device, B <= 8); bias is NULL or a host array of n
+ * device pointers (each [M_i] BF16 or NULL); y is a host array of n device
+ * pointers ([B][M_i] fp32).  ws/ws_bytes: device workspace of at least
+ * eq_gemv_multi_workspace_bytes(L, n, B); layer i uses the slice after those
+ * of layers 0..i-1.  Results equal eq_decode_gemv's for each layer.  Layers
+ * that cannot share one launch (rows not whole steps, different lane counts,
+ * activations too large for LDS) are run one launch each. */
+int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x, uint32_t B,
+                         const uint16_t *const *bias, float *const *y, void *ws,
+                         size_t ws_bytes, hipStream_t stream);
+
 /* Wait for `stream`, then report EQ_ECORRUPT if any decode since the last
  * eq_layer_prepare found a chunk whose stream or terminal states did not
  * check out, else EQ_OK (or EQ_EHIP). */

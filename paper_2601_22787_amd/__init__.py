@@ -54,6 +54,10 @@ SIGNATURES = {
     "eq_gemv_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer), ctypes.c_uint32]),
     "eq_decode_gemv": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp, _vp,
                                       _vp, ctypes.c_size_t, _vp]),
+    "eq_decode_bf16_multi": (ctypes.c_int, [_vp, _vp, ctypes.c_uint32, _vp]),
+    "eq_gemv_multi_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_uint32, ctypes.c_uint32]),
+    "eq_decode_gemv_multi": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp, _vp,
+                                            _vp, ctypes.c_size_t, _vp]),
     "eq_get_status": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp]),
     "eq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "eqe_alpha_search": (ctypes.c_float, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_double,
@@ -168,6 +172,64 @@ def eq_decode_gemv(L, x, B: int, bias, y, ws, stream=None) -> None:
     nbytes = ws.numel() * ws.element_size()
     _check("eq_decode_gemv", lib().eq_decode_gemv(ctypes.byref(r), px, B, pb, py, pw, nbytes,
                                                   _stream(stream)))
+
+
+def _layer_array(layers):
+    """Host array of eq_layer pointers (the views must outlive the call)."""
+    raws = [_raw(L) for L in layers]
+    arr = (ctypes.POINTER(eq_layer) * len(raws))(*[ctypes.pointer(r) for r in raws])
+    return arr, raws
+
+
+def _ptr_array(ptrs):
+    return (ctypes.c_void_p * len(ptrs))(*[p.value if p is not None else None for p in ptrs])
+
+
+def eq_decode_bf16_multi(layers, outs, stream=None) -> None:
+    """Block-wise decode of several layers: layer i to outs[i]."""
+    import torch
+    if len(layers) != len(outs):
+        raise ValueError("one output per layer")
+    arr, raws = _layer_array(layers)
+    for w in outs:
+        if w.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+            raise ValueError("outputs must hold 16-bit BF16 patterns")
+    ptrs = _ptr_array([_dptr(w, None, r.rows * r.cols) for w, r in zip(outs, raws)])
+    _check("eq_decode_bf16_multi",
+           lib().eq_decode_bf16_multi(arr, ptrs, len(raws), _stream(stream)))
+
+
+def eq_gemv_multi_workspace_bytes(layers, B: int) -> int:
+    arr, raws = _layer_array(layers)
+    return lib().eq_gemv_multi_workspace_bytes(arr, len(raws), B)
+
+
+def eq_decode_gemv_multi(layers, x, B: int, biases, ys, ws, stream=None) -> None:
+    """Fused decode-GEMV of several layers sharing the input x: ys[i] for
+    layer i; biases is None or a list (entries may be None)."""
+    import torch
+    if len(layers) != len(ys) or (biases is not None and len(biases) != len(layers)):
+        raise ValueError("one output (and bias) per layer")
+    arr, raws = _layer_array(layers)
+    if x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError("x must hold 16-bit BF16 patterns")
+    px = _dptr(x, None, B * raws[0].cols)
+    py = _ptr_array([_dptr(y, torch.float32, B * r.rows) for y, r in zip(ys, raws)])
+    pb = None
+    if biases is not None:
+        pb = _ptr_array([_dptr(b, None, r.rows) if b is not None else None
+                         for b, r in zip(biases, raws)])
+    nbytes = ws.numel() * ws.element_size()
+    _check("eq_decode_gemv_multi",
+           lib().eq_decode_gemv_multi(arr, len(raws), px, B, pb, py, _dptr(ws), nbytes,
+                                      _stream(stream)))
+
+
+def multi_workspace(layers, B: int):
+    """A device workspace for eq_decode_gemv_multi over `layers`."""
+    import torch
+    return torch.empty(eq_gemv_multi_workspace_bytes(layers, B), dtype=torch.uint8,
+                       device=layers[0].dev_blob.device)
 
 
 def eq_get_status(L, stream=None) -> int:

@@ -244,17 +244,24 @@ __global__ void pair_layout_kernel(const uint16_t *x, uint32_t N, uint32_t B, ui
   if (i < pair_bytes(B, N) / sizeof(uint32_t)) xp[i] = pair_entry(x, N, B, i);
 }
 
-// LDS of a decode block.  The value table comes first so that its byte
-// offsets fit the 16-bit immediate of LDS instructions.
-// rowtab[w] holds, for wavefront w decoding to BF16, the dequantised value
-// of every code in its current row; 512-byte aligned, so that the byte
-// address of an entry is (w << 9) | (2 * code).
-struct alignas(512) DecodeLds {
-  uint16_t rowtab[kMaxWaves][256];
+// Static LDS of a decode block: the value table first, so that its byte
+// offsets fit the 16-bit immediate of LDS instructions, then the slot table
+// (33 KiB, a multiple of 512 bytes).
+struct DecodeLds {
   uint32_t val[256];
   uint2 slot[kMaxSlots];
-  uint4 win[kMaxWaves][kWin / 8];
 };
+
+// Dynamic LDS of a decode block, sized for its wavefronts: one stream window
+// per wavefront, then the activations (GEMV: whole, or two tiles), then, for
+// BF16 output on whole-row steps, one 512-byte row table per wavefront at a
+// 512-byte aligned address, so that the byte address of an entry is
+// (table address) | (2 * code).
+constexpr uint32_t kWinBytes = kWin * sizeof(uint16_t);
+constexpr uint32_t kRowTabBytes = 256 * sizeof(uint16_t);
+__host__ __device__ inline size_t dyn_lds_bytes(uint32_t waves, size_t xbytes, bool rowtabs) {
+  return size_t(waves) * kWinBytes + xbytes + (rowtabs ? kRowTabBytes * (waves + 1) : 0);
+}
 
 // Stage the decode tables (and nothing else) into LDS.
 template <int MODE>
@@ -318,10 +325,11 @@ struct Decoder {
   uint32_t icol;     // column of the first symbol of the step being issued
 
   __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
-                                     DecodeLds &sm, uint32_t wave, const void *xl_)
-      : a(a_), slot(sm.slot), val(sm.val), win4(sm.win[wave]),
-        win(reinterpret_cast<const uint16_t *>(sm.win[wave])), xl(xl_), lane(lane_), c(c_),
-        rowtab(sm.rowtab[wave]) {
+                                     const DecodeLds &sm, uint4 *win4_, uint16_t *rowtab_,
+                                     const void *xl_)
+      : a(a_), slot(sm.slot), val(sm.val), win4(win4_),
+        win(reinterpret_cast<const uint16_t *>(win4_)), xl(xl_), lane(lane_), c(c_),
+        rowtab(rowtab_) {
     N = a.cols;
     k0 = c * a.chunk_syms;
     nc = min(a.chunk_syms, a.n - k0);
@@ -772,28 +780,31 @@ struct Decoder {
   }
 };
 
-// Each wavefront decodes chunks blockIdx.x * waves + wave, + gridDim.x * waves, ...
+// One block's share of a layer: block blk of nblk decodes chunks blk * waves
+// + wave, + nblk * waves, ...  Dynamic LDS (dyn): the wavefronts' stream
+// windows, then the activations (kXLds) or the row tables.
 template <int G, int MODE, bool UNIFORM, int XS, int NB>
-__global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
-  extern __shared__ uint4 x_dyn[];  // activations when XS == kXLds
-  __shared__ DecodeLds sm;
+__device__ __forceinline__ void decode_block(const Args &a, uint32_t blk, uint32_t nblk,
+                                             DecodeLds &sm, uint4 *dyn) {
+  const uint32_t nthreads = blockDim.x;
+  const uint32_t waves = uniform(nthreads / kWave);
+  uint4 *const xl = dyn + waves * (kWinBytes / sizeof(uint4));
   stage_tables<MODE>(a, sm);
   if (XS == kXLds) {
-    const uint32_t nthreads = blockDim.x;
     const uint32_t nx = a.batch * a.cols;
     if (Decoder<G, MODE, UNIFORM, XS, NB>::PAIR) {
-      uint32_t *xp = reinterpret_cast<uint32_t *>(x_dyn);
+      uint32_t *xp = reinterpret_cast<uint32_t *>(xl);
       const uint32_t np = pair_bytes(a.batch, a.cols) / sizeof(uint32_t);
       if (a.batch == 1 && (reinterpret_cast<uintptr_t>(a.x) & 7) == 0) {
-        for (uint32_t j = threadIdx.x; j < np / 4; j += nthreads) x_dyn[j] = pair_entries4(a.x, j);
+        for (uint32_t j = threadIdx.x; j < np / 4; j += nthreads) xl[j] = pair_entries4(a.x, j);
       } else {
         for (uint32_t i = threadIdx.x; i < np; i += nthreads) xp[i] = pair_entry(a.x, a.cols, a.batch, i);
       }
     } else if (nx % 8 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0) {
       const uint4 *xv = reinterpret_cast<const uint4 *>(a.x);
-      for (uint32_t i = threadIdx.x; i < nx / 8; i += nthreads) x_dyn[i] = xv[i];
+      for (uint32_t i = threadIdx.x; i < nx / 8; i += nthreads) xl[i] = xv[i];
     } else {
-      uint16_t *xs = reinterpret_cast<uint16_t *>(x_dyn);
+      uint16_t *xs = reinterpret_cast<uint16_t *>(xl);
       for (uint32_t i = threadIdx.x; i < nx; i += nthreads) xs[i] = a.x[i];
     }
   }
@@ -801,11 +812,43 @@ __global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
 
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint32_t wave = uniform(threadIdx.x / kWave);
-  const uint32_t waves = uniform(blockDim.x / kWave);
-  for (uint32_t c = uniform(blockIdx.x * waves + wave); c < a.n_chunks; c += gridDim.x * waves) {
-    Decoder<G, MODE, UNIFORM, XS, NB> d(a, c, lane, sm, wave, x_dyn);
+  uint16_t *rowtab = nullptr;
+  if (MODE == kBf16 && UNIFORM) {
+    char *base = reinterpret_cast<char *>(xl);
+    base += (0u - lds_addr(base)) & (kRowTabBytes - 1);
+    rowtab = reinterpret_cast<uint16_t *>(base) + wave * 256;
+  }
+  uint4 *const win = dyn + wave * (kWinBytes / sizeof(uint4));
+  for (uint32_t c = uniform(blk * waves + wave); c < a.n_chunks; c += nblk * waves) {
+    Decoder<G, MODE, UNIFORM, XS, NB> d(a, c, lane, sm, win, rowtab, xl);
     d.run();
   }
+}
+
+template <int G, int MODE, bool UNIFORM, int XS, int NB>
+__global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
+  extern __shared__ uint4 dyn[];
+  __shared__ DecodeLds sm;
+  decode_block<G, MODE, UNIFORM, XS, NB>(a, blockIdx.x, gridDim.x, sm, dyn);
+}
+
+// Several layers in one launch (whole-row steps, one lane count): blocks
+// [blk_end[i-1], blk_end[i]) decode layer i.  For the GEMV the layers share
+// the activations.
+constexpr uint32_t kMaxLayers = 8;
+struct MultiArgs {
+  Args a[kMaxLayers];
+  uint32_t blk_end[kMaxLayers];
+  uint32_t n;
+};
+
+template <int G, int MODE, int XS, int NB>
+__global__ __launch_bounds__(kMaxBlock) void multi_decode_kernel(MultiArgs m) {
+  extern __shared__ uint4 dyn[];
+  __shared__ DecodeLds sm;
+  uint32_t i = 0, b0 = 0;
+  while (i + 1 < m.n && blockIdx.x >= m.blk_end[i]) b0 = m.blk_end[i++];
+  decode_block<G, MODE, true, XS, NB>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0, sm, dyn);
 }
 
 // Fused GEMV for activations too large for LDS (whole-row steps, W >= 128).
@@ -817,7 +860,7 @@ __global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
 // wave within the class.
 template <int G, int NB>
 __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
-  extern __shared__ uint4 tiles[];  // 2 x tile
+  extern __shared__ uint4 dyn[];  // stream windows, then 2 x tile
   __shared__ DecodeLds sm;
   using Dec = Decoder<G, kGemv, true, kXTile, NB>;
   constexpr uint32_t W = Dec::W;
@@ -840,6 +883,7 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
   const uint32_t steps = a.chunk_syms / W;            // steps of a full chunk
   const uint32_t ntiles = (steps + T - 1) / T;
   const uint4 *src = reinterpret_cast<const uint4 *>(a.xp);
+  uint4 *const tiles = dyn + waves * (kWinBytes / sizeof(uint4));
 
   // tile k covers steps [k T, k T + T): 128-column blocks from col0/128 + k T W/128;
   // each thread moves 16-byte units threadIdx.x + s * nthreads, s < kStageRegs
@@ -862,7 +906,7 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
   store(0, 3, r3);
   __syncthreads();  // tables and the first tile are in
 
-  Dec d(a, has ? c : 0, lane, sm, wave, nullptr);
+  Dec d(a, has ? c : 0, lane, sm, dyn + wave * (kWinBytes / sizeof(uint4)), nullptr, nullptr);
   for (uint32_t k = 0; k < ntiles; ++k) {
     const bool more = k + 1 < ntiles;
     if (more) {
@@ -987,9 +1031,13 @@ DeviceFacts device_facts() {
 // Blocks of up to 16 wavefronts, one chunk per wavefront at a time.  With
 // fewer chunks than wavefront slots, the chunks are spread evenly over the
 // compute units (one block each); otherwise each wavefront loops over chunks.
+uint32_t launch_waves(uint32_t n_chunks, int cus) {
+  const uint32_t waves = (n_chunks + cus - 1) / cus;
+  return waves < 1 ? 1 : (waves > kMaxWaves ? kMaxWaves : waves);
+}
+
 void launch_shape(uint32_t n_chunks, int cus, dim3 &grid, dim3 &block) {
-  uint32_t waves = (n_chunks + cus - 1) / cus;
-  waves = waves < 1 ? 1 : (waves > kMaxWaves ? kMaxWaves : waves);
+  const uint32_t waves = launch_waves(n_chunks, cus);
   uint32_t blocks = (n_chunks + waves - 1) / waves;
   if (blocks > uint32_t(cus) * 4) blocks = uint32_t(cus) * 4;
   grid = dim3(blocks);
@@ -1012,11 +1060,14 @@ size_t xlds_bytes(const Args &a) {
 }
 
 // Activation placement of a GEMV launch.
-int gemv_xsrc(const Args &a, const DeviceFacts &f) {
+int gemv_xsrc(const Args &a, const DeviceFacts &f, uint32_t waves) {
   const bool uniform = a.cols % a.lanes == 0;
   const size_t xbytes = xlds_bytes(a);
-  if (xbytes <= kMaxXLdsBytes && kStaticLds + xbytes <= size_t(f.lds_per_block)) return kXLds;
-  if (uniform && a.lanes >= 128 && kStaticLds + 2 * kTileBytes <= size_t(f.lds_per_block))
+  if (xbytes <= kMaxXLdsBytes &&
+      kStaticLds + dyn_lds_bytes(waves, xbytes, false) <= size_t(f.lds_per_block))
+    return kXLds;
+  if (uniform && a.lanes >= 128 &&
+      kStaticLds + dyn_lds_bytes(kMaxWaves, 2 * kTileBytes, false) <= size_t(f.lds_per_block))
     return kXTile;
   return kXGlobal;
 }
@@ -1025,7 +1076,8 @@ template <int MODE, bool UNIFORM, int XS, int NB>
 void launch_mode(const Args &a, hipStream_t s, const DeviceFacts &f) {
   dim3 grid, block;
   launch_shape(a.n_chunks, f.cus, grid, block);
-  const size_t shm = XS == kXLds ? xlds_bytes(a) : 0;
+  const size_t shm = dyn_lds_bytes(block.x / kWave, XS == kXLds ? xlds_bytes(a) : 0,
+                                    MODE == kBf16 && UNIFORM);
   switch (a.lanes) {
     case 64:
       hipLaunchKernelGGL((decode_kernel<1, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
@@ -1053,7 +1105,7 @@ int launch_decode(const Args &a, hipStream_t s) {
   if (MODE != kGemv) {
     if (uniform) launch_batch<MODE, true, kXGlobal>(a, s, f);
     else launch_batch<MODE, false, kXGlobal>(a, s, f);
-  } else if (gemv_xsrc(a, f) == kXLds) {
+  } else if (gemv_xsrc(a, f, launch_waves(a.n_chunks, f.cus)) == kXLds) {
     if (uniform) launch_batch<MODE, true, kXLds>(a, s, f);
     else launch_batch<MODE, false, kXLds>(a, s, f);
   } else {
@@ -1087,13 +1139,56 @@ int launch_tiled(Args a, hipStream_t s, const DeviceFacts &f) {
   if (T < 1) T = 1;
   a.tile_steps = T;
   const dim3 grid(a.ncls * ((per_cls + waves - 1) / waves)), block(waves * kWave);
-  const size_t shm = 2 * size_t(T) * step_bytes;
+  const size_t shm = dyn_lds_bytes(waves, 2 * size_t(T) * step_bytes, false);
   if (W == 128) hipLaunchKernelGGL((gemv_tiled_kernel<2, NB>), grid, block, shm, s, a);
   else hipLaunchKernelGGL((gemv_tiled_kernel<4, NB>), grid, block, shm, s, a);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
 size_t round256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Multi-layer launch shape: enough wavefronts per block that two blocks per
+// compute unit hold every chunk; each layer gets whole blocks.
+uint32_t multi_shape(const MultiArgs &m, int cus, MultiArgs &out) {
+  uint64_t total = 0;
+  for (uint32_t i = 0; i < m.n; ++i) total += m.a[i].n_chunks;
+  uint32_t waves = uint32_t((total + 2 * uint64_t(cus) - 1) / (2 * uint64_t(cus)));
+  waves = waves < 1 ? 1 : (waves > kMaxWaves ? kMaxWaves : waves);
+  out = m;
+  uint32_t end = 0;
+  for (uint32_t i = 0; i < m.n; ++i) {
+    end += (m.a[i].n_chunks + waves - 1) / waves;
+    out.blk_end[i] = end;
+  }
+  return waves;
+}
+
+template <int MODE, int XS, int NB>
+int launch_multi(const MultiArgs &m0, size_t xbytes, hipStream_t s, const DeviceFacts &f) {
+  MultiArgs m;
+  const uint32_t waves = multi_shape(m0, f.cus, m);
+  const dim3 grid(m.blk_end[m.n - 1]), block(waves * kWave);
+  const size_t shm = dyn_lds_bytes(waves, xbytes, MODE == kBf16);
+  switch (m.a[0].lanes) {
+    case 64:
+      hipLaunchKernelGGL((multi_decode_kernel<1, MODE, XS, NB>), grid, block, shm, s, m);
+      break;
+    case 128:
+      hipLaunchKernelGGL((multi_decode_kernel<2, MODE, XS, NB>), grid, block, shm, s, m);
+      break;
+    default:
+      hipLaunchKernelGGL((multi_decode_kernel<4, MODE, XS, NB>), grid, block, shm, s, m);
+      break;
+  }
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+// Layers that can share one launch: whole-row steps, one lane count.
+bool joint_ok(const eq_layer *const *L, uint32_t n) {
+  for (uint32_t i = 0; i < n; ++i)
+    if (L[i]->cols % L[i]->lanes != 0 || L[i]->lanes != L[0]->lanes) return false;
+  return true;
+}
 
 }  // namespace
 
@@ -1150,7 +1245,7 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
   }
   const DeviceFacts f = device_facts();
   int rc;
-  if (gemv_xsrc(a, f) == kXTile) {
+  if (gemv_xsrc(a, f, launch_waves(L->n_chunks, f.cus)) == kXTile) {
     const uint32_t np = uint32_t(pair_bytes(B, L->cols) / sizeof(uint32_t));
     hipLaunchKernelGGL(pair_layout_kernel, dim3((np + 255) / 256), dim3(256), 0, stream, x,
                        L->cols, B, const_cast<uint32_t *>(a.xp));
@@ -1162,13 +1257,96 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
   }
   if (rc != EQ_OK) return rc;
   if (uniform) {
-    if (L->n_chunks > 1)
+    // rows split between chunks exist only when chunks do not hold whole rows
+    if (L->n_chunks > 1 && L->chunk_syms % L->cols != 0)
       hipLaunchKernelGGL(merge_rows_kernel, dim3((L->n_chunks + 254) / 256), dim3(256), 0, stream,
                          a);
   } else {
     const uint32_t n = L->rows * B;
     hipLaunchKernelGGL(finalize_rows_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a);
   }
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
+                                    hipStream_t stream) {
+  if (!L || !w || n < 1 || n > kMaxLayers) return EQ_EINVAL;
+  for (uint32_t i = 0; i < n; ++i)
+    if (!layer_ok(L[i]) || !w[i]) return EQ_EINVAL;
+  if (n == 1 || !joint_ok(L, n)) {
+    for (uint32_t i = 0; i < n; ++i) {
+      const int rc = eq_decode_bf16(L[i], w[i], stream);
+      if (rc != EQ_OK) return rc;
+    }
+    return EQ_OK;
+  }
+  MultiArgs m{};
+  m.n = n;
+  for (uint32_t i = 0; i < n; ++i) {
+    m.a[i] = make_args(L[i]);
+    m.a[i].wout = w[i];
+  }
+  return launch_multi<kBf16, kXGlobal, 1>(m, 0, stream, device_facts());
+}
+
+extern "C" size_t eq_gemv_multi_workspace_bytes(const eq_layer *const *L, uint32_t n, uint32_t B) {
+  if (!L || n < 1 || n > kMaxLayers) return 0;
+  size_t total = 0;
+  for (uint32_t i = 0; i < n; ++i) {
+    const size_t b = eq_gemv_workspace_bytes(L[i], B);
+    if (b == 0) return 0;
+    total += b;
+  }
+  return total;
+}
+
+extern "C" int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x,
+                                    uint32_t B, const uint16_t *const *bias, float *const *y,
+                                    void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!L || !y || !x || !ws || n < 1 || n > kMaxLayers || B < 1 || B > kMaxBatch)
+    return EQ_EINVAL;
+  for (uint32_t i = 0; i < n; ++i)
+    if (!layer_ok(L[i]) || !y[i] || L[i]->cols != L[0]->cols) return EQ_EINVAL;
+  if (ws_bytes < eq_gemv_multi_workspace_bytes(L, n, B)) return EQ_EINVAL;
+  // layer i's workspace follows those of layers 0 .. i-1
+  size_t off[kMaxLayers];
+  for (uint32_t i = 0, o = 0; i < n; ++i) {
+    off[i] = o;
+    o += eq_gemv_workspace_bytes(L[i], B);
+  }
+  const DeviceFacts f = device_facts();
+  MultiArgs m{};
+  m.n = n;
+  for (uint32_t i = 0; i < n; ++i) {
+    m.a[i] = make_args(L[i]);
+    m.a[i].x = x;
+    m.a[i].batch = B;
+    m.a[i].bias = bias ? bias[i] : nullptr;
+    m.a[i].y = y[i];
+    m.a[i].ws = reinterpret_cast<float *>(static_cast<char *>(ws) + off[i]);
+  }
+  MultiArgs shaped;
+  const uint32_t waves = multi_shape(m, f.cus, shaped);
+  const size_t xbytes = xlds_bytes(m.a[0]);
+  const bool joint = n > 1 && joint_ok(L, n) && xbytes <= kMaxXLdsBytes &&
+                     kStaticLds + dyn_lds_bytes(waves, xbytes, false) <= size_t(f.lds_per_block);
+  if (!joint) {
+    for (uint32_t i = 0; i < n; ++i) {
+      const int rc = eq_decode_gemv(L[i], x, B, bias ? bias[i] : nullptr, y[i],
+                                    static_cast<char *>(ws) + off[i],
+                                    eq_gemv_workspace_bytes(L[i], B), stream);
+      if (rc != EQ_OK) return rc;
+    }
+    return EQ_OK;
+  }
+  const int rc = B == 1 ? launch_multi<kGemv, kXLds, 1>(m, xbytes, stream, f)
+                        : (B == kMaxBatch ? launch_multi<kGemv, kXLds, kMaxBatch>(m, xbytes, stream, f)
+                                          : launch_multi<kGemv, kXLds, 0>(m, xbytes, stream, f));
+  if (rc != EQ_OK) return rc;
+  for (uint32_t i = 0; i < n; ++i)
+    if (L[i]->n_chunks > 1 && L[i]->chunk_syms % L[i]->cols != 0)
+      hipLaunchKernelGGL(merge_rows_kernel, dim3((L[i]->n_chunks + 254) / 256), dim3(256), 0,
+                         stream, m.a[i]);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 

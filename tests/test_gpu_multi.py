@@ -1,0 +1,188 @@
+"""GPU parity of block-wise decoding (several layers per launch, Sec. 2.2
+"Block-Wise Decompression Pipeline").
+
+Each layer's BF16 weights must be bit-exact against the oracle and equal to
+what the single-layer entry point writes.  The shared-input GEMV must equal
+the single-layer GEMV bit for bit (each chunk's partial sums are formed the
+same way whichever block runs it) and meet the 1e-2 bar against the oracle's
+fp64 GEMV on the decoded weights.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import config_matrices, small_spec
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def eq():
+    import paper_2601_22787_amd as m
+    m.lib()
+    assert torch.cuda.is_available()
+    return m
+
+
+def _dev():
+    return torch.device("cuda:0")
+
+
+def make(eq, M, N, C, lanes, bits, seed):
+    spec = small_spec(M, N, bits=bits, chunk=C, lanes=lanes, seed=seed)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, bits)
+    blob = eq.eqe_encode(w, alpha, chunk_syms=C, lanes=lanes)
+    return eq.Layer(blob, _dev()), blob, spec
+
+
+def bf16_single(eq, L):
+    out = torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev())
+    eq.eq_decode_bf16(L, out)
+    return out
+
+
+def oracle_bf16(blob):
+    rc, q = oracle.container_decode(blob)
+    assert rc == oracle.OK
+    return oracle.dequant(q, oracle.container_scales(blob))
+
+
+def rel_err(y, y_ref):
+    return np.abs(y - y_ref).max(axis=1) / np.maximum(np.abs(y_ref).max(axis=1), 1e-30)
+
+
+# A scaled-down transformer block: the layers of one joint launch share the
+# lane count and have whole-row steps; rows may straddle chunks (N = 1536).
+BLOCK = [  # M, N, C, lanes, bits
+    (512, 2048, 8192, 256, 2.0),
+    (128, 2048, 8192, 256, 3.0),
+    (128, 2048, 8192, 256, 4.0),
+    (96, 1536, 4096, 256, 2.0),
+    (1024, 512, 16384, 256, 3.0),
+]
+
+
+def test_bf16_multi_joint_and_per_layer(eq):
+    layers = [make(eq, *s, seed=500 + i) for i, s in enumerate(BLOCK)]
+    mixed = [make(eq, 40, 640, 1024, 64, 2.0, seed=601), make(eq, 16, 4160, 8192, 256, 3.0, seed=602)]
+    for group, name in ((layers, "joint"), (layers[:1], "one layer"), (mixed, "per-layer")):
+        say("bf16 multi", name, [(L.rows, L.cols) for L, _, _ in group])
+        outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev())
+                for L, _, _ in group]
+        eq.eq_decode_bf16_multi([L for L, _, _ in group], outs)
+        for (L, blob, _), out in zip(group, outs):
+            got = out.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)
+            assert np.array_equal(got, oracle_bf16(blob)), (name, L.rows, L.cols)
+            assert torch.equal(out, bf16_single(eq, L))
+            assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+@pytest.mark.parametrize("B", [1, 3, 8])
+def test_gemv_multi_matches_single_and_oracle(eq, B):
+    qkv = [make(eq, *s, seed=700 + i) for i, s in enumerate(BLOCK[:3])]
+    say("gemv multi qkv B", B)
+    spec = qkv[0][2]
+    x_bits = synth.activations(spec, B)
+    x = torch.from_numpy(x_bits.view(np.int16)).to(_dev())
+    biases = [torch.from_numpy(synth.bias(s).view(np.int16)).to(_dev()) if i != 1 else None
+              for i, (_, _, s) in enumerate(qkv)]
+    ys = [torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+          for L, _, _ in qkv]
+    Ls = [L for L, _, _ in qkv]
+    eq.eq_decode_gemv_multi(Ls, x, B, biases, ys, eq.multi_workspace(Ls, B))
+    for (L, blob, s), y, bias in zip(qkv, ys, biases):
+        y1 = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+        eq.eq_decode_gemv(L, x, B, bias, y1, L.workspace(B))
+        assert torch.equal(y, y1), "multi and single GEMV differ"
+        b_bits = None if bias is None else bias.cpu().numpy().view(np.uint16)
+        y_ref = oracle.gemv(oracle_bf16(blob), x_bits, b_bits)
+        err = rel_err(y.cpu().numpy(), y_ref)
+        assert (err <= TOL).all(), err
+        assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+def test_gemv_multi_straddling_rows_and_fallback(eq):
+    # rows straddle chunks (merge after the joint launch)
+    a = [make(eq, 96, 1536, 4096, 256, 2.0, seed=801), make(eq, 64, 1536, 4096, 256, 3.0, seed=802)]
+    # x too large for LDS at B = 8 (N = 8192): one launch per layer
+    b = [make(eq, 24, 8192, 16384, 256, 2.0, seed=803), make(eq, 8, 8192, 16384, 256, 4.0, seed=804)]
+    for group, B in ((a, 1), (a, 8), (b, 8), (b, 1)):
+        say("gemv multi", [(L.rows, L.cols) for L, _, _ in group], "B", B)
+        Ls = [L for L, _, _ in group]
+        x_bits = synth.activations(group[0][2], B)
+        x = torch.from_numpy(x_bits.view(np.int16)).to(_dev())
+        ys = [torch.empty((B, L.rows), dtype=torch.float32, device=_dev()) for L in Ls]
+        eq.eq_decode_gemv_multi(Ls, x, B, None, ys, eq.multi_workspace(Ls, B))
+        for (L, blob, _), y in zip(group, ys):
+            y1 = torch.empty((B, L.rows), dtype=torch.float32, device=_dev())
+            eq.eq_decode_gemv(L, x, B, None, y1, L.workspace(B))
+            assert torch.equal(y, y1)
+            err = rel_err(y.cpu().numpy(), oracle.gemv(oracle_bf16(blob), x_bits))
+            assert (err <= TOL).all(), err
+
+
+def test_multi_rejects_bad_arguments(eq):
+    L1, _, _ = make(eq, 64, 1024, 4096, 256, 2.0, seed=901)
+    L2, _, _ = make(eq, 64, 512, 4096, 256, 2.0, seed=902)
+    x = torch.zeros((1, 1024), dtype=torch.int16, device=_dev())
+    ys = [torch.empty((1, 64), dtype=torch.float32, device=_dev()) for _ in range(2)]
+    ws = eq.multi_workspace([L1, L1], 1)
+    with pytest.raises(eq.EqError):  # different N cannot share x
+        eq.eq_decode_gemv_multi([L1, L2], x, 1, None, ys, eq.multi_workspace([L1, L2], 1))
+    with pytest.raises(eq.EqError):  # workspace too small
+        eq.eq_decode_gemv_multi([L1, L1], x, 1, None, ys, ws[:16])
+    with pytest.raises(eq.EqError):  # more than 8 layers
+        outs = [torch.empty(64 * 1024, dtype=torch.int16, device=_dev()) for _ in range(9)]
+        eq.eq_decode_bf16_multi([L1] * 9, outs)
+
+
+def test_c5_layer0_qkv_block(eq):
+    """The config-5 layer-0 query/key/value projections (8192x8192 and two
+    1024x8192, 2 bits, 65536-symbol chunks, 256 lanes) in one launch: equal to
+    the single-layer paths (which the config-5 parity test checks against the
+    oracle), plus sampled rows against the oracle."""
+    specs = [s for s in config_matrices(5, layers=[0]) if s.name.split(".")[-1] in ("q", "k", "v")]
+    assert len(specs) == 3
+    Ls, blobs = [], []
+    for s in specs:
+        w = synth.weights(s)
+        alpha, _ = eq.eqe_alpha_search(w, s.target_bits, sample_rows=512)
+        blob = eq.eqe_encode(w, alpha, chunk_syms=s.chunk_syms, lanes=s.lanes, seed=s.seed,
+                             target_bits=s.target_bits)
+        Ls.append(eq.Layer(blob, _dev()))
+        blobs.append(blob)
+    say("config-5 qkv", [(L.rows, L.cols) for L in Ls])
+    outs = [torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev()) for L in Ls]
+    eq.eq_decode_bf16_multi(Ls, outs)
+    for L, out in zip(Ls, outs):
+        assert torch.equal(out, bf16_single(eq, L))
+    x_bits = synth.activations(specs[0], 1)
+    x = torch.from_numpy(x_bits.view(np.int16)).to(_dev())
+    ys = [torch.empty((1, L.rows), dtype=torch.float32, device=_dev()) for L in Ls]
+    eq.eq_decode_gemv_multi(Ls, x, 1, None, ys, eq.multi_workspace(Ls, 1))
+    rng = np.random.default_rng(5)
+    for L, blob, y, out in zip(Ls, blobs, ys, outs):
+        y1 = torch.empty((1, L.rows), dtype=torch.float32, device=_dev())
+        eq.eq_decode_gemv(L, x, 1, None, y1, L.workspace(1))
+        assert torch.equal(y, y1)
+        # sampled rows: the GPU's BF16 rows are the oracle's (checked chunk-wise by the
+        # config-5 parity test); here the GEMV of those rows in fp64
+        rows = rng.choice(L.rows, size=8, replace=False)
+        w_rows = out.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)[rows]
+        y_ref = oracle.gemv(w_rows, x_bits)
+        got = y.cpu().numpy()[:, rows]
+        err = np.abs(got - y_ref).max() / np.abs(y_ref).max()
+        assert err <= TOL, err
+        assert eq.eq_get_status(L) == eq.EQ_OK

@@ -37,7 +37,7 @@ ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 # conversion, per symbol pair) + B/2 (one dot2 per pair and batch row).
 ALG_OPS = {"bf16": 11.0, "gemv1": 10.0 + 0.5 + 0.5 + 0.5, "gemv8": 10.0 + 0.5 + 0.5 + 4.0}
 # Kernel (function) name of each op family's decode launch on these shapes.
-KERNEL = {"bf16": "decode_kernel<4, 1, true, 0, 1>", "gemv1": "decode_kernel<4, 2, true, 1, 1>",
+KERNEL = {"bf16": "multi_decode_kernel<4, 1, 0, 1>", "gemv1": "decode_kernel<4, 2, true, 1, 1>",
           "gemv8": "gemv_tiled_kernel<4, 8>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_config4.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2601_22787_amd", "csrc", "eq_decode.hip")
@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="target CPU time of each oracle baseline sample (1 thread, all threads)")
+    ap.add_argument("--workload", choices=("c4", "c5"), default="c4",
+                    help="c4: the 8192x28672 / 28672x8192 pair (default); c5: the 80-layer stack, "
+                         "block-wise vs per-matrix, decode-GEMV B=1 and decode to BF16")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
     return ap.parse_args()
@@ -169,12 +172,127 @@ def traffic_per_launch(op):
     return t["kernels"][op]["hbm_bytes"]
 
 
+def run_stack(args):
+    """Config 5: an 80-layer 70B-shaped stack (q/k/v/o 8192x8192, 1024x8192 x2,
+    8192x8192; gate/up 28672x8192; down 8192x28672), layer l coded at
+    (2, 3, 4)[l mod 3] bits.  One layer per entropy class is generated and
+    encoded; the 80 layers are distinct device copies of those three (the
+    kernels' work depends on the symbol statistics, not on the values, and
+    every copy is read from HBM).  Timed per pass over all 80 layers:
+    decode-GEMV at B = 1 block-wise (q|k|v and gate|up share their inputs;
+    4 launches per layer) and per matrix (7 launches), and decode to BF16
+    block-wise (one launch per layer into a block buffer) and per matrix."""
+    import numpy as np
+    import torch
+
+    import paper_2601_22787_amd as eq
+    import synth
+    from synth.configs import config_matrices
+
+    eq.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    names = ("q", "k", "v", "o", "gate", "up", "down")
+    proto = []  # per entropy class: {name: (spec, blob)}
+    for layer in range(3):
+        t0 = time.time()
+        d = {}
+        for spec in config_matrices(5, layers=[layer]):
+            w = synth.weights(spec)
+            alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
+            d[spec.name.split(".")[-1]] = (spec, eq.eqe_encode(
+                w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes, seed=spec.seed,
+                target_bits=spec.target_bits))
+        proto.append(d)
+        mb = sum(b.size for _, b in d.values()) / 1e6
+        print(f"[bench] stack class {layer}: {mb:.0f} MB in {time.time() - t0:.1f}s",
+              file=sys.stderr, flush=True)
+    nl = 80
+    layers = [{n: eq.Layer(proto[l % 3][n][1], dev) for n in names} for l in range(nl)]
+    params = sum(proto[l % 3][n][0].params for l in range(nl) for n in names)
+    cont_bytes = sum(proto[l % 3][n][1].size for l in range(nl) for n in names)
+    print(f"[bench] {nl} layers resident: {cont_bytes / 1e9:.2f} GB", file=sys.stderr, flush=True)
+    # inputs of a block: attention input (q, k, v), o input, MLP input (gate, up), down input
+    xs = {k: torch.from_numpy(synth.vector(0x5EED, 16 + i, n).view(np.int16)).to(dev).view(1, n)
+          for i, (k, n) in enumerate((("attn", 8192), ("o", 8192), ("mlp", 8192), ("down", 28672)))}
+    groups = ((("q", "k", "v"), "attn"), (("o",), "o"), (("gate", "up"), "mlp"), (("down",), "down"))
+    ys = {n: torch.empty(1, proto[0][n][0].rows, dtype=torch.float32, device=dev) for n in names}
+    ws_multi = {g: eq.multi_workspace([layers[0][n] for n in g], 1) for g, _ in groups}
+    ws_one = {n: layers[0][n].workspace(1) for n in names}
+    block_elems = sum(proto[0][n][0].params for n in names)
+    wbuf = torch.empty(block_elems, dtype=torch.int16, device=dev)
+    offs, o = {}, 0
+    for n in names:
+        offs[n] = o
+        o += proto[0][n][0].params
+    outs = [wbuf[offs[n]:offs[n] + proto[0][n][0].params] for n in names]
+
+    def gemv_block(Lset):
+        for g, xk in groups:
+            eq.eq_decode_gemv_multi([Lset[n] for n in g], xs[xk], 1, None, [ys[n] for n in g],
+                                    ws_multi[g])
+
+    def gemv_matrix(Lset):
+        for g, xk in groups:
+            for n in g:
+                eq.eq_decode_gemv(Lset[n], xs[xk], 1, None, ys[n], ws_one[n])
+
+    def bf16_block(Lset):
+        eq.eq_decode_bf16_multi([Lset[n] for n in names], outs)
+
+    def bf16_matrix(Lset):
+        for n, out in zip(names, outs):
+            eq.eq_decode_bf16(Lset[n], out)
+
+    def time_pass(fn, reps):
+        for Lset in layers[:3]:
+            fn(Lset)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            for Lset in layers:
+                fn(Lset)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    res = {}
+    for name, fn in (("gemv_b1_block", gemv_block), ("gemv_b1_per_matrix", gemv_matrix),
+                     ("bf16_block", bf16_block), ("bf16_per_matrix", bf16_matrix)):
+        ms = time_pass(fn, args.steps)
+        res[name] = {"ms_per_pass": round(ms, 3), "us_per_layer": round(1000 * ms / nl, 1),
+                     "gparams_per_s": round(params / ms / 1e6, 1)}
+        print(f"[bench] {name}: {ms:.2f} ms per pass", file=sys.stderr, flush=True)
+    for Lset in layers:
+        for n in names:
+            if eq.eq_get_status(Lset[n]) != eq.EQ_OK:
+                raise RuntimeError("decode status not OK")
+    gb = res["gemv_b1_block"]
+    print(json.dumps({
+        "metric": "decoded Gparams/s, 80-layer stack, fused decode-GEMV B=1 (block-wise launches)",
+        "value": gb["gparams_per_s"], "unit": "Gparams/s", "n_gpus": 1, "steps": args.steps,
+        "ms_per_step": gb["ms_per_pass"], "higher_is_better": True, "vs_baseline": None,
+        "dtype": "u32", "data": "synthetic",
+        "config": {"workload": "config 5: 80 layers x {q 8192x8192, k/v 1024x8192, o 8192x8192, "
+                               "gate/up 28672x8192, down 8192x28672}, (2,3,4)[l mod 3] bits, "
+                               "65536-symbol chunks, 256 lanes; 3 distinct layers, 80 device copies",
+                   "params": params, "container_gb": round(cont_bytes / 1e9, 3),
+                   "hbm_frac_compressed_block_gemv": round(
+                       cont_bytes / (gb["ms_per_pass"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "passes": res}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the path would shard by output rows, see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "c5":
+        run_stack(args)
+        return
     import numpy as np
     import torch
 
@@ -190,8 +308,7 @@ def main():
     ops = ["bf16", "gemv1", "gemv8"]
 
     # device buffers shared by all steps
-    nmax = max(s.params for s in specs)
-    wout = torch.empty(nmax, dtype=torch.int16, device=dev)
+    wouts = [torch.empty(spec.params, dtype=torch.int16, device=dev) for spec in specs]
     bufs = []
     for spec, w, blob, lays in layers:
         d = {}
@@ -201,28 +318,33 @@ def main():
             d[B] = (x, y, lays[0].workspace(B))
         bufs.append(d)
     infos = [blob_info(blob) for _, _, blob, _ in layers]
+    ALL = -1  # launch covering both matrices
 
-    def launch(op, mi, L):
-        if op == "bf16":
-            eq.eq_decode_bf16(L, wout)
-        else:
-            B = 1 if op == "gemv1" else 8
-            x, y, ws = bufs[mi][B]
-            eq.eq_decode_gemv(L, x, B, None, y, ws)
+    # One step: the layer's two matrices decoded to BF16 by one block-wise
+    # launch (they are decompressed together, as a block's weights are),
+    # then the fused GEMVs of each matrix at B = 1 and B = 8 (the two
+    # matrices read different inputs, so they are separate launches).
+    def launches(s):
+        Ls = [lays[s % len(lays)] for _, _, _, lays in layers]
+        yield ALL, "bf16", lambda: eq.eq_decode_bf16_multi(Ls, wouts)
+        for mi, L in enumerate(Ls):
+            for op in ("gemv1", "gemv8"):
+                B = 1 if op == "gemv1" else 8
+                x, y, ws = bufs[mi][B]
+                yield mi, op, (lambda L=L, x=x, B=B, y=y, ws=ws:
+                               eq.eq_decode_gemv(L, x, B, None, y, ws))
 
     def one_step(s, timers=None):
-        for mi, (spec, w, blob, lays) in enumerate(layers):
-            L = lays[s % len(lays)]
-            for op in ops:
-                if timers is None:
-                    launch(op, mi, L)
-                else:
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record()
-                    launch(op, mi, L)
-                    e1.record()
-                    timers.append((mi, op, e0, e1))
+        for mi, op, fn in launches(s):
+            if timers is None:
+                fn()
+            else:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                timers.append((mi, op, e0, e1))
 
     # Reference: a plain device-to-device copy of 256 MiB, the known-size
     # kernel against which HBM byte counters are calibrated.
@@ -264,36 +386,42 @@ def main():
     per = {}
     for mi, op, e0, e1 in timers:
         per.setdefault((mi, op), []).append(e0.elapsed_time(e1))
-    kernels = {}
+    mats = list(range(len(specs)))
+    kernels, fam = {}, {}
     for (mi, op), ts in per.items():
-        spec = specs[mi]
+        covered = mats if mi == ALL else [mi]
+        name = "layer" if mi == ALL else specs[mi].name
         B = 8 if op == "gemv8" else 1
         us = 1000.0 * sum(ts) / len(ts)
         q10, q50, q90 = (1000.0 * float(v) for v in np.percentile(ts, [10, 50, 90]))
-        nbytes = algorithmic_bytes(infos[mi], op, B)
-        comp = infos[mi]["file_bytes"] - 2 * (infos[mi]["padded_words"] - infos[mi]["total_words"])
-        tops = ALG_OPS[op] * spec.params / us / 1e6
-        kernels[f"{spec.name}.{op}"] = {
+        params = sum(specs[m].params for m in covered)
+        nbytes = sum(algorithmic_bytes(infos[m], op, B) for m in covered)
+        comp = sum(infos[m]["file_bytes"] - 2 * (infos[m]["padded_words"] - infos[m]["total_words"])
+                   for m in covered)
+        ops_alg = ALG_OPS[op] * params
+        tops = ops_alg / us / 1e6
+        kernels[f"{name}.{op}"] = {
             "us": round(us, 2), "us_p10": round(q10, 2), "us_p50": round(q50, 2),
-            "us_p90": round(q90, 2), "gparams_per_s": round(spec.params / us / 1e3, 1),
+            "us_p90": round(q90, 2), "params": params,
+            "gparams_per_s": round(params / us / 1e3, 1),
             "alg_bytes": nbytes, "gbs": round(nbytes / us / 1e3, 1),
             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
             "hbm_frac_compressed": round(comp / us / 1e3 / HBM_PEAK_GBS, 4),
             "alg_ops_per_param": ALG_OPS[op], "tops": round(tops, 2),
             "alu_frac": round(tops / ALU_PEAK_TOPS, 4)}
+        f = fam.setdefault(op, {"us": 0.0, "launches": 0, "bytes": 0, "ops": 0.0})
+        f["us"] += us
+        f["launches"] += 1
+        f["bytes"] += nbytes
+        f["ops"] += ops_alg
     # dominant kernel: the op family with the largest share of the step;
-    # figures per launch (mean over the two matrices)
-    fam = {}
-    for (mi, op), ts in per.items():
-        fam[op] = fam.get(op, 0.0) + sum(ts) / len(ts)
-    dom = max(fam, key=fam.get)
-    nmat = len(specs)
-    dom_us = 1000.0 * fam[dom] / nmat
-    dom_bytes = sum(algorithmic_bytes(infos[mi], dom, 8 if dom == "gemv8" else 1)
-                    for mi in range(nmat)) / nmat
-    dom_ops = ALG_OPS[dom] * sum(s.params for s in specs) / nmat
-    achieved_gbs = dom_bytes / dom_us / 1e3
-    achieved_tops = dom_ops / dom_us / 1e6
+    # figures per launch (mean over the family's launches)
+    dom = max(fam, key=lambda k: fam[k]["us"])
+    fd = fam[dom]
+    dom_us = fd["us"] / fd["launches"]
+    dom_bytes = fd["bytes"] / fd["launches"]
+    achieved_gbs = fd["bytes"] / fd["us"] / 1e3
+    achieved_tops = fd["ops"] / fd["us"] / 1e6
 
     params_per_step = sum(s.params for s in specs) * len(ops)
     value = params_per_step / (ms_per_step * 1e-3) / 1e9
@@ -305,8 +433,9 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
         "config": {"workload": "Llama-70B MLP layers 8192x28672 + 28672x8192, E4M3 at ~2.0 "
-                               "bits/param, 65536-symbol chunks, 256 rANS lanes/chunk; per step "
-                               "and matrix: " + ", ".join(ops),
+                               "bits/param, 65536-symbol chunks, 256 rANS lanes/chunk; per step: "
+                               "both matrices decoded to BF16 by one block-wise launch, then "
+                               "fused decode-GEMV B=1 and B=8 per matrix",
                    "entropy_bits": [round(i["entropy"], 4) for i in infos],
                    "container_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos],
                    "copies_rotated": args.copies},

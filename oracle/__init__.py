@@ -18,6 +18,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 OK, EINVAL, EFORMAT, ECORRUPT, ENOMEM = 0, -1, -2, -4, -5
+E4M3, INT8 = 1, 2  # base formats (container header field base_format)
 
 _u8p = ctypes.c_void_p
 _vp = ctypes.c_void_p
@@ -53,16 +54,24 @@ def lib():
         sig = {
             "or_e4m3_value": (ctypes.c_double, [ctypes.c_uint8]),
             "or_e4m3_round": (ctypes.c_uint8, [ctypes.c_float]),
+            "or_int8_value": (ctypes.c_double, [ctypes.c_uint8]),
+            "or_int8_round": (ctypes.c_uint8, [ctypes.c_float]),
+            "or_qmax": (ctypes.c_double, [ctypes.c_uint32]),
+            "or_code_value": (ctypes.c_double, [ctypes.c_uint32, ctypes.c_uint8]),
             "or_bf16_value": (ctypes.c_double, [ctypes.c_uint16]),
             "or_bf16_round": (ctypes.c_uint16, [ctypes.c_double]),
             "or_entropy_counts": (ctypes.c_double, [_vp, ctypes.c_uint32]),
             "or_entropy_codes": (ctypes.c_double, [_vp, ctypes.c_uint64]),
             "or_sparsity_entropy": (ctypes.c_double, [ctypes.c_double, ctypes.c_double]),
-            "or_row_scales": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float, _vp]),
-            "or_quantize": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, _vp]),
-            "or_dequant": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, _vp]),
+            "or_row_scales": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float,
+                                     ctypes.c_uint32, _vp]),
+            "or_quantize": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, ctypes.c_uint32,
+                                   _vp]),
+            "or_dequant": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, ctypes.c_uint32,
+                                  _vp]),
             "or_alpha_search": (ctypes.c_float, [_vp, ctypes.c_uint32, ctypes.c_uint32,
-                                                 ctypes.c_double, ctypes.POINTER(ctypes.c_double)]),
+                                                 ctypes.c_double, ctypes.c_uint32,
+                                                 ctypes.POINTER(ctypes.c_double)]),
             "or_freq_table": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, _vp,
                                              ctypes.POINTER(ctypes.c_uint32)]),
             "or_rans_encode": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
@@ -75,6 +84,7 @@ def lib():
             "or_container_build": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
                                                   ctypes.c_float, ctypes.c_uint32,
                                                   ctypes.c_uint32, ctypes.c_uint32,
+                                                  ctypes.c_uint32,
                                                   ctypes.c_uint64, ctypes.c_float,
                                                   ctypes.POINTER(ctypes.c_void_p),
                                                   ctypes.POINTER(ctypes.c_uint64)]),
@@ -110,6 +120,22 @@ def e4m3_round(v: float) -> int:
     return lib().or_e4m3_round(v)
 
 
+def int8_value(code: int) -> float:
+    return lib().or_int8_value(code)
+
+
+def int8_round(v: float) -> int:
+    return lib().or_int8_round(v)
+
+
+def qmax(fmt: int) -> float:
+    return lib().or_qmax(fmt)
+
+
+def code_value(fmt: int, code: int) -> float:
+    return lib().or_code_value(fmt, code)
+
+
 def bf16_value(bits: int) -> float:
     return lib().or_bf16_value(bits)
 
@@ -134,37 +160,37 @@ def sparsity_entropy(s: float, h_nz: float) -> float:
 
 
 # ---- quantiser ----
-def row_scales(w: np.ndarray, alpha: float) -> np.ndarray:
+def row_scales(w: np.ndarray, alpha: float, fmt: int = E4M3) -> np.ndarray:
     w = np.ascontiguousarray(w, dtype=np.uint16)
     M, N = w.shape
     out = np.empty(M, dtype=np.uint16)
-    lib().or_row_scales(_ptr(w), M, N, alpha, _ptr(out))
+    lib().or_row_scales(_ptr(w), M, N, alpha, fmt, _ptr(out))
     return out
 
 
-def quantize(w: np.ndarray, scale: np.ndarray) -> np.ndarray:
+def quantize(w: np.ndarray, scale: np.ndarray, fmt: int = E4M3) -> np.ndarray:
     w = np.ascontiguousarray(w, dtype=np.uint16)
     scale = np.ascontiguousarray(scale, dtype=np.uint16)
     M, N = w.shape
     out = np.empty((M, N), dtype=np.uint8)
-    lib().or_quantize(_ptr(w), M, N, _ptr(scale), _ptr(out))
+    lib().or_quantize(_ptr(w), M, N, _ptr(scale), fmt, _ptr(out))
     return out
 
 
-def dequant(q: np.ndarray, scale: np.ndarray) -> np.ndarray:
+def dequant(q: np.ndarray, scale: np.ndarray, fmt: int = E4M3) -> np.ndarray:
     q = np.ascontiguousarray(q, dtype=np.uint8)
     scale = np.ascontiguousarray(scale, dtype=np.uint16)
     M, N = q.shape
     out = np.empty((M, N), dtype=np.uint16)
-    lib().or_dequant(_ptr(q), M, N, _ptr(scale), _ptr(out))
+    lib().or_dequant(_ptr(q), M, N, _ptr(scale), fmt, _ptr(out))
     return out
 
 
-def alpha_search(w: np.ndarray, target_bits: float):
+def alpha_search(w: np.ndarray, target_bits: float, fmt: int = E4M3):
     w = np.ascontiguousarray(w, dtype=np.uint16)
     M, N = w.shape
     h = ctypes.c_double()
-    a = lib().or_alpha_search(_ptr(w), M, N, target_bits, ctypes.byref(h))
+    a = lib().or_alpha_search(_ptr(w), M, N, target_bits, fmt, ctypes.byref(h))
     return a, h.value
 
 
@@ -210,13 +236,13 @@ def rans_decode(words: np.ndarray, states: np.ndarray, n: int, lanes: int, P: in
 
 # ---- container ----
 def container_build(w: np.ndarray, alpha: float, P: int, chunk_syms: int, lanes: int,
-                    seed: int = 0, target_bits: float = 0.0) -> np.ndarray:
+                    seed: int = 0, target_bits: float = 0.0, fmt: int = E4M3) -> np.ndarray:
     w = np.ascontiguousarray(w, dtype=np.uint16)
     M, N = w.shape
     p = ctypes.c_void_p()
     nb = ctypes.c_uint64()
-    rc = lib().or_container_build(_ptr(w), M, N, alpha, P, chunk_syms, lanes, seed, target_bits,
-                                  ctypes.byref(p), ctypes.byref(nb))
+    rc = lib().or_container_build(_ptr(w), M, N, alpha, fmt, P, chunk_syms, lanes, seed,
+                                  target_bits, ctypes.byref(p), ctypes.byref(nb))
     if rc != OK:
         raise ValueError(f"or_container_build: {rc}")
     try:

@@ -51,6 +51,34 @@ uint8_t or_e4m3_round(float v) {
   return (uint8_t)((v < 0.0f ? 0x80 : 0x00) | c);
 }
 
+/* Int8 (the paper's alternative base format, Sec. 2.1 and Sec. 3.5):
+ * two's complement byte, symmetric range [-Qmax, Qmax] with Qmax = 127, so
+ * the code 0x80 (-128) never occurs. */
+double or_int8_value(uint8_t code) { return (double)(int8_t)code; }
+
+/* Nearest integer after clamping to [-127, 127] (Sec. 2.1 quantiser); a
+ * value exactly halfway between two integers goes to the even one. */
+uint8_t or_int8_round(float v) {
+  double a = (double)v;
+  if (a > 127.0) a = 127.0;
+  if (a < -127.0) a = -127.0;
+  double r = floor(a);
+  double d = a - r; /* exact, in [0, 1) */
+  if (d > 0.5 || (d == 0.5 && fmod(r, 2.0) != 0.0)) r += 1.0;
+  int iv = (int)r;
+  return (uint8_t)(int8_t)iv;
+}
+
+double or_qmax(uint32_t fmt) { return fmt == OR_FMT_INT8 ? 127.0 : 448.0; }
+
+double or_code_value(uint32_t fmt, uint8_t code) {
+  return fmt == OR_FMT_INT8 ? or_int8_value(code) : or_e4m3_value(code);
+}
+
+static uint8_t round_to_format(uint32_t fmt, float v) {
+  return fmt == OR_FMT_INT8 ? or_int8_round(v) : or_e4m3_round(v);
+}
+
 double or_bf16_value(uint16_t bits) {
   uint32_t u = (uint32_t)bits << 16;
   float f;
@@ -121,9 +149,10 @@ double or_sparsity_entropy(double s, double h_nz) {
 /* ------------------------------------------------------------------ */
 
 /* Channel-wise scales, one per output row.  AbsMax (eq. absmax) gives
- * max|W_i|/Qmax; alpha multiplies it (alpha = 1 is plain AbsMax).  Stored
- * in BF16. */
-void or_row_scales(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint16_t *scale) {
+ * max|W_i|/Qmax (Qmax of the base format); alpha multiplies it (alpha = 1
+ * is plain AbsMax).  Stored in BF16. */
+void or_row_scales(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
+                   uint16_t *scale) {
   for (uint32_t i = 0; i < M; ++i) {
     double amax = 0.0;
     for (uint32_t j = 0; j < N; ++j) {
@@ -131,44 +160,47 @@ void or_row_scales(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint1
       if (a > amax) amax = a;
     }
     scale[i] = (amax == 0.0) ? 0x3F80 /* 1.0 */
-                             : or_bf16_round((double)alpha * amax / 448.0);
+                             : or_bf16_round((double)alpha * amax / or_qmax(fmt));
   }
 }
 
-/* W_q = clamp(round(W/s), -Qmax, Qmax) with one fp32 division. */
-void or_quantize(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale, uint8_t *q) {
+/* W_q = clamp(round(W/s), -Qmax, Qmax) with one fp32 division, rounded in
+ * the base format. */
+void or_quantize(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale, uint32_t fmt,
+                 uint8_t *q) {
   for (uint32_t i = 0; i < M; ++i) {
     float s = (float)or_bf16_value(scale[i]);
     for (uint32_t j = 0; j < N; ++j) {
       uint64_t k = (uint64_t)i * N + j;
       float v = (float)or_bf16_value(w[k]) / s;
-      q[k] = or_e4m3_round(v);
+      q[k] = round_to_format(fmt, v);
     }
   }
 }
 
-/* W_hat = s * W_q: the exact product of an 8-bit and a <=4-bit
- * significand, rounded once to BF16. */
-void or_dequant(const uint8_t *q, uint32_t M, uint32_t N, const uint16_t *scale,
+/* W_hat = s * W_q: the product of the 8-bit BF16 significand and a code
+ * value of at most 7 significant bits (4 for E4M3) is exact in fp32; it is
+ * rounded once to BF16. */
+void or_dequant(const uint8_t *q, uint32_t M, uint32_t N, const uint16_t *scale, uint32_t fmt,
                 uint16_t *w_hat) {
   for (uint32_t i = 0; i < M; ++i) {
     double s = or_bf16_value(scale[i]);
     for (uint32_t j = 0; j < N; ++j) {
       uint64_t k = (uint64_t)i * N + j;
-      w_hat[k] = or_bf16_round(s * or_e4m3_value(q[k]));
+      w_hat[k] = or_bf16_round(s * or_code_value(fmt, q[k]));
     }
   }
 }
 
-static double entropy_at(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
+static double entropy_at(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
                          uint16_t *scale, uint8_t *q) {
-  or_row_scales(w, M, N, alpha, scale);
-  or_quantize(w, M, N, scale, q);
+  or_row_scales(w, M, N, alpha, fmt, scale);
+  or_quantize(w, M, N, scale, fmt, q);
   return or_entropy_codes(q, (uint64_t)M * N);
 }
 
 float or_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, double target_bits,
-                      double *h_out) {
+                      uint32_t fmt, double *h_out) {
   uint16_t *scale = (uint16_t *)malloc(sizeof(uint16_t) * M);
   uint8_t *q = (uint8_t *)malloc((size_t)M * N);
   if (!scale || !q) {
@@ -182,7 +214,7 @@ float or_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, double target_b
   for (int it = 0; it < 40; ++it) {
     double mid = 0.5 * (lo + hi);
     float alpha = (float)exp2(mid);
-    double h = entropy_at(w, M, N, alpha, scale, q);
+    double h = entropy_at(w, M, N, alpha, fmt, scale, q);
     double err = fabs(h - target_bits);
     if (err < best_err) {
       best_err = err;
@@ -430,12 +462,12 @@ static uint64_t align256(uint64_t v) { return (v + 255) & ~(uint64_t)255; }
  * little past the end of any chunk without leaving the section. */
 static uint64_t padded_words_for(uint64_t total) { return (total + 1024 + 127) & ~(uint64_t)127; }
 
-/* Alg. 1: scales, Q, vec (row-major), ANS encode per chunk. */
-int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t P,
-                       uint32_t chunk_syms, uint32_t lanes, uint64_t seed, float target_bits,
-                       uint8_t **blob_out, uint64_t *blob_bytes) {
+/* Alg. 1: scales, Q (base format fmt), vec (row-major), ANS encode per chunk. */
+int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
+                       uint32_t P, uint32_t chunk_syms, uint32_t lanes, uint64_t seed,
+                       float target_bits, uint8_t **blob_out, uint64_t *blob_bytes) {
   if (!w || M == 0 || N == 0 || P < 1 || P > 12 || lanes == 0 || lanes % 64 != 0 ||
-      chunk_syms == 0 || chunk_syms % lanes != 0)
+      chunk_syms == 0 || chunk_syms % lanes != 0 || (fmt != OR_FMT_E4M3 && fmt != OR_FMT_INT8))
     return OR_EINVAL;
   uint64_t n = (uint64_t)M * N;
   if (n >= (1ull << 32)) return OR_EINVAL;
@@ -451,8 +483,8 @@ int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, u
     rc = OR_ENOMEM;
     goto done;
   }
-  or_row_scales(w, M, N, alpha, scale);
-  or_quantize(w, M, N, scale, q);
+  or_row_scales(w, M, N, alpha, fmt, scale);
+  or_quantize(w, M, N, scale, fmt, q);
   uint64_t counts[256] = {0};
   for (uint64_t k = 0; k < n; ++k) counts[q[k]]++;
   uint8_t sym[256];
@@ -489,7 +521,7 @@ int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, u
   memcpy(b + H_MAGIC, "EQC1", 4);
   put32(b, H_VERSION, 1);
   put32(b, H_HEADER_BYTES, HEADER_BYTES);
-  put32(b, H_FORMAT, 1);
+  put32(b, H_FORMAT, fmt);
   put32(b, H_ROWS, M);
   put32(b, H_COLS, N);
   put32(b, H_CHUNK, chunk_syms);
@@ -564,7 +596,7 @@ int or_container_info(const uint8_t *b, uint64_t bytes, or_info *h) {
   h->off_words = get64(b, H_OFF_WORDS);
   h->file_bytes = get64(b, H_FILE_BYTES);
   uint64_t n = (uint64_t)h->rows * h->cols;
-  if (h->base_format != 1 || n == 0 || n >= (1ull << 32) || h->lanes == 0 ||
+  if ((h->base_format != OR_FMT_E4M3 && h->base_format != OR_FMT_INT8) || n == 0 || n >= (1ull << 32) || h->lanes == 0 ||
       h->lanes % 64 != 0 || h->chunk_syms == 0 || h->chunk_syms % h->lanes != 0 ||
       h->prob_bits < 1 || h->prob_bits > 12 || h->n_syms < 1 || h->n_syms > 256 ||
       h->n_chunks != (n + h->chunk_syms - 1) / h->chunk_syms ||

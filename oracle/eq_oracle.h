@@ -18,6 +18,7 @@
  *             view, QMatMul + bias).
  *   App. A.1  Float8 E4M3 base format, signed zeros resolved, byte-level
  *             ANS in fixed-size chunks.
+ *   Sec. 3.5  Int8 as the alternative base format (symmetric, Sec. 2.1).
  *   App. B.1  closed-form entropy of a sparse mixture, Tab. sparsity_entropy.
  *
  * The paper's ANS coder is a closed library whose format it does not give.
@@ -33,6 +34,8 @@
  *   fp32 division W/s, -0 stored as +0, BF16 scales
  *   s = bf16(fp64(alpha * absmax / 448)) (all-zero row: s = 1),
  *   dequantised weight = bf16(s * v(q)) rounded once from the exact product.
+ * Int8: Qmax = 127 (0x80 never occurs), clamp, then nearest integer with
+ *   ties to even; s = bf16(fp64(alpha * absmax / 127)).
  *
  * Parity pins for every function are in the test suite; none is unpinned.
  */
@@ -51,9 +54,15 @@ extern "C" {
 #define OR_ECORRUPT (-4)
 #define OR_ENOMEM (-5)
 
-/* ---- number formats (Sec. 2.1, App. A.1) ---- */
+/* ---- number formats (Sec. 2.1, App. A.1; Int8: Sec. 3.5 ablation) ---- */
+#define OR_FMT_E4M3 1 /* Float8 E4M3FN, Qmax 448 (the default base format) */
+#define OR_FMT_INT8 2 /* Int8 two's complement, symmetric, Qmax 127 */
 double or_e4m3_value(uint8_t code);   /* NaN for 0x7F / 0xFF */
 uint8_t or_e4m3_round(float v);       /* nearest E4M3FN code, ties to even */
+double or_int8_value(uint8_t code);   /* (int8_t)code */
+uint8_t or_int8_round(float v);       /* nearest integer in [-127, 127], ties to even */
+double or_qmax(uint32_t fmt);
+double or_code_value(uint32_t fmt, uint8_t code);
 double or_bf16_value(uint16_t bits);
 uint16_t or_bf16_round(double v);     /* nearest BF16, ties to even */
 
@@ -63,13 +72,16 @@ double or_entropy_codes(const uint8_t *q, uint64_t n);
 double or_sparsity_entropy(double s, double h_nz);
 
 /* ---- quantiser / dequantiser (Sec. 2.1) ---- */
-void or_row_scales(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint16_t *scale);
-void or_quantize(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale, uint8_t *q);
-void or_dequant(const uint8_t *q, uint32_t M, uint32_t N, const uint16_t *scale, uint16_t *w_hat);
+void or_row_scales(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
+                   uint16_t *scale);
+void or_quantize(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale, uint32_t fmt,
+                 uint8_t *q);
+void or_dequant(const uint8_t *q, uint32_t M, uint32_t N, const uint16_t *scale, uint32_t fmt,
+                uint16_t *w_hat);
 /* Bisection on log2(alpha) in [-4, 24] for the alpha whose entropy is
  * closest to target (the stand-in for the paper's lambda optimisation). */
 float or_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, double target_bits,
-                      double *h_out);
+                      uint32_t fmt, double *h_out);
 
 /* ---- frequency table (ANS metadata) ---- */
 int or_freq_table(const uint64_t counts[256], uint32_t P, uint8_t *sym, uint16_t *freq,
@@ -91,9 +103,9 @@ typedef struct or_info {
   uint64_t off_scale, off_sym, off_freq, off_chunk_off, off_chunk_state, off_words;
 } or_info;
 
-int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t P,
-                       uint32_t chunk_syms, uint32_t lanes, uint64_t seed, float target_bits,
-                       uint8_t **blob, uint64_t *blob_bytes);
+int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
+                       uint32_t P, uint32_t chunk_syms, uint32_t lanes, uint64_t seed,
+                       float target_bits, uint8_t **blob, uint64_t *blob_bytes);
 void or_free(void *p);
 int or_container_info(const uint8_t *blob, uint64_t blob_bytes, or_info *info);
 int or_container_decode_chunk(const uint8_t *blob, uint64_t blob_bytes, uint32_t chunk,

@@ -12,6 +12,8 @@ rotated so that compressed reads are not served from the 256 MB MALL.
 Prints one JSON line: the decode throughput of the whole step, per-kernel
 times (mean and p10/p50/p90), the HBM fraction of every kernel, the ALU
 roofline of the dominant kernel and the oracle's CPU throughput.
+--base-format int8 runs the same workload coded with the Int8 base format
+(the paper's alternative to Float8) instead of E4M3.
 """
 from __future__ import annotations
 
@@ -35,10 +37,18 @@ ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 # lane prefix count, word address, shift-or and select = 10) plus the use of
 # the symbol: BF16 output 1 (row-table address); GEMV 1 (byte pick and
 # conversion, per symbol pair) + B/2 (one dot2 per pair and batch row).
+# Int8 codes: one conversion per symbol and one pack per pair instead of the
+# byte pick and pair conversion (+0.5 per symbol).
 ALG_OPS = {"bf16": 11.0, "gemv1": 10.0 + 0.5 + 0.5 + 0.5, "gemv8": 10.0 + 0.5 + 0.5 + 4.0}
+ALG_OPS_INT8 = {"bf16": 11.0, "gemv1": 12.0, "gemv8": 15.5}
 # Kernel (function) name of each op family's decode launch on these shapes.
-KERNEL = {"bf16": "multi_decode_kernel<4, 1, 0, 1>", "gemv1": "decode_kernel<4, 2, true, 1, 1>",
-          "gemv8": "gemv_tiled_kernel<4, 8>"}
+# (template arguments: lanes / 64, op, [whole-row steps,] activation source,
+# batch, base format)
+KERNEL = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 1>",
+          "gemv1": "decode_kernel<4, 2, true, 1, 1, 1>", "gemv8": "gemv_tiled_kernel<4, 8, 1>"}
+KERNEL_INT8 = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 1>",
+               "gemv1": "decode_kernel<4, 2, true, 1, 1, 2>", "gemv8": "gemv_tiled_kernel<4, 8, 2>"}
+FORMATS = {"e4m3": 1, "int8": 2}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_config4.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2601_22787_amd", "csrc", "eq_decode.hip")
 
@@ -58,18 +68,20 @@ def parse():
                          "block-wise vs per-matrix, decode-GEMV B=1 and decode to BF16")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
+    ap.add_argument("--base-format", choices=tuple(FORMATS), default="e4m3",
+                    help="base format of the codes (c4 workload): E4M3 (default) or Int8")
     return ap.parse_args()
 
 
-def build_layers(eq, synth, specs, copies, dev):
+def build_layers(eq, synth, specs, copies, dev, fmt=1):
     """Encode each matrix once (product encoder), upload `copies` copies."""
     out = []
     for spec in specs:
         t0 = time.time()
         w = synth.weights(spec)
-        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
+        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512, base_format=fmt)
         blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
-                             seed=spec.seed, target_bits=spec.target_bits)
+                             seed=spec.seed, target_bits=spec.target_bits, base_format=fmt)
         layers = [eq.Layer(blob, dev) for _ in range(copies)]
         print(f"[bench] {spec.name} {spec.rows}x{spec.cols}: container {blob.size / 1e6:.1f} MB "
               f"built in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
@@ -98,7 +110,7 @@ def algorithmic_bytes(info, op, B):
     return cont + 2 * B * info["cols"] + 4 * B * info["rows"]
 
 
-def cpu_baseline(layers, target_s, threads):
+def cpu_baseline(layers, target_s, threads, fmt=1):
     """The oracle, as written, on a bounded sample: the first R rows of the
     8192x28672 matrix decoded from its container chunk by chunk, dequantised
     to BF16 and multiplied by one activation row in fp64.  Timed on one
@@ -125,7 +137,7 @@ def cpu_baseline(layers, target_s, threads):
             q[c * C:c * C + qc.size] = qc
 
         def rows(r0, r1):
-            w_hat = oracle.dequant(q[r0 * N:r1 * N].reshape(r1 - r0, N), scale[r0:r1])
+            w_hat = oracle.dequant(q[r0 * N:r1 * N].reshape(r1 - r0, N), scale[r0:r1], fmt)
             oracle.gemv(w_hat, x)
 
         if T == 1:
@@ -155,7 +167,7 @@ def cpu_baseline(layers, target_s, threads):
             "single_thread_sample": f"first {R1} rows, one thread, {t1:.1f}s"}
 
 
-def traffic_per_launch(op):
+def traffic_per_launch(op, fmt_name="e4m3"):
     """HBM bytes of one launch of `op`'s decode kernel, from the committed
     FETCH_SIZE / WRITE_SIZE counter summary, scaled by the counters' readings
     for a copy of known size; None if that summary was taken on another
@@ -167,9 +179,10 @@ def traffic_per_launch(op):
             sha = hashlib.sha256(f.read()).hexdigest()
     except OSError:
         return None
-    if t.get("source_sha256") != sha or op not in t.get("kernels", {}):
+    key = op if fmt_name == "e4m3" else f"{fmt_name}.{op}"
+    if t.get("source_sha256") != sha or key not in t.get("kernels", {}):
         return None
-    return t["kernels"][op]["hbm_bytes"]
+    return t["kernels"][key]["hbm_bytes"]
 
 
 def run_stack(args):
@@ -304,7 +317,10 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     specs = config_matrices(4)
-    layers = build_layers(eq, synth, specs, args.copies, dev)
+    fmt = FORMATS[args.base_format]
+    alg_ops = ALG_OPS if fmt == 1 else ALG_OPS_INT8
+    kernel_names = KERNEL if fmt == 1 else KERNEL_INT8
+    layers = build_layers(eq, synth, specs, args.copies, dev, fmt)
     ops = ["bf16", "gemv1", "gemv8"]
 
     # device buffers shared by all steps
@@ -398,7 +414,7 @@ def main():
         nbytes = sum(algorithmic_bytes(infos[m], op, B) for m in covered)
         comp = sum(infos[m]["file_bytes"] - 2 * (infos[m]["padded_words"] - infos[m]["total_words"])
                    for m in covered)
-        ops_alg = ALG_OPS[op] * params
+        ops_alg = alg_ops[op] * params
         tops = ops_alg / us / 1e6
         kernels[f"{name}.{op}"] = {
             "us": round(us, 2), "us_p10": round(q10, 2), "us_p50": round(q50, 2),
@@ -407,7 +423,7 @@ def main():
             "alg_bytes": nbytes, "gbs": round(nbytes / us / 1e3, 1),
             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
             "hbm_frac_compressed": round(comp / us / 1e3 / HBM_PEAK_GBS, 4),
-            "alg_ops_per_param": ALG_OPS[op], "tops": round(tops, 2),
+            "alg_ops_per_param": alg_ops[op], "tops": round(tops, 2),
             "alu_frac": round(tops / ALU_PEAK_TOPS, 4)}
         f = fam.setdefault(op, {"us": 0.0, "launches": 0, "bytes": 0, "ops": 0.0})
         f["us"] += us
@@ -432,17 +448,19 @@ def main():
         "value": round(value, 2), "unit": "Gparams/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
-        "config": {"workload": "Llama-70B MLP layers 8192x28672 + 28672x8192, E4M3 at ~2.0 "
+        "config": {"workload": f"Llama-70B MLP layers 8192x28672 + 28672x8192, "
+                               f"{args.base_format.upper()} at ~2.0 "
                                "bits/param, 65536-symbol chunks, 256 rANS lanes/chunk; per step: "
                                "both matrices decoded to BF16 by one block-wise launch, then "
                                "fused decode-GEMV B=1 and B=8 per matrix",
+                   "base_format": args.base_format,
                    "entropy_bits": [round(i["entropy"], 4) for i in infos],
                    "container_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos],
                    "copies_rotated": args.copies},
-        "roofline": {"bound": "alu", "kernel": KERNEL[dom], "op": dom,
+        "roofline": {"bound": "alu", "kernel": kernel_names[dom], "op": dom,
                      "achieved": round(achieved_tops, 2), "peak": round(ALU_PEAK_TOPS, 2),
                      "unit": "Tops/s", "frac": round(achieved_tops / ALU_PEAK_TOPS, 4),
-                     "traffic": traffic_per_launch(dom),
+                     "traffic": traffic_per_launch(dom, args.base_format),
                      "alg_bytes": round(dom_bytes), "us_per_launch": round(dom_us, 2),
                      "hbm": {"achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS,
                              "unit": "GB/s", "frac": round(achieved_gbs / HBM_PEAK_GBS, 4)}},
@@ -452,7 +470,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
-        result["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds, threads)
+        result["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds, threads, fmt)
     print(json.dumps(result), flush=True)
 
 

@@ -14,7 +14,8 @@
  *
  * Container (".eqc", one compressed layer; little-endian; every section
  * 256-byte aligned).  Header, 256 bytes:
- *   0 "EQC1"  4 version=1  8 header_bytes=256  12 base_format (1 = E4M3FN)
+ *   0 "EQC1"  4 version=1  8 header_bytes=256  12 base_format (1 = E4M3FN,
+ *   2 = Int8: the Float8 default and the Int8 alternative of Sec. 3.5)
  *   16 rows M  20 cols N  24 chunk_syms C  28 n_chunks = ceil(M*N/C)
  *   32 lanes W  36 prob_bits P  40 n_syms K  44 flags=0
  *   48 total_words (u64)  56 padded_words (u64)  64 seed (u64)
@@ -23,7 +24,9 @@
  *   chunk_state, words; 136 file_bytes (u64).
  * Sections:
  *   scale       u16[M]       BF16 bit patterns, one scale per output row
- *   sym         u8[K]        E4M3FN codes present, strictly ascending
+ *   sym         u8[K]        codes present, strictly ascending: E4M3FN bytes
+ *                            (never a NaN), or Int8 two's complement bytes in
+ *                            [-127, 127] (never 0x80)
  *   freq        u16[K]       frequencies, >= 1, summing to 2^P
  *   chunk_off   u32[n+1]     first stream word of each chunk; [n] = total_words
  *   chunk_state u32[n*W]     initial decoder state of every lane of every chunk
@@ -75,7 +78,7 @@ typedef struct eq_layer {
   uint32_t lanes;            /* W: 64, 128 or 256                                  */
   uint32_t prob_bits;        /* P: 1..12                                           */
   uint32_t n_syms;           /* K: 1..256                                          */
-  uint32_t reserved;
+  uint32_t base_format;      /* 1 = E4M3FN, 2 = Int8 (value v(q) of a code q)      */
   uint64_t total_words, padded_words;
   const uint16_t *scale;     /* device: the container's sections                   */
   const uint8_t *sym;
@@ -95,21 +98,24 @@ size_t eq_lut_bytes(void);
  * host copy is read only during the call.  `dev_lut` (eq_lut_bytes() bytes)
  * and `dev_status` (one int32) are device scratch owned by the caller and
  * tied to this layer.  Checks: magic/version/base format, sizes and
- * section bounds, ascending symbols, frequencies >= 1 summing to 2^P,
+ * section bounds, ascending symbols valid in the base format, frequencies
+ * >= 1 summing to 2^P,
  * monotone chunk offsets ending at total_words, padding >= 1024 words,
  * initial states in [2^16, 2^32), scales finite with magnitude in
- * [2^-117, 2^120) (so every dequantised product is exact in fp32).
+ * [2^-117, 2^120) (so every dequantised product s * v(q), an 8-bit by at
+ * most 7-bit significand product, is exact in fp32).
  * Returns EQ_OK, EQ_EINVAL or EQ_EFORMAT. */
 int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t blob_bytes, const void *dev_blob,
                   void *dev_lut, int32_t *dev_status);
 
 /* Build the layer's decode tables on the device (slot -> symbol/frequency/
- * offset, symbol -> E4M3 value; Sec. 2.2 metadata M) and clear its status
+ * offset, code -> value in the base format; Sec. 2.2 metadata M) and clear its status
  * word.  Must run (on the same stream, or be complete) before any decode. */
 int eq_layer_prepare(const eq_layer *L, hipStream_t stream);
 
-/* Alg. 2 lines 1-2: entropy-decode every chunk; codes[k] is the E4M3FN code of
- * element k of the row-major M x N matrix (M*N bytes, device). */
+/* Alg. 2 lines 1-2: entropy-decode every chunk; codes[k] is the code (E4M3FN
+ * or Int8 byte) of element k of the row-major M x N matrix (M*N bytes,
+ * device). */
 int eq_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t stream);
 
 /* Alg. 2 lines 1-2 plus the dequantiser of Sec. 2.1: w[i*N + j] =

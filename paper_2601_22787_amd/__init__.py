@@ -16,6 +16,7 @@ from ._build import LIB as _LIB_PATH
 from ._build import build as _build_lib
 
 EQ_OK, EQ_EINVAL, EQ_EFORMAT, EQ_EHIP, EQ_ECORRUPT = 0, -1, -2, -3, -4
+FMT_E4M3, FMT_INT8 = 1, 2  # base formats of the codes (container field base_format)
 
 _lib = None
 _vp = ctypes.c_void_p
@@ -31,7 +32,7 @@ class eq_layer(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_uint32), ("cols", ctypes.c_uint32),
                 ("chunk_syms", ctypes.c_uint32), ("n_chunks", ctypes.c_uint32),
                 ("lanes", ctypes.c_uint32), ("prob_bits", ctypes.c_uint32),
-                ("n_syms", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("n_syms", ctypes.c_uint32), ("base_format", ctypes.c_uint32),
                 ("total_words", ctypes.c_uint64), ("padded_words", ctypes.c_uint64),
                 ("scale", _vp), ("sym", _vp), ("freq", _vp), ("chunk_off", _vp),
                 ("chunk_state", _vp), ("words", _vp), ("lut", _vp), ("status", _vp)]
@@ -40,7 +41,8 @@ class eq_layer(ctypes.Structure):
 class eqe_params(ctypes.Structure):
     _fields_ = [("prob_bits", ctypes.c_uint32), ("chunk_syms", ctypes.c_uint32),
                 ("lanes", ctypes.c_uint32), ("threads", ctypes.c_uint32),
-                ("seed", ctypes.c_uint64), ("target_bits", ctypes.c_float)]
+                ("seed", ctypes.c_uint64), ("target_bits", ctypes.c_float),
+                ("base_format", ctypes.c_uint32)]
 
 
 # name -> (restype, argtypes): every symbol the public headers declare
@@ -61,7 +63,7 @@ SIGNATURES = {
     "eq_get_status": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp]),
     "eq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "eqe_alpha_search": (ctypes.c_float, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_double,
-                                          ctypes.c_uint32, ctypes.c_uint32,
+                                          ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                           ctypes.POINTER(ctypes.c_double)]),
     "eqe_encode": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float,
                                   ctypes.POINTER(eqe_params), ctypes.POINTER(ctypes.c_void_p),
@@ -238,21 +240,21 @@ def eq_get_status(L, stream=None) -> int:
 
 # ---------------------------------------------------------------- encoder ABI
 def eqe_alpha_search(w: np.ndarray, target_bits: float, sample_rows: int = 0,
-                     threads: int = 0):
+                     threads: int = 0, base_format: int = FMT_E4M3):
     w = np.ascontiguousarray(w, dtype=np.uint16)
     h = ctypes.c_double()
     a = lib().eqe_alpha_search(w.ctypes.data, w.shape[0], w.shape[1], target_bits, sample_rows,
-                               threads, ctypes.byref(h))
+                               threads, base_format, ctypes.byref(h))
     if a <= 0:
         raise EqError("eqe_alpha_search", EQ_EINVAL)
     return a, h.value
 
 
 def eqe_encode(w: np.ndarray, alpha: float, *, prob_bits: int = 12, chunk_syms: int,
-               lanes: int, threads: int = 0, seed: int = 0,
-               target_bits: float = 0.0) -> np.ndarray:
+               lanes: int, threads: int = 0, seed: int = 0, target_bits: float = 0.0,
+               base_format: int = FMT_E4M3) -> np.ndarray:
     w = np.ascontiguousarray(w, dtype=np.uint16)
-    prm = eqe_params(prob_bits, chunk_syms, lanes, threads, seed, target_bits)
+    prm = eqe_params(prob_bits, chunk_syms, lanes, threads, seed, target_bits, base_format)
     p = ctypes.c_void_p()
     nb = ctypes.c_uint64()
     rc = lib().eqe_encode(w.ctypes.data, w.shape[0], w.shape[1], alpha, ctypes.byref(prm),
@@ -287,6 +289,10 @@ class Layer:
     @property
     def cols(self) -> int:
         return self.raw.cols
+
+    @property
+    def base_format(self) -> int:
+        return self.raw.base_format
 
     def workspace(self, B: int):
         import torch

@@ -57,6 +57,7 @@ struct Args {
   float *y;
   float *ws;                    // row partials (uniform) or row sums (general shapes)
   const uint32_t *xp;           // activations in column-pair layout (tiled GEMV)
+  uint32_t fmt;                 // base format of the codes (kFmtE4M3 / kFmtInt8)
   uint32_t ncls;                // chunk classes sharing a start column (tiled GEMV)
   uint32_t tile_steps;          // steps per activation tile (tiled GEMV)
 };
@@ -149,6 +150,17 @@ __device__ inline uint32_t e4m3x2_to_bf16x2(uint32_t c) {
   return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c, 1.0f, false));
 }
 
+// BF16 pair of the values of the codes in bits 24..31 of two slot entries
+// (low half: lo's).  Exact: every E4M3 value and every integer in [-127,
+// 127] is a BF16 value.  E4M3: one byte permute and one hardware conversion.
+template <int FMT>
+__device__ inline uint32_t codes_to_bf16x2(uint32_t lo, uint32_t hi) {
+  if (FMT == kFmtInt8)
+    return pack_bf16(static_cast<float>(static_cast<int32_t>(lo) >> 24),
+                     static_cast<float>(static_cast<int32_t>(hi) >> 24));
+  return e4m3x2_to_bf16x2(__builtin_amdgcn_perm(hi, lo, 0x0c0c0703u));
+}
+
 // Value-table entry of the code in bits 24..31 of a slot entry.  Bits 13..23
 // of the entry are zero (f <= 2^12), so e >> 22 is already the byte offset.
 __device__ inline uint32_t code_value(const uint32_t *val_s, uint32_t e) {
@@ -164,11 +176,12 @@ __device__ inline uint4 load_words(const uint16_t *words, uint32_t i, uint32_t l
 // Decode tables.  Slot s of symbol k (cum_k <= s < cum_k + f_k):
 //   lut[2s]   = f_k | code_k << 24     (low 24 bits feed a 24-bit multiply-add)
 //   lut[2s+1] = s - cum_k
-// then lut[2 kMaxSlots + c] = fp32 bits of the E4M3 value of code c and
-// lut[2 kMaxSlots + 256 + c] = its BF16 bits (exact), zero-extended.
+// then lut[2 kMaxSlots + c] = fp32 bits of the value of code c in the base
+// format (E4M3FN, or Int8 two's complement) and lut[2 kMaxSlots + 256 + c] =
+// its BF16 bits (exact), zero-extended.
 __global__ __launch_bounds__(1024) void prepare_kernel(const uint8_t *sym, const uint16_t *freq,
-                                                       uint32_t K, uint32_t nslots, uint32_t *lut,
-                                                       int32_t *status) {
+                                                       uint32_t K, uint32_t nslots, uint32_t fmt,
+                                                       uint32_t *lut, int32_t *status) {
   __shared__ uint32_t cum_s[257];
   const uint32_t t = threadIdx.x;
   if (t == 0) {
@@ -191,7 +204,8 @@ __global__ __launch_bounds__(1024) void prepare_kernel(const uint8_t *sym, const
     lut[2 * s + 1] = s - cum_s[lo];
   }
   if (t < 256) {
-    const uint32_t bits = __float_as_uint(e4m3_value(t));
+    const float v = fmt == kFmtInt8 ? static_cast<float>(static_cast<int8_t>(t)) : e4m3_value(t);
+    const uint32_t bits = __float_as_uint(v);
     lut[2 * kMaxSlots + t] = bits;
     lut[2 * kMaxSlots + 256 + t] = bits >> 16;
   }
@@ -279,8 +293,10 @@ __device__ inline void stage_tables(const Args &a, DecodeLds &sm) {
 // (state g * 64 + lane); MODE selects what is done with each decoded symbol;
 // UNIFORM means every step of W symbols lies inside one matrix row (N is a
 // multiple of W); XS says where the GEMV reads activations; NB is the GEMV
-// batch when fixed at compile time (0: the runtime batch, up to 8).
-template <int G, int MODE, bool UNIFORM, int XS, int NB>
+// batch when fixed at compile time (0: the runtime batch, up to 8); FMT is
+// the base format of the codes where the GEMV converts them in registers
+// (PAIR); every other path reads the layer's value table.
+template <int G, int MODE, bool UNIFORM, int XS, int NB, int FMT = kFmtE4M3>
 struct Decoder {
   static constexpr uint32_t W = G * kWave;
   // GEMV on pairs of states (2q, 2q+1) of a lane: columns j and j + 64
@@ -413,14 +429,14 @@ struct Decoder {
   }
 
   // Row table of row r: bf16(s_r * v(code)) for every code, the exact
-  // product rounded once (NaN codes never occur in a valid container).
+  // product rounded once (codes outside the base format never occur in a
+  // valid container).  v comes from the fp32 value table.
   __device__ __forceinline__ void fill_rowtab(uint32_t r) {
     const float s = bf16_at(a.scale, r);
     const uint32_t c = 4 * lane;
-    const uint32_t lo = pack_bf16(s * __builtin_amdgcn_cvt_f32_fp8(c, 0),
-                                  s * __builtin_amdgcn_cvt_f32_fp8(c + 1, 0));
-    const uint32_t hi = pack_bf16(s * __builtin_amdgcn_cvt_f32_fp8(c + 2, 0),
-                                  s * __builtin_amdgcn_cvt_f32_fp8(c + 3, 0));
+    const uint32_t lo = pack_bf16(s * __uint_as_float(val[c]), s * __uint_as_float(val[c + 1]));
+    const uint32_t hi =
+        pack_bf16(s * __uint_as_float(val[c + 2]), s * __uint_as_float(val[c + 3]));
     reinterpret_cast<uint2 *>(rowtab)[lane] = make_uint2(lo, hi);
   }
 
@@ -491,11 +507,11 @@ struct Decoder {
 #pragma unroll
       for (int g = 0; g < G; g += 2) {
         const float s0 = bf16_at(a.scale, prow[g]);
-        const float v0 = s0 * __builtin_amdgcn_cvt_f32_fp8(e0[g], 3);
+        const float v0 = s0 * __uint_as_float(val[e0[g] >> 24]);
         float v1 = 0.0f;
         if (g + 1 < G) {
           const float s1 = bf16_at(a.scale, prow[g + 1]);
-          v1 = s1 * __builtin_amdgcn_cvt_f32_fp8(e0[g + 1], 3);
+          v1 = s1 * __uint_as_float(val[e0[g + 1] >> 24]);
         }
         const uint32_t h = pack_bf16(v0, v1);  // exact products, rounded once
         if (!TAIL || act[g])
@@ -518,8 +534,7 @@ struct Decoder {
       }
 #pragma unroll
       for (int q = 0; q < G / 2; ++q) {
-        const uint32_t w2 = e4m3x2_to_bf16x2(__builtin_amdgcn_perm(e0[2 * q + 1], e0[2 * q],
-                                                                  0x0c0c0703u));
+        const uint32_t w2 = codes_to_bf16x2<FMT>(e0[2 * q], e0[2 * q + 1]);
         if (NB == 1) {
           acc[0][0] = dot2_bf16(w2, xq[q * kWave], acc[0][0]);
         } else {
@@ -669,8 +684,7 @@ struct Decoder {
       okk[h] = kk;
     } else if (h & 1) {
       const int q = h / 2;
-      const uint32_t w2 =
-          e4m3x2_to_bf16x2(__builtin_amdgcn_perm(sym[h], sym[h - 1], 0x0c0c0703u));
+      const uint32_t w2 = codes_to_bf16x2<FMT>(sym[h - 1], sym[h]);
       if (NB == 1) {
         acc[0][0] = dot2_bf16(w2, xv1[q], acc[0][0]);
       } else {
@@ -783,7 +797,7 @@ struct Decoder {
 // One block's share of a layer: block blk of nblk decodes chunks blk * waves
 // + wave, + nblk * waves, ...  Dynamic LDS (dyn): the wavefronts' stream
 // windows, then the activations (kXLds) or the row tables.
-template <int G, int MODE, bool UNIFORM, int XS, int NB>
+template <int G, int MODE, bool UNIFORM, int XS, int NB, int FMT>
 __device__ __forceinline__ void decode_block(const Args &a, uint32_t blk, uint32_t nblk,
                                              DecodeLds &sm, uint4 *dyn) {
   const uint32_t nthreads = blockDim.x;
@@ -792,7 +806,7 @@ __device__ __forceinline__ void decode_block(const Args &a, uint32_t blk, uint32
   stage_tables<MODE>(a, sm);
   if (XS == kXLds) {
     const uint32_t nx = a.batch * a.cols;
-    if (Decoder<G, MODE, UNIFORM, XS, NB>::PAIR) {
+    if (Decoder<G, MODE, UNIFORM, XS, NB, FMT>::PAIR) {
       uint32_t *xp = reinterpret_cast<uint32_t *>(xl);
       const uint32_t np = pair_bytes(a.batch, a.cols) / sizeof(uint32_t);
       if (a.batch == 1 && (reinterpret_cast<uintptr_t>(a.x) & 7) == 0) {
@@ -820,16 +834,16 @@ __device__ __forceinline__ void decode_block(const Args &a, uint32_t blk, uint32
   }
   uint4 *const win = dyn + wave * (kWinBytes / sizeof(uint4));
   for (uint32_t c = uniform(blk * waves + wave); c < a.n_chunks; c += nblk * waves) {
-    Decoder<G, MODE, UNIFORM, XS, NB> d(a, c, lane, sm, win, rowtab, xl);
+    Decoder<G, MODE, UNIFORM, XS, NB, FMT> d(a, c, lane, sm, win, rowtab, xl);
     d.run();
   }
 }
 
-template <int G, int MODE, bool UNIFORM, int XS, int NB>
+template <int G, int MODE, bool UNIFORM, int XS, int NB, int FMT>
 __global__ __launch_bounds__(kMaxBlock) void decode_kernel(Args a) {
   extern __shared__ uint4 dyn[];
   __shared__ DecodeLds sm;
-  decode_block<G, MODE, UNIFORM, XS, NB>(a, blockIdx.x, gridDim.x, sm, dyn);
+  decode_block<G, MODE, UNIFORM, XS, NB, FMT>(a, blockIdx.x, gridDim.x, sm, dyn);
 }
 
 // Several layers in one launch (whole-row steps, one lane count): blocks
@@ -842,13 +856,13 @@ struct MultiArgs {
   uint32_t n;
 };
 
-template <int G, int MODE, int XS, int NB>
+template <int G, int MODE, int XS, int NB, int FMT>
 __global__ __launch_bounds__(kMaxBlock) void multi_decode_kernel(MultiArgs m) {
   extern __shared__ uint4 dyn[];
   __shared__ DecodeLds sm;
   uint32_t i = 0, b0 = 0;
   while (i + 1 < m.n && blockIdx.x >= m.blk_end[i]) b0 = m.blk_end[i++];
-  decode_block<G, MODE, true, XS, NB>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0, sm, dyn);
+  decode_block<G, MODE, true, XS, NB, FMT>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0, sm, dyn);
 }
 
 // Fused GEMV for activations too large for LDS (whole-row steps, W >= 128).
@@ -858,11 +872,11 @@ __global__ __launch_bounds__(kMaxBlock) void multi_decode_kernel(MultiArgs m) {
 // activations (from a.xp) into LDS, double-buffered, with one barrier per
 // tile.  Block b serves class b % ncls, chunks of index (b / ncls) * waves +
 // wave within the class.
-template <int G, int NB>
+template <int G, int NB, int FMT>
 __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
   extern __shared__ uint4 dyn[];  // stream windows, then 2 x tile
   __shared__ DecodeLds sm;
-  using Dec = Decoder<G, kGemv, true, kXTile, NB>;
+  using Dec = Decoder<G, kGemv, true, kXTile, NB, FMT>;
   constexpr uint32_t W = Dec::W;
   stage_tables<kGemv>(a, sm);
 
@@ -989,6 +1003,7 @@ Args make_args(const eq_layer *L) {
   a.prob_bits = L->prob_bits;
   a.padded_words = static_cast<uint32_t>(L->padded_words);
   a.n = L->rows * L->cols;
+  a.fmt = L->base_format;
   return a;
 }
 
@@ -996,7 +1011,7 @@ bool layer_ok(const eq_layer *L) {
   return L && L->lut && L->status && L->words && L->chunk_off && L->chunk_state && L->scale &&
          (L->lanes == 64 || L->lanes == 128 || L->lanes == 256) &&
          L->prob_bits >= kMinProbBits && L->prob_bits <= 12 && L->n_chunks > 0 && L->cols > 0 &&
-         L->rows > 0;
+         L->rows > 0 && (L->base_format == kFmtE4M3 || L->base_format == kFmtInt8);
 }
 
 constexpr size_t kStaticLds = sizeof(DecodeLds);
@@ -1072,7 +1087,15 @@ int gemv_xsrc(const Args &a, const DeviceFacts &f, uint32_t waves) {
   return kXGlobal;
 }
 
-template <int MODE, bool UNIFORM, int XS, int NB>
+// The base format a kernel is built for: only the in-register conversion of
+// the paired GEMV depends on it, every other path reads the layer's value
+// table, so those share the E4M3 build.
+template <int G, int MODE, bool UNIFORM, int XS, int NB, int FMT>
+constexpr int kernel_fmt() {
+  return Decoder<G, MODE, UNIFORM, XS, NB, kFmtE4M3>::PAIR ? FMT : int(kFmtE4M3);
+}
+
+template <int MODE, bool UNIFORM, int XS, int NB, int FMT>
 void launch_mode(const Args &a, hipStream_t s, const DeviceFacts &f) {
   dim3 grid, block;
   launch_shape(a.n_chunks, f.cus, grid, block);
@@ -1080,38 +1103,50 @@ void launch_mode(const Args &a, hipStream_t s, const DeviceFacts &f) {
                                     MODE == kBf16 && UNIFORM);
   switch (a.lanes) {
     case 64:
-      hipLaunchKernelGGL((decode_kernel<1, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
+      hipLaunchKernelGGL(
+          (decode_kernel<1, MODE, UNIFORM, XS, NB, kernel_fmt<1, MODE, UNIFORM, XS, NB, FMT>()>),
+          grid, block, shm, s, a);
       break;
     case 128:
-      hipLaunchKernelGGL((decode_kernel<2, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
+      hipLaunchKernelGGL(
+          (decode_kernel<2, MODE, UNIFORM, XS, NB, kernel_fmt<2, MODE, UNIFORM, XS, NB, FMT>()>),
+          grid, block, shm, s, a);
       break;
     default:
-      hipLaunchKernelGGL((decode_kernel<4, MODE, UNIFORM, XS, NB>), grid, block, shm, s, a);
+      hipLaunchKernelGGL(
+          (decode_kernel<4, MODE, UNIFORM, XS, NB, kernel_fmt<4, MODE, UNIFORM, XS, NB, FMT>()>),
+          grid, block, shm, s, a);
       break;
   }
 }
 
-template <int MODE, bool UNIFORM, int XS>
+template <int MODE, bool UNIFORM, int XS, int FMT>
 void launch_batch(const Args &a, hipStream_t s, const DeviceFacts &f) {
-  if (MODE != kGemv || a.batch == 1) launch_mode<MODE, UNIFORM, XS, 1>(a, s, f);
-  else if (a.batch == kMaxBatch) launch_mode<MODE, UNIFORM, XS, kMaxBatch>(a, s, f);
-  else launch_mode<MODE, UNIFORM, XS, 0>(a, s, f);
+  if (MODE != kGemv || a.batch == 1) launch_mode<MODE, UNIFORM, XS, 1, FMT>(a, s, f);
+  else if (a.batch == kMaxBatch) launch_mode<MODE, UNIFORM, XS, kMaxBatch, FMT>(a, s, f);
+  else launch_mode<MODE, UNIFORM, XS, 0, FMT>(a, s, f);
+}
+
+template <int MODE, int FMT>
+void launch_decode_fmt(const Args &a, hipStream_t s, const DeviceFacts &f) {
+  const bool uniform = a.cols % a.lanes == 0;
+  if (MODE != kGemv) {
+    if (uniform) launch_batch<MODE, true, kXGlobal, FMT>(a, s, f);
+    else launch_batch<MODE, false, kXGlobal, FMT>(a, s, f);
+  } else if (gemv_xsrc(a, f, launch_waves(a.n_chunks, f.cus)) == kXLds) {
+    if (uniform) launch_batch<MODE, true, kXLds, FMT>(a, s, f);
+    else launch_batch<MODE, false, kXLds, FMT>(a, s, f);
+  } else {
+    if (uniform) launch_batch<MODE, true, kXGlobal, FMT>(a, s, f);
+    else launch_batch<MODE, false, kXGlobal, FMT>(a, s, f);
+  }
 }
 
 template <int MODE>
 int launch_decode(const Args &a, hipStream_t s) {
   const DeviceFacts f = device_facts();
-  const bool uniform = a.cols % a.lanes == 0;
-  if (MODE != kGemv) {
-    if (uniform) launch_batch<MODE, true, kXGlobal>(a, s, f);
-    else launch_batch<MODE, false, kXGlobal>(a, s, f);
-  } else if (gemv_xsrc(a, f, launch_waves(a.n_chunks, f.cus)) == kXLds) {
-    if (uniform) launch_batch<MODE, true, kXLds>(a, s, f);
-    else launch_batch<MODE, false, kXLds>(a, s, f);
-  } else {
-    if (uniform) launch_batch<MODE, true, kXGlobal>(a, s, f);
-    else launch_batch<MODE, false, kXGlobal>(a, s, f);
-  }
+  if (MODE == kGemv && a.fmt == kFmtInt8) launch_decode_fmt<MODE, kFmtInt8>(a, s, f);
+  else launch_decode_fmt<MODE, kFmtE4M3>(a, s, f);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
@@ -1140,8 +1175,15 @@ int launch_tiled(Args a, hipStream_t s, const DeviceFacts &f) {
   a.tile_steps = T;
   const dim3 grid(a.ncls * ((per_cls + waves - 1) / waves)), block(waves * kWave);
   const size_t shm = dyn_lds_bytes(waves, 2 * size_t(T) * step_bytes, false);
-  if (W == 128) hipLaunchKernelGGL((gemv_tiled_kernel<2, NB>), grid, block, shm, s, a);
-  else hipLaunchKernelGGL((gemv_tiled_kernel<4, NB>), grid, block, shm, s, a);
+  const bool int8 = a.fmt == kFmtInt8;
+  if (W == 128 && int8)
+    hipLaunchKernelGGL((gemv_tiled_kernel<2, NB, kFmtInt8>), grid, block, shm, s, a);
+  else if (W == 128)
+    hipLaunchKernelGGL((gemv_tiled_kernel<2, NB, kFmtE4M3>), grid, block, shm, s, a);
+  else if (int8)
+    hipLaunchKernelGGL((gemv_tiled_kernel<4, NB, kFmtInt8>), grid, block, shm, s, a);
+  else
+    hipLaunchKernelGGL((gemv_tiled_kernel<4, NB, kFmtE4M3>), grid, block, shm, s, a);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
@@ -1163,30 +1205,47 @@ uint32_t multi_shape(const MultiArgs &m, int cus, MultiArgs &out) {
   return waves;
 }
 
-template <int MODE, int XS, int NB>
-int launch_multi(const MultiArgs &m0, size_t xbytes, hipStream_t s, const DeviceFacts &f) {
+template <int MODE, int XS, int NB, int FMT>
+int launch_multi_fmt(const MultiArgs &m0, size_t xbytes, hipStream_t s, const DeviceFacts &f) {
   MultiArgs m;
   const uint32_t waves = multi_shape(m0, f.cus, m);
   const dim3 grid(m.blk_end[m.n - 1]), block(waves * kWave);
   const size_t shm = dyn_lds_bytes(waves, xbytes, MODE == kBf16);
   switch (m.a[0].lanes) {
     case 64:
-      hipLaunchKernelGGL((multi_decode_kernel<1, MODE, XS, NB>), grid, block, shm, s, m);
+      hipLaunchKernelGGL(
+          (multi_decode_kernel<1, MODE, XS, NB, kernel_fmt<1, MODE, true, XS, NB, FMT>()>), grid,
+          block, shm, s, m);
       break;
     case 128:
-      hipLaunchKernelGGL((multi_decode_kernel<2, MODE, XS, NB>), grid, block, shm, s, m);
+      hipLaunchKernelGGL(
+          (multi_decode_kernel<2, MODE, XS, NB, kernel_fmt<2, MODE, true, XS, NB, FMT>()>), grid,
+          block, shm, s, m);
       break;
     default:
-      hipLaunchKernelGGL((multi_decode_kernel<4, MODE, XS, NB>), grid, block, shm, s, m);
+      hipLaunchKernelGGL(
+          (multi_decode_kernel<4, MODE, XS, NB, kernel_fmt<4, MODE, true, XS, NB, FMT>()>), grid,
+          block, shm, s, m);
       break;
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
-// Layers that can share one launch: whole-row steps, one lane count.
+// Layers of one launch share a base format (joint_ok).
+template <int MODE, int XS, int NB>
+int launch_multi(const MultiArgs &m, size_t xbytes, hipStream_t s, const DeviceFacts &f) {
+  if (MODE == kGemv && m.a[0].fmt == kFmtInt8)
+    return launch_multi_fmt<MODE, XS, NB, kFmtInt8>(m, xbytes, s, f);
+  return launch_multi_fmt<MODE, XS, NB, kFmtE4M3>(m, xbytes, s, f);
+}
+
+// Layers that can share one launch: whole-row steps, one lane count, one
+// base format.
 bool joint_ok(const eq_layer *const *L, uint32_t n) {
   for (uint32_t i = 0; i < n; ++i)
-    if (L[i]->cols % L[i]->lanes != 0 || L[i]->lanes != L[0]->lanes) return false;
+    if (L[i]->cols % L[i]->lanes != 0 || L[i]->lanes != L[0]->lanes ||
+        L[i]->base_format != L[0]->base_format)
+      return false;
   return true;
 }
 
@@ -1195,7 +1254,7 @@ bool joint_ok(const eq_layer *const *L, uint32_t n) {
 extern "C" int eq_layer_prepare(const eq_layer *L, hipStream_t stream) {
   if (!layer_ok(L) || !L->sym || !L->freq || L->n_syms < 1 || L->n_syms > 256) return EQ_EINVAL;
   hipLaunchKernelGGL(prepare_kernel, dim3(1), dim3(1024), 0, stream, L->sym, L->freq, L->n_syms,
-                     1u << L->prob_bits, L->lut, L->status);
+                     1u << L->prob_bits, L->base_format, L->lut, L->status);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 

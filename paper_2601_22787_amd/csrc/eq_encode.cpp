@@ -1,8 +1,9 @@
 // Host encoder for the compressed-layer container (declared in eq_encode.h).
 //
 // Alg. 1 of the paper (Sec. 2.2): AbsMax-based per-row scales (eq. absmax,
-// channel-wise as in Sec. 2.1), Float8 E4M3FN quantisation Q, row-major vec,
-// ANS entropy coding per chunk (App. A.1).  The coder is interleaved rANS
+// channel-wise as in Sec. 2.1), quantisation Q to the base format (Float8
+// E4M3FN, or Int8 as in the ablation of Sec. 3.5), row-major vec, ANS entropy
+// coding per chunk (App. A.1).  The coder is interleaved rANS
 // with a 32-bit state in [2^16, 2^32), 16-bit stream words and W lanes per
 // chunk; symbol k of a chunk is coded by lane k mod W at step k div W.
 #include "eq_encode.h"
@@ -88,22 +89,29 @@ uint8_t quantize_e4m3(float v) {
   return static_cast<uint8_t>(mag | (std::signbit(v) ? 0x80u : 0u));
 }
 
-struct Quantized {
-  std::vector<uint16_t> scale;
-  std::vector<uint8_t> codes;
-  uint64_t hist[256] = {};
-};
+// Int8 code of v: clamp to [-127, 127] (symmetric, so 0x80 never occurs),
+// then the nearest integer with ties to even (the default rounding mode).
+uint8_t quantize_int8(float v) {
+  const float c = std::min(127.0f, std::max(-127.0f, v));
+  return static_cast<uint8_t>(static_cast<int8_t>(std::nearbyint(c)));
+}
 
-uint16_t row_scale(const uint16_t *row, uint32_t N, float alpha) {
+constexpr uint32_t kFmtE4M3 = 1, kFmtInt8 = 2;
+
+double qmax(uint32_t fmt) { return fmt == kFmtInt8 ? 127.0 : 448.0; }
+
+uint16_t row_scale(const uint16_t *row, uint32_t N, float alpha, uint32_t fmt) {
   float amax = 0.0f;
   for (uint32_t j = 0; j < N; ++j) amax = std::max(amax, std::fabs(bf16_to_float(row[j])));
   if (amax == 0.0f) return 0x3F80;
-  return double_to_bf16(static_cast<double>(alpha) * static_cast<double>(amax) / 448.0);
+  return double_to_bf16(static_cast<double>(alpha) * static_cast<double>(amax) / qmax(fmt));
 }
 
 // Quantise the listed rows; codes are written only if `codes` is non-null.
-void quantize_rows(const uint16_t *w, uint32_t N, float alpha, const std::vector<uint32_t> &rows,
-                   unsigned threads, uint16_t *scale, uint8_t *codes, uint64_t hist[256]) {
+void quantize_rows(const uint16_t *w, uint32_t N, float alpha, uint32_t fmt,
+                   const std::vector<uint32_t> &rows, unsigned threads, uint16_t *scale,
+                   uint8_t *codes, uint64_t hist[256]) {
+  uint8_t (*const quantize)(float) = fmt == kFmtInt8 ? quantize_int8 : quantize_e4m3;
   const uint64_t n_rows = rows.size();
   const uint64_t per = 16;  // rows per task
   const uint64_t tasks = (n_rows + per - 1) / per;
@@ -113,12 +121,12 @@ void quantize_rows(const uint16_t *w, uint32_t N, float alpha, const std::vector
     for (uint64_t r = t * per; r < std::min(n_rows, (t + 1) * per); ++r) {
       const uint32_t i = rows[r];
       const uint16_t *src = w + static_cast<uint64_t>(i) * N;
-      uint16_t s = row_scale(src, N, alpha);
+      uint16_t s = row_scale(src, N, alpha, fmt);
       if (scale) scale[i] = s;
       const float sf = bf16_to_float(s);
       uint8_t *dst = codes ? codes + static_cast<uint64_t>(i) * N : nullptr;
       for (uint32_t j = 0; j < N; ++j) {
-        uint8_t q = quantize_e4m3(bf16_to_float(src[j]) / sf);
+        uint8_t q = quantize(bf16_to_float(src[j]) / sf);
         ++h[q];
         if (dst) dst[j] = q;
       }
@@ -235,8 +243,10 @@ uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
 }  // namespace
 
 extern "C" float eqe_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, double target_bits,
-                                  uint32_t sample_rows, uint32_t threads, double *h_out) {
-  if (!w || !M || !N) return -1.0f;
+                                  uint32_t sample_rows, uint32_t threads, uint32_t base_format,
+                                  double *h_out) {
+  if (base_format == 0) base_format = kFmtE4M3;
+  if (!w || !M || !N || (base_format != kFmtE4M3 && base_format != kFmtInt8)) return -1.0f;
   std::vector<uint32_t> rows;
   if (sample_rows && sample_rows < M) {
     for (uint32_t r = 0; r < sample_rows; ++r)
@@ -251,7 +261,7 @@ extern "C" float eqe_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, dou
     const double mid = 0.5 * (lo + hi);
     const float alpha = static_cast<float>(std::exp2(mid));
     uint64_t hist[256];
-    quantize_rows(w, N, alpha, rows, nt, nullptr, nullptr, hist);
+    quantize_rows(w, N, alpha, base_format, rows, nt, nullptr, nullptr, hist);
     const double h = entropy_bits(hist);
     if (std::fabs(h - target_bits) < best_err) {
       best_err = std::fabs(h - target_bits);
@@ -269,8 +279,9 @@ extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha
   if (!w || !p || !blob_out || !bytes_out || !M || !N) return -1;
   const uint64_t n = static_cast<uint64_t>(M) * N;
   const uint32_t W = p->lanes, C = p->chunk_syms, P = p->prob_bits;
+  const uint32_t fmt = p->base_format ? p->base_format : kFmtE4M3;
   if (n >= (uint64_t(1) << 32) || (W != 64 && W != 128 && W != 256) || C == 0 || C % W ||
-      P < 1 || P > 12 || !(alpha > 0.0f))
+      P < 1 || P > 12 || !(alpha > 0.0f) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
     return -1;
   const unsigned nt = worker_count(p->threads);
   try {
@@ -279,7 +290,7 @@ extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha
     std::vector<uint32_t> rows(M);
     for (uint32_t i = 0; i < M; ++i) rows[i] = i;
     uint64_t hist[256];
-    quantize_rows(w, N, alpha, rows, nt, scale.data(), codes.data(), hist);
+    quantize_rows(w, N, alpha, fmt, rows, nt, scale.data(), codes.data(), hist);
 
     std::vector<uint8_t> sym;
     std::vector<uint16_t> freq;
@@ -321,7 +332,7 @@ extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha
     std::memcpy(b, "EQC1", 4);
     put<uint32_t>(b, 4, 1);                  // version
     put<uint32_t>(b, 8, kHeaderBytes);
-    put<uint32_t>(b, 12, 1);                 // base format: E4M3FN
+    put<uint32_t>(b, 12, fmt);               // base format: 1 E4M3FN, 2 Int8
     put<uint32_t>(b, 16, M);
     put<uint32_t>(b, 20, N);
     put<uint32_t>(b, 24, C);

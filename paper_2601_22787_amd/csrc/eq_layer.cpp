@@ -20,7 +20,8 @@ bool section_ok(uint64_t off, uint64_t len, uint64_t file_bytes) {
 }
 
 // BF16 scale usable by the dequantiser: finite, normal, 2^-117 <= |s| < 2^120,
-// so s * v(q) is an exact fp32 product for every E4M3 value v(q).
+// so s * v(q) is an exact, normal fp32 product for every E4M3 value and every
+// Int8 value v(q).
 bool scale_ok(uint16_t s) {
   const int e = (s >> 7) & 0xFF;
   return e >= 127 - 117 && e <= 127 + 119;
@@ -35,7 +36,9 @@ extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
   if (!L || !host_blob || !dev_blob || !dev_lut || !dev_status) return EQ_EINVAL;
   const uint8_t *b = static_cast<const uint8_t *>(host_blob);
   if (bytes < 256 || std::memcmp(b, "EQC1", 4) != 0) return EQ_EFORMAT;
-  if (rd<uint32_t>(b, 4) != 1 || rd<uint32_t>(b, 8) != 256 || rd<uint32_t>(b, 12) != 1)
+  const uint32_t fmt = rd<uint32_t>(b, 12);
+  if (rd<uint32_t>(b, 4) != 1 || rd<uint32_t>(b, 8) != 256 ||
+      (fmt != eq_detail::kFmtE4M3 && fmt != eq_detail::kFmtInt8))
     return EQ_EFORMAT;
   const uint32_t M = rd<uint32_t>(b, 16), N = rd<uint32_t>(b, 20), C = rd<uint32_t>(b, 24);
   const uint32_t n_chunks = rd<uint32_t>(b, 28), W = rd<uint32_t>(b, 32);
@@ -65,7 +68,8 @@ extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
   uint32_t fsum = 0;
   for (uint32_t k = 0; k < K; ++k) {
     const uint8_t s = b[o_sym + k];
-    if ((s & 0x7F) == 0x7F) return EQ_EFORMAT;          // NaN code
+    if (fmt == eq_detail::kFmtE4M3 ? (s & 0x7F) == 0x7F : s == 0x80)
+      return EQ_EFORMAT;                                // E4M3 NaN / Int8 -128
     if (k && s <= b[o_sym + k - 1]) return EQ_EFORMAT;  // strictly ascending
     const uint16_t f = rd<uint16_t>(b, o_freq + 2ull * k);
     if (f == 0) return EQ_EFORMAT;
@@ -94,6 +98,7 @@ extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
   v.lanes = W;
   v.prob_bits = P;
   v.n_syms = K;
+  v.base_format = fmt;
   v.total_words = total;
   v.padded_words = padded;
   v.scale = reinterpret_cast<const uint16_t *>(d + o_scale);

@@ -79,7 +79,7 @@ def test_layer_init_rejects_bad_containers(blob):
     bad = {
         "magic": _patch(blob, 0, 0x31435158, np.uint32),
         "version": _patch(blob, 4, 2, np.uint32),
-        "format": _patch(blob, 12, 2, np.uint32),
+        "format": _patch(blob, 12, 3, np.uint32),
         "lanes": _patch(blob, 32, 96, np.uint32),
         "chunks": _patch(blob, 28, info.n_chunks + 1, np.uint32),
         "prob_bits_small": _patch(blob, 36, 7, np.uint32),
@@ -99,6 +99,26 @@ def test_layer_init_rejects_bad_containers(blob):
     assert rc == eq.EQ_EFORMAT
     L = eq.eq_layer()
     assert eq.lib().eq_layer_init(ctypes.byref(L), None, 0, None, None, None) == eq.EQ_EINVAL
+
+
+def test_layer_init_base_formats(blob):
+    """Int8 containers validate and report their format; a symbol outside the
+    base format (E4M3 NaN, Int8 -128) is rejected."""
+    w = synth.weights(small_spec(24, 256, seed=8))
+    b8 = eq.eqe_encode(w, 20.0, chunk_syms=1024, lanes=64, base_format=eq.FMT_INT8)
+    rc, L = _init(b8)
+    assert rc == eq.EQ_OK and L.base_format == eq.FMT_INT8
+    rc, L = _init(blob)
+    assert rc == eq.EQ_OK and L.base_format == eq.FMT_E4M3
+    # the first negative code (sign bit set) can be lowered to 0x80 (Int8) or
+    # to 0x7F (E4M3) without breaking the ascending order
+    for cont, bad_code in ((b8, 0x80), (blob, 0x7F)):
+        info = oracle.container_info(cont)
+        syms = cont[info.off_sym:info.off_sym + info.n_syms]
+        k = int(np.argmax(syms >= 0x80))
+        assert syms[k] > bad_code and (k == 0 or syms[k - 1] < bad_code)
+        rc, _ = _init(_patch(cont, info.off_sym + k, bad_code, np.uint8))
+        assert rc == eq.EQ_EFORMAT
 
 
 def test_workspace_size_and_argument_checks(blob):

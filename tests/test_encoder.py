@@ -31,6 +31,26 @@ def test_small_containers_identical_to_oracle(M, N, C, lanes, alpha, outliers):
     assert (a == b).all()
 
 
+@pytest.mark.parametrize("M,N,C,lanes,alpha,outliers", [
+    (5, 77, 128, 64, 3.0, False), (33, 1000, 1024, 256, 40.0, False),
+    (64, 256, 4096, 128, 0.5, True), (9, 4160, 8192, 256, 9.0, True)])
+def test_int8_containers_identical_to_oracle(M, N, C, lanes, alpha, outliers):
+    w = synth.weights(small_spec(M, N, seed=3 * M + N, outliers=outliers))
+    a = eq.eqe_encode(w, alpha, chunk_syms=C, lanes=lanes, threads=3, base_format=eq.FMT_INT8)
+    b = oracle.container_build(w, alpha, 12, C, lanes, fmt=oracle.INT8)
+    assert (a == b).all()
+    assert oracle.container_info(a).base_format == oracle.INT8
+
+
+@pytest.mark.parametrize("bits", [2.0, 4.0])
+def test_int8_alpha_search_hits_target(c1_weights, bits):
+    spec, w = c1_weights
+    alpha, h = eq.eqe_alpha_search(w, bits, base_format=eq.FMT_INT8)
+    assert abs(h - bits) <= 0.05
+    q = oracle.quantize(w, oracle.row_scales(w, alpha, oracle.INT8), oracle.INT8)
+    assert oracle.entropy_codes(q) == pytest.approx(h, abs=1e-9)
+
+
 def test_zero_matrix_and_thread_independence():
     w = np.zeros((8, 128), dtype=np.uint16)
     assert (eq.eqe_encode(w, 1.0, chunk_syms=256, lanes=64) ==
@@ -49,6 +69,8 @@ def test_rejects_bad_arguments():
             eq.eqe_encode(w, 1.0, **kw)
     with pytest.raises(eq.EqError):
         eq.eqe_encode(w, -1.0, chunk_syms=256, lanes=64)
+    with pytest.raises(eq.EqError):
+        eq.eqe_encode(w, 1.0, chunk_syms=256, lanes=64, base_format=3)
 
 
 @pytest.mark.parametrize("bits", [2.0, 3.0, 4.0])

@@ -53,6 +53,49 @@ float eqe_alpha_search(const uint16_t *w_bf16, uint32_t M, uint32_t N, double ta
 int eqe_encode(const uint16_t *w_bf16, uint32_t M, uint32_t N, float alpha,
                const eqe_params *params, uint8_t **blob, uint64_t *blob_bytes);
 
+/* Encode w with the given per-row scales (BF16 bit patterns, M of them,
+ * each positive and within [2^-117, 2^120)) instead of alpha * AbsMax, e.g.
+ * the result of eqe_rd_scales.  Same outputs and return codes as eqe_encode
+ * (-1 also for an unusable scale); the header's alpha field is 0. */
+int eqe_encode_scaled(const uint16_t *w_bf16, uint32_t M, uint32_t N, const uint16_t *scale_bf16,
+                      const eqe_params *params, uint8_t **blob, uint64_t *blob_bytes);
+
+/* ---- scale optimisation: Sec. 2.2, eq. optimization (Alg. 1 line 2) ----
+ * F(S) = ||W - S W_q||_1 / ||W||_1 + lambda * ||W_q||_1 / (M N),  W_q = Q(W / S),
+ * minimised over the per-row scales S from the AbsMax start (eq. absmax)
+ * with L-BFGS and the straight-through estimator for Q's rounding. */
+typedef struct eqe_rd_params {
+  double lambda;        /* regularisation weight (>= 0)                              */
+  double lr;            /* L-BFGS step length; <= 0: 0.25 if lambda > 30, else 1.0  */
+  uint32_t iters;       /* L-BFGS iterations; 0: 200                                 */
+  uint32_t history;     /* L-BFGS curvature pairs kept; 0: 20                        */
+  uint32_t threads;     /* 0: one per online CPU, at most 16                         */
+  uint32_t base_format; /* 1 = E4M3FN (0 is read as 1), 2 = Int8                     */
+} eqe_rd_params;
+
+/* F at the scales `scale` (M positive doubles); *grad (optional, M doubles)
+ * receives the straight-through gradient (dQ/du = 1 inside [-Qmax, Qmax], 0
+ * where the clamp is active) and *distortion (optional) the first term.
+ * Returns NaN on bad arguments. */
+double eqe_rd_objective(const uint16_t *w_bf16, uint32_t M, uint32_t N, uint32_t base_format,
+                        double lambda, const double *scale, uint32_t threads, double *grad,
+                        double *distortion);
+
+/* Optimise the scales; outputs (each optional): the scales as doubles, the
+ * same rounded to BF16 (nearest, ties to even) for eqe_encode_scaled, and
+ * the lowest F reached.  Returns 0, -1 (bad arguments) or -5 (memory). */
+int eqe_rd_scales(const uint16_t *w_bf16, uint32_t M, uint32_t N, const eqe_rd_params *params,
+                  double *scale, uint16_t *scale_bf16, double *objective);
+
+/* lambda whose optimised BF16 scales give codes with empirical entropy
+ * (eq. emp_entropy) closest to target_bits: bisection on log2(lambda) over
+ * [-8, 16] (18 steps), optimising and measuring on sample_rows evenly spaced
+ * rows (all rows if 0 or >= M); params->lambda is ignored.  Returns 0 and
+ * writes *lambda and *h (entropy on the rows searched), or -1 / -5. */
+int eqe_rd_lambda_search(const uint16_t *w_bf16, uint32_t M, uint32_t N, double target_bits,
+                         uint32_t sample_rows, const eqe_rd_params *params, double *lambda,
+                         double *h);
+
 void eqe_free(void *p);
 
 #ifdef __cplusplus

@@ -89,6 +89,21 @@ def lib():
                                                   ctypes.POINTER(ctypes.c_void_p),
                                                   ctypes.POINTER(ctypes.c_uint64)]),
             "or_free": (None, [_vp]),
+            "or_container_build_scaled": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                                         _vp, ctypes.c_uint32, ctypes.c_uint32,
+                                                         ctypes.c_uint32, ctypes.c_uint32,
+                                                         ctypes.c_uint64, ctypes.c_float,
+                                                         ctypes.POINTER(ctypes.c_void_p),
+                                                         ctypes.POINTER(ctypes.c_uint64)]),
+            "or_rd_objective": (ctypes.c_double, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                                  ctypes.c_uint32, ctypes.c_double, _vp, _vp,
+                                                  _vp]),
+            "or_rd_scales": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                            ctypes.c_uint32, ctypes.c_double, ctypes.c_uint32,
+                                            ctypes.c_uint32, ctypes.c_double, _vp, _vp]),
+            "or_lbfgs_quadratic": (ctypes.c_int, [ctypes.c_uint32, _vp, ctypes.c_double, _vp,
+                                                  ctypes.c_uint32, ctypes.c_uint32,
+                                                  ctypes.c_double, _vp, _vp]),
             "or_container_info": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.POINTER(Info)]),
             "or_container_decode_chunk": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.c_uint32,
                                                          _vp]),
@@ -250,6 +265,65 @@ def container_build(w: np.ndarray, alpha: float, P: int, chunk_syms: int, lanes:
     finally:
         lib().or_free(p)
     return out
+
+
+def container_build_scaled(w: np.ndarray, scale: np.ndarray, P: int, chunk_syms: int,
+                           lanes: int, seed: int = 0, target_bits: float = 0.0,
+                           fmt: int = E4M3) -> np.ndarray:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    scale = np.ascontiguousarray(scale, dtype=np.uint16)
+    M, N = w.shape
+    p = ctypes.c_void_p()
+    nb = ctypes.c_uint64()
+    rc = lib().or_container_build_scaled(_ptr(w), M, N, _ptr(scale), fmt, P, chunk_syms, lanes,
+                                         seed, target_bits, ctypes.byref(p), ctypes.byref(nb))
+    if rc != OK:
+        raise ValueError(f"or_container_build_scaled: {rc}")
+    try:
+        out = np.frombuffer(ctypes.string_at(p.value, nb.value), dtype=np.uint8).copy()
+    finally:
+        lib().or_free(p)
+    return out
+
+
+# ---- scale optimisation (Sec. 2.2 eq. optimization) ----
+def rd_objective(w: np.ndarray, scale: np.ndarray, lam: float, fmt: int = E4M3):
+    """(F, straight-through gradient, distortion term)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    s = np.ascontiguousarray(scale, dtype=np.float64)
+    M, N = w.shape
+    g = np.empty(M, dtype=np.float64)
+    d = ctypes.c_double()
+    f = lib().or_rd_objective(_ptr(w), M, N, fmt, lam, _ptr(s), _ptr(g), ctypes.byref(d))
+    return f, g, d.value
+
+
+def rd_scales(w: np.ndarray, lam: float, iters: int = 200, history: int = 20, lr: float = 0.0,
+              fmt: int = E4M3):
+    """(scales, lowest F); lr <= 0: 0.25 if lam > 30 else 1.0 (App. A.1)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M, N = w.shape
+    if lr <= 0:
+        lr = 0.25 if lam > 30 else 1.0
+    s = np.empty(M, dtype=np.float64)
+    f = ctypes.c_double()
+    rc = lib().or_rd_scales(_ptr(w), M, N, fmt, lam, iters, history, lr, _ptr(s), ctypes.byref(f))
+    if rc != OK:
+        raise ValueError(f"or_rd_scales: {rc}")
+    return s, f.value
+
+
+def lbfgs_quadratic(a: np.ndarray, b: float, c: np.ndarray, x0: np.ndarray, iters: int,
+                    history: int = 20, lr: float = 1.0):
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    c = np.ascontiguousarray(c, dtype=np.float64)
+    x = np.ascontiguousarray(x0, dtype=np.float64).copy()
+    f = ctypes.c_double()
+    rc = lib().or_lbfgs_quadratic(a.size, _ptr(a), b, _ptr(c), iters, history, lr, _ptr(x),
+                                  ctypes.byref(f))
+    if rc != OK:
+        raise ValueError(f"or_lbfgs_quadratic: {rc}")
+    return x, f.value
 
 
 def container_info(blob: np.ndarray) -> Info:

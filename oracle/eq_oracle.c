@@ -462,10 +462,12 @@ static uint64_t align256(uint64_t v) { return (v + 255) & ~(uint64_t)255; }
  * little past the end of any chunk without leaving the section. */
 static uint64_t padded_words_for(uint64_t total) { return (total + 1024 + 127) & ~(uint64_t)127; }
 
-/* Alg. 1: scales, Q (base format fmt), vec (row-major), ANS encode per chunk. */
-int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
-                       uint32_t P, uint32_t chunk_syms, uint32_t lanes, uint64_t seed,
-                       float target_bits, uint8_t **blob_out, uint64_t *blob_bytes) {
+/* Alg. 1: scales (alpha * AbsMax, or the given ones), Q (base format fmt),
+ * vec (row-major), ANS encode per chunk. */
+static int container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
+                           const uint16_t *given, uint32_t fmt, uint32_t P, uint32_t chunk_syms,
+                           uint32_t lanes, uint64_t seed, float target_bits, uint8_t **blob_out,
+                           uint64_t *blob_bytes) {
   if (!w || M == 0 || N == 0 || P < 1 || P > 12 || lanes == 0 || lanes % 64 != 0 ||
       chunk_syms == 0 || chunk_syms % lanes != 0 || (fmt != OR_FMT_E4M3 && fmt != OR_FMT_INT8))
     return OR_EINVAL;
@@ -483,7 +485,8 @@ int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, u
     rc = OR_ENOMEM;
     goto done;
   }
-  or_row_scales(w, M, N, alpha, fmt, scale);
+  if (given) memcpy(scale, given, sizeof(uint16_t) * M);
+  else or_row_scales(w, M, N, alpha, fmt, scale);
   or_quantize(w, M, N, scale, fmt, q);
   uint64_t counts[256] = {0};
   for (uint64_t k = 0; k < n; ++k) counts[q[k]]++;
@@ -533,7 +536,7 @@ int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, u
   put64(b, H_TOTAL_WORDS, total);
   put64(b, H_PADDED_WORDS, padded);
   put64(b, H_SEED, seed);
-  putf(b, H_ALPHA, alpha);
+  putf(b, H_ALPHA, given ? 0.0f : alpha);
   putf(b, H_TARGET, target_bits);
   putf(b, H_ENTROPY, (float)or_entropy_counts(counts, 256));
   put64(b, H_OFF_SCALE, o_scale);
@@ -567,6 +570,22 @@ done:
   free(chunk_off);
   free(states);
   return rc;
+}
+
+int or_container_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha, uint32_t fmt,
+                       uint32_t P, uint32_t chunk_syms, uint32_t lanes, uint64_t seed,
+                       float target_bits, uint8_t **blob_out, uint64_t *blob_bytes) {
+  return container_build(w, M, N, alpha, NULL, fmt, P, chunk_syms, lanes, seed, target_bits,
+                         blob_out, blob_bytes);
+}
+
+int or_container_build_scaled(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale,
+                              uint32_t fmt, uint32_t P, uint32_t chunk_syms, uint32_t lanes,
+                              uint64_t seed, float target_bits, uint8_t **blob_out,
+                              uint64_t *blob_bytes) {
+  if (!scale) return OR_EINVAL;
+  return container_build(w, M, N, 0.0f, scale, fmt, P, chunk_syms, lanes, seed, target_bits,
+                         blob_out, blob_bytes);
 }
 
 void or_free(void *p) { free(p); }
@@ -659,6 +678,196 @@ int or_container_decode(const uint8_t *b, uint64_t bytes, uint8_t *q) {
     if (rc != OR_OK && worst == OR_OK) worst = rc;
   }
   return worst;
+}
+
+/* ------------------------------------------------------------------ */
+/* Scale optimisation, Sec. 2.2 eq. optimization (Alg. 1 line 2)        */
+/* ------------------------------------------------------------------ */
+
+static double sign_of(double v) { return v > 0.0 ? 1.0 : (v < 0.0 ? -1.0 : 0.0); }
+
+/* d(W, W_hat) = ||W - W_hat||_1 / ||W||_1 (relative entry-wise l1 loss) plus
+ * lambda R(W_q) with R the entry-wise l1 norm of the quantised values per
+ * entry.  W_hat = s_i * W_q with s_i unrounded.  Straight-through estimator
+ * for the rounding of Q: d W_q / d s_i = -W / s_i^2 where |W/s_i| <= Qmax
+ * (0 where the clamp acts), so d W_hat / d s_i = W_q + s_i d W_q / d s_i. */
+double or_rd_objective(const uint16_t *w, uint32_t M, uint32_t N, uint32_t fmt, double lambda,
+                       const double *s, double *grad, double *dist) {
+  double wl1 = 0.0;
+  for (uint64_t k = 0; k < (uint64_t)M * N; ++k) wl1 += fabs(or_bf16_value(w[k]));
+  double qmax = or_qmax(fmt), dsum = 0.0, rsum = 0.0, mn = (double)M * (double)N;
+  for (uint32_t i = 0; i < M; ++i) {
+    double gd = 0.0, gr = 0.0;
+    for (uint32_t j = 0; j < N; ++j) {
+      double wv = or_bf16_value(w[(uint64_t)i * N + j]);
+      float u = (float)wv / (float)s[i];
+      double v = or_code_value(fmt, round_to_format(fmt, u));
+      double diff = s[i] * v - wv;
+      dsum += fabs(diff);
+      rsum += fabs(v);
+      double dv = (fabs((double)u) <= qmax) ? -wv / (s[i] * s[i]) : 0.0;
+      gd += sign_of(diff) * (v + s[i] * dv);
+      gr += sign_of(v) * dv;
+    }
+    if (grad) grad[i] = (wl1 > 0.0 ? gd / wl1 : 0.0) + lambda * gr / mn;
+  }
+  double d = wl1 > 0.0 ? dsum / wl1 : 0.0;
+  if (dist) *dist = d;
+  return d + lambda * rsum / mn;
+}
+
+static double vdot(const double *a, const double *b, uint32_t n) {
+  double t = 0.0;
+  for (uint32_t i = 0; i < n; ++i) t += a[i] * b[i];
+  return t;
+}
+
+/* L-BFGS (Liu and Nocedal 1989), fixed step length lr.  Direction: the
+ * two-loop recursion over the newest `history` pairs (s_k = x_{k+1} - x_k,
+ * y_k = g_{k+1} - g_k, kept only if y_k.s_k > 1e-10) with initial matrix
+ * (s.y / y.y) I from the newest pair; the first step is lr min(1, 1/|g|_1)
+ * along -g.  Stops after `iters` steps, when |g|_inf <= 1e-12, or when f
+ * changes by less than 1e-10; the iterate with the lowest f is returned. */
+int or_lbfgs(uint32_t n, double *x, or_fg_fn fg, void *ctx, const double *lower, uint32_t iters,
+             uint32_t history, double lr, double *f_out) {
+  if (n == 0 || history == 0) return OR_EINVAL;
+  double *g = malloc(sizeof(double) * n), *gn = malloc(sizeof(double) * n);
+  double *xn = malloc(sizeof(double) * n), *q = malloc(sizeof(double) * n);
+  double *best = malloc(sizeof(double) * n), *alpha = malloc(sizeof(double) * history);
+  double *S = malloc(sizeof(double) * n * history), *Y = malloc(sizeof(double) * n * history);
+  double *rho = malloc(sizeof(double) * history);
+  int rc = OR_OK;
+  if (!g || !gn || !xn || !q || !best || !alpha || !S || !Y || !rho) {
+    rc = OR_ENOMEM;
+    goto out;
+  }
+  double f = fg(x, g, ctx), fbest = f;
+  memcpy(best, x, sizeof(double) * n);
+  uint32_t k = 0; /* pairs stored, oldest first: pair a at S + a n */
+  for (uint32_t it = 0; it < iters; ++it) {
+    double ginf = 0.0, g1 = 0.0;
+    for (uint32_t i = 0; i < n; ++i) {
+      if (fabs(g[i]) > ginf) ginf = fabs(g[i]);
+      g1 += fabs(g[i]);
+    }
+    if (ginf <= 1e-12) break;
+    memcpy(q, g, sizeof(double) * n);
+    for (uint32_t a = k; a-- > 0;) {
+      alpha[a] = rho[a] * vdot(S + (uint64_t)a * n, q, n);
+      for (uint32_t i = 0; i < n; ++i) q[i] -= alpha[a] * Y[(uint64_t)a * n + i];
+    }
+    double gamma = 1.0;
+    if (k) {
+      const double *sl = S + (uint64_t)(k - 1) * n, *yl = Y + (uint64_t)(k - 1) * n;
+      gamma = vdot(sl, yl, n) / vdot(yl, yl, n);
+    }
+    for (uint32_t i = 0; i < n; ++i) q[i] *= gamma;
+    for (uint32_t a = 0; a < k; ++a) {
+      double beta = rho[a] * vdot(Y + (uint64_t)a * n, q, n);
+      for (uint32_t i = 0; i < n; ++i) q[i] += S[(uint64_t)a * n + i] * (alpha[a] - beta);
+    }
+    double t = lr;
+    if (it == 0) t = lr * (1.0 / g1 < 1.0 ? 1.0 / g1 : 1.0);
+    for (uint32_t i = 0; i < n; ++i) {
+      xn[i] = x[i] - t * q[i];
+      if (lower && xn[i] < lower[i]) xn[i] = lower[i];
+    }
+    double fn = fg(xn, gn, ctx);
+    /* curvature pair */
+    double ys = 0.0;
+    for (uint32_t i = 0; i < n; ++i) ys += (gn[i] - g[i]) * (xn[i] - x[i]);
+    if (ys > 1e-10) {
+      if (k == history) { /* drop the oldest */
+        memmove(S, S + n, sizeof(double) * n * (history - 1));
+        memmove(Y, Y + n, sizeof(double) * n * (history - 1));
+        memmove(rho, rho + 1, sizeof(double) * (history - 1));
+        --k;
+      }
+      for (uint32_t i = 0; i < n; ++i) {
+        S[(uint64_t)k * n + i] = xn[i] - x[i];
+        Y[(uint64_t)k * n + i] = gn[i] - g[i];
+      }
+      rho[k] = 1.0 / ys;
+      ++k;
+    }
+    int flat = fabs(fn - f) < 1e-10;
+    memcpy(x, xn, sizeof(double) * n);
+    memcpy(g, gn, sizeof(double) * n);
+    f = fn;
+    if (f < fbest) {
+      fbest = f;
+      memcpy(best, x, sizeof(double) * n);
+    }
+    if (flat) break;
+  }
+  memcpy(x, best, sizeof(double) * n);
+  if (f_out) *f_out = fbest;
+out:
+  free(g);
+  free(gn);
+  free(xn);
+  free(q);
+  free(best);
+  free(alpha);
+  free(S);
+  free(Y);
+  free(rho);
+  return rc;
+}
+
+typedef struct {
+  const uint16_t *w;
+  uint32_t M, N, fmt;
+  double lambda;
+} rd_ctx;
+
+static double rd_fg(const double *x, double *g, void *ctx) {
+  const rd_ctx *c = (const rd_ctx *)ctx;
+  return or_rd_objective(c->w, c->M, c->N, c->fmt, c->lambda, x, g, NULL);
+}
+
+int or_rd_scales(const uint16_t *w, uint32_t M, uint32_t N, uint32_t fmt, double lambda,
+                 uint32_t iters, uint32_t history, double lr, double *s_out, double *f_out) {
+  if (!w || !s_out || M == 0 || N == 0 || !(lambda >= 0.0)) return OR_EINVAL;
+  double *lower = malloc(sizeof(double) * M);
+  if (!lower) return OR_ENOMEM;
+  for (uint32_t i = 0; i < M; ++i) { /* eq. absmax: max|W_i| / Qmax (zero rows: 1) */
+    double amax = 0.0;
+    for (uint32_t j = 0; j < N; ++j) {
+      double a = fabs(or_bf16_value(w[(uint64_t)i * N + j]));
+      if (a > amax) amax = a;
+    }
+    s_out[i] = amax > 0.0 ? amax / or_qmax(fmt) : 1.0;
+    lower[i] = 1e-6 * s_out[i];
+  }
+  rd_ctx c = {w, M, N, fmt, lambda};
+  int rc = or_lbfgs(M, s_out, rd_fg, &c, lower, iters, history, lr, f_out);
+  free(lower);
+  return rc;
+}
+
+typedef struct {
+  uint32_t n;
+  const double *a, *c;
+  double b;
+} quad_ctx;
+
+static double quad_fg(const double *x, double *g, void *ctx) {
+  const quad_ctx *q = (const quad_ctx *)ctx;
+  double sum = 0.0, f = 0.0;
+  for (uint32_t i = 0; i < q->n; ++i) sum += x[i] - q->c[i];
+  for (uint32_t i = 0; i < q->n; ++i) {
+    double d = x[i] - q->c[i];
+    f += 0.5 * q->a[i] * d * d;
+    g[i] = q->a[i] * d + q->b * sum;
+  }
+  return f + 0.5 * q->b * sum * sum;
+}
+
+int or_lbfgs_quadratic(uint32_t n, const double *a, double b, const double *c, uint32_t iters,
+                       uint32_t history, double lr, double *x, double *f_out) {
+  quad_ctx q = {n, a, c, b};
+  return or_lbfgs(n, x, quad_fg, &q, NULL, iters, history, lr, f_out);
 }
 
 /* ------------------------------------------------------------------ */

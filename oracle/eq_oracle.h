@@ -112,6 +112,30 @@ int or_container_decode_chunk(const uint8_t *blob, uint64_t blob_bytes, uint32_t
                               uint8_t *q);
 int or_container_decode(const uint8_t *blob, uint64_t blob_bytes, uint8_t *q);
 
+/* ---- scale optimisation (Sec. 2.2 eq. optimization; Alg. 1 line 2) ----
+ * F(S) = sum|W - S*W_q| / sum|W| + lambda * sum|W_q| / (M N), W_q = Q(W/S)
+ * (u = W/S in fp32, as the quantiser), with the straight-through gradient
+ * dQ/du = 1 where |u| <= Qmax and 0 where the clamp acts. */
+double or_rd_objective(const uint16_t *w, uint32_t M, uint32_t N, uint32_t fmt, double lambda,
+                       const double *s, double *grad, double *dist);
+/* Generic L-BFGS with a fixed step (two-loop recursion), for the objective
+ * fg (returns f, writes the gradient); lower (optional) bounds each x_i from
+ * below; returns the best iterate in x and its f in *f_out. */
+typedef double (*or_fg_fn)(const double *x, double *g, void *ctx);
+int or_lbfgs(uint32_t n, double *x, or_fg_fn fg, void *ctx, const double *lower, uint32_t iters,
+             uint32_t history, double lr, double *f_out);
+/* AbsMax start, then or_lbfgs on or_rd_objective with lower bound 1e-6 x start. */
+int or_rd_scales(const uint16_t *w, uint32_t M, uint32_t N, uint32_t fmt, double lambda,
+                 uint32_t iters, uint32_t history, double lr, double *s_out, double *f_out);
+/* Test problem for or_lbfgs: f(x) = 1/2 sum a_i (x_i - c_i)^2 + 1/2 b (sum (x_i - c_i))^2. */
+int or_lbfgs_quadratic(uint32_t n, const double *a, double b, const double *c, uint32_t iters,
+                       uint32_t history, double lr, double *x, double *f_out);
+/* Container with the given BF16 scales (else as or_container_build; alpha 0). */
+int or_container_build_scaled(const uint16_t *w, uint32_t M, uint32_t N, const uint16_t *scale,
+                              uint32_t fmt, uint32_t P, uint32_t chunk_syms, uint32_t lanes,
+                              uint64_t seed, float target_bits, uint8_t **blob,
+                              uint64_t *blob_bytes);
+
 /* ---- linear layer (Sec. 2.1): y[b][i] = sum_j w_hat[i][j] x[b][j] + bias[i] in fp64 ---- */
 void or_gemv(const uint16_t *w_hat, uint32_t M, uint32_t N, const uint16_t *x, uint32_t B,
              const uint16_t *bias, double *y);

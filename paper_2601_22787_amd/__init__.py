@@ -45,6 +45,12 @@ class eqe_params(ctypes.Structure):
                 ("base_format", ctypes.c_uint32)]
 
 
+class eqe_rd_params(ctypes.Structure):
+    _fields_ = [("lambda_", ctypes.c_double), ("lr", ctypes.c_double),
+                ("iters", ctypes.c_uint32), ("history", ctypes.c_uint32),
+                ("threads", ctypes.c_uint32), ("base_format", ctypes.c_uint32)]
+
+
 # name -> (restype, argtypes): every symbol the public headers declare
 SIGNATURES = {
     "eq_lut_bytes": (ctypes.c_size_t, []),
@@ -68,6 +74,19 @@ SIGNATURES = {
     "eqe_encode": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float,
                                   ctypes.POINTER(eqe_params), ctypes.POINTER(ctypes.c_void_p),
                                   ctypes.POINTER(ctypes.c_uint64)]),
+    "eqe_encode_scaled": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp,
+                                         ctypes.POINTER(eqe_params),
+                                         ctypes.POINTER(ctypes.c_void_p),
+                                         ctypes.POINTER(ctypes.c_uint64)]),
+    "eqe_rd_objective": (ctypes.c_double, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                           ctypes.c_double, _vp, ctypes.c_uint32, _vp, _vp]),
+    "eqe_rd_scales": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                     ctypes.POINTER(eqe_rd_params), _vp, _vp, _vp]),
+    "eqe_rd_lambda_search": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                            ctypes.c_double, ctypes.c_uint32,
+                                            ctypes.POINTER(eqe_rd_params),
+                                            ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_double)]),
     "eqe_free": (None, [_vp]),
 }
 
@@ -252,20 +271,75 @@ def eqe_alpha_search(w: np.ndarray, target_bits: float, sample_rows: int = 0,
 
 def eqe_encode(w: np.ndarray, alpha: float, *, prob_bits: int = 12, chunk_syms: int,
                lanes: int, threads: int = 0, seed: int = 0, target_bits: float = 0.0,
-               base_format: int = FMT_E4M3) -> np.ndarray:
+               base_format: int = FMT_E4M3, scale_bf16: np.ndarray | None = None) -> np.ndarray:
+    """eqe_encode, or eqe_encode_scaled when scale_bf16 (uint16[M]) is given."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     prm = eqe_params(prob_bits, chunk_syms, lanes, threads, seed, target_bits, base_format)
     p = ctypes.c_void_p()
     nb = ctypes.c_uint64()
-    rc = lib().eqe_encode(w.ctypes.data, w.shape[0], w.shape[1], alpha, ctypes.byref(prm),
-                          ctypes.byref(p), ctypes.byref(nb))
-    _check("eqe_encode", rc)
+    if scale_bf16 is None:
+        rc = lib().eqe_encode(w.ctypes.data, w.shape[0], w.shape[1], alpha, ctypes.byref(prm),
+                              ctypes.byref(p), ctypes.byref(nb))
+        _check("eqe_encode", rc)
+    else:
+        sc = np.ascontiguousarray(scale_bf16, dtype=np.uint16)
+        if sc.size != w.shape[0]:
+            raise ValueError("one scale per row")
+        rc = lib().eqe_encode_scaled(w.ctypes.data, w.shape[0], w.shape[1], sc.ctypes.data,
+                                     ctypes.byref(prm), ctypes.byref(p), ctypes.byref(nb))
+        _check("eqe_encode_scaled", rc)
     try:
         out = np.empty(nb.value, dtype=np.uint8)
         ctypes.memmove(out.ctypes.data, p.value, nb.value)
     finally:
         lib().eqe_free(p)
     return out
+
+
+def _rd_params(lam, iters, history, lr, threads, base_format):
+    return eqe_rd_params(lam, lr, iters, history, threads, base_format)
+
+
+def eqe_rd_objective(w: np.ndarray, scale: np.ndarray, lam: float, base_format: int = FMT_E4M3,
+                     threads: int = 0):
+    """(F, straight-through gradient, distortion term) at the given scales."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    sc = np.ascontiguousarray(scale, dtype=np.float64)
+    g = np.empty(w.shape[0], dtype=np.float64)
+    d = ctypes.c_double()
+    f = lib().eqe_rd_objective(w.ctypes.data, w.shape[0], w.shape[1], base_format, lam,
+                               sc.ctypes.data, threads, g.ctypes.data, ctypes.byref(d))
+    if np.isnan(f):
+        raise EqError("eqe_rd_objective", EQ_EINVAL)
+    return f, g, d.value
+
+
+def eqe_rd_scales(w: np.ndarray, lam: float, *, iters: int = 0, history: int = 0, lr: float = 0.0,
+                  threads: int = 0, base_format: int = FMT_E4M3):
+    """(scales as float64, scales as BF16 bit patterns, lowest F)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M = w.shape[0]
+    prm = _rd_params(lam, iters, history, lr, threads, base_format)
+    s64 = np.empty(M, dtype=np.float64)
+    s16 = np.empty(M, dtype=np.uint16)
+    f = ctypes.c_double()
+    _check("eqe_rd_scales", lib().eqe_rd_scales(w.ctypes.data, M, w.shape[1], ctypes.byref(prm),
+                                                 s64.ctypes.data, s16.ctypes.data, ctypes.byref(f)))
+    return s64, s16, f.value
+
+
+def eqe_rd_lambda_search(w: np.ndarray, target_bits: float, sample_rows: int = 0, *,
+                         iters: int = 0, history: int = 0, lr: float = 0.0, threads: int = 0,
+                         base_format: int = FMT_E4M3):
+    """(lambda, entropy over the rows searched)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    prm = _rd_params(0.0, iters, history, lr, threads, base_format)
+    lam, h = ctypes.c_double(), ctypes.c_double()
+    _check("eqe_rd_lambda_search",
+           lib().eqe_rd_lambda_search(w.ctypes.data, w.shape[0], w.shape[1], target_bits,
+                                      sample_rows, ctypes.byref(prm), ctypes.byref(lam),
+                                      ctypes.byref(h)))
+    return lam.value, h.value
 
 
 # ---------------------------------------------------------------- layer object

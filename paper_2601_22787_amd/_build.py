@@ -29,7 +29,7 @@ def build(verbose: bool = False) -> str:
     """Always recompiles; returns the path of libeq.so."""
     os.makedirs(BUILD, exist_ok=True)
     objs = []
-    for src in ("eq_encode.cpp", "eq_layer.cpp"):
+    for src in ("eq_encode.cpp", "eq_rd.cpp", "eq_layer.cpp"):
         obj = os.path.join(BUILD, src + ".o")
         _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)

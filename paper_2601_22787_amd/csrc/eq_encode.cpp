@@ -108,9 +108,11 @@ uint16_t row_scale(const uint16_t *row, uint32_t N, float alpha, uint32_t fmt) {
 }
 
 // Quantise the listed rows; codes are written only if `codes` is non-null.
+// Row i's scale is given[i] when `given` is non-null, else the AbsMax scale
+// times alpha.
 void quantize_rows(const uint16_t *w, uint32_t N, float alpha, uint32_t fmt,
                    const std::vector<uint32_t> &rows, unsigned threads, uint16_t *scale,
-                   uint8_t *codes, uint64_t hist[256]) {
+                   uint8_t *codes, uint64_t hist[256], const uint16_t *given = nullptr) {
   uint8_t (*const quantize)(float) = fmt == kFmtInt8 ? quantize_int8 : quantize_e4m3;
   const uint64_t n_rows = rows.size();
   const uint64_t per = 16;  // rows per task
@@ -121,7 +123,7 @@ void quantize_rows(const uint16_t *w, uint32_t N, float alpha, uint32_t fmt,
     for (uint64_t r = t * per; r < std::min(n_rows, (t + 1) * per); ++r) {
       const uint32_t i = rows[r];
       const uint16_t *src = w + static_cast<uint64_t>(i) * N;
-      uint16_t s = row_scale(src, N, alpha, fmt);
+      uint16_t s = given ? given[i] : row_scale(src, N, alpha, fmt);
       if (scale) scale[i] = s;
       const float sf = bf16_to_float(s);
       uint8_t *dst = codes ? codes + static_cast<uint64_t>(i) * N : nullptr;
@@ -274,15 +276,29 @@ extern "C" float eqe_alpha_search(const uint16_t *w, uint32_t M, uint32_t N, dou
   return best;
 }
 
-extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
-                          const eqe_params *p, uint8_t **blob_out, uint64_t *bytes_out) {
+namespace {
+
+// Scale usable by the decoder (finite, normal, 2^-117 <= s < 2^120, so
+// every dequantised product is exact in fp32) and positive.
+bool scale_usable(uint16_t s) {
+  const int e = (s >> 7) & 0xFF;
+  return !(s & 0x8000) && e >= 127 - 117 && e <= 127 + 119;
+}
+
+// Alg. 1: quantise with the AbsMax scales times alpha, or with the given
+// scales when `given` is non-null (alpha is then recorded as 0), and encode.
+int encode_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const uint16_t *given,
+                const eqe_params *p, uint8_t **blob_out, uint64_t *bytes_out) {
   if (!w || !p || !blob_out || !bytes_out || !M || !N) return -1;
   const uint64_t n = static_cast<uint64_t>(M) * N;
   const uint32_t W = p->lanes, C = p->chunk_syms, P = p->prob_bits;
   const uint32_t fmt = p->base_format ? p->base_format : kFmtE4M3;
   if (n >= (uint64_t(1) << 32) || (W != 64 && W != 128 && W != 256) || C == 0 || C % W ||
-      P < 1 || P > 12 || !(alpha > 0.0f) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
+      P < 1 || P > 12 || (!given && !(alpha > 0.0f)) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
     return -1;
+  if (given)
+    for (uint32_t i = 0; i < M; ++i)
+      if (!scale_usable(given[i])) return -1;
   const unsigned nt = worker_count(p->threads);
   try {
     std::vector<uint16_t> scale(M);
@@ -290,7 +306,7 @@ extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha
     std::vector<uint32_t> rows(M);
     for (uint32_t i = 0; i < M; ++i) rows[i] = i;
     uint64_t hist[256];
-    quantize_rows(w, N, alpha, fmt, rows, nt, scale.data(), codes.data(), hist);
+    quantize_rows(w, N, alpha, fmt, rows, nt, scale.data(), codes.data(), hist, given);
 
     std::vector<uint8_t> sym;
     std::vector<uint16_t> freq;
@@ -344,7 +360,7 @@ extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha
     put<uint64_t>(b, 48, total);
     put<uint64_t>(b, 56, padded);
     put<uint64_t>(b, 64, p->seed);
-    put<float>(b, 72, alpha);
+    put<float>(b, 72, given ? 0.0f : alpha);
     put<float>(b, 76, p->target_bits);
     put<float>(b, 80, static_cast<float>(entropy_bits(hist)));
     put<uint64_t>(b, 88, o_scale);
@@ -365,6 +381,64 @@ extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha
     });
     *blob_out = b;
     *bytes_out = bytes;
+    return 0;
+  } catch (const std::bad_alloc &) {
+    return -5;
+  }
+}
+
+}  // namespace
+
+extern "C" int eqe_encode(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
+                          const eqe_params *p, uint8_t **blob_out, uint64_t *bytes_out) {
+  return encode_impl(w, M, N, alpha, nullptr, p, blob_out, bytes_out);
+}
+
+extern "C" int eqe_encode_scaled(const uint16_t *w, uint32_t M, uint32_t N,
+                                 const uint16_t *scale_bf16, const eqe_params *p,
+                                 uint8_t **blob_out, uint64_t *bytes_out) {
+  if (!scale_bf16) return -1;
+  return encode_impl(w, M, N, 0.0f, scale_bf16, p, blob_out, bytes_out);
+}
+
+extern "C" int eqe_rd_lambda_search(const uint16_t *w, uint32_t M, uint32_t N,
+                                    double target_bits, uint32_t sample_rows,
+                                    const eqe_rd_params *prm, double *lambda_out, double *h_out) {
+  if (!w || !M || !N || !prm || !lambda_out) return -1;
+  const uint32_t fmt = prm->base_format ? prm->base_format : kFmtE4M3;
+  if (fmt != kFmtE4M3 && fmt != kFmtInt8) return -1;
+  try {
+    // the rows searched, copied contiguously
+    const uint32_t R = (sample_rows && sample_rows < M) ? sample_rows : M;
+    std::vector<uint16_t> sub(static_cast<uint64_t>(R) * N);
+    for (uint32_t r = 0; r < R; ++r) {
+      const uint64_t i = R == M ? r : static_cast<uint64_t>(r) * M / R;
+      std::memcpy(sub.data() + static_cast<uint64_t>(r) * N, w + i * N, 2ull * N);
+    }
+    std::vector<uint32_t> rows(R);
+    for (uint32_t r = 0; r < R; ++r) rows[r] = r;
+    std::vector<uint16_t> sb(R);
+    const unsigned nt = worker_count(prm->threads);
+    double lo = -8.0, hi = 16.0, best_err = INFINITY, best_h = 0.0, best = 1.0;
+    for (int it = 0; it < 18; ++it) {
+      const double mid = 0.5 * (lo + hi);
+      eqe_rd_params q = *prm;
+      q.lambda = std::exp2(mid);
+      q.base_format = fmt;
+      const int rc = eqe_rd_scales(sub.data(), R, N, &q, nullptr, sb.data(), nullptr);
+      if (rc != 0) return rc;
+      uint64_t hist[256];
+      quantize_rows(sub.data(), N, 0.0f, fmt, rows, nt, nullptr, nullptr, hist, sb.data());
+      const double h = entropy_bits(hist);
+      if (std::fabs(h - target_bits) < best_err) {
+        best_err = std::fabs(h - target_bits);
+        best = q.lambda;
+        best_h = h;
+      }
+      (h > target_bits ? lo : hi) = mid;  // larger lambda -> lower entropy
+    }
+    *lambda_out = best;
+    if (h_out) *h_out = best_h;
     return 0;
   } catch (const std::bad_alloc &) {
     return -5;

@@ -89,7 +89,7 @@ int eqe_rd_scales(const uint16_t *w_bf16, uint32_t M, uint32_t N, const eqe_rd_p
 
 /* lambda whose optimised BF16 scales give codes with empirical entropy
  * (eq. emp_entropy) closest to target_bits: bisection on log2(lambda) over
- * [-8, 16] (18 steps), optimising and measuring on sample_rows evenly spaced
+ * [-8, 16] (14 steps), optimising and measuring on sample_rows evenly spaced
  * rows (all rows if 0 or >= M); params->lambda is ignored.  Returns 0 and
  * writes *lambda and *h (entropy on the rows searched), or -1 / -5. */
 int eqe_rd_lambda_search(const uint16_t *w_bf16, uint32_t M, uint32_t N, double target_bits,

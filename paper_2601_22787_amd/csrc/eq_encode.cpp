@@ -420,7 +420,7 @@ extern "C" int eqe_rd_lambda_search(const uint16_t *w, uint32_t M, uint32_t N,
     std::vector<uint16_t> sb(R);
     const unsigned nt = worker_count(prm->threads);
     double lo = -8.0, hi = 16.0, best_err = INFINITY, best_h = 0.0, best = 1.0;
-    for (int it = 0; it < 18; ++it) {
+    for (int it = 0; it < 14; ++it) {
       const double mid = 0.5 * (lo + hi);
       eqe_rd_params q = *prm;
       q.lambda = std::exp2(mid);

@@ -53,28 +53,34 @@ float bf16_value(uint16_t b) {
   return f;
 }
 
+// Nearest integer of |x| < 2^22, ties to even: adding and subtracting
+// 1.5 * 2^23 rounds in the default (nearest-even) mode without a libm call.
+inline float round_even(float x) {
+  const volatile float big = 12582912.0f;  // kept out of constant folding
+  return (x + big) - big;
+}
+
 // Value of the nearest E4M3FN number to v after clamping to +-448 (ties to
 // even), computed on the float bit pattern: normal range by rounding the
 // significand to 3 bits in place, subnormal range (|v| < 2^-6) on the grid
 // k * 2^-9.
+// Both candidates are formed and one is selected, so that the loop over a
+// row stays free of data-dependent branches.
 float q_e4m3(float v) {
-  float a = std::fabs(v);
-  if (a > 448.0f) a = 448.0f;
-  float r;
-  if (a < 0.015625f) {
-    r = std::nearbyint(a * 512.0f) * 0.001953125f;
-  } else {
-    uint32_t b;
-    std::memcpy(&b, &a, 4);
-    b = (b + 0x7FFFFu + ((b >> 20) & 1u)) & ~0xFFFFFu;
-    std::memcpy(&r, &b, 4);
-  }
-  return std::signbit(v) ? -r : r;
+  const float a = std::min(std::fabs(v), 448.0f);
+  const float sub = round_even(a * 512.0f) * 0.001953125f;
+  uint32_t b;
+  std::memcpy(&b, &a, 4);
+  b = (b + 0x7FFFFu + ((b >> 20) & 1u)) & ~0xFFFFFu;
+  float nrm;
+  std::memcpy(&nrm, &b, 4);
+  const float r = a < 0.015625f ? sub : nrm;
+  return std::copysign(r, v);
 }
 
-float q_int8(float v) { return std::nearbyint(std::min(127.0f, std::max(-127.0f, v))); }
+float q_int8(float v) { return round_even(std::min(127.0f, std::max(-127.0f, v))); }
 
-double sgn(double v) { return v > 0.0 ? 1.0 : (v < 0.0 ? -1.0 : 0.0); }
+double sgn(double v) { return static_cast<double>(int(v > 0.0) - int(v < 0.0)); }
 
 struct Problem {
   const uint16_t *w;
@@ -96,6 +102,7 @@ double evaluate(const Problem &p, const double *s, double *grad, double *dist) {
   parallel_rows(p.M, p.threads, [&](uint32_t i) {
     const uint16_t *row = p.w + static_cast<uint64_t>(i) * p.N;
     const double si = s[i];
+    const double inv_s2 = 1.0 / (si * si);
     const float sf = static_cast<float>(si);
     double d = 0.0, r = 0.0, gd = 0.0, gr = 0.0;
     for (uint32_t j = 0; j < p.N; ++j) {
@@ -106,7 +113,7 @@ double evaluate(const Problem &p, const double *s, double *grad, double *dist) {
       d += std::fabs(diff);
       r += std::fabs(v);
       if (grad) {
-        const double dv = std::fabs(u) <= p.qmax ? -static_cast<double>(wf) / (si * si) : 0.0;
+        const double dv = (std::fabs(u) <= p.qmax) * (-static_cast<double>(wf) * inv_s2);
         gd += sgn(diff) * (v + si * dv);
         gr += sgn(v) * dv;
       }

@@ -164,6 +164,31 @@ int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x
                          const uint16_t *const *bias, float *const *y, void *ws,
                          size_t ws_bytes, hipStream_t stream);
 
+/* Prefill (B > 8 tokens): the linear layer y = x W_hat^T + b on the matrix
+ * cores (Sec. 2.1), from the decoded codes.  The paper decompresses a
+ * block's weights to a Float8 buffer and runs an FP8-weight / 16-bit
+ * activation GEMM (Sec. 2.2 block-wise pipeline, App. A.1); these entry
+ * points do the same with one byte per weight: eq_decode_codes writes the
+ * codes, eq_gemm_codes converts them to BF16 in registers, multiplies with
+ * MFMA (fp32 accumulation) and applies s_i and the bias once per output.
+ * Requirements: N (cols) a multiple of 16; codes and x 16-byte aligned. */
+
+/* Workspace bytes of eq_decode_gemm: the M*N codes, rounded up to 256. */
+size_t eq_gemm_workspace_bytes(const eq_layer *L);
+
+/* y[t][i] = s_i * sum_j v(codes[i][j]) x[t][j] + bias[i] for t < B, any
+ * B >= 1.  codes is [M][N] (the output of eq_decode_codes for this layer,
+ * device), x is [B][N] BF16 (device), bias is [M] BF16 or NULL, y is
+ * [B][M] fp32 (device).  Returns EQ_OK, EQ_EINVAL or EQ_EHIP. */
+int eq_gemm_codes(const eq_layer *L, const uint8_t *codes, const uint16_t *x, uint32_t B,
+                  const uint16_t *bias, float *y, hipStream_t stream);
+
+/* eq_decode_codes into ws (at least eq_gemm_workspace_bytes(L) bytes,
+ * device, 16-byte aligned), then eq_gemm_codes: Alg. 2 for a batch of B
+ * tokens. */
+int eq_decode_gemm(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
+                   float *y, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Wait for `stream`, then report EQ_ECORRUPT if any decode since the last
  * eq_layer_prepare found a chunk whose stream or terminal states did not
  * check out, else EQ_OK (or EQ_EHIP). */

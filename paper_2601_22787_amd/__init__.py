@@ -66,6 +66,11 @@ SIGNATURES = {
     "eq_gemv_multi_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_uint32, ctypes.c_uint32]),
     "eq_decode_gemv_multi": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp, _vp,
                                             _vp, ctypes.c_size_t, _vp]),
+    "eq_gemm_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer)]),
+    "eq_gemm_codes": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, _vp, ctypes.c_uint32, _vp, _vp,
+                                     _vp]),
+    "eq_decode_gemm": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp, _vp,
+                                      _vp, ctypes.c_size_t, _vp]),
     "eq_get_status": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp]),
     "eq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "eqe_alpha_search": (ctypes.c_float, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_double,
@@ -253,6 +258,38 @@ def multi_workspace(layers, B: int):
                        device=layers[0].dev_blob.device)
 
 
+def eq_gemm_workspace_bytes(L) -> int:
+    return lib().eq_gemm_workspace_bytes(ctypes.byref(_raw(L)))
+
+
+def eq_gemm_codes(L, codes, x, B: int, bias, y, stream=None) -> None:
+    """Prefill GEMM from decoded codes: y[B][M] = x[B][N] W_hat^T + bias."""
+    import torch
+    r = _raw(L)
+    if x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError("x must hold 16-bit BF16 patterns")
+    pc = _dptr(codes, torch.uint8, r.rows * r.cols)
+    px = _dptr(x, None, B * r.cols)
+    pb = _dptr(bias, None, r.rows) if bias is not None else None
+    py = _dptr(y, torch.float32, B * r.rows)
+    _check("eq_gemm_codes", lib().eq_gemm_codes(ctypes.byref(r), pc, px, B, pb, py,
+                                                _stream(stream)))
+
+
+def eq_decode_gemm(L, x, B: int, bias, y, ws, stream=None) -> None:
+    """Prefill: decode the codes into ws, then the MFMA GEMM."""
+    import torch
+    r = _raw(L)
+    if x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError("x must hold 16-bit BF16 patterns")
+    px = _dptr(x, None, B * r.cols)
+    pb = _dptr(bias, None, r.rows) if bias is not None else None
+    py = _dptr(y, torch.float32, B * r.rows)
+    nbytes = ws.numel() * ws.element_size()
+    _check("eq_decode_gemm", lib().eq_decode_gemm(ctypes.byref(r), px, B, pb, py, _dptr(ws),
+                                                  nbytes, _stream(stream)))
+
+
 def eq_get_status(L, stream=None) -> int:
     return lib().eq_get_status(ctypes.byref(_raw(L)), _stream(stream))
 
@@ -371,6 +408,11 @@ class Layer:
     def workspace(self, B: int):
         import torch
         return torch.empty(eq_gemv_workspace_bytes(self, B), dtype=torch.uint8,
+                           device=self.dev_blob.device)
+
+    def gemm_workspace(self):
+        import torch
+        return torch.empty(eq_gemm_workspace_bytes(self), dtype=torch.uint8,
                            device=self.dev_blob.device)
 
 

@@ -33,9 +33,10 @@ def build(verbose: bool = False) -> str:
         obj = os.path.join(BUILD, src + ".o")
         _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
-    obj = os.path.join(BUILD, "eq_decode.hip.o")
-    _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, "eq_decode.hip"), "-o", obj])
-    objs.append(obj)
+    for src in ("eq_decode.hip", "eq_gemm.hip"):
+        obj = os.path.join(BUILD, src + ".o")
+        _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        objs.append(obj)
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", *objs, "-o", tmp])
     os.replace(tmp, LIB)

@@ -1,0 +1,174 @@
+"""GPU parity of the prefill path (B > 8 tokens): decode to codes, then the
+W8A16 MFMA GEMM with the scale applied per output (Sec. 2.1 linear layer on
+the dequantised weights; the paper's decompress-then-FP8-GEMM pipeline).
+
+Bar: max|y - y_ref| / max|y_ref| <= 1e-2 per token row against the oracle's
+fp64 GEMM on the decoded BF16 weights (as for the GEMV), plus exact outputs
+for one-hot tokens (y = s_i v(q_ij), a single product), on ragged shapes
+(tokens, rows and columns not multiples of the 128 x 128 x 64 tile), both
+base formats, and sampled rows and tokens of the full-size 8192 x 28672
+layer."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import config_matrices, small_spec
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def eq():
+    import paper_2601_22787_amd as m
+    m.lib()
+    assert torch.cuda.is_available()
+    return m
+
+
+def _dev():
+    return torch.device("cuda:0")
+
+
+def encode(eq, w, bits, C, lanes, fmt):
+    alpha, _ = eq.eqe_alpha_search(w, bits, base_format=fmt)
+    return eq.eqe_encode(w, alpha, chunk_syms=C, lanes=lanes, base_format=fmt)
+
+
+def tokens(spec, B):
+    return np.stack([synth.vector(spec.seed, 100 + t, spec.cols) for t in range(B)])
+
+
+def gpu_gemm(eq, L, x_bits, bias_bits=None):
+    B = x_bits.shape[0]
+    x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+    bias = None if bias_bits is None else torch.from_numpy(bias_bits.view(np.int16)).to(_dev())
+    y = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+    eq.eq_decode_gemm(L, x, B, bias, y, L.gemm_workspace())
+    return y.cpu().numpy()
+
+
+def rel_err(y, y_ref):
+    return np.abs(y - y_ref).max(axis=1) / np.maximum(np.abs(y_ref).max(axis=1), 1e-30)
+
+
+SHAPES = [
+    # M, N, C, lanes, bits, B
+    (64, 256, 4096, 64, 2.0, 16),
+    (100, 320, 1024, 64, 3.0, 37),     # ragged rows, columns (320 = 5 x 64) and tokens
+    (256, 1024, 4096, 128, 2.0, 129),  # two token tiles, one token past the first
+    (37, 4096, 16384, 256, 4.0, 300),
+    (300, 208, 2048, 64, 2.5, 9),      # N = 208: a partial 64-column stage
+]
+
+
+@pytest.mark.parametrize("fmt", [1, 2])
+@pytest.mark.parametrize("M,N,C,lanes,bits,B", SHAPES)
+def test_gemm_shapes(eq, M, N, C, lanes, bits, B, fmt):
+    say("gemm", M, N, B, "format", fmt)
+    spec = small_spec(M, N, bits=bits, chunk=C, lanes=lanes, seed=4000 + M + N)
+    w = synth.weights(spec)
+    blob = encode(eq, w, bits, C, lanes, fmt)
+    L = eq.Layer(blob, _dev())
+    rc, q = oracle.container_decode(blob)
+    assert rc == oracle.OK
+    w_ref = oracle.dequant(q, oracle.container_scales(blob), fmt)
+    x = tokens(spec, B)
+    bias = synth.bias(spec)
+    for b in (None, bias):
+        y = gpu_gemm(eq, L, x, b)
+        err = rel_err(y, oracle.gemv(w_ref, x, b))
+        assert np.isfinite(y).all() and (err <= TOL).all(), err.max()
+    assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+@pytest.mark.parametrize("fmt", [1, 2])
+def test_gemm_one_hot_exact(eq, fmt):
+    """One-hot tokens select single weights: y_ti = s_i v(q_ij) exactly (one
+    product, no rounding), over every code of the base format."""
+    if fmt == 1:
+        codes = [c for c in range(256) if (c & 0x7F) != 0x7F and c != 0x80]
+    else:
+        codes = [c for c in range(256) if c != 0x80]
+    vals = np.array([oracle.code_value(fmt, c) for c in codes])
+    M, N = 40, 512
+    w = np.zeros((M, N), dtype=np.uint16)
+    for i in range(M):
+        row = np.resize(np.roll(vals, 29 * i), N) * (2.0 ** ((i % 7) - 3))
+        w[i] = [synth.to_bf16(float(v)) for v in row]
+    blob = eq.eqe_encode(w, 1.0, chunk_syms=4096, lanes=64, base_format=fmt)
+    L = eq.Layer(blob, _dev())
+    rc, q = oracle.container_decode(blob)
+    assert rc == oracle.OK and len(np.unique(q)) == len(codes)
+    scale = synth.bf16_to_f32(oracle.container_scales(blob)).astype(np.float64)
+    cols = np.arange(0, N, 3)
+    x = np.zeros((cols.size, N), dtype=np.uint16)
+    x[np.arange(cols.size), cols] = 0x3F80
+    y = gpu_gemm(eq, L, x)
+    for t, j in enumerate(cols):
+        exact = scale * np.array([oracle.code_value(fmt, int(c)) for c in q[:, j]])
+        assert np.array_equal(y[t].astype(np.float64), exact), j
+
+
+def test_gemm_codes_entry_and_checks(eq):
+    spec = small_spec(96, 512, bits=2.0, chunk=4096, lanes=64, seed=4100)
+    w = synth.weights(spec)
+    blob = encode(eq, w, 2.0, 4096, 64, 1)
+    L = eq.Layer(blob, _dev())
+    x_bits = tokens(spec, 20)
+    x = torch.from_numpy(x_bits.view(np.int16)).to(_dev())
+    codes = torch.empty(spec.params, dtype=torch.uint8, device=_dev())
+    eq.eq_decode_codes(L, codes)
+    y1 = torch.empty(20, spec.rows, dtype=torch.float32, device=_dev())
+    eq.eq_gemm_codes(L, codes, x, 20, None, y1)
+    y2 = torch.from_numpy(gpu_gemm(eq, L, x_bits)).to(_dev())
+    assert torch.equal(y1, y2)
+    # the GEMV computes the same products (different summation order)
+    y3 = torch.empty(8, spec.rows, dtype=torch.float32, device=_dev())
+    eq.eq_decode_gemv(L, x[:8].contiguous(), 8, None, y3, L.workspace(8))
+    assert (rel_err(y3.cpu().numpy(), y1[:8].cpu().numpy()) < 1e-5).all()
+    with pytest.raises(eq.EqError):  # misaligned activations
+        eq.eq_gemm_codes(L, codes, x.view(-1)[1:].view(torch.int16), 1, None, y1)
+    with pytest.raises(eq.EqError):  # workspace too small
+        eq.eq_decode_gemm(L, x, 20, None, y1, L.gemm_workspace()[:100])
+    spec2 = small_spec(8, 200, bits=2.0, chunk=1600, lanes=64, seed=4101)
+    L2 = eq.Layer(encode(eq, synth.weights(spec2), 2.0, 1600, 64, 1), _dev())
+    with pytest.raises(eq.EqError):  # N not a multiple of 16
+        eq.eq_decode_gemm(L2, torch.zeros(200, dtype=torch.int16, device=_dev()), 1, None,
+                          torch.empty(8, dtype=torch.float32, device=_dev()), L2.gemm_workspace())
+
+
+@pytest.mark.parametrize("fmt", [1, 2])
+def test_gemm_config4_full_size_sampled(eq, fmt):
+    """The 8192x28672 layer at 256 tokens: sampled rows x sampled tokens
+    against the oracle's fp64 GEMM of the same rows (codes from the oracle's
+    quantiser on the generated weights)."""
+    spec = config_matrices(4)[0]
+    say("gemm config 4", fmt)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512, base_format=fmt)
+    blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
+                         base_format=fmt)
+    L = eq.Layer(blob, _dev())
+    B = 256
+    x = tokens(spec, B)
+    y = gpu_gemm(eq, L, x)
+    assert eq.eq_get_status(L) == eq.EQ_OK and np.isfinite(y).all()
+    r = np.random.default_rng(12)
+    rows = sorted(set(r.choice(spec.rows, 8, replace=False).tolist()) | {0, spec.rows - 1})
+    toks = sorted(set(r.choice(B, 6, replace=False).tolist()) | {0, B - 1})
+    scale = oracle.container_scales(blob)
+    w_rows = oracle.dequant(oracle.quantize(w[rows], scale[rows], fmt), scale[rows], fmt)
+    y_ref = oracle.gemv(w_rows, x[toks])
+    err = rel_err(y[np.ix_(toks, rows)], y_ref)
+    assert (err <= TOL).all(), err

@@ -9,6 +9,8 @@
 // are applied once per output in the epilogue, as QMatMul(W_q, S, x) does.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "eq.h"
 #include "eq_internal.h"
 
@@ -21,17 +23,19 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-// Block tile: kBT tokens x kBO output rows, kBK input columns per stage.
-// Four wavefronts, each owning a 64 x 64 quarter as 2 x 2 MFMA tiles of
+// Block tile: BT tokens x BO output rows, kBK input columns per stage, with
+// the block's wavefronts each owning a WT x WO sub-tile as MFMA tiles of
 // 32 x 32.  LDS rows are padded (X: 144 B per token row, codes: 72 B per
 // output row) so that the 16-byte and 8-byte fragment reads of a quarter
-// wavefront fall into distinct banks.
-constexpr int kBT = 128, kBO = 128, kBK = 64;
-constexpr int kThreads = 256;
+// wavefront fall into distinct banks.  Two LDS stages (dynamic LDS).
+constexpr int kBK = 64;
 constexpr int kXStride = kBK * 2 + 16;  // bytes per token row of the X tile
 constexpr int kCStride = kBK + 8;       // bytes per output row of the code tile
-constexpr int kXTileBytes = kBT * kXStride;
-constexpr int kCTileBytes = kBO * kCStride;
+
+template <int BT, int BO>
+constexpr int stage_bytes() {
+  return BT * kXStride + BO * kCStride;
+}
 
 struct GemmArgs {
   const uint8_t *codes;   // [M][N]
@@ -40,6 +44,8 @@ struct GemmArgs {
   const uint16_t *bias;   // [M] BF16 or null
   float *y;               // [B][M]
   uint32_t B, M, N;
+  uint32_t gx, gy;        // output-row blocks, token blocks
+  uint32_t group;         // token blocks per group of the launch order
 };
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
@@ -68,35 +74,63 @@ __device__ inline bf16x8 codes_to_bf16x8(uint2 c) {
   return __builtin_bit_cast(bf16x8, r);
 }
 
-// One block: tokens [t0, t0 + 128) x output rows [o0, o0 + 128).  Stage k
-// holds input columns [64 k, 64 k + 64); the next stage's global loads are in
-// flight in registers while the current one is multiplied, and are written to
-// the other LDS buffer afterwards (one barrier per stage).  Out-of-range
+// Launch order.  Workgroups are dealt to the 8 XCDs round robin (each XCD
+// has its own L2), so block i is renumbered so that every XCD receives a
+// contiguous range of the logical order; the logical order walks groups of
+// `group` token blocks, output-row block by output-row block, so that the
+// blocks resident on one XCD share few X and code tiles.  The grid is padded
+// to a multiple of 8; padding blocks exit at once.
+__device__ inline bool block_tile(const GemmArgs &a, uint32_t &ob, uint32_t &tb) {
+  const uint32_t nb = a.gx * a.gy;
+  const uint32_t per = gridDim.x / 8;
+  const uint32_t logical = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (logical >= nb) return false;
+  const uint32_t span = a.group * a.gx;          // blocks per group of token blocks
+  const uint32_t first = (logical / span) * a.group;
+  const uint32_t rows = min(a.group, a.gy - first);
+  const uint32_t in = logical % span;
+  tb = first + in % rows;
+  ob = in / rows;
+  return true;
+}
+
+// One block: tokens [tb BT, +BT) x output rows [ob BO, +BO).  Stage k holds
+// input columns [64 k, 64 k + 64); the next stage's global loads are in
+// flight in registers while the current one is multiplied, and are written
+// to the other LDS buffer afterwards (one barrier per stage).  Out-of-range
 // tokens, rows and columns are loaded as zeros (N is a multiple of 16, so a
 // 16-byte chunk is either wholly inside a row or wholly past its end).
-template <int FMT>
-__global__ __launch_bounds__(kThreads) void gemm_codes_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t xs[2][kXTileBytes];
-  __shared__ __attribute__((aligned(16))) uint8_t cs[2][kCTileBytes];
+template <int FMT, int BT, int BO, int WT, int WO>
+__global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(GemmArgs a) {
+  constexpr int kWaves = (BT / WT) * (BO / WO);
+  constexpr int kThreads = kWaves * 64;
+  constexpr int kXChunks = BT * (kBK * 2 / 16) / kThreads;  // 16-byte chunks per thread
+  constexpr int kCChunks = BO * (kBK / 16) / kThreads;
+  constexpr int TI = WT / 32, TJ = WO / 32;                   // MFMA tiles per wave
+  static_assert(kXChunks * kThreads == BT * 8 && kCChunks * kThreads == BO * 4, "staging");
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  uint32_t ob, tb;
+  if (!block_tile(a, ob, tb)) return;
   const uint32_t N = a.N;
-  const uint32_t o0 = blockIdx.x * kBO, t0 = blockIdx.y * kBT;
+  const uint32_t o0 = ob * BO, t0 = tb * BT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wt = wave >> 1, wo = wave & 1;
+  const int wt = wave / (BO / WO), wo = wave % (BO / WO);
   const int r32 = lane & 31, g = lane >> 5;
+  uint8_t *const xs0 = smem;
+  uint8_t *const cs0 = smem + BT * kXStride;
+  constexpr int kStage = stage_bytes<BT, BO>();
 
-  // global -> register staging: X 1024 chunks of 16 B (4 per thread), codes
-  // 512 chunks (2 per thread)
-  uint4 xr[4], cr[2];
+  uint4 xr[kXChunks], cr[kCChunks];
   auto gload = [&](uint32_t k0) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < kXChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 3, col = c & 7;
       const uint32_t t = t0 + row, k = k0 + col * 8;
       xr[r] = (t < a.B && k < N) ? *reinterpret_cast<const uint4 *>(a.x + size_t(t) * N + k)
                                  : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
+    for (int r = 0; r < kCChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 2, col = c & 3;
       const uint32_t o = o0 + row, k = k0 + col * 16;
       cr[r] = (o < a.M && k < N) ? *reinterpret_cast<const uint4 *>(a.codes + size_t(o) * N + k)
@@ -104,25 +138,26 @@ __global__ __launch_bounds__(kThreads) void gemm_codes_kernel(GemmArgs a) {
     }
   };
   auto lstore = [&](int buf) {
+    uint8_t *const xs = xs0 + buf * kStage, *const cs = cs0 + buf * kStage;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < kXChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 3, col = c & 7;
-      *reinterpret_cast<uint4 *>(&xs[buf][row * kXStride + col * 16]) = xr[r];
+      *reinterpret_cast<uint4 *>(xs + row * kXStride + col * 16) = xr[r];
     }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
+    for (int r = 0; r < kCChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 2, col = c & 3;
-      uint2 *d = reinterpret_cast<uint2 *>(&cs[buf][row * kCStride + col * 16]);
+      uint2 *d = reinterpret_cast<uint2 *>(cs + row * kCStride + col * 16);
       d[0] = make_uint2(cr[r].x, cr[r].y);
       d[1] = make_uint2(cr[r].z, cr[r].w);
     }
   };
 
-  floatx16 acc[2][2];
+  floatx16 acc[TI][TJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
@@ -132,27 +167,28 @@ __global__ __launch_bounds__(kThreads) void gemm_codes_kernel(GemmArgs a) {
   __syncthreads();
   for (uint32_t kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
+    const uint8_t *const xs = xs0 + cur * kStage, *const cs = cs0 + cur * kStage;
     if (kt + 1 < nk) gload((kt + 1) * kBK);
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
       // fragments: lane (r32, g) holds 8 consecutive columns ks*16 + 8g ..
       // of token row r32 (A) and of output row r32 (B)
-      bf16x8 af[2], bf[2];
+      bf16x8 af[TI], bf[TJ];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int row = wt * 64 + i * 32 + r32;
-        af[i] = *reinterpret_cast<const bf16x8 *>(&xs[cur][row * kXStride + (ks * 16 + g * 8) * 2]);
+      for (int i = 0; i < TI; ++i) {
+        const int row = wt * WT + i * 32 + r32;
+        af[i] = *reinterpret_cast<const bf16x8 *>(xs + row * kXStride + (ks * 16 + g * 8) * 2);
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int row = wo * 64 + j * 32 + r32;
-        const uint2 c = *reinterpret_cast<const uint2 *>(&cs[cur][row * kCStride + ks * 16 + g * 8]);
-        bf[j] = codes_to_bf16x8<FMT>(c);
+      for (int j = 0; j < TJ; ++j) {
+        const int row = wo * WO + j * 32 + r32;
+        bf[j] = codes_to_bf16x8<FMT>(
+            *reinterpret_cast<const uint2 *>(cs + row * kCStride + ks * 16 + g * 8));
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) lstore(cur ^ 1);
@@ -162,25 +198,65 @@ __global__ __launch_bounds__(kThreads) void gemm_codes_kernel(GemmArgs a) {
   // epilogue: element v of lane (r32, g) in tile (i, j) is token row
   // 8 (v / 4) + 4 g + v % 4 and output row r32 of that tile
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const uint32_t o = o0 + wo * 64 + j * 32 + r32;
+  for (int j = 0; j < TJ; ++j) {
+    const uint32_t o = o0 + wo * WO + j * 32 + r32;
     if (o >= a.M) continue;
     const float s = bf16_to_f32(a.scale[o]);
     const float b = a.bias ? bf16_to_f32(a.bias[o]) : 0.0f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const uint32_t t = t0 + wt * 64 + i * 32 + 8 * (v / 4) + 4 * g + (v % 4);
+        const uint32_t t = t0 + wt * WT + i * 32 + 8 * (v / 4) + 4 * g + (v % 4);
         if (t < a.B) a.y[size_t(t) * a.M + o] = s * acc[i][j][v] + b;
       }
   }
 }
 
+template <int FMT, int BT, int BO, int WT, int WO>
+void launch_gemm(GemmArgs a, hipStream_t stream) {
+  constexpr int kThreads = (BT / WT) * (BO / WO) * 64;
+  a.gx = (a.M + BO - 1) / BO;
+  a.gy = (a.B + BT - 1) / BT;
+  a.group = 4;
+  const uint32_t nb = a.gx * a.gy;
+  const dim3 grid((nb + 7) / 8 * 8), block(kThreads);
+  constexpr size_t shm = 2 * stage_bytes<BT, BO>();
+  hipLaunchKernelGGL((gemm_codes_kernel<FMT, BT, BO, WT, WO>), grid, block, shm, stream, a);
+}
+
+// 256 x 256 tiles (8 wavefronts of 128 x 64; twice the operand reuse) when
+// they still give every compute unit a block, else 128 x 128 tiles (4
+// wavefronts of 64 x 64), which give four times as many blocks and pad fewer
+// tokens.
+template <int FMT>
+void launch_gemm_fmt(const GemmArgs &a, hipStream_t stream, int cus) {
+  const uint64_t big = uint64_t((a.M + 255) / 256) * ((a.B + 255) / 256);
+  if (big >= uint64_t(cus)) launch_gemm<FMT, 256, 256, 128, 64>(a, stream);
+  else launch_gemm<FMT, 128, 128, 64, 64>(a, stream);
+}
+
+// Compute units of the current device, queried once per device.
+int compute_units() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int c = cached[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c <= 0)
+      c = 256;
+    cached[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+
 bool gemm_shape_ok(const eq_layer *L, uint32_t B) {
+  // the grid (blocks of 128 x 128 at least) stays below 2^31 workgroups
   return L && L->scale && L->rows > 0 && L->cols > 0 && L->cols % 16 == 0 && B >= 1 &&
          (L->base_format == kFmtE4M3 || L->base_format == kFmtInt8) &&
-         uint64_t(B) * L->cols < (uint64_t(1) << 40);
+         uint64_t(B) * L->cols < (uint64_t(1) << 40) &&
+         ((uint64_t(B) + 127) / 128) * ((uint64_t(L->rows) + 127) / 128) < (uint64_t(1) << 30);
 }
 
 }  // namespace
@@ -194,12 +270,10 @@ extern "C" int eq_gemm_codes(const eq_layer *L, const uint8_t *codes, const uint
                              uint32_t B, const uint16_t *bias, float *y, hipStream_t stream) {
   if (!gemm_shape_ok(L, B) || !codes || !x || !y) return EQ_EINVAL;
   if ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(x)) & 15) return EQ_EINVAL;
-  GemmArgs a{codes, x, L->scale, bias, y, B, L->rows, L->cols};
-  const dim3 grid((L->rows + kBO - 1) / kBO, (B + kBT - 1) / kBT), block(kThreads);
-  if (L->base_format == kFmtInt8)
-    hipLaunchKernelGGL(gemm_codes_kernel<kFmtInt8>, grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL(gemm_codes_kernel<kFmtE4M3>, grid, block, 0, stream, a);
+  GemmArgs a{codes, x, L->scale, bias, y, B, L->rows, L->cols, 0, 0, 0};
+  const int cus = compute_units();
+  if (L->base_format == kFmtInt8) launch_gemm_fmt<kFmtInt8>(a, stream, cus);
+  else launch_gemm_fmt<kFmtE4M3>(a, stream, cus);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 

@@ -148,27 +148,42 @@ def test_gemm_codes_entry_and_checks(eq):
                           torch.empty(8, dtype=torch.float32, device=_dev()), L2.gemm_workspace())
 
 
-@pytest.mark.parametrize("fmt", [1, 2])
-def test_gemm_config4_full_size_sampled(eq, fmt):
-    """The 8192x28672 layer at 256 tokens: sampled rows x sampled tokens
-    against the oracle's fp64 GEMM of the same rows (codes from the oracle's
-    quantiser on the generated weights)."""
-    spec = config_matrices(4)[0]
-    say("gemm config 4", fmt)
-    w = synth.weights(spec)
-    alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512, base_format=fmt)
-    blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
-                         base_format=fmt)
-    L = eq.Layer(blob, _dev())
-    B = 256
+def _sampled(eq, spec, w, blob, L, B, fmt, seed):
+    """Sampled rows x sampled tokens (always the first and last) of the
+    prefill output against the oracle's fp64 GEMM of the same rows, whose
+    codes come from the oracle's quantiser on the generated weights."""
     x = tokens(spec, B)
     y = gpu_gemm(eq, L, x)
     assert eq.eq_get_status(L) == eq.EQ_OK and np.isfinite(y).all()
-    r = np.random.default_rng(12)
+    r = np.random.default_rng(seed)
     rows = sorted(set(r.choice(spec.rows, 8, replace=False).tolist()) | {0, spec.rows - 1})
     toks = sorted(set(r.choice(B, 6, replace=False).tolist()) | {0, B - 1})
     scale = oracle.container_scales(blob)
     w_rows = oracle.dequant(oracle.quantize(w[rows], scale[rows], fmt), scale[rows], fmt)
-    y_ref = oracle.gemv(w_rows, x[toks])
-    err = rel_err(y[np.ix_(toks, rows)], y_ref)
+    err = rel_err(y[np.ix_(toks, rows)], oracle.gemv(w_rows, x[toks]))
     assert (err <= TOL).all(), err
+
+
+@pytest.mark.parametrize("fmt", [1, 2])
+def test_gemm_config4_full_size_sampled(eq, fmt):
+    """The 8192x28672 layer at 256 tokens (128 x 128 tiles) and the
+    28672x8192 layer at 768 tokens (336 blocks of 256 x 256)."""
+    for spec, B in zip(config_matrices(4), (256, 768)):
+        say("gemm config 4", spec.name, B, fmt)
+        w = synth.weights(spec)
+        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512, base_format=fmt)
+        blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
+                             base_format=fmt)
+        L = eq.Layer(blob, _dev())
+        _sampled(eq, spec, w, blob, L, B, fmt, 12 + B)
+        del L
+
+
+def test_gemm_large_tiles_ragged(eq):
+    """256 x 256 tiles on a shape ragged in every dimension: 4000 rows, 272
+    columns (four 64-column stages and a 16-column one), 4100 tokens."""
+    spec = small_spec(4000, 272, bits=3.0, chunk=16384, lanes=64, seed=4200)
+    w = synth.weights(spec)
+    blob = encode(eq, w, 3.0, 16384, 64, 1)
+    L = eq.Layer(blob, _dev())
+    _sampled(eq, spec, w, blob, L, 4100, 1, 99)

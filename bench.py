@@ -63,9 +63,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="target CPU time of each oracle baseline sample (1 thread, all threads)")
-    ap.add_argument("--workload", choices=("c4", "c5"), default="c4",
+    ap.add_argument("--workload", choices=("c4", "c5", "prefill"), default="c4",
                     help="c4: the 8192x28672 / 28672x8192 pair (default); c5: the 80-layer stack, "
-                         "block-wise vs per-matrix, decode-GEMV B=1 and decode to BF16")
+                         "block-wise vs per-matrix, decode-GEMV B=1 and decode to BF16; prefill: "
+                         "the c4 pair at --tokens tokens, decode to codes + MFMA GEMM")
+    ap.add_argument("--tokens", type=int, default=2048, help="prefill batch (tokens)")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
     ap.add_argument("--base-format", choices=tuple(FORMATS), default="e4m3",
@@ -297,6 +299,100 @@ def run_stack(args):
         "passes": res}), flush=True)
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix throughput, published
+
+
+def run_prefill(args):
+    """Prefill of the config-4 pair: per matrix, the codes decoded into the
+    workspace and the W8A16 MFMA GEMM over --tokens tokens (eq_decode_gemm).
+    Roofline of the GEMM kernel: 2 M N B flops per launch against the dense
+    bf16 peak."""
+    import numpy as np
+    import torch
+
+    import paper_2601_22787_amd as eq
+    import synth
+    from synth.configs import config_matrices
+
+    eq.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    fmt = FORMATS[args.base_format]
+    specs = config_matrices(4)
+    layers = build_layers(eq, synth, specs, 1, dev, fmt)
+    B = args.tokens
+    bufs = []
+    for spec, w, blob, lays in layers:
+        x = torch.from_numpy(np.stack([synth.vector(spec.seed, 100 + t % 64, spec.cols)
+                                       for t in range(B)]).view(np.int16)).to(dev)
+        y = torch.empty(B, spec.rows, dtype=torch.float32, device=dev)
+        bufs.append((lays[0], x, y, lays[0].gemm_workspace()))
+
+    def step(timers=None):
+        for mi, (L, x, y, ws) in enumerate(bufs):
+            codes = ws[:L.rows * L.cols]
+            for op, fn in (("decode_codes", lambda: eq.eq_decode_codes(L, codes)),
+                           ("gemm", lambda: eq.eq_gemm_codes(L, codes, x, B, None, y))):
+                if timers is None:
+                    fn()
+                    continue
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                timers.append((mi, op, e0, e1))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    timers = []
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(args.steps):
+        step(timers)
+    t1.record()
+    torch.cuda.synchronize()
+    for L, _, _, _ in bufs:
+        if eq.eq_get_status(L) != eq.EQ_OK:
+            raise RuntimeError("decode status not OK")
+    ms = t0.elapsed_time(t1) / args.steps
+    per = {}
+    for mi, op, e0, e1 in timers:
+        per.setdefault((mi, op), []).append(e0.elapsed_time(e1) * 1000.0)
+    kernels, g_us, g_flops = {}, 0.0, 0.0
+    for (mi, op), ts in sorted(per.items()):
+        spec = specs[mi]
+        us = float(np.mean(ts))
+        d = {"us": round(us, 2), "us_p50": round(float(np.median(ts)), 2)}
+        if op == "gemm":
+            flops = 2.0 * spec.params * B
+            d["tflops"] = round(flops / us / 1e6, 1)
+            d["mfma_frac"] = round(flops / us / 1e6 / MFMA_BF16_PEAK_TFLOPS, 4)
+            g_us += us
+            g_flops += flops
+        else:
+            d["gparams_per_s"] = round(spec.params / us / 1e3, 1)
+        kernels[f"{spec.name}.{op}"] = d
+    achieved = g_flops / g_us / 1e6
+    params = sum(s.params for s in specs)
+    print(json.dumps({
+        "metric": "prefill tokens/s through the 8192x28672 and 28672x8192 layers (decode to codes "
+                  "+ W8A16 MFMA GEMM); GEMM TFLOP/s and % of the bf16 matrix peak",
+        "value": round(B / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"prefill of the Llama-70B MLP pair 8192x28672 + 28672x8192, "
+                               f"{args.base_format.upper()} codes at ~2.0 bits/param, {B} tokens",
+                   "tokens": B, "params": params, "base_format": args.base_format},
+        "roofline": {"bound": "mfma", "kernel": "gemm_codes_kernel", "op": "gemm",
+                     "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "us_per_launch": round(g_us / len(specs), 2)},
+        "kernels": kernels}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -305,6 +401,9 @@ def main():
         sys.exit(2)
     if args.workload == "c5":
         run_stack(args)
+        return
+    if args.workload == "prefill":
+        run_prefill(args)
         return
     import numpy as np
     import torch

@@ -120,36 +120,42 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
   uint8_t *const cs0 = smem + BT * kXStride;
   constexpr int kStage = stage_bytes<BT, BO>();
 
-  uint4 xr[kXChunks], cr[kCChunks];
-  auto gload = [&](uint32_t k0) {
+  // two register sets of staged loads: the loads of stage k + 2 are issued
+  // while stage k is multiplied, and written to LDS at the end of stage
+  // k + 1, so each load has two stages of compute to arrive
+  struct Staged {
+    uint4 x[kXChunks], c[kCChunks];
+  };
+  auto gload = [&](Staged &st, uint32_t k0) {
 #pragma unroll
     for (int r = 0; r < kXChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 3, col = c & 7;
       const uint32_t t = t0 + row, k = k0 + col * 8;
-      xr[r] = (t < a.B && k < N) ? *reinterpret_cast<const uint4 *>(a.x + size_t(t) * N + k)
-                                 : make_uint4(0, 0, 0, 0);
+      st.x[r] = (t < a.B && k < N) ? *reinterpret_cast<const uint4 *>(a.x + size_t(t) * N + k)
+                                   : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int r = 0; r < kCChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 2, col = c & 3;
       const uint32_t o = o0 + row, k = k0 + col * 16;
-      cr[r] = (o < a.M && k < N) ? *reinterpret_cast<const uint4 *>(a.codes + size_t(o) * N + k)
-                                 : make_uint4(0, 0, 0, 0);
+      st.c[r] = (o < a.M && k < N)
+                    ? *reinterpret_cast<const uint4 *>(a.codes + size_t(o) * N + k)
+                    : make_uint4(0, 0, 0, 0);
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](const Staged &st, int buf) {
     uint8_t *const xs = xs0 + buf * kStage, *const cs = cs0 + buf * kStage;
 #pragma unroll
     for (int r = 0; r < kXChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 3, col = c & 7;
-      *reinterpret_cast<uint4 *>(xs + row * kXStride + col * 16) = xr[r];
+      *reinterpret_cast<uint4 *>(xs + row * kXStride + col * 16) = st.x[r];
     }
 #pragma unroll
     for (int r = 0; r < kCChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 2, col = c & 3;
       uint2 *d = reinterpret_cast<uint2 *>(cs + row * kCStride + col * 16);
-      d[0] = make_uint2(cr[r].x, cr[r].y);
-      d[1] = make_uint2(cr[r].z, cr[r].w);
+      d[0] = make_uint2(st.c[r].x, st.c[r].y);
+      d[1] = make_uint2(st.c[r].z, st.c[r].w);
     }
   };
 
@@ -161,39 +167,55 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-  const uint32_t nk = (N + kBK - 1) / kBK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (uint32_t kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const uint8_t *const xs = xs0 + cur * kStage, *const cs = cs0 + cur * kStage;
-    if (kt + 1 < nk) gload((kt + 1) * kBK);
+  // fragments of 16 columns ks*16 ..: lane (r32, g) holds the 8 consecutive
+  // columns ks*16 + 8g .. of token row r32 (A) and of output row r32 (B)
+  auto frags = [&](const uint8_t *xs, const uint8_t *cs, int ks, bf16x8 *af, bf16x8 *bf) {
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      const int row = wt * WT + i * 32 + r32;
+      af[i] = *reinterpret_cast<const bf16x8 *>(xs + row * kXStride + (ks * 16 + g * 8) * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int row = wo * WO + j * 32 + r32;
+      bf[j] = codes_to_bf16x8<FMT>(
+          *reinterpret_cast<const uint2 *>(cs + row * kCStride + ks * 16 + g * 8));
+    }
+  };
+  auto compute = [&](int buf) {
+    const uint8_t *const xs = xs0 + buf * kStage, *const cs = cs0 + buf * kStage;
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      // fragments: lane (r32, g) holds 8 consecutive columns ks*16 + 8g ..
-      // of token row r32 (A) and of output row r32 (B)
       bf16x8 af[TI], bf[TJ];
-#pragma unroll
-      for (int i = 0; i < TI; ++i) {
-        const int row = wt * WT + i * 32 + r32;
-        af[i] = *reinterpret_cast<const bf16x8 *>(xs + row * kXStride + (ks * 16 + g * 8) * 2);
-      }
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int row = wo * WO + j * 32 + r32;
-        bf[j] = codes_to_bf16x8<FMT>(
-            *reinterpret_cast<const uint2 *>(cs + row * kCStride + ks * 16 + g * 8));
-      }
+      frags(xs, cs, ks, af, bf);
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) lstore(cur ^ 1);
+  };
+
+  // stage kt: LDS buffer kt & 1; register set p holds stage kt + 1 on entry
+  // and receives stage kt + 2 (sets alternate, so the loop is unrolled by 2)
+  const uint32_t nk = (N + kBK - 1) / kBK;
+  Staged s0, s1;
+  gload(s0, 0);
+  lstore(s0, 0);
+  if (nk > 1) gload(s1, kBK);
+  __syncthreads();
+  auto stage = [&](uint32_t kt, Staged &next, Staged &after) {
+    if (kt + 2 < nk) gload(after, (kt + 2) * kBK);
+    compute(kt & 1);
+    if (kt + 1 < nk) lstore(next, (kt + 1) & 1);
     __syncthreads();
+  };
+  uint32_t kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    stage(kt, s1, s0);
+    stage(kt + 1, s0, s1);
   }
+  if (kt < nk) stage(kt, s1, s0);
 
   // epilogue: element v of lane (r32, g) in tile (i, j) is token row
   // 8 (v / 4) + 4 g + v % 4 and output row r32 of that tile

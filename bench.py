@@ -326,13 +326,15 @@ def run_prefill(args):
         x = torch.from_numpy(np.stack([synth.vector(spec.seed, 100 + t % 64, spec.cols)
                                        for t in range(B)]).view(np.int16)).to(dev)
         y = torch.empty(B, spec.rows, dtype=torch.float32, device=dev)
-        bufs.append((lays[0], x, y, lays[0].gemm_workspace()))
+        bufs.append((lays[0], x, y, lays[0].gemm_workspace(B)))
 
     def step(timers=None):
         for mi, (L, x, y, ws) in enumerate(bufs):
-            codes = ws[:L.rows * L.cols]
+            code_bytes = (L.rows * L.cols + 255) // 256 * 256
+            codes, part = ws[:L.rows * L.cols], ws[code_bytes:]
+            part = part if part.numel() else None
             for op, fn in (("decode_codes", lambda: eq.eq_decode_codes(L, codes)),
-                           ("gemm", lambda: eq.eq_gemm_codes(L, codes, x, B, None, y))):
+                           ("gemm", lambda: eq.eq_gemm_codes(L, codes, x, B, None, y, part))):
                 if timers is None:
                     fn()
                     continue

@@ -173,19 +173,30 @@ int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x
  * MFMA (fp32 accumulation) and applies s_i and the bias once per output.
  * Requirements: N (cols) a multiple of 16; codes and x 16-byte aligned. */
 
-/* Workspace bytes of eq_decode_gemm: the M*N codes, rounded up to 256. */
-size_t eq_gemm_workspace_bytes(const eq_layer *L);
+/* Workspace bytes of eq_gemm_codes for B tokens: room for the partial sums
+ * when the input columns are cut into slices (split-K, chosen when the
+ * output tiles alone would leave compute units idle); 0 when no slicing is
+ * needed (or on bad arguments). */
+size_t eq_gemm_codes_workspace_bytes(const eq_layer *L, uint32_t B);
+
+/* Workspace bytes of eq_decode_gemm for B tokens: the M*N codes, rounded up
+ * to 256, then eq_gemm_codes_workspace_bytes(L, B). */
+size_t eq_gemm_workspace_bytes(const eq_layer *L, uint32_t B);
 
 /* y[t][i] = s_i * sum_j v(codes[i][j]) x[t][j] + bias[i] for t < B, any
  * B >= 1.  codes is [M][N] (the output of eq_decode_codes for this layer,
  * device), x is [B][N] BF16 (device), bias is [M] BF16 or NULL, y is
- * [B][M] fp32 (device).  Returns EQ_OK, EQ_EINVAL or EQ_EHIP. */
+ * [B][M] fp32 (device), ws/ws_bytes a device workspace of at least
+ * eq_gemm_codes_workspace_bytes(L, B) bytes (4-byte aligned; may be NULL
+ * when that is 0).  Sliced sums are added in slice order, so results do
+ * not depend on timing.  Returns EQ_OK, EQ_EINVAL or EQ_EHIP. */
 int eq_gemm_codes(const eq_layer *L, const uint8_t *codes, const uint16_t *x, uint32_t B,
-                  const uint16_t *bias, float *y, hipStream_t stream);
+                  const uint16_t *bias, float *y, void *ws, size_t ws_bytes,
+                  hipStream_t stream);
 
-/* eq_decode_codes into ws (at least eq_gemm_workspace_bytes(L) bytes,
- * device, 16-byte aligned), then eq_gemm_codes: Alg. 2 for a batch of B
- * tokens. */
+/* eq_decode_codes into the start of ws (at least eq_gemm_workspace_bytes(L,
+ * B) bytes, device, 16-byte aligned), then eq_gemm_codes with the rest of
+ * ws: Alg. 2 for a batch of B tokens. */
 int eq_decode_gemm(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
                    float *y, void *ws, size_t ws_bytes, hipStream_t stream);
 

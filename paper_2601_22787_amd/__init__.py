@@ -66,9 +66,10 @@ SIGNATURES = {
     "eq_gemv_multi_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_uint32, ctypes.c_uint32]),
     "eq_decode_gemv_multi": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp, _vp,
                                             _vp, ctypes.c_size_t, _vp]),
-    "eq_gemm_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer)]),
+    "eq_gemm_codes_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer), ctypes.c_uint32]),
+    "eq_gemm_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer), ctypes.c_uint32]),
     "eq_gemm_codes": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, _vp, ctypes.c_uint32, _vp, _vp,
-                                     _vp]),
+                                     _vp, ctypes.c_size_t, _vp]),
     "eq_decode_gemm": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp, _vp,
                                       _vp, ctypes.c_size_t, _vp]),
     "eq_get_status": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp]),
@@ -258,12 +259,17 @@ def multi_workspace(layers, B: int):
                        device=layers[0].dev_blob.device)
 
 
-def eq_gemm_workspace_bytes(L) -> int:
-    return lib().eq_gemm_workspace_bytes(ctypes.byref(_raw(L)))
+def eq_gemm_codes_workspace_bytes(L, B: int) -> int:
+    return lib().eq_gemm_codes_workspace_bytes(ctypes.byref(_raw(L)), B)
 
 
-def eq_gemm_codes(L, codes, x, B: int, bias, y, stream=None) -> None:
-    """Prefill GEMM from decoded codes: y[B][M] = x[B][N] W_hat^T + bias."""
+def eq_gemm_workspace_bytes(L, B: int) -> int:
+    return lib().eq_gemm_workspace_bytes(ctypes.byref(_raw(L)), B)
+
+
+def eq_gemm_codes(L, codes, x, B: int, bias, y, ws=None, stream=None) -> None:
+    """Prefill GEMM from decoded codes: y[B][M] = x[B][N] W_hat^T + bias; ws:
+    eq_gemm_codes_workspace_bytes(L, B) bytes (None when that is 0)."""
     import torch
     r = _raw(L)
     if x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
@@ -272,7 +278,9 @@ def eq_gemm_codes(L, codes, x, B: int, bias, y, stream=None) -> None:
     px = _dptr(x, None, B * r.cols)
     pb = _dptr(bias, None, r.rows) if bias is not None else None
     py = _dptr(y, torch.float32, B * r.rows)
-    _check("eq_gemm_codes", lib().eq_gemm_codes(ctypes.byref(r), pc, px, B, pb, py,
+    pw = _dptr(ws) if ws is not None else None
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("eq_gemm_codes", lib().eq_gemm_codes(ctypes.byref(r), pc, px, B, pb, py, pw, nbytes,
                                                 _stream(stream)))
 
 
@@ -410,9 +418,10 @@ class Layer:
         return torch.empty(eq_gemv_workspace_bytes(self, B), dtype=torch.uint8,
                            device=self.dev_blob.device)
 
-    def gemm_workspace(self):
+    def gemm_workspace(self, B: int):
+        """Workspace of eq_decode_gemm for B tokens."""
         import torch
-        return torch.empty(eq_gemm_workspace_bytes(self), dtype=torch.uint8,
+        return torch.empty(eq_gemm_workspace_bytes(self, B), dtype=torch.uint8,
                            device=self.dev_blob.device)
 
 

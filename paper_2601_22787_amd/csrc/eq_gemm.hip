@@ -46,6 +46,9 @@ struct GemmArgs {
   uint32_t B, M, N;
   uint32_t gx, gy;        // output-row blocks, token blocks
   uint32_t group;         // token blocks per group of the launch order
+  uint32_t splits;        // slices of the input columns (split-K), >= 1
+  uint32_t split_stages;  // 64-column stages per slice
+  float *part;            // [splits][B][M] partial sums when splits > 1
 };
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
@@ -76,15 +79,19 @@ __device__ inline bf16x8 codes_to_bf16x8(uint2 c) {
 
 // Launch order.  Workgroups are dealt to the 8 XCDs round robin (each XCD
 // has its own L2), so block i is renumbered so that every XCD receives a
-// contiguous range of the logical order; the logical order walks groups of
-// `group` token blocks, output-row block by output-row block, so that the
-// blocks resident on one XCD share few X and code tiles.  The grid is padded
-// to a multiple of 8; padding blocks exit at once.
-__device__ inline bool block_tile(const GemmArgs &a, uint32_t &ob, uint32_t &tb) {
+// contiguous range of the logical order.  The logical order is slice by
+// slice of the input columns, and within a slice walks groups of `group`
+// token blocks, output-row block by output-row block, so that the blocks
+// resident on one XCD share few X and code tiles.  The grid is padded to a
+// multiple of 8; padding blocks exit at once.
+__device__ inline bool block_tile(const GemmArgs &a, uint32_t &ob, uint32_t &tb,
+                                  uint32_t &split) {
   const uint32_t nb = a.gx * a.gy;
   const uint32_t per = gridDim.x / 8;
-  const uint32_t logical = (blockIdx.x % 8) * per + blockIdx.x / 8;
-  if (logical >= nb) return false;
+  uint32_t logical = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (logical >= nb * a.splits) return false;
+  split = logical / nb;
+  logical %= nb;
   const uint32_t span = a.group * a.gx;          // blocks per group of token blocks
   const uint32_t first = (logical / span) * a.group;
   const uint32_t rows = min(a.group, a.gy - first);
@@ -109,8 +116,8 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
   constexpr int TI = WT / 32, TJ = WO / 32;                   // MFMA tiles per wave
   static_assert(kXChunks * kThreads == BT * 8 && kCChunks * kThreads == BO * 4, "staging");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  uint32_t ob, tb;
-  if (!block_tile(a, ob, tb)) return;
+  uint32_t ob, tb, split;
+  if (!block_tile(a, ob, tb, split)) return;
   const uint32_t N = a.N;
   const uint32_t o0 = ob * BO, t0 = tb * BT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -198,14 +205,18 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
 
   // stage kt: LDS buffer kt & 1; register set p holds stage kt + 1 on entry
   // and receives stage kt + 2 (sets alternate, so the loop is unrolled by 2)
-  const uint32_t nk = (N + kBK - 1) / kBK;
+  // this block's slice: stages [split * split_stages, +split_stages) of all
+  // (N + 63) / 64 (the launcher makes every slice non-empty)
+  const uint32_t k_first = split * a.split_stages;
+  const uint32_t nk = min(a.split_stages, (N + kBK - 1) / kBK - k_first);
+  const uint32_t kbase = k_first * kBK;
   Staged s0, s1;
-  gload(s0, 0);
+  gload(s0, kbase);
   lstore(s0, 0);
-  if (nk > 1) gload(s1, kBK);
+  if (nk > 1) gload(s1, kbase + kBK);
   __syncthreads();
   auto stage = [&](uint32_t kt, Staged &next, Staged &after) {
-    if (kt + 2 < nk) gload(after, (kt + 2) * kBK);
+    if (kt + 2 < nk) gload(after, kbase + (kt + 2) * kBK);
     compute(kt & 1);
     if (kt + 1 < nk) lstore(next, (kt + 1) & 1);
     __syncthreads();
@@ -218,7 +229,9 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
   if (kt < nk) stage(kt, s1, s0);
 
   // epilogue: element v of lane (r32, g) in tile (i, j) is token row
-  // 8 (v / 4) + 4 g + v % 4 and output row r32 of that tile
+  // 8 (v / 4) + 4 g + v % 4 and output row r32 of that tile.  One slice:
+  // y = s * sum + bias; several: the slice's raw sums, reduced afterwards.
+  float *const part = a.part + size_t(split) * a.B * a.M;
 #pragma unroll
   for (int j = 0; j < TJ; ++j) {
     const uint32_t o = o0 + wo * WO + j * 32 + r32;
@@ -230,9 +243,23 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const uint32_t t = t0 + wt * WT + i * 32 + 8 * (v / 4) + 4 * g + (v % 4);
-        if (t < a.B) a.y[size_t(t) * a.M + o] = s * acc[i][j][v] + b;
+        if (t >= a.B) continue;
+        if (a.splits > 1) part[size_t(t) * a.M + o] = acc[i][j][v];
+        else a.y[size_t(t) * a.M + o] = s * acc[i][j][v] + b;
       }
   }
+}
+
+// y[t][o] = s_o * (partial sums of the slices, in slice order) + bias_o:
+// the same result whatever the timing of the slices.
+__global__ void reduce_splits_kernel(GemmArgs a) {
+  const size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const size_t n = size_t(a.B) * a.M;
+  if (i >= n) return;
+  const uint32_t o = uint32_t(i % a.M);
+  float sum = 0.0f;
+  for (uint32_t k = 0; k < a.splits; ++k) sum += a.part[k * n + i];
+  a.y[i] = bf16_to_f32(a.scale[o]) * sum + (a.bias ? bf16_to_f32(a.bias[o]) : 0.0f);
 }
 
 template <int FMT, int BT, int BO, int WT, int WO>
@@ -241,21 +268,55 @@ void launch_gemm(GemmArgs a, hipStream_t stream) {
   a.gx = (a.M + BO - 1) / BO;
   a.gy = (a.B + BT - 1) / BT;
   a.group = 4;
-  const uint32_t nb = a.gx * a.gy;
+  const uint32_t nb = a.gx * a.gy * a.splits;
   const dim3 grid((nb + 7) / 8 * 8), block(kThreads);
   constexpr size_t shm = 2 * stage_bytes<BT, BO>();
   hipLaunchKernelGGL((gemm_codes_kernel<FMT, BT, BO, WT, WO>), grid, block, shm, stream, a);
 }
 
-// 256 x 256 tiles (8 wavefronts of 128 x 64; twice the operand reuse) when
-// they still give every compute unit a block, else 128 x 128 tiles (4
-// wavefronts of 64 x 64), which give four times as many blocks and pad fewer
-// tokens.
+// Tile and split-K choice: 256 x 256 tiles (8 wavefronts of 128 x 64; twice
+// the operand reuse) when they still give every compute unit a block, else
+// 128 x 128 tiles (4 wavefronts of 64 x 64), which give four times as many
+// blocks and pad fewer tokens; when even those leave compute units idle,
+// the input columns are cut into slices (at most 16, each at least 4 stages
+// of 64 columns) whose partial sums are reduced in slice order.
+struct GemmPlan {
+  bool big;
+  uint32_t splits, split_stages;
+};
+
+GemmPlan plan_gemm(uint32_t B, uint32_t M, uint32_t N, int cus) {
+  GemmPlan p{false, 1, 0};
+  const uint32_t stages = (N + kBK - 1) / kBK;
+  p.split_stages = stages;
+  const uint64_t big = uint64_t((M + 255) / 256) * ((B + 255) / 256);
+  if (big >= uint64_t(cus)) {
+    p.big = true;
+    return p;
+  }
+  const uint64_t tiles = uint64_t((M + 127) / 128) * ((B + 127) / 128);
+  if (tiles >= uint64_t(cus)) return p;
+  uint64_t want = (uint64_t(cus) + tiles - 1) / tiles;
+  want = want < 16 ? want : 16;
+  const uint64_t cap = stages / 4;
+  const uint64_t sp = want < cap ? want : cap;
+  if (sp <= 1) return p;
+  p.split_stages = uint32_t((stages + sp - 1) / sp);
+  p.splits = (stages + p.split_stages - 1) / p.split_stages;  // every slice non-empty
+  return p;
+}
+
 template <int FMT>
-void launch_gemm_fmt(const GemmArgs &a, hipStream_t stream, int cus) {
-  const uint64_t big = uint64_t((a.M + 255) / 256) * ((a.B + 255) / 256);
-  if (big >= uint64_t(cus)) launch_gemm<FMT, 256, 256, 128, 64>(a, stream);
+void launch_gemm_fmt(GemmArgs a, const GemmPlan &p, hipStream_t stream) {
+  a.splits = p.splits;
+  a.split_stages = p.split_stages;
+  if (p.big) launch_gemm<FMT, 256, 256, 128, 64>(a, stream);
   else launch_gemm<FMT, 128, 128, 64, 64>(a, stream);
+  if (p.splits > 1) {
+    const size_t n = size_t(a.B) * a.M;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(uint32_t((n + 255) / 256)), dim3(256), 0, stream,
+                       a);
+  }
 }
 
 // Compute units of the current device, queried once per device.
@@ -281,21 +342,38 @@ bool gemm_shape_ok(const eq_layer *L, uint32_t B) {
          ((uint64_t(B) + 127) / 128) * ((uint64_t(L->rows) + 127) / 128) < (uint64_t(1) << 30);
 }
 
+size_t round256(size_t v) { return (v + 255) / 256 * 256; }
+
+size_t partial_bytes(const eq_layer *L, uint32_t B) {
+  const GemmPlan p = plan_gemm(B, L->rows, L->cols, compute_units());
+  return p.splits > 1 ? round256(size_t(p.splits) * B * L->rows * sizeof(float)) : 0;
+}
+
 }  // namespace
 
-extern "C" size_t eq_gemm_workspace_bytes(const eq_layer *L) {
-  if (!L || L->rows == 0 || L->cols == 0) return 0;
-  return (size_t(L->rows) * L->cols + 255) / 256 * 256;
+extern "C" size_t eq_gemm_codes_workspace_bytes(const eq_layer *L, uint32_t B) {
+  if (!gemm_shape_ok(L, B)) return 0;
+  return partial_bytes(L, B);
+}
+
+extern "C" size_t eq_gemm_workspace_bytes(const eq_layer *L, uint32_t B) {
+  if (!gemm_shape_ok(L, B)) return 0;
+  return round256(size_t(L->rows) * L->cols) + partial_bytes(L, B);
 }
 
 extern "C" int eq_gemm_codes(const eq_layer *L, const uint8_t *codes, const uint16_t *x,
-                             uint32_t B, const uint16_t *bias, float *y, hipStream_t stream) {
+                             uint32_t B, const uint16_t *bias, float *y, void *ws,
+                             size_t ws_bytes, hipStream_t stream) {
   if (!gemm_shape_ok(L, B) || !codes || !x || !y) return EQ_EINVAL;
   if ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(x)) & 15) return EQ_EINVAL;
-  GemmArgs a{codes, x, L->scale, bias, y, B, L->rows, L->cols, 0, 0, 0};
-  const int cus = compute_units();
-  if (L->base_format == kFmtInt8) launch_gemm_fmt<kFmtInt8>(a, stream, cus);
-  else launch_gemm_fmt<kFmtE4M3>(a, stream, cus);
+  const GemmPlan p = plan_gemm(B, L->rows, L->cols, compute_units());
+  if (p.splits > 1 && (!ws || ws_bytes < partial_bytes(L, B) ||
+                       (reinterpret_cast<uintptr_t>(ws) & 3)))
+    return EQ_EINVAL;
+  GemmArgs a{codes, x, L->scale, bias, y, B, L->rows, L->cols, 0, 0, 0, 1, 0,
+             static_cast<float *>(ws)};
+  if (L->base_format == kFmtInt8) launch_gemm_fmt<kFmtInt8>(a, p, stream);
+  else launch_gemm_fmt<kFmtE4M3>(a, p, stream);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
@@ -303,9 +381,11 @@ extern "C" int eq_decode_gemm(const eq_layer *L, const uint16_t *x, uint32_t B,
                               const uint16_t *bias, float *y, void *ws, size_t ws_bytes,
                               hipStream_t stream) {
   if (!gemm_shape_ok(L, B) || !x || !y || !ws) return EQ_EINVAL;
-  if (ws_bytes < eq_gemm_workspace_bytes(L)) return EQ_EINVAL;
+  if (ws_bytes < eq_gemm_workspace_bytes(L, B)) return EQ_EINVAL;
   uint8_t *codes = static_cast<uint8_t *>(ws);
+  const size_t code_bytes = round256(size_t(L->rows) * L->cols);
   const int rc = eq_decode_codes(L, codes, stream);
   if (rc != EQ_OK) return rc;
-  return eq_gemm_codes(L, codes, x, B, bias, y, stream);
+  return eq_gemm_codes(L, codes, x, B, bias, y, codes + code_bytes, ws_bytes - code_bytes,
+                       stream);
 }

@@ -54,7 +54,7 @@ def gpu_gemm(eq, L, x_bits, bias_bits=None):
     x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
     bias = None if bias_bits is None else torch.from_numpy(bias_bits.view(np.int16)).to(_dev())
     y = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
-    eq.eq_decode_gemm(L, x, B, bias, y, L.gemm_workspace())
+    eq.eq_decode_gemm(L, x, B, bias, y, L.gemm_workspace(B))
     return y.cpu().numpy()
 
 
@@ -130,7 +130,9 @@ def test_gemm_codes_entry_and_checks(eq):
     codes = torch.empty(spec.params, dtype=torch.uint8, device=_dev())
     eq.eq_decode_codes(L, codes)
     y1 = torch.empty(20, spec.rows, dtype=torch.float32, device=_dev())
-    eq.eq_gemm_codes(L, codes, x, 20, None, y1)
+    nws = eq.eq_gemm_codes_workspace_bytes(L, 20)
+    ws = torch.empty(nws, dtype=torch.uint8, device=_dev()) if nws else None
+    eq.eq_gemm_codes(L, codes, x, 20, None, y1, ws)
     y2 = torch.from_numpy(gpu_gemm(eq, L, x_bits)).to(_dev())
     assert torch.equal(y1, y2)
     # the GEMV computes the same products (different summation order)
@@ -138,14 +140,43 @@ def test_gemm_codes_entry_and_checks(eq):
     eq.eq_decode_gemv(L, x[:8].contiguous(), 8, None, y3, L.workspace(8))
     assert (rel_err(y3.cpu().numpy(), y1[:8].cpu().numpy()) < 1e-5).all()
     with pytest.raises(eq.EqError):  # misaligned activations
-        eq.eq_gemm_codes(L, codes, x.view(-1)[1:].view(torch.int16), 1, None, y1)
+        eq.eq_gemm_codes(L, codes, x.view(-1)[1:].view(torch.int16), 1, None, y1, ws)
     with pytest.raises(eq.EqError):  # workspace too small
-        eq.eq_decode_gemm(L, x, 20, None, y1, L.gemm_workspace()[:100])
+        eq.eq_decode_gemm(L, x, 20, None, y1, L.gemm_workspace(20)[:100])
     spec2 = small_spec(8, 200, bits=2.0, chunk=1600, lanes=64, seed=4101)
     L2 = eq.Layer(encode(eq, synth.weights(spec2), 2.0, 1600, 64, 1), _dev())
     with pytest.raises(eq.EqError):  # N not a multiple of 16
         eq.eq_decode_gemm(L2, torch.zeros(200, dtype=torch.int16, device=_dev()), 1, None,
-                          torch.empty(8, dtype=torch.float32, device=_dev()), L2.gemm_workspace())
+                          torch.empty(8, dtype=torch.float32, device=_dev()),
+                          torch.empty(256, dtype=torch.uint8, device=_dev()))
+
+
+@pytest.mark.parametrize("N,B", [(4096, 20), (4112, 9), (2048, 128)])
+def test_gemm_split_k(eq, N, B):
+    """Few output tiles and long rows: the input columns are cut into slices
+    (16 slices of 4 stages; 13 uneven slices of 5 of 65 stages; 8 of 4), the
+    partial sums reduced in slice order.  Within the bar, deterministic, and
+    the workspace is required."""
+    say("split-K", N, B)
+    spec = small_spec(100, N, bits=2.0, chunk=8192, lanes=64, seed=4300 + N + B)
+    w = synth.weights(spec)
+    blob = encode(eq, w, 2.0, 8192, 64, 1)
+    L = eq.Layer(blob, _dev())
+    assert eq.eq_gemm_codes_workspace_bytes(L, B) > 0
+    rc, q = oracle.container_decode(blob)
+    w_ref = oracle.dequant(q, oracle.container_scales(blob))
+    x = tokens(spec, B)
+    bias = synth.bias(spec)
+    y = gpu_gemm(eq, L, x, bias)
+    err = rel_err(y, oracle.gemv(w_ref, x, bias))
+    assert np.isfinite(y).all() and (err <= TOL).all(), err.max()
+    assert np.array_equal(y, gpu_gemm(eq, L, x, bias))
+    codes = torch.empty(spec.params, dtype=torch.uint8, device=_dev())
+    eq.eq_decode_codes(L, codes)
+    xt = torch.from_numpy(x.view(np.int16)).to(_dev())
+    yt = torch.empty(B, spec.rows, dtype=torch.float32, device=_dev())
+    with pytest.raises(eq.EqError):  # the slices need the workspace
+        eq.eq_gemm_codes(L, codes, xt, B, None, yt, None)
 
 
 def _sampled(eq, spec, w, blob, L, B, fmt, seed):

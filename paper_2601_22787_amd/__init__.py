@@ -430,8 +430,8 @@ def _raw(L) -> eq_layer:
 
 
 def smoke() -> None:
-    """One small decode (codes, BF16) and fused GEMV (B = 1, 3) on cuda:0,
-    checked against the CPU oracle."""
+    """One small decode (codes, BF16), fused GEMV (B = 3) and prefill (24
+    tokens) on cuda:0, checked against the CPU oracle."""
     import sys
 
     import torch
@@ -469,4 +469,15 @@ def smoke() -> None:
     y_ref = oracle.gemv(w_ref, synth.activations(spec, B))
     err = np.abs(y.cpu().numpy() - y_ref).max(axis=1) / np.abs(y_ref).max(axis=1)
     assert (err <= 1e-2).all(), f"gemv error {err}"
-    print(f"smoke ok: codes/bf16 bit-exact, gemv max rel err {err.max():.2e}")
+    # prefill: decode to codes + matrix-core GEMM over 24 tokens
+    T = 24
+    xt_bits = np.stack([synth.vector(spec.seed, 40 + t, spec.cols) for t in range(T)])
+    xt = torch.from_numpy(xt_bits.view(np.int16)).to(dev)
+    yt = torch.empty(T, spec.rows, dtype=torch.float32, device=dev)
+    eq_decode_gemm(L, xt, T, None, yt, L.gemm_workspace(T))
+    _check("eq_get_status", eq_get_status(L))
+    yt_ref = oracle.gemv(w_ref, xt_bits)
+    err_t = np.abs(yt.cpu().numpy() - yt_ref).max(axis=1) / np.abs(yt_ref).max(axis=1)
+    assert (err_t <= 1e-2).all(), f"prefill error {err_t}"
+    print(f"smoke ok: codes/bf16 bit-exact, gemv max rel err {err.max():.2e}, "
+          f"prefill max rel err {err_t.max():.2e}")

@@ -91,6 +91,10 @@ def test_layer_init_rejects_bad_containers(blob):
         "scale_inf": _patch(blob, info.off_scale + 6, 0x7F80, np.uint16),
         "padding": _patch(blob, 56, info.total_words + 8, np.uint64),
         "section": _patch(blob, 128, 1 << 40, np.uint64),
+        # M * N >= 2^32 (element indices are 32-bit), the chunk count adjusted
+        "too_large": _patch(_patch(_patch(blob, 16, 65536, np.uint32), 20, 65536, np.uint32),
+                            28, (1 << 32) // 2048, np.uint32),
+        "empty": _patch(blob, 16, 0, np.uint32),
     }
     for name, b in bad.items():
         rc, _ = _init(b)

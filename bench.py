@@ -398,8 +398,9 @@ def run_prefill(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              f"(the path would shard by output rows, see DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: runs on one GPU only; --gpus {args.gpus} is not supported (several "
+              f"GPUs would each hold and decode their own output rows of every layer)",
+              file=sys.stderr)
         sys.exit(2)
     if args.workload == "c5":
         run_stack(args)

@@ -105,8 +105,11 @@ __device__ inline bool block_tile(const GemmArgs &a, uint32_t &ob, uint32_t &tb,
 // input columns [64 k, 64 k + 64); the next stage's global loads are in
 // flight in registers while the current one is multiplied, and are written
 // to the other LDS buffer afterwards (one barrier per stage).  Out-of-range
-// tokens, rows and columns are loaded as zeros (N is a multiple of 16, so a
-// 16-byte chunk is either wholly inside a row or wholly past its end).
+// tokens, rows and columns read as zeros (N is a multiple of 16, so a
+// 16-byte chunk is either wholly inside a row or wholly past its end): every
+// lane loads from an address clamped into the matrix and selects zero at
+// the LDS store, so the loads are unconditional and the wait before the
+// stores covers only the stage being stored, not the one issued after it.
 template <int FMT, int BT, int BO, int WT, int WO>
 __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(GemmArgs a) {
   constexpr int kWaves = (BT / WT) * (BO / WO);
@@ -132,22 +135,27 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
   // k + 1, so each load has two stages of compute to arrive
   struct Staged {
     uint4 x[kXChunks], c[kCChunks];
+    uint32_t ok;  // bit r: x chunk r in range; bit 16 + r: code chunk r
   };
   auto gload = [&](Staged &st, uint32_t k0) {
+    st.ok = 0;
 #pragma unroll
     for (int r = 0; r < kXChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 3, col = c & 7;
       const uint32_t t = t0 + row, k = k0 + col * 8;
-      st.x[r] = (t < a.B && k < N) ? *reinterpret_cast<const uint4 *>(a.x + size_t(t) * N + k)
-                                   : make_uint4(0, 0, 0, 0);
+      const uint4 v = *reinterpret_cast<const uint4 *>(a.x + size_t(min(t, a.B - 1)) * N +
+                                                       min(k, N - 8));
+      st.x[r] = v;
+      st.ok |= uint32_t(t < a.B && k < N) << r;
     }
 #pragma unroll
     for (int r = 0; r < kCChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 2, col = c & 3;
       const uint32_t o = o0 + row, k = k0 + col * 16;
-      st.c[r] = (o < a.M && k < N)
-                    ? *reinterpret_cast<const uint4 *>(a.codes + size_t(o) * N + k)
-                    : make_uint4(0, 0, 0, 0);
+      const uint4 v = *reinterpret_cast<const uint4 *>(a.codes + size_t(min(o, a.M - 1)) * N +
+                                                       min(k, N - 16));
+      st.c[r] = v;
+      st.ok |= uint32_t(o < a.M && k < N) << (16 + r);
     }
   };
   auto lstore = [&](const Staged &st, int buf) {
@@ -155,14 +163,16 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
 #pragma unroll
     for (int r = 0; r < kXChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 3, col = c & 7;
-      *reinterpret_cast<uint4 *>(xs + row * kXStride + col * 16) = st.x[r];
+      *reinterpret_cast<uint4 *>(xs + row * kXStride + col * 16) =
+          (st.ok >> r & 1) ? st.x[r] : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int r = 0; r < kCChunks; ++r) {
       const int c = tid + kThreads * r, row = c >> 2, col = c & 3;
+      const uint4 v = (st.ok >> (16 + r) & 1) ? st.c[r] : make_uint4(0, 0, 0, 0);
       uint2 *d = reinterpret_cast<uint2 *>(cs + row * kCStride + col * 16);
-      d[0] = make_uint2(st.c[r].x, st.c[r].y);
-      d[1] = make_uint2(st.c[r].z, st.c[r].w);
+      d[0] = make_uint2(v.x, v.y);
+      d[1] = make_uint2(v.z, v.w);
     }
   };
 
@@ -216,7 +226,9 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
   if (nk > 1) gload(s1, kbase + kBK);
   __syncthreads();
   auto stage = [&](uint32_t kt, Staged &next, Staged &after) {
-    if (kt + 2 < nk) gload(after, kbase + (kt + 2) * kBK);
+    // near the end the last stage is loaded again (and not stored): the
+    // loads stay unconditional, so the waits can count them exactly
+    gload(after, kbase + min(kt + 2, nk - 1) * kBK);
     compute(kt & 1);
     if (kt + 1 < nk) lstore(next, (kt + 1) & 1);
     __syncthreads();

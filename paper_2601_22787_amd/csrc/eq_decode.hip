@@ -106,6 +106,9 @@ __device__ inline uint32_t lds_addr(const void *p) {
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
 }
 __device__ inline uint32_t lds_read_u16(uint32_t addr) { return *(lds_u16 *)(addr); }
+__device__ inline void lds_write_u16(uint32_t addr, uint32_t v) {
+  *(__attribute__((address_space(3))) uint16_t *)(addr) = static_cast<uint16_t>(v);
+}
 
 // Byte address of the row-table entry of the code in bits 24..31 of a slot
 // entry e (bits 13..23 of e are zero, so e >> 23 is twice the code); tab is
@@ -273,8 +276,10 @@ struct DecodeLds {
 // (table address) | (2 * code).
 constexpr uint32_t kWinBytes = kWin * sizeof(uint16_t);
 constexpr uint32_t kRowTabBytes = 256 * sizeof(uint16_t);
+// BF16 output (uniform rows): per wavefront a row table and a staging area
+// of one step's values (at most 256 BF16 values, the size of a row table).
 __host__ __device__ inline size_t dyn_lds_bytes(uint32_t waves, size_t xbytes, bool rowtabs) {
-  return size_t(waves) * kWinBytes + xbytes + (rowtabs ? kRowTabBytes * (waves + 1) : 0);
+  return size_t(waves) * kWinBytes + xbytes + (rowtabs ? kRowTabBytes * (2 * waves + 1) : 0);
 }
 
 // Stage the decode tables (and nothing else) into LDS.
@@ -318,6 +323,10 @@ struct Decoder {
   __amdgpu_buffer_rsrc_t out_rsrc;
   uint32_t row, first_row, row_end;
   uint16_t *rowtab;  // this wavefront's row table (BF16 output, uniform rows)
+  // BF16 output of the pipelined steps: a step's values are written to the
+  // staging area in column order, then each lane reads back its G adjacent
+  // columns and stores them with one store (instead of one per state).
+
   uint32_t tab;      // its LDS address over 512
   uint32_t prow[G], pcol[G];
   float acc[UNIFORM ? 1 : G][kMaxBatch];
@@ -329,6 +338,7 @@ struct Decoder {
   static constexpr bool PIPE =
       G >= 2 && (MODE == kCodes || (UNIFORM && (MODE == kBf16 || PAIR)));
   static constexpr int LAG = G / 2;  // processing trails issue by LAG states
+  static constexpr bool STAGED = PIPE && MODE == kBf16;
   uint2 ent[G];      // slot entries in flight
   uint32_t qv[G];    // x >> P of the state whose entry is in flight
   uint64_t nd[G];    // renormalisation masks of the last processed step
@@ -336,16 +346,23 @@ struct Decoder {
   uint32_t sym[G];   // slot entry .x of the last processed step (code in bits 24..31)
   uint32_t outv[G];  // BF16 values in flight, stored at step offset okk[g]
   uint32_t okk[G];
+  uint32_t stg;                // staging area (LDS byte address) + 2 * lane
+  bool staged;                 // output through the staging area (wave-uniform)
+  uint32_t pend[G > 1 ? G / 2 : 1];  // a step's G values of this lane, read back
+  uint32_t pkk;                // their step offset
+  bool pend_valid;
   uint32_t xv1[G / 2 > 0 ? G / 2 : 1];    // activation pairs of a state pair (batch 1)
   uint4 xv8[G / 2 > 0 ? G / 2 : 1][2];     // (batch > 1), per 4-row batch group
   uint32_t icol;     // column of the first symbol of the step being issued
 
   __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
                                      const DecodeLds &sm, uint4 *win4_, uint16_t *rowtab_,
-                                     const void *xl_)
+                                     const void *xl_, uint16_t *stage_ = nullptr)
       : a(a_), slot(sm.slot), val(sm.val), win4(win4_),
         win(reinterpret_cast<const uint16_t *>(win4_)), xl(xl_), lane(lane_), c(c_),
         rowtab(rowtab_) {
+    staged = uniform(stage_ != nullptr ? 1u : 0u) != 0;
+    stg = stage_ ? uniform(lds_addr(stage_)) + 2 * lane_ : 0;
     N = a.cols;
     k0 = c * a.chunk_syms;
     nc = min(a.chunk_syms, a.n - k0);
@@ -651,15 +668,56 @@ struct Decoder {
     }
   }
 
+  // Staged BF16 output of the pipelined steps: a step's values are written to
+  // the wavefront's staging area in column order (state g of lane l at column
+  // 64 g + l); then each lane reads back its G adjacent columns (G lane ..)
+  // and stores them with one store, when the next step is read back (or at
+  // the end of the run).  One store per step instead of one per state.
+  __device__ __forceinline__ void stage_put(int g, uint32_t v) {
+    lds_write_u16(stg + 2 * kWave * g, v);
+  }
+  __device__ __forceinline__ void stage_store() {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    if (G >= 4)
+      __builtin_amdgcn_raw_buffer_store_b64(u32x2{pend[0], pend[G >= 4 ? 1 : 0]}, out_rsrc,
+                                            2 * G * lane, 2 * pkk, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b32(pend[0], out_rsrc, 2 * G * lane, 2 * pkk, 0);
+  }
+  // Read back the staged step at chunk offset kk (storing the previous one).
+  __device__ __forceinline__ void stage_get(uint32_t kk) {
+    typedef const __attribute__((address_space(3))) uint64_t lds_u64;
+    typedef const __attribute__((address_space(3))) uint32_t lds_u32;
+    if (pend_valid) stage_store();
+    const uint32_t addr = stg + 2 * (G - 1) * lane;  // staging area + 2 G lane
+    if (G >= 4) {
+      const uint64_t v = *(lds_u64 *)(addr);
+      pend[0] = static_cast<uint32_t>(v);
+      pend[G >= 4 ? 1 : 0] = static_cast<uint32_t>(v >> 32);
+    } else {
+      pend[0] = *(lds_u32 *)(addr);
+    }
+    pkk = kk;
+    pend_valid = true;
+  }
+
   // Issue state g of step t: finish its renormalisation from the previous
-  // step (unless FIRST), store its pending BF16 value, start its slot read.
-  template <bool FIRST>
+  // step (unless FIRST), put out its pending BF16 value (STG: into the
+  // staging area; after the last state, read the step back), start its slot
+  // read.
+  template <bool FIRST, bool STG>
   __device__ __forceinline__ void pissue(int g, const uint32_t *xt) {
     if (!FIRST) {
       x[g] = select_by_mask(nd[g], x[g], (x[g] << 16) | wd[g]);
-      if (MODE == kBf16)
-        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
-                                              2 * (lane + g * kWave), 2 * okk[g], 0);
+      if (MODE == kBf16) {
+        if (STG) {
+          stage_put(g, outv[g]);
+          if (g == G - 1) stage_get(okk[g]);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
+                                                2 * (lane + g * kWave), 2 * okk[g], 0);
+        }
+      }
     }
     ent[g] = slot[x[g] & mask];
     qv[g] = x[g] >> P;
@@ -711,14 +769,21 @@ struct Decoder {
   // of step t.  xt: step t's activation tile (kXTile), stride xs per step.
   __device__ __forceinline__ void prun(uint32_t t, uint32_t t_end, const uint32_t *xt,
                                        uint32_t xs) {
+    if (STAGED && staged) prun_impl<true>(t, t_end, xt, xs);
+    else prun_impl<false>(t, t_end, xt, xs);
+  }
+  template <bool STG>
+  __device__ __forceinline__ void prun_impl(uint32_t t, uint32_t t_end, const uint32_t *xt,
+                                            uint32_t xs) {
     static_assert(2 * W <= kWin - kHalf, "a step and a half must fit the window");
+    if (STG) pend_valid = false;
     slide();
     if (MODE != kCodes) {
       row_check(t);
       icol = k0 + t * W + N - row_end;
     }
 #pragma unroll
-    for (int g = 0; g < G; ++g) pissue<true>(g, xt);
+    for (int g = 0; g < G; ++g) pissue<true, STG>(g, xt);
 #pragma unroll
     for (int h = 0; h < LAG; ++h) pproc(h, t * W);
     for (++t; t < t_end; ++t) {
@@ -731,7 +796,7 @@ struct Decoder {
       }
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        pissue<false>(g, xt);
+        pissue<false, STG>(g, xt);
         if (g < LAG) {
           pproc(g + G - LAG, (t - 1) * W);
         } else {
@@ -745,9 +810,15 @@ struct Decoder {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       x[g] = select_by_mask(nd[g], x[g], (x[g] << 16) | wd[g]);
-      if (MODE == kBf16)
+      if (MODE == kBf16 && !STG)
         __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
                                               2 * (lane + g * kWave), 2 * okk[g], 0);
+    }
+    if (STG) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) stage_put(g, outv[g]);
+      stage_get(okk[G - 1]);
+      stage_store();
     }
   }
 
@@ -826,15 +897,19 @@ __device__ __forceinline__ void decode_block(const Args &a, uint32_t blk, uint32
 
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint32_t wave = uniform(threadIdx.x / kWave);
-  uint16_t *rowtab = nullptr;
+  uint16_t *rowtab = nullptr, *stage = nullptr;
   if (MODE == kBf16 && UNIFORM) {
     char *base = reinterpret_cast<char *>(xl);
     base += (0u - lds_addr(base)) & (kRowTabBytes - 1);
     rowtab = reinterpret_cast<uint16_t *>(base) + wave * 256;
+    // staged output (G values per store) needs the output's steps aligned
+    constexpr uintptr_t step_align = 2 * G;
+    if (G >= 2 && (reinterpret_cast<uintptr_t>(a.wout) & (step_align - 1)) == 0)
+      stage = reinterpret_cast<uint16_t *>(base) + (waves + wave) * 256;
   }
   uint4 *const win = dyn + wave * (kWinBytes / sizeof(uint4));
   for (uint32_t c = uniform(blk * waves + wave); c < a.n_chunks; c += nblk * waves) {
-    Decoder<G, MODE, UNIFORM, XS, NB, FMT> d(a, c, lane, sm, win, rowtab, xl);
+    Decoder<G, MODE, UNIFORM, XS, NB, FMT> d(a, c, lane, sm, win, rowtab, xl, stage);
     d.run();
   }
 }
@@ -1190,12 +1265,13 @@ int launch_tiled(Args a, hipStream_t s, const DeviceFacts &f) {
 size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
 // Multi-layer launch shape: enough wavefronts per block that two blocks per
-// compute unit hold every chunk; each layer gets whole blocks.
-uint32_t multi_shape(const MultiArgs &m, int cus, MultiArgs &out) {
+// compute unit hold every chunk (at most max_waves); each layer gets whole
+// blocks.
+uint32_t multi_shape(const MultiArgs &m, int cus, uint32_t max_waves, MultiArgs &out) {
   uint64_t total = 0;
   for (uint32_t i = 0; i < m.n; ++i) total += m.a[i].n_chunks;
   uint32_t waves = uint32_t((total + 2 * uint64_t(cus) - 1) / (2 * uint64_t(cus)));
-  waves = waves < 1 ? 1 : (waves > kMaxWaves ? kMaxWaves : waves);
+  waves = waves < 1 ? 1 : (waves > max_waves ? max_waves : waves);
   out = m;
   uint32_t end = 0;
   for (uint32_t i = 0; i < m.n; ++i) {
@@ -1208,7 +1284,14 @@ uint32_t multi_shape(const MultiArgs &m, int cus, MultiArgs &out) {
 template <int MODE, int XS, int NB, int FMT>
 int launch_multi_fmt(const MultiArgs &m0, size_t xbytes, hipStream_t s, const DeviceFacts &f) {
   MultiArgs m;
-  const uint32_t waves = multi_shape(m0, f.cus, m);
+  // BF16: no more wavefronts than let two blocks share a compute unit's LDS
+  // (16 would leave room for one, with row tables and staging areas)
+  uint32_t max_waves = kMaxWaves;
+  if (MODE == kBf16)
+    while (max_waves > 1 &&
+           2 * (kStaticLds + dyn_lds_bytes(max_waves, xbytes, true)) > size_t(f.lds_per_block))
+      --max_waves;
+  const uint32_t waves = multi_shape(m0, f.cus, max_waves, m);
   const dim3 grid(m.blk_end[m.n - 1]), block(waves * kWave);
   const size_t shm = dyn_lds_bytes(waves, xbytes, MODE == kBf16);
   switch (m.a[0].lanes) {
@@ -1385,7 +1468,7 @@ extern "C" int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const 
     m.a[i].ws = reinterpret_cast<float *>(static_cast<char *>(ws) + off[i]);
   }
   MultiArgs shaped;
-  const uint32_t waves = multi_shape(m, f.cus, shaped);
+  const uint32_t waves = multi_shape(m, f.cus, kMaxWaves, shaped);
   const size_t xbytes = xlds_bytes(m.a[0]);
   const bool joint = n > 1 && joint_ok(L, n) && xbytes <= kMaxXLdsBytes &&
                      kStaticLds + dyn_lds_bytes(waves, xbytes, false) <= size_t(f.lds_per_block);

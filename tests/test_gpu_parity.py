@@ -346,3 +346,39 @@ def test_config4_full_size_sampled(eq, c4_layers):
             err = rel_err(y[:, rows], y_ref)
             assert (err <= TOL).all(), (spec.name, B, err)
             assert np.isfinite(y).all()
+
+
+@pytest.mark.parametrize("lanes,N", [(128, 1024), (256, 2048)])
+def test_bf16_output_alignment(eq, lanes, N):
+    """Full steps of W = 128 and 256 write a step's values through the
+    wavefront's LDS staging area, G adjacent columns per lane and store, when
+    the output is aligned to G values; otherwise one value per state and
+    store.  Both give the oracle's BF16 and codes bit for bit, through the
+    single-layer and the block-wise launch, at output offsets of 0 to 3
+    elements."""
+    say("bf16 alignment", lanes, N)
+    spec = small_spec(48, N, bits=2.0, chunk=8192, lanes=lanes, seed=5100 + lanes)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, 2.0)
+    blob = eq.eqe_encode(w, alpha, chunk_syms=8192, lanes=lanes)
+    L = eq.Layer(blob, _dev())
+    rc, q_ref = oracle.container_decode(blob)
+    assert rc == oracle.OK
+    w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
+    n = spec.rows * spec.cols
+    for off in range(4):
+        full = torch.full((n + 8,), -1, dtype=torch.int16, device=_dev())
+        eq.eq_decode_bf16(L, full[off:off + n])
+        got = full.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got[off:off + n].reshape(spec.rows, N), w_ref), off
+        assert (got[:off] == 0xFFFF).all() and (got[off + n:] == 0xFFFF).all(), off
+        full.fill_(-1)
+        eq.eq_decode_bf16_multi([L, L], [full[off:off + n], full[off:off + n]])
+        got = full.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got[off:off + n].reshape(spec.rows, N), w_ref), off
+        codes = torch.full((n + 8,), 0xA5, dtype=torch.uint8, device=_dev())
+        eq.eq_decode_codes(L, codes[off:off + n])
+        got = codes.cpu().numpy()
+        assert np.array_equal(got[off:off + n].reshape(spec.rows, N), q_ref), off
+        assert (got[:off] == 0xA5).all() and (got[off + n:] == 0xA5).all(), off
+    assert eq.eq_get_status(L) == eq.EQ_OK

@@ -35,18 +35,20 @@ ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 # Algorithmic 32-bit lane-ops per decoded symbol: the decode step (slot
 # mask, slot index, x >> P, multiply-add, renormalisation compare, two-part
 # lane prefix count, word address, shift-or and select = 10) plus the use of
-# the symbol: BF16 output 1 (row-table address); GEMV 1 (byte pick and
-# conversion, per symbol pair) + B/2 (one dot2 per pair and batch row).
+# the symbol: BF16 output 2.5 (code conversion, scale multiply, half a pack
+# of two values); GEMV 1 (byte pick and conversion, per symbol pair) + B/2
+# (one dot2 per pair and batch row).
 # Int8 codes: one conversion per symbol and one pack per pair instead of the
 # byte pick and pair conversion (+0.5 per symbol).
-ALG_OPS = {"bf16": 11.0, "gemv1": 10.0 + 0.5 + 0.5 + 0.5, "gemv8": 10.0 + 0.5 + 0.5 + 4.0}
-ALG_OPS_INT8 = {"bf16": 11.0, "gemv1": 12.0, "gemv8": 15.5}
+ALG_OPS = {"bf16": 10.0 + 1.0 + 1.0 + 0.5, "gemv1": 10.0 + 0.5 + 0.5 + 0.5,
+           "gemv8": 10.0 + 0.5 + 0.5 + 4.0}
+ALG_OPS_INT8 = {"bf16": 12.5, "gemv1": 12.0, "gemv8": 15.5}
 # Kernel (function) name of each op family's decode launch on these shapes.
 # (template arguments: lanes / 64, op, [whole-row steps,] activation source,
 # batch, base format)
 KERNEL = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 1>",
           "gemv1": "decode_kernel<4, 2, true, 1, 1, 1>", "gemv8": "gemv_tiled_kernel<4, 8, 1>"}
-KERNEL_INT8 = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 1>",
+KERNEL_INT8 = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 2>",
                "gemv1": "decode_kernel<4, 2, true, 1, 1, 2>", "gemv8": "gemv_tiled_kernel<4, 8, 2>"}
 FORMATS = {"e4m3": 1, "int8": 2}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_config4.json")

@@ -164,6 +164,14 @@ __device__ inline uint32_t codes_to_bf16x2(uint32_t lo, uint32_t hi) {
   return e4m3x2_to_bf16x2(__builtin_amdgcn_perm(hi, lo, 0x0c0c0703u));
 }
 
+// Value of the code in bits 24..31 of a slot entry, exactly (E4M3FN: the
+// hardware's conversion of that byte; Int8: the sign-extended byte).
+template <int FMT>
+__device__ inline float code_f32(uint32_t e) {
+  if (FMT == kFmtInt8) return static_cast<float>(static_cast<int32_t>(e) >> 24);
+  return __builtin_amdgcn_cvt_f32_fp8(static_cast<int>(e), 3);
+}
+
 // Value-table entry of the code in bits 24..31 of a slot entry.  Bits 13..23
 // of the entry are zero (f <= 2^12), so e >> 22 is already the byte offset.
 __device__ inline uint32_t code_value(const uint32_t *val_s, uint32_t e) {
@@ -323,6 +331,7 @@ struct Decoder {
   __amdgpu_buffer_rsrc_t out_rsrc;
   uint32_t row, first_row, row_end;
   uint16_t *rowtab;  // this wavefront's row table (BF16 output, uniform rows)
+  float srow;        // its row's scale
   // BF16 output of the pipelined steps: a step's values are written to the
   // staging area in column order, then each lane reads back its G adjacent
   // columns and stores them with one store (instead of one per state).
@@ -339,6 +348,10 @@ struct Decoder {
       G >= 2 && (MODE == kCodes || (UNIFORM && (MODE == kBf16 || PAIR)));
   static constexpr int LAG = G / 2;  // processing trails issue by LAG states
   static constexpr bool STAGED = PIPE && MODE == kBf16;
+  // BF16 values of the pipelined steps computed on the VALU from the code and
+  // the row's scale (two per pack), not looked up in the row table: the row
+  // table's scattered two-byte reads were the LDS's busiest traffic.
+  static constexpr bool VBF16 = PIPE && MODE == kBf16;
   uint2 ent[G];      // slot entries in flight
   uint32_t qv[G];    // x >> P of the state whose entry is in flight
   uint64_t nd[G];    // renormalisation masks of the last processed step
@@ -450,6 +463,7 @@ struct Decoder {
   // valid container).  v comes from the fp32 value table.
   __device__ __forceinline__ void fill_rowtab(uint32_t r) {
     const float s = bf16_at(a.scale, r);
+    srow = s;
     const uint32_t c = 4 * lane;
     const uint32_t lo = pack_bf16(s * __uint_as_float(val[c]), s * __uint_as_float(val[c + 1]));
     const uint32_t hi =
@@ -738,7 +752,24 @@ struct Decoder {
       __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(sym[h] >> 24), out_rsrc,
                                            lane + h * kWave, kk, 0);
     } else if (MODE == kBf16) {
-      outv[h] = lds_read_u16(rowtab_addr(tab, sym[h]));
+      if (VBF16) {
+        // bf16(s * v): the fp32 product is exact, rounded once, as in the row
+        // table.  G = 4: for the pair (h - 1, h), one pack (state h - 1's value
+        // is first stored after state h is processed); G = 2: state 0's value
+        // is stored before state 1 is processed, so one value at a time.
+        if (G >= 4) {
+          if (h & 1) {
+            const uint32_t pr = pack_bf16(srow * code_f32<FMT>(sym[(h - 1) & (G - 1)]),
+                                          srow * code_f32<FMT>(sym[h]));
+            outv[(h - 1) & (G - 1)] = pr;
+            outv[h] = pr >> 16;
+          }
+        } else {
+          outv[h] = pack_bf16(srow * code_f32<FMT>(sym[h]), 0.0f);
+        }
+      } else {
+        outv[h] = lds_read_u16(rowtab_addr(tab, sym[h]));
+      }
       okk[h] = kk;
     } else if (h & 1) {
       const int q = h / 2;
@@ -1162,12 +1193,15 @@ int gemv_xsrc(const Args &a, const DeviceFacts &f, uint32_t waves) {
   return kXGlobal;
 }
 
-// The base format a kernel is built for: only the in-register conversion of
-// the paired GEMV depends on it, every other path reads the layer's value
-// table, so those share the E4M3 build.
+// The base format a kernel is built for: only the in-register conversions
+// (paired GEMV, pipelined BF16 steps) depend on it; every other path reads
+// the layer's value table, so those share the E4M3 build.
 template <int G, int MODE, bool UNIFORM, int XS, int NB, int FMT>
 constexpr int kernel_fmt() {
-  return Decoder<G, MODE, UNIFORM, XS, NB, kFmtE4M3>::PAIR ? FMT : int(kFmtE4M3);
+  return Decoder<G, MODE, UNIFORM, XS, NB, kFmtE4M3>::PAIR ||
+                 Decoder<G, MODE, UNIFORM, XS, NB, kFmtE4M3>::VBF16
+             ? FMT
+             : int(kFmtE4M3);
 }
 
 template <int MODE, bool UNIFORM, int XS, int NB, int FMT>
@@ -1220,7 +1254,8 @@ void launch_decode_fmt(const Args &a, hipStream_t s, const DeviceFacts &f) {
 template <int MODE>
 int launch_decode(const Args &a, hipStream_t s) {
   const DeviceFacts f = device_facts();
-  if (MODE == kGemv && a.fmt == kFmtInt8) launch_decode_fmt<MODE, kFmtInt8>(a, s, f);
+  if ((MODE == kGemv || MODE == kBf16) && a.fmt == kFmtInt8)
+    launch_decode_fmt<MODE, kFmtInt8>(a, s, f);
   else launch_decode_fmt<MODE, kFmtE4M3>(a, s, f);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
@@ -1317,7 +1352,7 @@ int launch_multi_fmt(const MultiArgs &m0, size_t xbytes, hipStream_t s, const De
 // Layers of one launch share a base format (joint_ok).
 template <int MODE, int XS, int NB>
 int launch_multi(const MultiArgs &m, size_t xbytes, hipStream_t s, const DeviceFacts &f) {
-  if (MODE == kGemv && m.a[0].fmt == kFmtInt8)
+  if ((MODE == kGemv || MODE == kBf16) && m.a[0].fmt == kFmtInt8)
     return launch_multi_fmt<MODE, XS, NB, kFmtInt8>(m, xbytes, s, f);
   return launch_multi_fmt<MODE, XS, NB, kFmtE4M3>(m, xbytes, s, f);
 }

@@ -211,6 +211,16 @@ __global__ __launch_bounds__((BT / WT) * (BO / WO) * 64) void gemm_codes_kernel(
         for (int j = 0; j < TJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
+    // issue order: the first 16 columns' fragment reads, then one matrix
+    // instruction and one of the later fragment reads in turn (left to the
+    // compiler, the reads of a step come in one burst before its products)
+    __builtin_amdgcn_sched_group_barrier(0x100, TI + TJ, 0);  // LDS reads
+#pragma unroll
+    for (int r = 0; r < 3 * (TI + TJ); ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // matrix instruction
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * TI * TJ, 0);
   };
 
   // stage kt: LDS buffer kt & 1; register set p holds stage kt + 1 on entry

@@ -186,3 +186,21 @@ def test_c5_layer0_qkv_block(eq):
         err = np.abs(got - y_ref).max() / np.abs(y_ref).max()
         assert err <= TOL, err
         assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+def test_bf16_multi_wave_cap(eq):
+    """8192 chunks in one launch (8 layers of 1024 x 1024, 1024-symbol chunks,
+    256 lanes): two blocks per compute unit would need 16 wavefronts each, more
+    than fit twice in a compute unit's LDS with row tables and staging areas;
+    the launch is capped at 15, so blocks take several chunks each.  Every
+    layer is bit-exact against the oracle."""
+    layers = [make(eq, 1024, 1024, 1024, 256, 2.0 + 0.25 * i, seed=700 + i) for i in range(8)]
+    assert sum(oracle.container_info(blob).n_chunks for _, blob, _ in layers) == 8192
+    say("bf16 multi wave cap", len(layers))
+    outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev())
+            for L, _, _ in layers]
+    eq.eq_decode_bf16_multi([L for L, _, _ in layers], outs)
+    for (L, blob, _), out in zip(layers, outs):
+        got = out.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)
+        assert np.array_equal(got, oracle_bf16(blob)), (L.rows, L.cols)
+        assert eq.eq_get_status(L) == eq.EQ_OK

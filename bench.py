@@ -171,6 +171,26 @@ def cpu_baseline(layers, target_s, threads, fmt=1):
             "single_thread_sample": f"first {R1} rows, one thread, {t1:.1f}s"}
 
 
+def run_env():
+    """Device, software and host facts recorded with every result."""
+    import platform
+    import torch
+    props = torch.cuda.get_device_properties(0)
+    cpu = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"device": props.name, "arch": getattr(props, "gcnArchName", ""),
+            "compute_units": props.multi_processor_count,
+            "hbm_gib": round(props.total_memory / 2**30, 1), "hip": torch.version.hip,
+            "torch": torch.__version__, "cpu": cpu, "host_cores": os.cpu_count()}
+
+
 def traffic_per_launch(op, fmt_name="e4m3"):
     """HBM bytes of one launch of `op`'s decode kernel, from the committed
     FETCH_SIZE / WRITE_SIZE counter summary, scaled by the counters' readings
@@ -291,7 +311,7 @@ def run_stack(args):
         "metric": "decoded Gparams/s, 80-layer stack, fused decode-GEMV B=1 (block-wise launches)",
         "value": gb["gparams_per_s"], "unit": "Gparams/s", "n_gpus": 1, "steps": args.steps,
         "ms_per_step": gb["ms_per_pass"], "higher_is_better": True, "vs_baseline": None,
-        "dtype": "u32", "data": "synthetic",
+        "dtype": "u32", "data": "synthetic", "env": run_env(),
         "config": {"workload": "config 5: 80 layers x {q 8192x8192, k/v 1024x8192, o 8192x8192, "
                                "gate/up 28672x8192, down 8192x28672}, (2,3,4)[l mod 3] bits, "
                                "65536-symbol chunks, 256 lanes; 3 distinct layers, 80 device copies",
@@ -387,6 +407,7 @@ def run_prefill(args):
         "value": round(B / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "env": run_env(),
         "config": {"workload": f"prefill of the Llama-70B MLP pair 8192x28672 + 28672x8192, "
                                f"{args.base_format.upper()} codes at ~2.0 bits/param, {B} tokens",
                    "tokens": B, "params": params, "base_format": args.base_format},
@@ -571,6 +592,7 @@ def main():
         "kernels": kernels,
         "copy_reference_gbs": round(copy_gbs, 1),
         "wall_s_timed": round(wall, 3),
+        "env": run_env(),
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)

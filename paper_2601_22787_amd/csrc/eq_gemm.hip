@@ -296,29 +296,27 @@ void launch_gemm(GemmArgs a, hipStream_t stream) {
   hipLaunchKernelGGL((gemm_codes_kernel<FMT, BT, BO, WT, WO>), grid, block, shm, stream, a);
 }
 
-// Tile and split-K choice: 256 x 256 tiles (8 wavefronts of 128 x 64; twice
-// the operand reuse) when they still give every compute unit a block, else
-// 128 x 128 tiles (4 wavefronts of 64 x 64), which give four times as many
-// blocks and pad fewer tokens; when even those leave compute units idle,
-// the input columns are cut into slices (at most 16, each at least 4 stages
-// of 64 columns) whose partial sums are reduced in slice order.
+// Tile and split-K choice.  A 256 x 256 block (8 wavefronts of 128 x 64)
+// does a stage's work at about 1.4x the rate of 128 x 128 blocks (4
+// wavefronts of 64 x 64; measured per stage on the config-4 matrices), so it
+// is used unless its padding (tokens and rows rounded up to 256) costs more
+// than that.  When the tiles leave compute units idle, the input columns are
+// cut into slices (at most 16, each at least 4 stages of 64 columns) whose
+// partial sums are reduced in slice order: 256 x 256 blocks one per compute
+// unit, 128 x 128 blocks at least one per compute unit (two fit).
 struct GemmPlan {
   bool big;
   uint32_t splits, split_stages;
 };
 
 GemmPlan plan_gemm(uint32_t B, uint32_t M, uint32_t N, int cus) {
-  GemmPlan p{false, 1, 0};
   const uint32_t stages = (N + kBK - 1) / kBK;
-  p.split_stages = stages;
-  const uint64_t big = uint64_t((M + 255) / 256) * ((B + 255) / 256);
-  if (big >= uint64_t(cus)) {
-    p.big = true;
-    return p;
-  }
-  const uint64_t tiles = uint64_t((M + 127) / 128) * ((B + 127) / 128);
+  const uint64_t t256 = uint64_t((M + 255) / 256) * ((B + 255) / 256);
+  const uint64_t t128 = uint64_t((M + 127) / 128) * ((B + 127) / 128);
+  GemmPlan p{10 * 4 * t256 <= 14 * t128, 1, stages};  // padded areas, in 128 x 128 units
+  const uint64_t tiles = p.big ? t256 : t128;
   if (tiles >= uint64_t(cus)) return p;
-  uint64_t want = (uint64_t(cus) + tiles - 1) / tiles;
+  uint64_t want = p.big ? uint64_t(cus) / tiles : (uint64_t(cus) + tiles - 1) / tiles;
   want = want < 16 ? want : 16;
   const uint64_t cap = stages / 4;
   const uint64_t sp = want < cap ? want : cap;

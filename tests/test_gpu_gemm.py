@@ -66,7 +66,7 @@ SHAPES = [
     # M, N, C, lanes, bits, B
     (64, 256, 4096, 64, 2.0, 16),
     (100, 320, 1024, 64, 3.0, 37),     # ragged rows, columns (320 = 5 x 64) and tokens
-    (256, 1024, 4096, 128, 2.0, 129),  # two token tiles, one token past the first
+    (256, 1024, 4096, 128, 2.0, 129),  # one 256 x 256 tile, 4 slices; 129 tokens
     (37, 4096, 16384, 256, 4.0, 300),
     (300, 208, 2048, 64, 2.5, 9),      # N = 208: a partial 64-column stage
 ]
@@ -179,6 +179,25 @@ def test_gemm_split_k(eq, N, B):
         eq.eq_gemm_codes(L, codes, xt, B, None, yt, None)
 
 
+def test_gemm_large_tiles_split_k(eq):
+    """256 x 256 tiles with split-K: 300 rows x 250 tokens (two row tiles, one
+    token tile) over 1040 columns, 17 stages with a 16-column last one, cut
+    into slices of 5, 5, 5 and 2 stages; within the bar, deterministic."""
+    spec = small_spec(300, 1040, bits=2.0, chunk=8192, lanes=64, seed=4400)
+    w = synth.weights(spec)
+    blob = encode(eq, w, 2.0, 8192, 64, 1)
+    L = eq.Layer(blob, _dev())
+    assert eq.eq_gemm_codes_workspace_bytes(L, 250) > 0
+    rc, q = oracle.container_decode(blob)
+    w_ref = oracle.dequant(q, oracle.container_scales(blob))
+    x = tokens(spec, 250)
+    bias = synth.bias(spec)
+    y = gpu_gemm(eq, L, x, bias)
+    err = rel_err(y, oracle.gemv(w_ref, x, bias))
+    assert np.isfinite(y).all() and (err <= TOL).all(), err.max()
+    assert np.array_equal(y, gpu_gemm(eq, L, x, bias))
+
+
 def _sampled(eq, spec, w, blob, L, B, fmt, seed):
     """Sampled rows x sampled tokens (always the first and last) of the
     prefill output against the oracle's fp64 GEMM of the same rows, whose
@@ -197,8 +216,9 @@ def _sampled(eq, spec, w, blob, L, B, fmt, seed):
 
 @pytest.mark.parametrize("fmt", [1, 2])
 def test_gemm_config4_full_size_sampled(eq, fmt):
-    """The 8192x28672 layer at 256 tokens (128 x 128 tiles) and the
-    28672x8192 layer at 768 tokens (336 blocks of 256 x 256)."""
+    """The 8192x28672 layer at 256 tokens (32 tiles of 256 x 256, 8 slices of
+    56 stages) and the 28672x8192 layer at 768 tokens (336 blocks of 256 x
+    256)."""
     for spec, B in zip(config_matrices(4), (256, 768)):
         say("gemm config 4", spec.name, B, fmt)
         w = synth.weights(spec)

@@ -1,0 +1,101 @@
+"""HIP graph capture of the library's entry points.  A call only launches
+kernels on the given stream (no allocation, memset or synchronisation), so a
+serving loop can capture a layer's decode, GEMVs and prefill GEMM once and
+replay them.  Every replay, with other work on the stream between replays,
+must give the eager results: bit for bit where the kernels are deterministic
+(codes, BF16, whole-row GEMV, GEMM with split-K), within 1e-6 for the
+general-shape GEMV (fp32 atomics).  The outputs are overwritten before each
+replay, so stale values cannot pass."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from synth.configs import small_spec
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def eq():
+    import paper_2601_22787_amd as m
+    m.lib()
+    assert torch.cuda.is_available()
+    return m
+
+
+def _dev():
+    return torch.device("cuda:0")
+
+
+def layer(eq, M, N, C, lanes, seed):
+    spec = small_spec(M, N, bits=2.0, chunk=C, lanes=lanes, seed=seed)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, 2.0)
+    return eq.Layer(eq.eqe_encode(w, alpha, chunk_syms=C, lanes=lanes), _dev()), spec
+
+
+def xs(spec, B):
+    return torch.from_numpy(synth.activations(spec, B).view(np.int16)).to(_dev())
+
+
+def test_graph_replays_match_eager(eq):
+    Lu, su = layer(eq, 64, 2048, 8192, 256, 6000)    # whole-row steps
+    Lv, _ = layer(eq, 48, 2048, 8192, 256, 6001)
+    Lg, sg = layer(eq, 37, 1000, 4096, 64, 6002)     # rows across steps (atomics)
+    x1, x8, xg, xb = xs(su, 1), xs(su, 8), xs(sg, 3), xs(su, 40)
+    bias = torch.from_numpy(synth.bias(su).view(np.int16)).to(_dev())
+    n = su.rows * su.cols
+    bufs = {
+        "codes": torch.empty(n, dtype=torch.uint8, device=_dev()),
+        "bf16": torch.empty(n, dtype=torch.int16, device=_dev()),
+        "m0": torch.empty(n, dtype=torch.int16, device=_dev()),
+        "m1": torch.empty(Lv.rows * Lv.cols, dtype=torch.int16, device=_dev()),
+        "y1": torch.empty(1, Lu.rows, dtype=torch.float32, device=_dev()),
+        "y8": torch.empty(8, Lu.rows, dtype=torch.float32, device=_dev()),
+        "yg": torch.empty(3, Lg.rows, dtype=torch.float32, device=_dev()),
+        "yb": torch.empty(40, Lu.rows, dtype=torch.float32, device=_dev()),
+    }
+    ws1, ws8, wsg, wsb = Lu.workspace(1), Lu.workspace(8), Lg.workspace(3), Lu.gemm_workspace(40)
+    assert eq.eq_gemm_codes_workspace_bytes(Lu, 40) > 0  # split-K path
+
+    def calls():
+        eq.eq_decode_codes(Lu, bufs["codes"])
+        eq.eq_decode_bf16(Lu, bufs["bf16"])
+        eq.eq_decode_bf16_multi([Lu, Lv], [bufs["m0"], bufs["m1"]])
+        eq.eq_decode_gemv(Lu, x1, 1, None, bufs["y1"], ws1)
+        eq.eq_decode_gemv(Lu, x8, 8, bias, bufs["y8"], ws8)
+        eq.eq_decode_gemv(Lg, xg, 3, None, bufs["yg"], wsg)
+        eq.eq_decode_gemm(Lu, xb, 40, None, bufs["yb"], wsb)
+
+    calls()
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in bufs.items()}
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    for rep in range(3):
+        say("replay", rep)
+        for v in bufs.values():
+            v.fill_(-1 if v.dtype != torch.float32 else float("nan"))
+        # other work on the stream between replays
+        other = torch.empty(1, Lu.rows, dtype=torch.float32, device=_dev())
+        eq.eq_decode_gemv(Lu, x1, 1, None, other, Lu.workspace(1))
+        (torch.randn(256, 256, device=_dev()) @ torch.randn(256, 256, device=_dev())).sum()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in bufs:
+            if k == "yg":
+                assert torch.allclose(bufs[k], ref[k], rtol=1e-6, atol=1e-6), (rep, k)
+            else:
+                assert torch.equal(bufs[k], ref[k]), (rep, k)
+        assert torch.equal(other, ref["y1"])
+    for L in (Lu, Lv, Lg):
+        assert eq.eq_get_status(L) == eq.EQ_OK

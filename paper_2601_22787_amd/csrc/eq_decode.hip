@@ -134,6 +134,23 @@ __device__ inline uint32_t select_by_mask(uint64_t m, uint32_t a, uint32_t b) {
   return r;
 }
 
+// Renormalisation of the lanes whose bit is set in m: x = (x << 16) | w on
+// those lanes (x < 2^16 there; only the low 16 bits of w are used), x
+// unchanged on the others.  One v_perm_b32 under exec = exec & m instead of a
+// shift-or and a select: the two scalar instructions that narrow and restore
+// exec issue beside other waves' vector work.  They write SCC.
+__device__ inline uint32_t renorm_lanes(uint64_t m, uint32_t x, uint32_t w) {
+  uint64_t saved;
+  // result bytes 3..0 = x byte 1, x byte 0, w byte 1, w byte 0
+  asm("s_and_saveexec_b64 %1, %2\n\t"
+      "v_perm_b32 %0, %0, %3, %4\n\t"
+      "s_mov_b64 exec, %1"
+      : "+v"(x), "=&s"(saved)
+      : "s"(m), "v"(w), "s"(0x05040100u)
+      : "scc");
+  return x;
+}
+
 // Read-only inputs seen through the constant address space, so that loads
 // at wave-uniform addresses become scalar (SMEM) loads and never wait on the
 // vector memory counter.
@@ -715,6 +732,13 @@ struct Decoder {
     pend_valid = true;
   }
 
+  // BF16 value of state g for its store: the pair packs of the pipelined
+  // steps leave an odd state's value in the high half, which a d16_hi store
+  // writes directly.
+  __device__ __forceinline__ uint32_t out_half(int g) const {
+    return (VBF16 && G >= 4 && (g & 1)) ? outv[g] >> 16 : outv[g];
+  }
+
   // Issue state g of step t: finish its renormalisation from the previous
   // step (unless FIRST), put out its pending BF16 value (STG: into the
   // staging area; after the last state, read the step back), start its slot
@@ -722,13 +746,13 @@ struct Decoder {
   template <bool FIRST, bool STG>
   __device__ __forceinline__ void pissue(int g, const uint32_t *xt) {
     if (!FIRST) {
-      x[g] = select_by_mask(nd[g], x[g], (x[g] << 16) | wd[g]);
+      x[g] = renorm_lanes(nd[g], x[g], wd[g]);
       if (MODE == kBf16) {
         if (STG) {
-          stage_put(g, outv[g]);
+          stage_put(g, out_half(g));
           if (g == G - 1) stage_get(okk[g]);
         } else {
-          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
+          __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(out_half(g)), out_rsrc,
                                                 2 * (lane + g * kWave), 2 * okk[g], 0);
         }
       }
@@ -762,7 +786,7 @@ struct Decoder {
             const uint32_t pr = pack_bf16(srow * code_f32<FMT>(sym[(h - 1) & (G - 1)]),
                                           srow * code_f32<FMT>(sym[h]));
             outv[(h - 1) & (G - 1)] = pr;
-            outv[h] = pr >> 16;
+            outv[h] = pr;  // its high half (see out_half)
           }
         } else {
           outv[h] = pack_bf16(srow * code_f32<FMT>(sym[h]), 0.0f);
@@ -818,6 +842,8 @@ struct Decoder {
 #pragma unroll
     for (int h = 0; h < LAG; ++h) pproc(h, t * W);
     for (++t; t < t_end; ++t) {
+      // t stays a plain scalar counter (not rewritten into a vector one)
+      asm("" : "+s"(t));
       // words read since the last check: at most one step and a half
       slide();
       xt += xs;
@@ -840,14 +866,14 @@ struct Decoder {
     for (int h = LAG; h < G; ++h) pproc(h, (t - 1) * W);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      x[g] = select_by_mask(nd[g], x[g], (x[g] << 16) | wd[g]);
+      x[g] = renorm_lanes(nd[g], x[g], wd[g]);
       if (MODE == kBf16 && !STG)
-        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(outv[g]), out_rsrc,
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(out_half(g)), out_rsrc,
                                               2 * (lane + g * kWave), 2 * okk[g], 0);
     }
     if (STG) {
 #pragma unroll
-      for (int g = 0; g < G; ++g) stage_put(g, outv[g]);
+      for (int g = 0; g < G; ++g) stage_put(g, out_half(g));
       stage_get(okk[G - 1]);
       stage_store();
     }

@@ -32,17 +32,20 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 # Vector ALU: 256 CUs x 4 SIMDs x 16 lanes, one 32-bit lane-op per lane and
 # clock at 2.4 GHz (packed FP32 not counted: the path is integer work).
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
-# Algorithmic 32-bit lane-ops per decoded symbol: the decode step (slot
-# mask, slot index, x >> P, multiply-add, renormalisation compare, two-part
-# lane prefix count, word address, shift-or and select = 10) plus the use of
-# the symbol: BF16 output 2.5 (code conversion, scale multiply, half a pack
-# of two values); GEMV 1 (byte pick and conversion, per symbol pair) + B/2
-# (one dot2 per pair and batch row).
+# Algorithmic issue slots of the vector-ALU port per decoded symbol (32-bit
+# lane-ops; a matrix-core instruction also takes one slot): the decode step
+# (slot mask, slot index, x >> P, multiply-add, renormalisation compare,
+# two-part lane prefix count, word address, and the renormalising merge as one
+# byte permute under a narrowed exec mask = 9) plus the use of the symbol:
+# BF16 output 2.5 (code conversion, scale multiply, half a pack of two
+# values); GEMV 1 (byte pick and conversion, per symbol pair) plus, at batch
+# 1, one dot2 per pair (0.5) and, at batch 8, one 4x4x4 MFMA per batch row
+# and four symbols (2).
 # Int8 codes: one conversion per symbol and one pack per pair instead of the
-# byte pick and pair conversion (+0.5 per symbol).
-ALG_OPS = {"bf16": 10.0 + 1.0 + 1.0 + 0.5, "gemv1": 10.0 + 0.5 + 0.5 + 0.5,
-           "gemv8": 10.0 + 0.5 + 0.5 + 4.0}
-ALG_OPS_INT8 = {"bf16": 12.5, "gemv1": 12.0, "gemv8": 15.5}
+# byte pick and pair conversion (+0.5 per symbol on the GEMV).
+ALG_OPS = {"bf16": 9.0 + 1.0 + 1.0 + 0.5, "gemv1": 9.0 + 0.5 + 0.5 + 0.5,
+           "gemv8": 9.0 + 0.5 + 0.5 + 2.0}
+ALG_OPS_INT8 = {"bf16": 11.5, "gemv1": 11.0, "gemv8": 12.5}
 # Kernel (function) name of each op family's decode launch on these shapes.
 # (template arguments: lanes / 64, op, [whole-row steps,] activation source,
 # batch, base format)

@@ -64,6 +64,8 @@ struct Args {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float float2v __attribute__((ext_vector_type(2)));
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef float float4v __attribute__((ext_vector_type(4)));
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
@@ -88,6 +90,26 @@ __device__ inline float e4m3_value(uint32_t c) {
   else mag = __uint_as_float(((e + 120u) << 23) | (m << 20));
   if ((c & 0x7Fu) == 0x7Fu) mag = __uint_as_float(0x7FC00000u);
   return (c & 0x80u) ? -mag : mag;
+}
+
+// One v_mfma_f32_4x4x4_16b_bf16: 16 blocks of 4 lanes, C[i][j] += sum_k
+// A[i][k] B[k][j], where lane 4 blk + i holds row i of A (four BF16 in two
+// registers, low half first) and lane 4 blk + j holds column j of B and
+// column j of C (register i = row i).  The diagonal C[j][j], register
+// (lane & 3) of lane 4 blk + j, is therefore the lane's own four-term dot
+// product of its A and B values; the other registers hold cross terms.
+__device__ inline float4v mfma_dot4(uint32_t a01, uint32_t a23, uint32_t b01, uint32_t b23,
+                                    float4v c) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(__builtin_bit_cast(short4v, u32x2{a01, a23}),
+                                                __builtin_bit_cast(short4v, u32x2{b01, b23}),
+                                                c, 0, 0, 0);
+}
+
+// The lane's own entry of an mfma_dot4 accumulator.
+__device__ inline float mfma_diag(float4v c, uint32_t lane) {
+  const uint32_t j = lane & 3u;
+  return j == 0 ? c.x : j == 1 ? c.y : j == 2 ? c.z : c.w;
 }
 
 __device__ inline float wave_sum(float v) {
@@ -281,9 +303,23 @@ __device__ inline uint4 pair_entries4(const uint16_t *x, uint32_t j) {
                     __builtin_amdgcn_perm(hi.y, lo.y, 0x07060302u));
 }
 
-__global__ void pair_layout_kernel(const uint16_t *x, uint32_t N, uint32_t B, uint32_t *xp) {
+// Batch 8 with W = 256 (the matrix-core GEMV, N a multiple of 256): the same
+// pairs, ordered so that one 16-byte load holds both pairs of a lane's step
+// for two batch rows.  Entry i = ((m * 4 + r) * 64 + l) * 4 + e holds the
+// pair (x[b][c], x[b][c + 64]) with c = 256 m + 128 (e & 1) + l and
+// b = 2 r + (e >> 1).
+__device__ inline uint32_t quad_entry(const uint16_t *x, uint32_t N, uint32_t i) {
+  const uint32_t e = i & 3u, l = (i >> 2) & 63u, r = (i >> 8) & 3u, m = i >> 10;
+  const uint32_t b = 2 * r + (e >> 1);
+  const uint16_t *row = x + size_t(b) * N + 256 * m + 128 * (e & 1u) + l;
+  return uint32_t(row[0]) | (uint32_t(row[64]) << 16);
+}
+
+__global__ void pair_layout_kernel(const uint16_t *x, uint32_t N, uint32_t B, uint32_t quad,
+                                   uint32_t *xp) {
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < pair_bytes(B, N) / sizeof(uint32_t)) xp[i] = pair_entry(x, N, B, i);
+  if (i < pair_bytes(B, N) / sizeof(uint32_t))
+    xp[i] = quad ? quad_entry(x, N, i) : pair_entry(x, N, B, i);
 }
 
 // Static LDS of a decode block: the value table first, so that its byte
@@ -369,6 +405,15 @@ struct Decoder {
   // the row's scale (two per pack), not looked up in the row table: the row
   // table's scattered two-byte reads were the LDS's busiest traffic.
   static constexpr bool VBF16 = PIPE && MODE == kBf16;
+  // Batch-8 GEMV of the pipelined steps on the matrix cores: once both state
+  // pairs of a lane are converted, one 4x4x4 MFMA per batch row adds the
+  // lane's four products (its diagonal entry, see mfma_dot4) where eight
+  // v_dot2 would.  The MFMA shares the VALU's issue port, so this halves the
+  // issue slots of the products.
+  static constexpr bool MFMA8 = PAIR && PIPE && G == 4 && NB == 8;
+  float4v macc[MFMA8 ? kMaxBatch : 1];
+  uint32_t w01;      // BF16 weights of state pair 0 (MFMA8), waiting for pair 1
+  uint4 xq8[MFMA8 ? 4 : 1];  // a step's activation pairs for batch rows 2 r, 2 r + 1 (MFMA8)
   uint2 ent[G];      // slot entries in flight
   uint32_t qv[G];    // x >> P of the state whose entry is in flight
   uint64_t nd[G];    // renormalisation masks of the last processed step
@@ -450,6 +495,8 @@ struct Decoder {
       for (int b = 0; b < kMaxBatch; ++b) acc[g][b] = 0.0f;
 #pragma unroll
     for (int g = 0; g < G; ++g) pending[g] = false;
+#pragma unroll
+    for (int b = 0; b < (MFMA8 ? kMaxBatch : 1); ++b) macc[b] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
   }
 
   __device__ __forceinline__ uint32_t xbits(uint32_t b, uint32_t col) const {
@@ -464,6 +511,10 @@ struct Decoder {
     const float bb = a.bias ? bf16_at(a.bias, r) : 0.0f;
 #pragma unroll
     for (int b = 0; b < kMaxBatch; ++b) {
+      if (MFMA8) {
+        acc[0][b] += mfma_diag(macc[b], lane);
+        macc[b] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+      }
       if (b < nb) {
         const float sum = wave_sum(acc[0][b]);
         if (lane == 0) {
@@ -568,6 +619,20 @@ struct Decoder {
         if (g + 1 < G && (!TAIL || act[g + 1]))
           __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h >> 16), out_rsrc,
                                                 2 * (lane + (g + 1) * kWave), 2 * kk, 0);
+      }
+    } else if (MFMA8) {
+      // batch 8, quad layout: the step's 256 columns are one block of 1024 entries
+      const uint32_t *xq = XS == kXTile
+                               ? xt + 4 * lane
+                               : reinterpret_cast<const uint32_t *>(xl) +
+                                     ((k0 + kk + N - row_end) >> 8) * 1024 + 4 * lane;
+      const uint32_t w0 = codes_to_bf16x2<FMT>(e0[0], e0[1]);
+      const uint32_t w1 = codes_to_bf16x2<FMT>(e0[2], e0[3]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint4 xv = *reinterpret_cast<const uint4 *>(xq + r * 256);
+        acc[0][2 * r] = dot2_bf16(w1, xv.y, dot2_bf16(w0, xv.x, acc[0][2 * r]));
+        acc[0][2 * r + 1] = dot2_bf16(w1, xv.w, dot2_bf16(w0, xv.z, acc[0][2 * r + 1]));
       }
     } else if (PAIR) {
       // pairs of this step's 128-column blocks: xq + (q * BG + bg) * 64 * bw
@@ -685,6 +750,16 @@ struct Decoder {
   // Activation pairs of state pair q for the step whose first column is col
   // (kXLds) or whose tile is at xt (kXTile).
   __device__ __forceinline__ void load_x(int q, uint32_t col, const uint32_t *xt) {
+    if (MFMA8) {
+      // all eight batch rows of both pairs at once, after the step's last state
+      if (q == G / 2 - 1) {
+        const uint32_t *xq = (XS == kXTile ? xt : reinterpret_cast<const uint32_t *>(xl) +
+                                                      (col >> 8) * 1024) + 4 * lane;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) xq8[r] = *reinterpret_cast<const uint4 *>(xq + r * 256);
+      }
+      return;
+    }
     constexpr uint32_t bw = NB == 1 ? 1 : 4;
     const uint32_t BG = NB == 1 ? 1 : (nb + 3) / 4;
     const uint32_t *xq;
@@ -800,6 +875,16 @@ struct Decoder {
       const uint32_t w2 = codes_to_bf16x2<FMT>(sym[h - 1], sym[h]);
       if (NB == 1) {
         acc[0][0] = dot2_bf16(w2, xv1[q], acc[0][0]);
+      } else if (MFMA8) {
+        if (q == 0) {
+          w01 = w2;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            macc[2 * r] = mfma_dot4(xq8[r].x, xq8[r].y, w01, w2, macc[2 * r]);
+            macc[2 * r + 1] = mfma_dot4(xq8[r].z, xq8[r].w, w01, w2, macc[2 * r + 1]);
+          }
+        }
       } else {
         const uint32_t BG = (nb + 3) / 4;
 #pragma unroll
@@ -937,7 +1022,9 @@ __device__ __forceinline__ void decode_block(const Args &a, uint32_t blk, uint32
     if (Decoder<G, MODE, UNIFORM, XS, NB, FMT>::PAIR) {
       uint32_t *xp = reinterpret_cast<uint32_t *>(xl);
       const uint32_t np = pair_bytes(a.batch, a.cols) / sizeof(uint32_t);
-      if (a.batch == 1 && (reinterpret_cast<uintptr_t>(a.x) & 7) == 0) {
+      if (Decoder<G, MODE, UNIFORM, XS, NB, FMT>::MFMA8) {
+        for (uint32_t i = threadIdx.x; i < np; i += nthreads) xp[i] = quad_entry(a.x, a.cols, i);
+      } else if (a.batch == 1 && (reinterpret_cast<uintptr_t>(a.x) & 7) == 0) {
         for (uint32_t j = threadIdx.x; j < np / 4; j += nthreads) xl[j] = pair_entries4(a.x, j);
       } else {
         for (uint32_t i = threadIdx.x; i < np; i += nthreads) xp[i] = pair_entry(a.x, a.cols, a.batch, i);
@@ -1450,8 +1537,10 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
   int rc;
   if (gemv_xsrc(a, f, launch_waves(L->n_chunks, f.cus)) == kXTile) {
     const uint32_t np = uint32_t(pair_bytes(B, L->cols) / sizeof(uint32_t));
+    // the matrix-core GEMV (batch 8, 256 lanes) reads the quad layout
+    const uint32_t quad = B == kMaxBatch && L->lanes == 256 ? 1u : 0u;
     hipLaunchKernelGGL(pair_layout_kernel, dim3((np + 255) / 256), dim3(256), 0, stream, x,
-                       L->cols, B, const_cast<uint32_t *>(a.xp));
+                       L->cols, B, quad, const_cast<uint32_t *>(a.xp));
     rc = (B == 1) ? launch_tiled<1>(a, stream, f)
                   : (B == kMaxBatch ? launch_tiled<kMaxBatch>(a, stream, f)
                                     : launch_tiled<0>(a, stream, f));

@@ -120,6 +120,16 @@ __device__ inline float wave_sum(float v) {
 
 __device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Wave issue priority 3 - q (q = 0..3, wave-uniform).
+__device__ inline void set_prio_down(uint32_t q) {
+  switch (q) {
+    case 0: __builtin_amdgcn_s_setprio(3); break;
+    case 1: __builtin_amdgcn_s_setprio(2); break;
+    case 2: __builtin_amdgcn_s_setprio(1); break;
+    default: __builtin_amdgcn_s_setprio(0); break;
+  }
+}
+
 // LDS pointers as 32-bit byte addresses, so that wave-uniform positions can
 // live in scalar registers and be advanced by scalar arithmetic.
 typedef __attribute__((address_space(3))) const uint16_t lds_u16;
@@ -429,6 +439,16 @@ struct Decoder {
   uint32_t xv1[G / 2 > 0 ? G / 2 : 1];    // activation pairs of a state pair (batch 1)
   uint4 xv8[G / 2 > 0 ? G / 2 : 1][2];     // (batch > 1), per 4-row batch group
   uint32_t icol;     // column of the first symbol of the step being issued
+  // Issue priority of the pipelined steps: 3 until step prio_at[0], then 2,
+  // 1 and from prio_at[2] on 0.  The wave arbiter prefers higher priority
+  // and, among equals, older waves; at one priority the waves started first
+  // run ahead and the last ones finish alone on a compute unit, with nothing
+  // to hide their latencies.  Lowering a wave's priority as it passes these
+  // points lets the waves behind it catch up; the last stage is short, so
+  // the waves of a compute unit finish close together.
+  // (Not for the tiled GEMV, whose waves meet at a barrier every tile.)
+  static constexpr bool PRIO = XS != kXTile;
+  uint32_t prio_at[3];
 
   __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
                                      const DecodeLds &sm, uint4 *win4_, uint16_t *rowtab_,
@@ -444,6 +464,9 @@ struct Decoder {
     P = a.prob_bits;
     mask = (1u << P) - 1;
     full = nc / W;
+    prio_at[0] = full / 2;
+    prio_at[1] = full - full / 4;
+    prio_at[2] = full - full / 16;
     nb = NB ? NB : static_cast<int>(a.batch);
 #pragma unroll
     for (int g = 0; g < G; ++g) x[g] = a.chunk_state[c * W + g * kWave + lane];
@@ -926,7 +949,16 @@ struct Decoder {
     for (int g = 0; g < G; ++g) pissue<true, STG>(g, xt);
 #pragma unroll
     for (int h = 0; h < LAG; ++h) pproc(h, t * W);
-    for (++t; t < t_end; ++t) {
+    for (++t; t < t_end;) {
+      // Issue priority 3 - (stage of the chunk reached, see prio_at).
+      uint32_t seg_end = t_end;
+      if (PRIO) {
+        const uint32_t q = (t >= prio_at[0]) + (t >= prio_at[1]) + (t >= prio_at[2]);
+        seg_end =
+            min(t_end, q == 0 ? prio_at[0] : q == 1 ? prio_at[1] : q == 2 ? prio_at[2] : t_end);
+        set_prio_down(q);
+      }
+      for (; t < seg_end; ++t) {
       // t stays a plain scalar counter (not rewritten into a vector one)
       asm("" : "+s"(t));
       // words read since the last check: at most one step and a half
@@ -945,6 +977,7 @@ struct Decoder {
           if (g == LAG) row_check(t);
           pproc(g - LAG, t * W);
         }
+      }
       }
     }
 #pragma unroll

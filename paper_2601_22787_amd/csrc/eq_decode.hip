@@ -446,8 +446,9 @@ struct Decoder {
   // to hide their latencies.  Lowering a wave's priority as it passes these
   // points lets the waves behind it catch up; the last stage is short, so
   // the waves of a compute unit finish close together.
-  // (Not for the tiled GEMV, whose waves meet at a barrier every tile.)
-  static constexpr bool PRIO = XS != kXTile;
+  // The tiled GEMV's waves meet at a barrier every tile: there the points
+  // divide each tile's steps the same way.
+  static constexpr bool PRIO = true;
   uint32_t prio_at[3];
 
   __device__ __forceinline__ Decoder(const Args &a_, uint32_t c_, uint32_t lane_,
@@ -939,6 +940,12 @@ struct Decoder {
   __device__ __forceinline__ void prun_impl(uint32_t t, uint32_t t_end, const uint32_t *xt,
                                             uint32_t xs) {
     static_assert(2 * W <= kWin - kHalf, "a step and a half must fit the window");
+    if (XS == kXTile) {
+      const uint32_t n = t_end - t;
+      prio_at[0] = t + n / 2;
+      prio_at[1] = t + n - n / 4;
+      prio_at[2] = t + n - n / 16;
+    }
     if (STG) pend_valid = false;
     slide();
     if (MODE != kCodes) {

@@ -27,7 +27,8 @@ constexpr uint32_t kHalf = 512;               // stream words per window half (1
 constexpr uint32_t kWin = 2 * kHalf;          // per-wave LDS window of stream words
 constexpr int32_t kBufferFlags = 0x00020000;  // buffer resource word 3 (gfx9 family)
 constexpr uint32_t kMaxXLdsBytes = 64 * 1024; // activations staged whole up to this size
-constexpr uint32_t kTileBytes = 32 * 1024;    // one activation tile (two are in LDS)
+constexpr uint32_t kTileBytes = 48 * 1024;    // one activation tile at most (two are in LDS)
+constexpr uint32_t kMinTileBytes = 32 * 1024; // tiles at least this large, or no tiling
 constexpr uint32_t kStageRegs = 4;            // 16-byte registers per thread to stage a tile
 
 enum Mode { kCodes = 0, kBf16 = 1, kGemv = 2 };
@@ -1341,7 +1342,7 @@ int gemv_xsrc(const Args &a, const DeviceFacts &f, uint32_t waves) {
       kStaticLds + dyn_lds_bytes(waves, xbytes, false) <= size_t(f.lds_per_block))
     return kXLds;
   if (uniform && a.lanes >= 128 &&
-      kStaticLds + dyn_lds_bytes(kMaxWaves, 2 * kTileBytes, false) <= size_t(f.lds_per_block))
+      kStaticLds + dyn_lds_bytes(kMaxWaves, 2 * kMinTileBytes, false) <= size_t(f.lds_per_block))
     return kXTile;
   return kXGlobal;
 }
@@ -1431,9 +1432,16 @@ int launch_tiled(Args a, hipStream_t s, const DeviceFacts &f) {
   }
   const uint32_t step_bytes =
       uint32_t(pair_bytes(a.batch, W));  // W columns of column-paired activations
+  // Steps per tile: up to kTileBytes, as many as the block's threads stage
+  // with their registers, and two tiles beside the tables and windows in LDS
+  // (longer tiles mean fewer barriers, where the block's waves wait for the
+  // slowest).
   uint32_t T = kTileBytes / step_bytes;
   const uint32_t max_by_regs = kStageRegs * waves * kWave * 16 / step_bytes;
   if (T > max_by_regs) T = max_by_regs;
+  while (T > 1 && kStaticLds + dyn_lds_bytes(waves, 2 * size_t(T) * step_bytes, false) >
+                      size_t(f.lds_per_block))
+    --T;
   if (T < 1) T = 1;
   a.tile_steps = T;
   const dim3 grid(a.ncls * ((per_cls + waves - 1) / waves)), block(waves * kWave);

@@ -1160,20 +1160,33 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
   uint4 *const tiles = dyn + waves * (kWinBytes / sizeof(uint4));
 
   // tile k covers steps [k T, k T + T): 128-column blocks from col0/128 + k T W/128;
-  // each thread moves 16-byte units threadIdx.x + s * nthreads, s < kStageRegs
+  // each thread moves 16-byte units i = threadIdx.x + s * nthreads, s < kStageRegs,
+  // unit i from block (tile's first block + i / blk_u4) mod nblk.  Both terms are
+  // kept reduced mod nblk (the first advanced once per tile), so a unit's block
+  // takes one compare and subtract instead of a division.
   static_assert(kStageRegs == 4, "staging uses four registers");
-  auto fetch = [&](uint32_t k, uint32_t s) -> uint4 {
+  const uint32_t adv = (T * (W / 128)) % nblk;
+  uint32_t qoff[kStageRegs], roff[kStageRegs];
+#pragma unroll
+  for (uint32_t s = 0; s < kStageRegs; ++s) {
+    const uint32_t i = threadIdx.x + s * nthreads;
+    qoff[s] = (i / blk_u4) % nblk;
+    roff[s] = i % blk_u4;
+  }
+  auto fetch = [&](uint32_t base, uint32_t s) -> uint4 {
     const uint32_t i = threadIdx.x + s * nthreads;
     if (i >= tile_u4) return uint4{0, 0, 0, 0};
-    const uint32_t blk = (col0 / 128 + k * T * (W / 128) + i / blk_u4) % nblk;
-    return src[blk * blk_u4 + i % blk_u4];
+    uint32_t blk = base + qoff[s];
+    blk -= blk >= nblk ? nblk : 0;
+    return src[blk * blk_u4 + roff[s]];
   };
   auto store = [&](uint32_t buf, uint32_t s, const uint4 v) {
     const uint32_t i = threadIdx.x + s * nthreads;
     if (i < tile_u4) tiles[buf * tile_u4 + i] = v;
   };
 
-  uint4 r0 = fetch(0, 0), r1 = fetch(0, 1), r2 = fetch(0, 2), r3 = fetch(0, 3);
+  uint32_t base = col0 / 128;  // first block of tile 0 (col0 < N)
+  uint4 r0 = fetch(base, 0), r1 = fetch(base, 1), r2 = fetch(base, 2), r3 = fetch(base, 3);
   store(0, 0, r0);
   store(0, 1, r1);
   store(0, 2, r2);
@@ -1184,10 +1197,12 @@ __global__ __launch_bounds__(kMaxBlock) void gemv_tiled_kernel(Args a) {
   for (uint32_t k = 0; k < ntiles; ++k) {
     const bool more = k + 1 < ntiles;
     if (more) {
-      r0 = fetch(k + 1, 0);
-      r1 = fetch(k + 1, 1);
-      r2 = fetch(k + 1, 2);
-      r3 = fetch(k + 1, 3);
+      base += adv;  // first block of tile k + 1
+      base -= base >= nblk ? nblk : 0;
+      r0 = fetch(base, 0);
+      r1 = fetch(base, 1);
+      r2 = fetch(base, 2);
+      r3 = fetch(base, 3);
     }
     if (has) {
       const uint32_t *tile = reinterpret_cast<const uint32_t *>(tiles + (k & 1) * tile_u4);

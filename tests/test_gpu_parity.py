@@ -100,6 +100,10 @@ EDGE = [
     # partial last chunk; W = 128)
     (24, 4352, 8192, 256, 2.0, False),
     (32, 4224, 4096, 128, 3.0, True),
+    # 4001 chunks in 17 classes: 16 wavefronts per block on 256 compute units,
+    # where two 48 KiB tiles no longer fit LDS beside the tables and windows
+    # (tiles of 11 steps); 16-step chunks, partial last tile and chunk
+    (3765, 4352, 4096, 256, 2.0, False),
 ]
 
 

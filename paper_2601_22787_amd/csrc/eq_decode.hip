@@ -1475,14 +1475,22 @@ int launch_tiled(Args a, hipStream_t s, const DeviceFacts &f) {
 
 size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 
-// Multi-layer launch shape: enough wavefronts per block that two blocks per
-// compute unit hold every chunk (at most max_waves); each layer gets whole
-// blocks.
+// Multi-layer launch shape: the fewest wavefronts per block (at most
+// max_waves) for which two blocks per compute unit hold every chunk.  Each
+// layer gets whole blocks, so the count is checked after rounding each
+// layer's blocks up: blocks beyond two per compute unit would run as a
+// second round and double the launch's time.
 uint32_t multi_shape(const MultiArgs &m, int cus, uint32_t max_waves, MultiArgs &out) {
   uint64_t total = 0;
   for (uint32_t i = 0; i < m.n; ++i) total += m.a[i].n_chunks;
-  uint32_t waves = uint32_t((total + 2 * uint64_t(cus) - 1) / (2 * uint64_t(cus)));
+  const uint64_t slots = 2 * uint64_t(cus);
+  uint32_t waves = uint32_t((total + slots - 1) / slots);
   waves = waves < 1 ? 1 : (waves > max_waves ? max_waves : waves);
+  for (; waves < max_waves; ++waves) {
+    uint64_t blocks = 0;
+    for (uint32_t i = 0; i < m.n; ++i) blocks += (m.a[i].n_chunks + waves - 1) / waves;
+    if (blocks <= slots) break;
+  }
   out = m;
   uint32_t end = 0;
   for (uint32_t i = 0; i < m.n; ++i) {

@@ -204,3 +204,34 @@ def test_bf16_multi_wave_cap(eq):
         got = out.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)
         assert np.array_equal(got, oracle_bf16(blob)), (L.rows, L.cols)
         assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+def test_multi_shape_one_round_of_blocks(eq):
+    """Chunk counts 2048, 256 and 256 (the 70B q/k/v projections at
+    32768-symbol chunks, here with one-step chunks): five wavefronts per block
+    would need 410 + 52 + 52 = 514 blocks, more than two per compute unit on
+    256 units, so the launch takes six (428 blocks).  Results equal the
+    single-layer paths and the oracle."""
+    qkv = [make(eq, 64, 8192, 256, 256, 2.0, seed=951), make(eq, 8, 8192, 256, 256, 3.0, seed=952),
+           make(eq, 8, 8192, 256, 256, 4.0, seed=953)]
+    Ls = [L for L, _, _ in qkv]
+    say("multi shape", [(L.rows, L.cols) for L in Ls])
+    outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev()) for L in Ls]
+    eq.eq_decode_bf16_multi(Ls, outs)
+    for (L, blob, _), out in zip(qkv, outs):
+        got = out.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)
+        assert np.array_equal(got, oracle_bf16(blob))
+        assert torch.equal(out, bf16_single(eq, L))
+    for B in (1, 8):
+        x_bits = synth.activations(qkv[0][2], B)
+        x = torch.from_numpy(x_bits.view(np.int16)).to(_dev())
+        ys = [torch.empty((B, L.rows), dtype=torch.float32, device=_dev()) for L in Ls]
+        eq.eq_decode_gemv_multi(Ls, x, B, None, ys, eq.multi_workspace(Ls, B))
+        for (L, blob, _), y in zip(qkv, ys):
+            y1 = torch.empty((B, L.rows), dtype=torch.float32, device=_dev())
+            eq.eq_decode_gemv(L, x, B, None, y1, L.workspace(B))
+            assert torch.equal(y, y1)
+            err = rel_err(y.cpu().numpy(), oracle.gemv(oracle_bf16(blob), x_bits))
+            assert (err <= TOL).all(), err
+    for L in Ls:
+        assert eq.eq_get_status(L) == eq.EQ_OK

@@ -1479,17 +1479,36 @@ size_t round256(size_t v) { return (v + 255) / 256 * 256; }
 // max_waves) for which two blocks per compute unit hold every chunk.  Each
 // layer gets whole blocks, so the count is checked after rounding each
 // layer's blocks up: blocks beyond two per compute unit would run as a
-// second round and double the launch's time.
+// second round and double the launch's time.  Launches that need several
+// rounds anyway are balanced across compute units instead (below).
 uint32_t multi_shape(const MultiArgs &m, int cus, uint32_t max_waves, MultiArgs &out) {
   uint64_t total = 0;
   for (uint32_t i = 0; i < m.n; ++i) total += m.a[i].n_chunks;
   const uint64_t slots = 2 * uint64_t(cus);
   uint32_t waves = uint32_t((total + slots - 1) / slots);
   waves = waves < 1 ? 1 : (waves > max_waves ? max_waves : waves);
-  for (; waves < max_waves; ++waves) {
-    uint64_t blocks = 0;
-    for (uint32_t i = 0; i < m.n; ++i) blocks += (m.a[i].n_chunks + waves - 1) / waves;
-    if (blocks <= slots) break;
+  auto blocks_at = [&](uint32_t w) {
+    uint64_t b = 0;
+    for (uint32_t i = 0; i < m.n; ++i) b += (m.a[i].n_chunks + w - 1) / w;
+    return b;
+  };
+  for (; waves < max_waves; ++waves)
+    if (blocks_at(waves) <= slots) break;
+  // More blocks than one round holds even at max_waves: blocks are handed to
+  // compute units as others finish, so the busiest unit decodes about
+  // ceil(blocks / cus) * waves chunks.  Take the wave count in
+  // [max_waves / 2, max_waves] that makes this smallest (the larger on
+  // ties): a partial last round otherwise leaves units idle while others
+  // still decode two blocks.
+  if (blocks_at(waves) > slots) {
+    uint64_t best = ~uint64_t(0);
+    for (uint32_t w = max_waves; w >= 1 && w >= (max_waves + 1) / 2; --w) {
+      const uint64_t load = (blocks_at(w) + cus - 1) / cus * w;
+      if (load < best) {
+        best = load;
+        waves = w;
+      }
+    }
   }
   out = m;
   uint32_t end = 0;

@@ -71,10 +71,11 @@ def parse():
                          "captured HIP graph of the step")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="target CPU time of each oracle baseline sample (1 thread, all threads)")
-    ap.add_argument("--workload", choices=("c4", "c5", "prefill"), default="c4",
+    ap.add_argument("--workload", choices=("c4", "c5", "c123", "prefill"), default="c4",
                     help="c4: the 8192x28672 / 28672x8192 pair (default); c5: the 80-layer stack, "
-                         "block-wise vs per-matrix, decode-GEMV B=1 and decode to BF16; prefill: "
-                         "the c4 pair at --tokens tokens, decode to codes + MFMA GEMM")
+                         "block-wise vs per-matrix, decode-GEMV B=1 and decode to BF16; c123: "
+                         "every matrix of configs 1-3, decode to BF16 and decode-GEMV B=1; "
+                         "prefill: the c4 pair at --tokens tokens, decode to codes + MFMA GEMM")
     ap.add_argument("--tokens", type=int, default=2048, help="prefill batch (tokens)")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
@@ -339,6 +340,79 @@ def run_stack(args):
         "passes": res}), flush=True)
 
 
+def run_small(args):
+    """Configs 1-3 (1024x1024; the 4096x4096 Llama-2-7B attention projection;
+    its 11008x4096 / 4096x11008 MLP matrices): for each matrix, decode to BF16
+    and the fused decode-GEMV at B = 1, each launch timed alone with HIP events
+    over `--copies` rotated container copies.  Reports us per launch,
+    Gparams/s and the fraction of the HBM peak on the algorithmic bytes."""
+    import numpy as np
+    import torch
+
+    import paper_2601_22787_amd as eq
+    import synth
+    from synth.configs import config_matrices
+
+    eq.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    rows = []
+    for cfg in (1, 2, 3):
+        specs = config_matrices(cfg)
+        for spec, w, blob, lays in build_layers(eq, synth, specs, args.copies, dev):
+            del w
+            info = blob_info(blob)
+            out = torch.empty(spec.params, dtype=torch.int16, device=dev)
+            x = torch.from_numpy(synth.activations(spec, 1).view(np.int16)).to(dev)
+            y = torch.empty(1, spec.rows, dtype=torch.float32, device=dev)
+            ws = lays[0].workspace(1)
+            fns = {"bf16": lambda L: eq.eq_decode_bf16(L, out),
+                   "gemv1": lambda L: eq.eq_decode_gemv(L, x, 1, None, y, ws)}
+            for op, fn in fns.items():
+                for i in range(args.warmup):
+                    fn(lays[i % len(lays)])
+                ev = []
+                for i in range(args.steps):
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    fn(lays[i % len(lays)])
+                    e1.record()
+                    ev.append((e0, e1))
+                torch.cuda.synchronize()
+                ts = [1000.0 * a.elapsed_time(b) for a, b in ev]
+                us = sum(ts) / len(ts)
+                nbytes = algorithmic_bytes(info, op, 1)
+                rows.append({"config": cfg, "matrix": spec.name, "shape": [spec.rows, spec.cols],
+                             "chunk_syms": spec.chunk_syms, "lanes": spec.lanes,
+                             "entropy_bits": round(info["entropy"], 4),
+                             "container_mb": round(info["file_bytes"] / 1e6, 3), "op": op,
+                             "us": round(us, 2),
+                             "us_p50": round(float(np.percentile(ts, 50)), 2),
+                             "gparams_per_s": round(spec.params / us / 1e3, 1),
+                             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)})
+                print(f"[bench] config {cfg} {spec.name} {op}: {us:.1f} us", file=sys.stderr,
+                      flush=True)
+            for L in lays:
+                if eq.eq_get_status(L) != eq.EQ_OK:
+                    raise RuntimeError("decode status not OK")
+            del lays, out
+            torch.cuda.empty_cache()
+    params = sum(r["shape"][0] * r["shape"][1] for r in rows if r["op"] == "gemv1")
+    us_gemv = sum(r["us"] for r in rows if r["op"] == "gemv1")
+    print(json.dumps({
+        "metric": "decoded Gparams/s, configs 1-3, fused decode-GEMV B=1 over every matrix "
+                  "(launches timed one by one)",
+        "value": round(params / us_gemv / 1e3, 1), "unit": "Gparams/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+        "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+        "config": {"workload": "config 1: 1024x1024, 2 bits, 4096-symbol chunks; config 2: "
+                               "4096x4096, 3 bits, 16384-symbol chunks; config 3: 11008x4096 x2 "
+                               "and 4096x11008 with 0.1% outliers, 2 bits, 16384-symbol chunks",
+                   "copies_rotated": args.copies},
+        "matrices": rows, "env": run_env()}), flush=True)
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix throughput, published
 
 
@@ -448,6 +522,9 @@ def main():
         return
     if args.workload == "prefill":
         run_prefill(args)
+        return
+    if args.workload == "c123":
+        run_small(args)
         return
     import numpy as np
     import torch

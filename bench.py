@@ -192,10 +192,30 @@ def run_env():
                     break
     except OSError:
         pass
-    return {"device": props.name, "arch": getattr(props, "gcnArchName", ""),
-            "compute_units": props.multi_processor_count,
-            "hbm_gib": round(props.total_memory / 2**30, 1), "hip": torch.version.hip,
-            "torch": torch.__version__, "cpu": cpu, "host_cores": os.cpu_count()}
+    env = {"device": props.name, "arch": getattr(props, "gcnArchName", ""),
+           "compute_units": props.multi_processor_count,
+           "hbm_gib": round(props.total_memory / 2**30, 1), "hip": torch.version.hip,
+           "torch": torch.__version__, "cpu": cpu, "host_cores": os.cpu_count()}
+    env.update(gpu_clocks())
+    return env
+
+
+def gpu_clocks():
+    """Shader and memory clock levels the driver lists in sysfs (MHz), with the
+    level current when read; empty where the files are not readable."""
+    import glob
+    out = {}
+    for kind, key in (("sclk", "sclk_mhz"), ("mclk", "mclk_mhz")):
+        for path in sorted(glob.glob(f"/sys/class/drm/card*/device/pp_dpm_{kind}")):
+            try:
+                with open(path) as f:
+                    levels = [ln.split(":", 1)[1].strip() for ln in f if ":" in ln]
+            except OSError:
+                continue
+            if levels:
+                out[key] = levels  # a trailing '*' marks the current level
+                break
+    return out
 
 
 def traffic_per_launch(op, fmt_name="e4m3"):

@@ -163,19 +163,20 @@ def cpu_baseline(layers, target_s, threads, fmt=1):
         return time.perf_counter() - t0
 
     def sample(T):
+        # rows sized from a short probe run; then the median of three runs
         R0 = 8 * T
         t0 = run(R0, T)
         R = int(min(info.rows, max(R0, R0 * target_s / max(t0, 1e-6))))
-        return R, run(R, T)
+        return R, sorted(run(R, T) for _ in range(3))[1]
 
     R1, t1 = sample(1)
     RT, tT = sample(threads)
     return {"value": RT * N / tT / 1e9, "unit": "Gparams/s", "cores": threads, "kind": "oracle",
             "sample": f"first {RT} rows ({RT * N} params) of the 8192x28672 matrix: oracle rANS "
                       f"decode per chunk + BF16 dequantisation + fp64 GEMV (B=1) on {threads} "
-                      f"threads over chunks and row blocks, {tT:.1f}s",
+                      f"threads over chunks and row blocks, median of 3 runs, {tT:.1f}s each",
             "single_thread_value": R1 * N / t1 / 1e9,
-            "single_thread_sample": f"first {R1} rows, one thread, {t1:.1f}s"}
+            "single_thread_sample": f"first {R1} rows, one thread, median of 3 runs, {t1:.1f}s each"}
 
 
 def run_env():

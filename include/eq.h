@@ -76,7 +76,7 @@ typedef struct eq_layer {
   uint32_t chunk_syms;       /* C                                                  */
   uint32_t n_chunks;
   uint32_t lanes;            /* W: 64, 128 or 256                                  */
-  uint32_t prob_bits;        /* P: 1..12                                           */
+  uint32_t prob_bits;        /* P: 8..12                                           */
   uint32_t n_syms;           /* K: 1..256                                          */
   uint32_t base_format;      /* 1 = E4M3FN, 2 = Int8 (value v(q) of a code q)      */
   uint64_t total_words, padded_words;
@@ -95,10 +95,12 @@ size_t eq_lut_bytes(void);
 
 /* Validate the container `host_blob` (blob_bytes long, host memory) and fill
  * *L with pointers into `dev_blob`, a device copy of the same bytes.  The
- * host copy is read only during the call.  `dev_lut` (eq_lut_bytes() bytes)
- * and `dev_status` (one int32) are device scratch owned by the caller and
- * tied to this layer.  Checks: magic/version/base format, sizes and
- * section bounds, ascending symbols valid in the base format, frequencies
+ * host copy is read only during the call.  `dev_blob` and `dev_lut`
+ * (eq_lut_bytes() bytes) must be 256-byte aligned (EQ_EINVAL otherwise);
+ * `dev_lut` and `dev_status` (one int32) are device scratch owned by the
+ * caller and tied to this layer.  Checks: magic/version/base format, sizes
+ * and section bounds, 8 <= P <= 12 (the kernels multiply f by x >> P with
+ * 24-bit operands), ascending symbols valid in the base format, frequencies
  * >= 1 summing to 2^P,
  * monotone chunk offsets ending at total_words, padding >= 1024 words,
  * initial states in [2^16, 2^32), scales finite with magnitude in
@@ -128,7 +130,9 @@ size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B);
 
 /* Alg. 2 fused: y[b][i] = s_i * sum_j v(q_ij) x[b][j] + bias[i] for
  * b < B <= 8, without materialising the weights.  x is [B][N] BF16 (device),
- * bias is [M] BF16 or NULL, y is [B][M] fp32 (device).  The row sum is
+ * bias is [M] BF16 or NULL (2-byte alignment suffices), y is [B][M] fp32
+ * (device).  Results are reproducible run to run: partial sums are always
+ * added in a fixed order.  The row sum is
  * accumulated in fp32 and scaled by s_i once, as QMatMul(W_q, S, x) does.
  * ws/ws_bytes: device workspace of at least eq_gemv_workspace_bytes(L, B). */
 int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,

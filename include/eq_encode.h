@@ -26,7 +26,7 @@ extern "C" {
 #endif
 
 typedef struct eqe_params {
-  uint32_t prob_bits;   /* P: probability precision, 1..12 (12 recommended)          */
+  uint32_t prob_bits;   /* P: probability precision, 8..12 (12 recommended)          */
   uint32_t chunk_syms;  /* C: symbols per chunk, a positive multiple of lanes       */
   uint32_t lanes;       /* W: interleaved coder states per chunk, 64, 128 or 256    */
   uint32_t threads;     /* worker threads; 0 = one per online CPU, at most 16       */
@@ -49,7 +49,7 @@ float eqe_alpha_search(const uint16_t *w_bf16, uint32_t M, uint32_t N, double ta
  * Qmax) to the base format of params and encode it.  On success *blob receives a buffer from malloc holding the
  * whole container (free it with eqe_free) and *blob_bytes its size.
  * Returns 0, -1 (bad arguments: M*N >= 2^32, lanes not 64/128/256, C not a
- * multiple of lanes, P outside 1..12, unknown base format) or -5 (out of memory). */
+ * multiple of lanes, P outside 8..12, unknown base format) or -5 (out of memory). */
 int eqe_encode(const uint16_t *w_bf16, uint32_t M, uint32_t N, float alpha,
                const eqe_params *params, uint8_t **blob, uint64_t *blob_bytes);
 

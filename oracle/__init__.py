@@ -371,3 +371,98 @@ def gemv(w_hat: np.ndarray, x: np.ndarray, bias: np.ndarray | None = None) -> np
     y = np.empty((B, M), dtype=np.float64)
     lib().or_gemv(_ptr(w_hat), M, N, _ptr(x), B, _ptr(bias), _ptr(y))
     return y
+
+
+# ---- the same routines over independent pieces on several host threads ----
+# Chunks are independent decode units and rows independent dequantisation and
+# GEMV units, so these give exactly the single-threaded results; ctypes
+# releases the interpreter lock for the duration of each C call.
+def _threads(threads: int) -> int:
+    if threads > 0:
+        return threads
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _row_blocks(M: int, n: int):
+    step = max(1, (M + n - 1) // n)
+    return [(r, min(M, r + step)) for r in range(0, M, step)]
+
+
+def container_decode_par(blob: np.ndarray, threads: int = 0):
+    """container_decode, chunk by chunk on `threads` host threads; returns the
+    worst return code (OK only if every chunk decoded cleanly) and the codes."""
+    from concurrent.futures import ThreadPoolExecutor
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = container_info(blob)
+    q = np.zeros(info.n_chunks * info.chunk_syms, dtype=np.uint8)
+    L = lib()
+
+    def one(c):
+        return L.or_container_decode_chunk(_ptr(blob), blob.size, c,
+                                           q.ctypes.data + c * info.chunk_syms)
+
+    with ThreadPoolExecutor(_threads(threads)) as ex:
+        rcs = list(ex.map(one, range(info.n_chunks)))
+    bad = [rc for rc in rcs if rc != OK]
+    return (bad[0] if bad else OK), q[:info.rows * info.cols].reshape(info.rows, info.cols)
+
+
+def dequant_par(q: np.ndarray, scale: np.ndarray, fmt: int = E4M3, threads: int = 0):
+    from concurrent.futures import ThreadPoolExecutor
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    scale = np.ascontiguousarray(scale, dtype=np.uint16)
+    M, N = q.shape
+    out = np.empty((M, N), dtype=np.uint16)
+    L = lib()
+
+    def one(rr):
+        r0, r1 = rr
+        L.or_dequant(q.ctypes.data + r0 * N, r1 - r0, N, scale.ctypes.data + 2 * r0, fmt,
+                     out.ctypes.data + 2 * r0 * N)
+
+    with ThreadPoolExecutor(_threads(threads)) as ex:
+        list(ex.map(one, _row_blocks(M, 4 * _threads(threads))))
+    return out
+
+
+def gemv_par(w_hat: np.ndarray, x: np.ndarray, bias: np.ndarray | None = None,
+             threads: int = 0) -> np.ndarray:
+    """gemv over row blocks on several threads (each row's sum is the same)."""
+    from concurrent.futures import ThreadPoolExecutor
+    w_hat = np.ascontiguousarray(w_hat, dtype=np.uint16)
+    x = np.ascontiguousarray(np.atleast_2d(x), dtype=np.uint16)
+    M, N = w_hat.shape
+    B = x.shape[0]
+    if bias is not None:
+        bias = np.ascontiguousarray(bias, dtype=np.uint16)
+    y = np.empty((B, M), dtype=np.float64)
+    L = lib()
+
+    def one(rr):
+        r0, r1 = rr
+        part = np.empty((B, r1 - r0), dtype=np.float64)
+        L.or_gemv(w_hat.ctypes.data + 2 * r0 * N, r1 - r0, N, _ptr(x), B,
+                  None if bias is None else bias.ctypes.data + 2 * r0, _ptr(part))
+        y[:, r0:r1] = part
+
+    with ThreadPoolExecutor(_threads(threads)) as ex:
+        list(ex.map(one, _row_blocks(M, 4 * _threads(threads))))
+    return y
+
+
+def quantize_par(w: np.ndarray, scale: np.ndarray, fmt: int = E4M3, threads: int = 0):
+    from concurrent.futures import ThreadPoolExecutor
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    scale = np.ascontiguousarray(scale, dtype=np.uint16)
+    M, N = w.shape
+    out = np.empty((M, N), dtype=np.uint8)
+    L = lib()
+
+    def one(rr):
+        r0, r1 = rr
+        L.or_quantize(w.ctypes.data + 2 * r0 * N, r1 - r0, N, scale.ctypes.data + 2 * r0, fmt,
+                      out.ctypes.data + r0 * N)
+
+    with ThreadPoolExecutor(_threads(threads)) as ex:
+        list(ex.map(one, _row_blocks(M, 4 * _threads(threads))))
+    return out

@@ -468,7 +468,7 @@ static int container_build(const uint16_t *w, uint32_t M, uint32_t N, float alph
                            const uint16_t *given, uint32_t fmt, uint32_t P, uint32_t chunk_syms,
                            uint32_t lanes, uint64_t seed, float target_bits, uint8_t **blob_out,
                            uint64_t *blob_bytes) {
-  if (!w || M == 0 || N == 0 || P < 1 || P > 12 || lanes == 0 || lanes % 64 != 0 ||
+  if (!w || M == 0 || N == 0 || P < 8 || P > 12 || lanes == 0 || lanes % 64 != 0 ||
       chunk_syms == 0 || chunk_syms % lanes != 0 || (fmt != OR_FMT_E4M3 && fmt != OR_FMT_INT8))
     return OR_EINVAL;
   uint64_t n = (uint64_t)M * N;
@@ -617,7 +617,7 @@ int or_container_info(const uint8_t *b, uint64_t bytes, or_info *h) {
   uint64_t n = (uint64_t)h->rows * h->cols;
   if ((h->base_format != OR_FMT_E4M3 && h->base_format != OR_FMT_INT8) || n == 0 || n >= (1ull << 32) || h->lanes == 0 ||
       h->lanes % 64 != 0 || h->chunk_syms == 0 || h->chunk_syms % h->lanes != 0 ||
-      h->prob_bits < 1 || h->prob_bits > 12 || h->n_syms < 1 || h->n_syms > 256 ||
+      h->prob_bits < 8 || h->prob_bits > 12 || h->n_syms < 1 || h->n_syms > 256 ||
       h->n_chunks != (n + h->chunk_syms - 1) / h->chunk_syms ||
       h->padded_words < h->total_words || h->file_bytes > bytes)
     return OR_EFORMAT;

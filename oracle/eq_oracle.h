@@ -24,7 +24,9 @@
  * The paper's ANS coder is a closed library whose format it does not give.
  * The coder here is interleaved rANS (Duda 2014; Giesen 2014 for the
  * interleaving), with these parameters, all recorded in the container:
- *   P      probability precision, M = 2^P, 1 <= P <= 12
+ *   P      probability precision, M = 2^P: 1 <= P <= 12 for the coder
+ *          functions; a container takes 8 <= P <= 12 (a decoder may then
+ *          compute f * (x >> P) with 24-bit operands)
  *   W      lanes: independent coder states per chunk (multiple of 64)
  *   state  32-bit, normalised interval [2^16, 2^32), 16-bit stream words
  * Symbol k of a chunk belongs to lane k mod W at step k div W.

@@ -191,10 +191,14 @@ typedef const __attribute__((address_space(4))) uint32_t const_u32;
 
 __device__ inline const_u32 *as_const(const void *p) { return (const_u32 *)(p); }
 
-// BF16 element i of a read-only array (i wave-uniform), via its aligned dword.
+// BF16 element i of a read-only array (i wave-uniform), via the aligned dword
+// that holds it.  The array needs only 2-byte alignment (a bias may be a view
+// at an odd element): scalar loads ignore the low two address bits, so the
+// dword is addressed explicitly and the half picked by bit 1 of the address.
 __device__ inline float bf16_at(const uint16_t *base, uint32_t i) {
-  const uint32_t w = as_const(base)[i >> 1];
-  return __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  const uintptr_t at = reinterpret_cast<uintptr_t>(base) + 2 * uintptr_t(i);
+  const uint32_t w = *as_const(reinterpret_cast<const void *>(at & ~uintptr_t(3)));
+  return __uint_as_float((at & 2) ? (w & 0xFFFF0000u) : (w << 16));
 }
 
 // Two E4M3FN codes (bytes 0 and 1 of c) to the BF16 pair of their values
@@ -402,8 +406,7 @@ struct Decoder {
 
   uint32_t tab;      // its LDS address over 512
   uint32_t prow[G], pcol[G];
-  float acc[UNIFORM ? 1 : G][kMaxBatch];
-  bool pending[G];
+  float acc[1][kMaxBatch];
 
   // Software pipeline over the states of a lane (full steps, see prun): a
   // state's slot entry is read while the states issued before it are
@@ -515,11 +518,7 @@ struct Decoder {
       }
     }
 #pragma unroll
-    for (int g = 0; g < (UNIFORM ? 1 : G); ++g)
-#pragma unroll
-      for (int b = 0; b < kMaxBatch; ++b) acc[g][b] = 0.0f;
-#pragma unroll
-    for (int g = 0; g < G; ++g) pending[g] = false;
+    for (int b = 0; b < kMaxBatch; ++b) acc[0][b] = 0.0f;
 #pragma unroll
     for (int b = 0; b < (MFMA8 ? kMaxBatch : 1); ++b) macc[b] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
   }
@@ -689,33 +688,23 @@ struct Decoder {
           }
         }
       }
-    } else {
+    } else if (MODE == kGemv) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         if (!act[g]) continue;
         const uint32_t v = code_value(val, e0[g]);  // BF16 value in the low half
-        const uint32_t col = UNIFORM ? (k0 + kk + N - row_end) + g * kWave + lane : pcol[g];
+        const uint32_t col = (k0 + kk + N - row_end) + g * kWave + lane;
 #pragma unroll
         for (int b = 0; b < kMaxBatch; ++b)
-          if (b < nb)
-            acc[UNIFORM ? 0 : g][b] = dot2_bf16(v, xbits(b, col), acc[UNIFORM ? 0 : g][b]);
-        if (!UNIFORM) pending[g] = true;
+          if (b < nb) acc[0][b] = dot2_bf16(v, xbits(b, col), acc[0][b]);
       }
     }
-    if (!UNIFORM && MODE != kCodes) {
+    if (!UNIFORM && MODE == kBf16) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         // advance this state's position by one step (W symbols)
         pcol[g] += W;
         if (pcol[g] >= N) {
-          if (MODE == kGemv && pending[g]) {
-#pragma unroll
-            for (int b = 0; b < kMaxBatch; ++b) {
-              if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
-              acc[g][b] = 0.0f;
-            }
-            pending[g] = false;
-          }
           prow[g] += pcol[g] / N;
           pcol[g] %= N;
         }
@@ -752,18 +741,7 @@ struct Decoder {
   // Close the chunk: last row sums, end-of-chunk check (every state back at
   // 2^16, stream used up exactly).
   __device__ __forceinline__ void finish() {
-    if (MODE == kGemv) {
-      if (UNIFORM) {
-        flush_uniform(row);
-      } else {
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-          if (pending[g])
-#pragma unroll
-            for (int b = 0; b < kMaxBatch; ++b)
-              if (b < nb) atomicAdd(&a.ws[b * a.rows + prow[g]], acc[g][b]);
-      }
-    }
+    if (MODE == kGemv) flush_uniform(row);
     bool bad = wb + (ra - wa) / 2 != p_end;
 #pragma unroll
     for (int g = 0; g < G; ++g) bad |= x[g] != kStateLow;
@@ -1248,18 +1226,37 @@ __global__ void merge_rows_kernel(Args a) {
   }
 }
 
-__global__ void fill_zero_kernel(float *p, uint32_t n) {
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0.0f;
-}
-
-// General shapes: y = s * (atomically accumulated row sums) + bias.
-__global__ void finalize_rows_kernel(Args a) {
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= a.rows * a.batch) return;
-  const uint32_t r = i % a.rows;
-  const float bb = a.bias ? bf16_to_f32(a.bias[r]) : 0.0f;
-  a.y[i] = bf16_to_f32(a.scale[r]) * a.ws[i] + bb;
+// Rows whose steps are not whole (N not a multiple of W): the GEMV runs on
+// the decoded codes, one block per row, each thread summing a fixed stride of
+// columns and the block reducing in a fixed tree, so y does not depend on
+// timing.  y = s * sum_j v(codes[r][j]) x[b][j] + bias.
+constexpr int kRowThreads = 256;
+__global__ __launch_bounds__(kRowThreads) void codes_gemv_kernel(Args a, const uint8_t *codes) {
+  __shared__ float part[kRowThreads / kWave][kMaxBatch];
+  const uint32_t r = blockIdx.x, t = threadIdx.x, N = a.cols;
+  const uint8_t *q = codes + size_t(r) * N;
+  const float *val = reinterpret_cast<const float *>(a.lut + 2 * kMaxSlots);
+  float acc[kMaxBatch];
+#pragma unroll
+  for (int b = 0; b < kMaxBatch; ++b) acc[b] = 0.0f;
+  for (uint32_t j = t; j < N; j += kRowThreads) {
+    const float v = val[q[j]];
+#pragma unroll
+    for (int b = 0; b < kMaxBatch; ++b)
+      if (b < int(a.batch)) acc[b] += v * bf16_to_f32(a.x[size_t(b) * N + j]);
+  }
+#pragma unroll
+  for (int b = 0; b < kMaxBatch; ++b) {
+    const float sum = wave_sum(acc[b]);
+    if ((t & (kWave - 1)) == 0) part[t / kWave][b] = sum;
+  }
+  __syncthreads();
+  if (t < a.batch) {
+    float sum = 0.0f;
+    for (int w = 0; w < kRowThreads / kWave; ++w) sum += part[w][t];
+    const float bb = a.bias ? bf16_to_f32(a.bias[r]) : 0.0f;
+    a.y[size_t(t) * a.rows + r] = bf16_to_f32(a.scale[r]) * sum + bb;
+  }
 }
 
 Args make_args(const eq_layer *L) {
@@ -1412,11 +1409,9 @@ void launch_decode_fmt(const Args &a, hipStream_t s, const DeviceFacts &f) {
     if (uniform) launch_batch<MODE, true, kXGlobal, FMT>(a, s, f);
     else launch_batch<MODE, false, kXGlobal, FMT>(a, s, f);
   } else if (gemv_xsrc(a, f, launch_waves(a.n_chunks, f.cus)) == kXLds) {
-    if (uniform) launch_batch<MODE, true, kXLds, FMT>(a, s, f);
-    else launch_batch<MODE, false, kXLds, FMT>(a, s, f);
+    launch_batch<MODE, true, kXLds, FMT>(a, s, f);  // GEMV: whole-row steps only
   } else {
-    if (uniform) launch_batch<MODE, true, kXGlobal, FMT>(a, s, f);
-    else launch_batch<MODE, false, kXGlobal, FMT>(a, s, f);
+    launch_batch<MODE, true, kXGlobal, FMT>(a, s, f);
   }
 }
 
@@ -1593,13 +1588,14 @@ extern "C" int eq_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t stream
   return launch_decode<kBf16>(a, stream);
 }
 
-// Workspace: row partials (2 per chunk and batch row) or row sums (general
-// shapes), then room for the column-paired activations.
+// Workspace: row partials (2 per chunk and batch row), then room for the
+// column-paired activations; for rows that are not whole steps, the decoded
+// codes (one byte per weight).
 extern "C" size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
   if (!layer_ok(L) || B < 1 || B > kMaxBatch) return 0;
-  const size_t floats =
-      (L->cols % L->lanes == 0) ? size_t(2) * L->n_chunks * B : size_t(L->rows) * B;
-  return round256(floats * sizeof(float)) + round256(pair_bytes(B, L->cols));
+  if (L->cols % L->lanes != 0) return round256(size_t(L->rows) * L->cols);
+  return round256(size_t(2) * L->n_chunks * B * sizeof(float)) +
+         round256(pair_bytes(B, L->cols));
 }
 
 extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
@@ -1615,14 +1611,18 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
   a.bias = bias;
   a.y = y;
   a.ws = static_cast<float *>(ws);
-  const bool uniform = L->cols % L->lanes == 0;
-  const size_t part_bytes =
-      round256((uniform ? size_t(2) * L->n_chunks * B : size_t(L->rows) * B) * sizeof(float));
-  a.xp = reinterpret_cast<const uint32_t *>(static_cast<char *>(ws) + part_bytes);
-  if (!uniform) {
-    const uint32_t n = L->rows * B;
-    hipLaunchKernelGGL(fill_zero_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a.ws, n);
+  if (L->cols % L->lanes != 0) {
+    // rows that are not whole steps: decode the codes, then a fixed-order GEMV
+    uint8_t *codes = static_cast<uint8_t *>(ws);
+    a.codes = codes;
+    int rc = launch_decode<kCodes>(a, stream);
+    if (rc != EQ_OK) return rc;
+    hipLaunchKernelGGL(codes_gemv_kernel, dim3(L->rows), dim3(kRowThreads), 0, stream, a,
+                       static_cast<const uint8_t *>(codes));
+    return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
   }
+  const size_t part_bytes = round256(size_t(2) * L->n_chunks * B * sizeof(float));
+  a.xp = reinterpret_cast<const uint32_t *>(static_cast<char *>(ws) + part_bytes);
   const DeviceFacts f = device_facts();
   int rc;
   if (gemv_xsrc(a, f, launch_waves(L->n_chunks, f.cus)) == kXTile) {
@@ -1638,15 +1638,10 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
     rc = launch_decode<kGemv>(a, stream);
   }
   if (rc != EQ_OK) return rc;
-  if (uniform) {
-    // rows split between chunks exist only when chunks do not hold whole rows
-    if (L->n_chunks > 1 && L->chunk_syms % L->cols != 0)
-      hipLaunchKernelGGL(merge_rows_kernel, dim3((L->n_chunks + 254) / 256), dim3(256), 0, stream,
-                         a);
-  } else {
-    const uint32_t n = L->rows * B;
-    hipLaunchKernelGGL(finalize_rows_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a);
-  }
+  // rows split between chunks exist only when chunks do not hold whole rows
+  if (L->n_chunks > 1 && L->chunk_syms % L->cols != 0)
+    hipLaunchKernelGGL(merge_rows_kernel, dim3((L->n_chunks + 254) / 256), dim3(256), 0, stream,
+                       a);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 

@@ -294,7 +294,7 @@ int encode_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const ui
   const uint32_t W = p->lanes, C = p->chunk_syms, P = p->prob_bits;
   const uint32_t fmt = p->base_format ? p->base_format : kFmtE4M3;
   if (n >= (uint64_t(1) << 32) || (W != 64 && W != 128 && W != 256) || C == 0 || C % W ||
-      P < 1 || P > 12 || (!given && !(alpha > 0.0f)) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
+      P < 8 || P > 12 || (!given && !(alpha > 0.0f)) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
     return -1;
   if (given)
     for (uint32_t i = 0; i < M; ++i)

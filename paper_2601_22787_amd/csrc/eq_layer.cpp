@@ -34,6 +34,10 @@ extern "C" size_t eq_lut_bytes(void) { return eq_detail::kLutBytes; }
 extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
                              const void *dev_blob, void *dev_lut, int32_t *dev_status) {
   if (!L || !host_blob || !dev_blob || !dev_lut || !dev_status) return EQ_EINVAL;
+  // sections are 256-byte aligned within the blob; the kernels read them with
+  // dword (and wider) loads
+  if ((reinterpret_cast<uintptr_t>(dev_blob) | reinterpret_cast<uintptr_t>(dev_lut)) & 255)
+    return EQ_EINVAL;
   const uint8_t *b = static_cast<const uint8_t *>(host_blob);
   if (bytes < 256 || std::memcmp(b, "EQC1", 4) != 0) return EQ_EFORMAT;
   const uint32_t fmt = rd<uint32_t>(b, 12);

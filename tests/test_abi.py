@@ -48,12 +48,21 @@ def blob():
     return eq.eqe_encode(w, 300.0, chunk_syms=2048, lanes=128)
 
 
-def _init(b):
+_FAKE = np.zeros(1024, dtype=np.uint8)
+
+
+def _fake_ptr(offset=0):
+    """A 256-byte aligned host address (plus offset) standing in for device
+    pointers: eq_layer_init never dereferences them."""
+    base = _FAKE.ctypes.data
+    return (base + 255) // 256 * 256 + offset
+
+
+def _init(b, dev_offset=0):
     b = np.ascontiguousarray(b, dtype=np.uint8)
-    fake = np.zeros(64, dtype=np.uint8)  # stand-in device pointers: never dereferenced
     L = eq.eq_layer()
-    rc = eq.lib().eq_layer_init(ctypes.byref(L), b.ctypes.data, b.size, fake.ctypes.data,
-                                fake.ctypes.data, fake.ctypes.data)
+    rc = eq.lib().eq_layer_init(ctypes.byref(L), b.ctypes.data, b.size, _fake_ptr(dev_offset),
+                                _fake_ptr(), _fake_ptr())
     return rc, L
 
 
@@ -139,3 +148,42 @@ def test_workspace_size_and_argument_checks(blob):
                                    fake.ctypes.data, 1 << 20, None) == eq.EQ_EINVAL
     assert eq.lib().eq_decode_gemv(ctypes.byref(L), fake.ctypes.data, 2, None, fake.ctypes.data,
                                    fake.ctypes.data, 4, None) == eq.EQ_EINVAL
+
+
+def test_layer_init_requires_aligned_device_copy(blob):
+    """Sections are read with dword and wider loads: a device copy that is not
+    256-byte aligned is refused before any launch."""
+    assert _init(blob)[0] == eq.EQ_OK
+    for off in (2, 4, 128):
+        assert _init(blob, dev_offset=off)[0] == eq.EQ_EINVAL, off
+
+
+@pytest.mark.parametrize("P", [8, 12])
+def test_probability_precision_edges(P):
+    """The container format takes 8 <= P <= 12 (the kernels multiply f by
+    x >> P with 24-bit operands): the oracle's and the product's encoders
+    write byte-identical containers at both edges and the library accepts
+    them; below the range both encoders refuse to write one and the library
+    rejects a header that claims it."""
+    w = synth.weights(small_spec(24, 384, seed=30 + P))
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    ref = oracle.container_build(w, alpha, P, 1024, 64)
+    blob = eq.eqe_encode(w, alpha, prob_bits=P, chunk_syms=1024, lanes=64)
+    assert np.array_equal(blob, ref)
+    rc, L = _init(blob)
+    assert rc == eq.EQ_OK and L.prob_bits == P
+    rc_dec, q = oracle.container_decode(ref)
+    assert rc_dec == oracle.OK and np.array_equal(q, oracle.quantize(w, oracle.container_scales(ref)))
+
+
+def test_probability_precision_below_range_rejected():
+    w = synth.weights(small_spec(8, 256, seed=37))
+    with pytest.raises(ValueError):
+        oracle.container_build(w, 300.0, 7, 1024, 64)
+    with pytest.raises(eq.EqError):
+        eq.eqe_encode(w, 300.0, prob_bits=7, chunk_syms=1024, lanes=64)
+    ref = oracle.container_build(w, 300.0, 8, 1024, 64)
+    bad = _patch(ref, 36, 7, np.uint32)
+    with pytest.raises(ValueError):
+        oracle.container_info(bad)
+    assert _init(bad)[0] == eq.EQ_EFORMAT

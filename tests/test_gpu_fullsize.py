@@ -1,0 +1,181 @@
+"""Whole-matrix GPU parity at the full sizes of the Llama-70B workloads.
+
+Config 4 (the 8192x28672 / 28672x8192 MLP pair) and the three distinct layers
+of the config-5 stack (one per entropy class, all seven matrices) are
+compared element by element against the oracle, with no sampling:
+  - codes (Alg. 2 lines 1-2) and BF16 weights (plus the dequantiser of
+    Sec. 2.1) bit-exact, through the single-layer entry points and through
+    the block-wise launches the benchmark times (Sec. 2.2 block-wise
+    decompression);
+  - the codes also equal the oracle quantiser applied to the generated
+    weights;
+  - every output of the fused GEMV (Alg. 2 line 3) within the normwise bar
+    max|y - y_ref| / max|y_ref| <= 1e-2 per batch row against the oracle's
+    fp64 GEMV on the decoded BF16 weights; the elementwise error over the
+    entries with |y_ref| >= 1e-3 max|y_ref| is printed beside it.
+The oracle decodes chunk by chunk on several host threads (chunks are
+independent), which gives its single-threaded result exactly.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import config_matrices
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def eq():
+    import paper_2601_22787_amd as m
+    m.lib()
+    assert torch.cuda.is_available()
+    return m
+
+
+def _dev():
+    return torch.device("cuda:0")
+
+
+def errors(y, y_ref):
+    """(normwise, elementwise) error per batch row: max|dy| / max|y_ref|, and
+    max |dy| / |y_ref| over entries with |y_ref| >= 1e-3 max|y_ref|."""
+    d = np.abs(y.astype(np.float64) - y_ref)
+    m = np.abs(y_ref).max(axis=1, keepdims=True)
+    norm = d.max(axis=1) / np.maximum(m[:, 0], 1e-300)
+    big = np.abs(y_ref) >= 1e-3 * m
+    elem = np.where(big, d / np.maximum(np.abs(y_ref), 1e-300), 0.0).max(axis=1)
+    return norm, elem
+
+
+def build(eq, spec):
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
+    blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes, seed=spec.seed,
+                         target_bits=spec.target_bits)
+    assert abs(oracle.container_info(blob).entropy_bits - spec.target_bits) <= 0.05
+    return w, blob
+
+
+def reference(w, blob):
+    """Oracle codes and BF16 weights of a whole container."""
+    rc, q_ref = oracle.container_decode_par(blob)
+    assert rc == oracle.OK
+    scale = oracle.container_scales(blob)
+    assert np.array_equal(oracle.quantize_par(w, scale), q_ref)
+    return q_ref, oracle.dequant_par(q_ref, scale)
+
+
+def gpu_codes(eq, L):
+    out = torch.empty(L.rows * L.cols, dtype=torch.uint8, device=_dev())
+    eq.eq_decode_codes(L, out)
+    return out.cpu().numpy().reshape(L.rows, L.cols)
+
+
+def to_np_bf16(t, L):
+    return t.cpu().numpy().view(np.uint16).reshape(L.rows, L.cols)
+
+
+def check_gemv(eq, name, L, w_ref, x_bits, y):
+    y_ref = oracle.gemv_par(w_ref, x_bits)
+    norm, elem = errors(y, y_ref)
+    say(f"  {name} B={x_bits.shape[0]} GEMV error normwise {norm.max():.2e} "
+        f"elementwise {elem.max():.2e}")
+    assert np.isfinite(y).all() and (norm <= TOL).all(), (name, norm)
+
+
+def gemv_single(eq, L, x_bits):
+    B = x_bits.shape[0]
+    x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+    y = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+    eq.eq_decode_gemv(L, x, B, None, y, L.workspace(B))
+    return y.cpu().numpy()
+
+
+def test_config4_whole_matrices(eq):
+    """Both config-4 matrices, every chunk and every GEMV row: codes; BF16
+    through the block-wise launch of the pair (7168 chunks in one grid, as the
+    benchmark launches it) and through the single-layer entry point; GEMV at
+    B = 1 and B = 8 through the launches the benchmark times."""
+    layers = []
+    for spec in config_matrices(4):
+        say("config 4 build", spec.name, spec.rows, spec.cols)
+        w, blob = build(eq, spec)
+        layers.append((spec, w, blob, eq.Layer(blob, _dev())))
+    Ls = [L for _, _, _, L in layers]
+    outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev()) for L in Ls]
+    eq.eq_decode_bf16_multi(Ls, outs)
+    for (spec, w, blob, L), out in zip(layers, outs):
+        say("config 4 parity", spec.name)
+        q_ref, w_ref = reference(w, blob)
+        assert np.array_equal(gpu_codes(eq, L), q_ref), spec.name
+        assert np.array_equal(to_np_bf16(out, L), w_ref), spec.name
+        one = torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev())
+        eq.eq_decode_bf16(L, one)
+        assert torch.equal(one, out)
+        del one
+        for B in (1, 8):
+            x_bits = synth.activations(spec, B)
+            check_gemv(eq, spec.name, L, w_ref, x_bits, gemv_single(eq, L, x_bits))
+        assert eq.eq_get_status(L) == eq.EQ_OK
+        del w_ref, q_ref
+
+
+# Inputs of a config-5 block: attention input (q, k, v), o input, MLP input
+# (gate, up), down input.
+GROUPS = ((("q", "k", "v"), 8192), (("o",), 8192), (("gate", "up"), 8192), (("down",), 28672))
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2])
+def test_config5_layer_whole(eq, layer):
+    """One config-5 layer of each entropy class (layer l at (2, 3, 4)[l mod 3]
+    bits), all seven matrices whole: codes and BF16 through the single-layer
+    entry points and through one block-wise BF16 launch of the whole layer;
+    the GEMV at B = 1 through the block-wise launches the benchmark times
+    (q|k|v, o, gate|up, down sharing their inputs) and per matrix."""
+    specs = {s.name.split(".")[-1]: s for s in config_matrices(5, layers=[layer])}
+    built = {}
+    for n, spec in specs.items():
+        say("config 5 build", layer, n, spec.rows, spec.cols, spec.target_bits)
+        w, blob = build(eq, spec)
+        built[n] = (w, blob, eq.Layer(blob, _dev()))
+    names = list(specs)
+    Ls = [built[n][2] for n in names]
+    outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev()) for L in Ls]
+    eq.eq_decode_bf16_multi(Ls, outs)
+    ys = {}
+    for i, (g, ncols) in enumerate(GROUPS):
+        x_bits = synth.vector(0x5EED, 16 + i, ncols).reshape(1, ncols)
+        x = torch.from_numpy(x_bits.view(np.int16)).to(_dev()).view(1, ncols)
+        gl = [built[n][2] for n in g]
+        gy = [torch.full((1, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+              for L in gl]
+        eq.eq_decode_gemv_multi(gl, x, 1, None, gy, eq.multi_workspace(gl, 1))
+        for n, y in zip(g, gy):
+            ys[n] = (x_bits, y.cpu().numpy())
+    for n, out in zip(names, outs):
+        w, blob, L = built[n]
+        say("config 5 parity", layer, n)
+        q_ref, w_ref = reference(w, blob)
+        assert np.array_equal(gpu_codes(eq, L), q_ref), n
+        assert np.array_equal(to_np_bf16(out, L), w_ref), n
+        one = torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev())
+        eq.eq_decode_bf16(L, one)
+        assert torch.equal(one, out), n
+        del one
+        x_bits, y_blk = ys[n]
+        assert np.array_equal(y_blk, gemv_single(eq, L, x_bits)), n
+        check_gemv(eq, n, L, w_ref, x_bits, y_blk)
+        assert eq.eq_get_status(L) == eq.EQ_OK
+        del w_ref, q_ref

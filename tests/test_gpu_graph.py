@@ -2,9 +2,9 @@
 kernels on the given stream (no allocation, memset or synchronisation), so a
 serving loop can capture a layer's decode, GEMVs and prefill GEMM once and
 replay them.  Every replay, with other work on the stream between replays,
-must give the eager results: bit for bit where the kernels are deterministic
-(codes, BF16, whole-row GEMV, GEMM with split-K), within 1e-6 for the
-general-shape GEMV (fp32 atomics).  The outputs are overwritten before each
+must give the eager results bit for bit: every kernel adds its partial sums
+in a fixed order (codes, BF16, whole-row GEMV, the general-shape GEMV over
+decoded codes, GEMM with split-K).  The outputs are overwritten before each
 replay, so stale values cannot pass."""
 import sys
 
@@ -49,7 +49,7 @@ def xs(spec, B):
 def test_graph_replays_match_eager(eq):
     Lu, su = layer(eq, 64, 2048, 8192, 256, 6000)    # whole-row steps
     Lv, _ = layer(eq, 48, 2048, 8192, 256, 6001)
-    Lg, sg = layer(eq, 37, 1000, 4096, 64, 6002)     # rows across steps (atomics)
+    Lg, sg = layer(eq, 37, 1000, 4096, 64, 6002)     # rows across steps (GEMV on decoded codes)
     x1, x8, xg, xb = xs(su, 1), xs(su, 8), xs(sg, 3), xs(su, 40)
     bias = torch.from_numpy(synth.bias(su).view(np.int16)).to(_dev())
     n = su.rows * su.cols
@@ -92,10 +92,7 @@ def test_graph_replays_match_eager(eq):
         g.replay()
         torch.cuda.synchronize()
         for k in bufs:
-            if k == "yg":
-                assert torch.allclose(bufs[k], ref[k], rtol=1e-6, atol=1e-6), (rep, k)
-            else:
-                assert torch.equal(bufs[k], ref[k]), (rep, k)
+            assert torch.equal(bufs[k], ref[k]), (rep, k)
         assert torch.equal(other, ref["y1"])
     for L in (Lu, Lv, Lg):
         assert eq.eq_get_status(L) == eq.EQ_OK

@@ -203,6 +203,37 @@ def test_one_hot_and_zero_inputs(eq):
     assert np.array_equal(y0, np.stack([synth.bf16_to_f32(bias)] * 2))
 
 
+def test_bias_view_at_odd_element(eq):
+    """A bias that is a view one element into a tensor (2-byte aligned, not
+    4): rows that a chunk holds whole (config-1 shape: four rows per
+    4096-symbol chunk) and rows split between chunks read the same bias
+    entry as the oracle."""
+    for M, N, C in ((256, 1024, 4096), (40, 640, 1024)):
+        say("bias view", M, N, C)
+        spec = small_spec(M, N, bits=2.0, chunk=C, lanes=64, seed=4400 + M)
+        w = synth.weights(spec)
+        blob = eq.eqe_encode(w, eq.eqe_alpha_search(w, 2.0)[0], chunk_syms=C, lanes=64)
+        L = eq.Layer(blob, _dev())
+        _, q_ref = oracle.container_decode(blob)
+        w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
+        bias_bits = synth.bias(spec)
+        backing = torch.zeros(M + 2, dtype=torch.int16, device=_dev())
+        backing[1:M + 1] = torch.from_numpy(bias_bits.view(np.int16)).to(_dev())
+        bias = backing[1:M + 1]
+        assert bias.data_ptr() % 4 == 2
+        for B in (1, 8):
+            x = synth.activations(spec, B)
+            xt = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(_dev())
+            y = torch.full((B, M), float("nan"), dtype=torch.float32, device=_dev())
+            eq.eq_decode_gemv(L, xt, B, bias, y, L.workspace(B))
+            y = y.cpu().numpy()
+            assert (rel_err(y, oracle.gemv(w_ref, x, bias_bits)) <= TOL).all()
+            # x = 0: y is the bias, exactly
+            y0 = torch.full((B, M), float("nan"), dtype=torch.float32, device=_dev())
+            eq.eq_decode_gemv(L, torch.zeros_like(xt), B, bias, y0, L.workspace(B))
+            assert np.array_equal(y0.cpu().numpy(), np.stack([synth.bf16_to_f32(bias_bits)] * B))
+
+
 def test_deterministic_and_streams(eq):
     say("determinism")
     spec = small_spec(256, 2048, bits=2.0, chunk=16384, lanes=64, seed=8)
@@ -245,111 +276,6 @@ def test_corrupted_stream_flagged(eq):
         eq.eq_layer_prepare(L)  # clears the status word
         assert eq.eq_get_status(L) == eq.EQ_OK
     assert flagged >= 1
-
-
-@pytest.fixture(scope="module")
-def c4_layers(eq):
-    out = []
-    for spec in config_matrices(4):
-        say("config 4 build", spec.name)
-        w = synth.weights(spec)
-        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
-        blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
-                             seed=spec.seed, target_bits=spec.target_bits)
-        out.append((spec, w, alpha, blob, eq.Layer(blob, _dev())))
-    return out
-
-
-def _check_sampled(eq, spec, w, blob, L, r, batches=(1,), n_chunks=6, n_rows=4):
-    """Sampled parity at full size: chunks bit-exact (codes against the
-    oracle's decode and quantiser, BF16 against the oracle's dequantiser),
-    GEMV rows within the bar."""
-    info = oracle.container_info(blob)
-    scale = oracle.container_scales(blob)
-    q = gpu_codes(eq, L).ravel()
-    wb = gpu_bf16(eq, L).ravel()
-    assert eq.eq_get_status(L) == eq.EQ_OK
-    chunks = sorted(set(r.choice(info.n_chunks, min(n_chunks, info.n_chunks),
-                                 replace=False).tolist()) | {0, info.n_chunks - 1})
-    for c in chunks:
-        rc, q_ref = oracle.container_decode_chunk(blob, c)
-        assert rc == oracle.OK
-        k0, n = _chunk_rows(info, c)
-        assert np.array_equal(q[k0:k0 + n], q_ref), (spec.name, c)
-        r0, r1 = k0 // spec.cols, (k0 + n - 1) // spec.cols + 1
-        q_rows = oracle.quantize(w[r0:r1], scale[r0:r1]).ravel()
-        assert np.array_equal(q_rows[k0 - r0 * spec.cols:][:n], q_ref)
-        w_rows = oracle.dequant(q_rows.reshape(r1 - r0, spec.cols), scale[r0:r1]).ravel()
-        assert np.array_equal(wb[k0:k0 + n], w_rows[k0 - r0 * spec.cols:][:n])
-    rows = sorted(set(r.choice(spec.rows, n_rows, replace=False).tolist()) | {0, spec.rows - 1})
-    w_rows = oracle.dequant(oracle.quantize(w[rows], scale[rows]), scale[rows])
-    for B in batches:
-        x = synth.activations(spec, B)
-        y = gpu_gemv(eq, L, x)
-        err = rel_err(y[:, rows], oracle.gemv(w_rows, x))
-        assert np.isfinite(y).all() and (err <= TOL).all(), (spec.name, B, err)
-
-
-@pytest.mark.parametrize("layer", [0, 1, 2])
-def test_config5_layer_per_entropy_class(eq, layer):
-    """The 80-layer 70B-shaped stack: one full layer of each entropy class
-    (layer l targets (2, 3, 4)[l mod 3] bits), all seven matrices at full size
-    in the benchmark's launch configuration."""
-    r = np.random.default_rng(500 + layer)
-    for spec in config_matrices(5, layers=[layer]):
-        say("config 5", spec.name, spec.rows, spec.cols, spec.target_bits)
-        w = synth.weights(spec)
-        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
-        blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
-                             seed=spec.seed, target_bits=spec.target_bits)
-        assert abs(oracle.container_info(blob).entropy_bits - spec.target_bits) <= 0.05
-        L = eq.Layer(blob, _dev())
-        _check_sampled(eq, spec, w, blob, L, r)
-        del L
-
-
-def _chunk_rows(info, c):
-    k0 = c * info.chunk_syms
-    n = min(info.chunk_syms, info.rows * info.cols - k0)
-    return k0, n
-
-
-def test_config4_full_size_sampled(eq, c4_layers):
-    """Full 8192x28672 and 28672x8192 layers in the launch configuration the
-    benchmark times: sampled chunks bit-exact (codes, BF16), sampled rows of
-    the fused GEMV at B = 1 and 8 against the oracle."""
-    r = np.random.default_rng(44)
-    for spec, w, alpha, blob, L in c4_layers:
-        say("config 4 parity", spec.name)
-        info = oracle.container_info(blob)
-        assert abs(info.entropy_bits - spec.target_bits) <= 0.05
-        scale = oracle.container_scales(blob)
-        q = gpu_codes(eq, L).ravel()
-        wb = gpu_bf16(eq, L).ravel()
-        assert eq.eq_get_status(L) == eq.EQ_OK
-        chunks = sorted(set(r.choice(info.n_chunks, 10, replace=False).tolist()) |
-                        {0, info.n_chunks - 1})
-        for c in chunks:
-            rc, q_ref = oracle.container_decode_chunk(blob, c)
-            assert rc == oracle.OK
-            k0, n = _chunk_rows(info, c)
-            assert np.array_equal(q[k0:k0 + n], q_ref), c
-            r0, r1 = k0 // spec.cols, (k0 + n - 1) // spec.cols + 1
-            # the oracle quantiser on the generated weights gives the same codes
-            q_rows = oracle.quantize(w[r0:r1], scale[r0:r1]).ravel()
-            assert np.array_equal(q_rows[k0 - r0 * spec.cols:][:n], q_ref)
-            w_rows = oracle.dequant(q_rows.reshape(r1 - r0, spec.cols), scale[r0:r1]).ravel()
-            assert np.array_equal(wb[k0:k0 + n], w_rows[k0 - r0 * spec.cols:][:n])
-        rows = sorted(set(r.choice(spec.rows, 6, replace=False).tolist()) | {0, spec.rows - 1})
-        w_rows = oracle.dequant(oracle.quantize(w[rows], scale[rows]), scale[rows])
-        for B in (1, 8):
-            x = synth.activations(spec, B)
-            y = gpu_gemv(eq, L, x)
-            y_ref = oracle.gemv(w_rows, x)
-            # normwise over the sampled rows
-            err = rel_err(y[:, rows], y_ref)
-            assert (err <= TOL).all(), (spec.name, B, err)
-            assert np.isfinite(y).all()
 
 
 @pytest.mark.parametrize("lanes,N", [(128, 1024), (256, 2048)])

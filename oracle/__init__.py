@@ -36,10 +36,23 @@ class Info(ctypes.Structure):
                  "off_words")]
 
 
+class Info2(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint32) for n in
+                ("rows", "cols", "chunk_syms", "n_chunks", "lanes", "prob_bits", "n_syms",
+                 "base_format", "tile_cols", "n_quads", "n_pairs", "n_singles", "tau")] + \
+               [(n, ctypes.c_uint64) for n in
+                ("total_words", "padded_words", "seed", "file_bytes")] + \
+               [(n, ctypes.c_float) for n in ("alpha", "target_bits", "entropy_bits")] + \
+               [(n, ctypes.c_uint64) for n in
+                ("off_scale", "off_phr", "off_freq", "off_chunk_off", "off_chunk_state",
+                 "off_words")]
+
+
 def build() -> str:
     """Compile liboracle.so (always recompiles)."""
     cmd = ["gcc", "-O2", "-std=c99", "-D_GNU_SOURCE", "-fPIC", "-shared", "-ffp-contract=off",
-           "-fno-fast-math", os.path.join(_HERE, "eq_oracle.c"), "-o", _LIB_PATH + ".tmp", "-lm"]
+           "-fno-fast-math", os.path.join(_HERE, "eq_oracle.c"), os.path.join(_HERE, "eq_phrase.c"),
+           "-o", _LIB_PATH + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
     return _LIB_PATH
@@ -110,6 +123,27 @@ def lib():
             "or_container_decode": (ctypes.c_int, [_vp, ctypes.c_uint64, _vp]),
             "or_gemv": (None, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp,
                                _vp]),
+            "or_freq_norm": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp]),
+            "or_tile_geometry": (None, [ctypes.c_uint32] * 5 + [_vp] * 4),
+            "or_phrase_dict": (ctypes.c_int, [_vp] + [ctypes.c_uint32] * 6 + [_vp] * 4),
+            "or_phrase_parse": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp,
+                                               ctypes.c_uint32, _vp, ctypes.c_uint32, _vp, _vp]),
+            "or_prans_encode": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_uint32, _vp,
+                                               ctypes.c_uint32, ctypes.c_uint32, _vp,
+                                               ctypes.c_uint64, _vp, _vp]),
+            "or_prans_decode": (ctypes.c_int, [_vp, ctypes.c_uint64, _vp, _vp, ctypes.c_uint32,
+                                               _vp, _vp, ctypes.c_uint32, ctypes.c_uint32, _vp,
+                                               _vp, _vp]),
+            "or_container2_build": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
+                                                   ctypes.c_float, _vp, ctypes.c_uint32,
+                                                   ctypes.c_uint32, ctypes.c_uint32,
+                                                   ctypes.c_uint32, ctypes.c_uint64,
+                                                   ctypes.c_float, ctypes.POINTER(ctypes.c_void_p),
+                                                   ctypes.POINTER(ctypes.c_uint64)]),
+            "or_container2_info": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.POINTER(Info2)]),
+            "or_container2_decode_chunk": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.c_uint32,
+                                                          _vp]),
+            "or_container2_decode": (ctypes.c_int, [_vp, ctypes.c_uint64, _vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -354,7 +388,8 @@ def container_decode(blob: np.ndarray):
 
 
 def container_scales(blob: np.ndarray) -> np.ndarray:
-    info = container_info(blob)
+    """The BF16 row scales (either container version)."""
+    info = container2_info(blob) if container_version(blob) == 2 else container_info(blob)
     return np.frombuffer(blob[info.off_scale:info.off_scale + 2 * info.rows].tobytes(),
                          dtype=np.uint16).copy()
 
@@ -466,3 +501,172 @@ def quantize_par(w: np.ndarray, scale: np.ndarray, fmt: int = E4M3, threads: int
     with ThreadPoolExecutor(_threads(threads)) as ex:
         list(ex.map(one, _row_blocks(M, 4 * _threads(threads))))
     return out
+
+
+
+# ---- container version 2: tiles and aligned phrases ----
+V2_RES = 12      # frequency resolution R (a symbol's probability in multiples of 2^-R)
+
+
+def freq_norm(counts, R: int) -> np.ndarray:
+    c = np.ascontiguousarray(counts, dtype=np.uint64)
+    f = np.zeros(c.size, dtype=np.uint16)
+    rc = lib().or_freq_norm(_ptr(c), c.size, R, _ptr(f))
+    if rc != OK:
+        raise ValueError(f"or_freq_norm: {rc}")
+    return f
+
+
+def tile_geometry(M: int, N: int, TR: int, TC: int, c: int):
+    """(row0, col0, rows, cols) of chunk c."""
+    v = [ctypes.c_uint32() for _ in range(4)]
+    lib().or_tile_geometry(M, N, TR, TC, c, *[ctypes.addressof(x) for x in v])
+    return tuple(x.value for x in v)
+
+
+def phrase_dict(q: np.ndarray, TR: int, TC: int, R: int = V2_RES, tau: int = 1):
+    """(DQ, DP): quad and pair values (little-endian code bytes), ascending."""
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    M, N = q.shape
+    quads = np.zeros(1 << (R - 1), dtype=np.uint32)
+    pairs = np.zeros(1 << (R - 2), dtype=np.uint32)
+    nq, np_ = ctypes.c_uint32(), ctypes.c_uint32()
+    rc = lib().or_phrase_dict(_ptr(q), M, N, TR, TC, R, tau, _ptr(quads), ctypes.addressof(nq),
+                              _ptr(pairs), ctypes.addressof(np_))
+    if rc != OK:
+        raise ValueError(f"or_phrase_dict: {rc}")
+    return quads[:nq.value].copy(), pairs[:np_.value].copy()
+
+
+def phrase_parse(u: np.ndarray, quads, pairs, singles) -> np.ndarray:
+    u = np.ascontiguousarray(u, dtype=np.uint8)
+    quads = np.ascontiguousarray(quads, dtype=np.uint32)
+    pairs = np.ascontiguousarray(pairs, dtype=np.uint32)
+    singles = np.ascontiguousarray(singles, dtype=np.uint8)
+    out = np.zeros(max(u.size, 1), dtype=np.uint32)
+    n = ctypes.c_uint32()
+    rc = lib().or_phrase_parse(_ptr(u), u.size, _ptr(quads) if quads.size else None, quads.size,
+                               _ptr(pairs) if pairs.size else None, pairs.size,
+                               _ptr(singles) if singles.size else None, singles.size, _ptr(out),
+                               ctypes.addressof(n))
+    if rc != OK:
+        raise ValueError(f"or_phrase_parse: {rc}")
+    return out[:n.value].copy()
+
+
+def prans_encode(tokens, freq, R: int):
+    """tokens: one sequence of symbol indices per state.  Returns (words, states)."""
+    W = len(tokens)
+    lens = np.array([len(t) for t in tokens], dtype=np.uint32)
+    off = np.zeros(W, dtype=np.uint64)
+    off[1:] = np.cumsum(lens.astype(np.uint64))[:-1]
+    flat = np.ascontiguousarray(np.concatenate([np.asarray(t, dtype=np.uint32) for t in tokens])
+                                if lens.sum() else np.zeros(1, dtype=np.uint32))
+    freq = np.ascontiguousarray(freq, dtype=np.uint16)
+    cap = int(lens.sum()) + 16
+    words = np.zeros(cap, dtype=np.uint16)
+    states = np.zeros(W, dtype=np.uint32)
+    nw = ctypes.c_uint64()
+    rc = lib().or_prans_encode(_ptr(flat), _ptr(off), _ptr(lens), W, _ptr(freq), freq.size, R,
+                               _ptr(words), cap, ctypes.addressof(nw), _ptr(states))
+    if rc != OK:
+        raise ValueError(f"or_prans_encode: {rc}")
+    return words[:nw.value].copy(), states
+
+
+def prans_decode(words, states, need, freq, plen, R: int):
+    """Returns (rc, list of symbol sequences per state)."""
+    words = np.ascontiguousarray(words, dtype=np.uint16)
+    states = np.ascontiguousarray(states, dtype=np.uint32)
+    need = np.ascontiguousarray(need, dtype=np.uint32)
+    freq = np.ascontiguousarray(freq, dtype=np.uint16)
+    plen = np.ascontiguousarray(plen, dtype=np.uint8)
+    W = states.size
+    off = np.zeros(W, dtype=np.uint64)
+    off[1:] = np.cumsum(need.astype(np.uint64))[:-1]
+    tok = np.zeros(int(need.sum()) + 1, dtype=np.uint32)
+    got = np.zeros(W, dtype=np.uint32)
+    wp = words if words.size else np.zeros(1, dtype=np.uint16)
+    rc = lib().or_prans_decode(_ptr(wp), words.size, _ptr(states), _ptr(need), W, _ptr(freq),
+                               _ptr(plen), freq.size, R, _ptr(tok), _ptr(off), _ptr(got))
+    return rc, [tok[int(off[s]):int(off[s]) + int(got[s])].copy() for s in range(W)]
+
+
+def container2_build(w: np.ndarray, alpha: float, TR: int, TC: int, R: int = V2_RES,
+                     seed: int = 0, target_bits: float = 0.0, fmt: int = E4M3,
+                     scale: np.ndarray | None = None) -> np.ndarray:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M, N = w.shape
+    if scale is not None:
+        scale = np.ascontiguousarray(scale, dtype=np.uint16)
+    p = ctypes.c_void_p()
+    nb = ctypes.c_uint64()
+    rc = lib().or_container2_build(_ptr(w), M, N, alpha, _ptr(scale), fmt, R, TR, TC, seed,
+                                   target_bits, ctypes.byref(p), ctypes.byref(nb))
+    if rc != OK:
+        raise ValueError(f"or_container2_build: {rc}")
+    try:
+        out = np.frombuffer(ctypes.string_at(p.value, nb.value), dtype=np.uint8).copy()
+    finally:
+        lib().or_free(p)
+    return out
+
+
+def container2_info(blob: np.ndarray) -> Info2:
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = Info2()
+    rc = lib().or_container2_info(_ptr(blob), blob.size, ctypes.byref(info))
+    if rc != OK:
+        raise ValueError(f"or_container2_info: {rc}")
+    return info
+
+
+def container_version(blob: np.ndarray) -> int:
+    return int(np.frombuffer(np.ascontiguousarray(blob[4:8]).tobytes(), dtype=np.uint32)[0])
+
+
+def container2_decode_chunk(blob: np.ndarray, c: int):
+    """(rc, codes of tile c as a rows x cols array)."""
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = container2_info(blob)
+    r0, c0, rows, cols = tile_geometry(info.rows, info.cols, info.lanes, info.tile_cols, c)
+    t = np.zeros(max(rows * cols, 1), dtype=np.uint8)
+    rc = lib().or_container2_decode_chunk(_ptr(blob), blob.size, c, _ptr(t))
+    return rc, t[:rows * cols].reshape(rows, cols)
+
+
+def container2_decode(blob: np.ndarray):
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = container2_info(blob)
+    q = np.zeros((info.rows, info.cols), dtype=np.uint8)
+    rc = lib().or_container2_decode(_ptr(blob), blob.size, _ptr(q))
+    return rc, q
+
+
+def container2_decode_par(blob: np.ndarray, threads: int = 0):
+    """container2_decode, tile by tile on several host threads."""
+    from concurrent.futures import ThreadPoolExecutor
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    info = container2_info(blob)
+    q = np.zeros((info.rows, info.cols), dtype=np.uint8)
+
+    def one(c):
+        rc, t = container2_decode_chunk(blob, c)
+        r0, c0, rows, cols = tile_geometry(info.rows, info.cols, info.lanes, info.tile_cols, c)
+        q[r0:r0 + rows, c0:c0 + cols] = t
+        return rc
+
+    with ThreadPoolExecutor(_threads(threads)) as ex:
+        rcs = list(ex.map(one, range(info.n_chunks)))
+    bad = [rc for rc in rcs if rc != OK]
+    return (bad[0] if bad else OK), q
+
+
+def container2_phrases(blob: np.ndarray):
+    """(codes [n][4], lengths [n], freq [n]) of the container's alphabet."""
+    info = container2_info(blob)
+    n = info.n_syms
+    codes = blob[info.off_phr:info.off_phr + 4 * n].reshape(n, 4).copy()
+    plen = np.array([4] * info.n_quads + [2] * info.n_pairs + [1] * info.n_singles, dtype=np.uint8)
+    freq = np.frombuffer(blob[info.off_freq:info.off_freq + 2 * n].tobytes(), dtype=np.uint16).copy()
+    return codes, plen, freq

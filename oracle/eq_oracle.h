@@ -138,6 +138,49 @@ int or_container_build_scaled(const uint16_t *w, uint32_t M, uint32_t N, const u
                               uint64_t seed, float target_bits, uint8_t **blob,
                               uint64_t *blob_bytes);
 
+/* ---- container version 2: tile order and aligned phrases (eq_phrase.c) ----
+ * Tiles of TR rows x TC columns are the chunks (row s of a tile is the
+ * segment of coder state s); each segment is coded as aligned quads, pairs
+ * and single codes from a per-layer dictionary; rANS at M = 2^16 with
+ * frequencies in multiples of 2^(16-R). */
+typedef struct or_info2 {
+  uint32_t rows, cols, chunk_syms, n_chunks, lanes, prob_bits, n_syms, base_format;
+  uint32_t tile_cols, n_quads, n_pairs, n_singles, tau;
+  uint64_t total_words, padded_words, seed, file_bytes;
+  float alpha, target_bits, entropy_bits;
+  uint64_t off_scale, off_phr, off_freq, off_chunk_off, off_chunk_state, off_words;
+} or_info2;
+
+/* counts of n symbols (each >= 1) to frequencies >= 1 summing to 2^R, by the
+ * rule of or_freq_table (a frequency of 2^16 is stored as 0) */
+int or_freq_norm(const uint64_t *cnt, uint32_t n, uint32_t R, uint16_t *freq);
+void or_tile_geometry(uint32_t M, uint32_t N, uint32_t TR, uint32_t TC, uint32_t c,
+                      uint32_t *row0, uint32_t *col0, uint32_t *rows, uint32_t *cols);
+/* DQ (<= 2^(R-1) values, quad share threshold tau * 2^-(R+2)) and DP
+ * (<= 2^(R-2) values), each ascending */
+int or_phrase_dict(const uint8_t *q, uint32_t M, uint32_t N, uint32_t TR, uint32_t TC,
+                   uint32_t R, uint32_t tau, uint32_t *quads, uint32_t *n_quads, uint32_t *pairs,
+                   uint32_t *n_pairs);
+/* symbol indices of one segment (quads, then pairs, then singles) */
+int or_phrase_parse(const uint8_t *u, uint32_t w, const uint32_t *quads, uint32_t nq,
+                    const uint32_t *pairs, uint32_t np, const uint8_t *singles, uint32_t ns,
+                    uint32_t *out, uint32_t *n_out);
+int or_prans_encode(const uint32_t *tok, const uint64_t *off, const uint32_t *len, uint32_t W,
+                    const uint16_t *freq, uint32_t n_sym, uint32_t R, uint16_t *words,
+                    uint64_t max_words, uint64_t *n_words, uint32_t *states);
+int or_prans_decode(const uint16_t *words, uint64_t n_words, const uint32_t *states,
+                    const uint32_t *need, uint32_t W, const uint16_t *freq, const uint8_t *plen,
+                    uint32_t n_sym, uint32_t R, uint32_t *tok, const uint64_t *off,
+                    uint32_t *got);
+int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
+                        const uint16_t *given_scale, uint32_t fmt, uint32_t R, uint32_t TR,
+                        uint32_t TC, uint64_t seed, float target_bits, uint8_t **blob,
+                        uint64_t *blob_bytes);
+int or_container2_info(const uint8_t *blob, uint64_t blob_bytes, or_info2 *info);
+int or_container2_decode_chunk(const uint8_t *blob, uint64_t blob_bytes, uint32_t chunk,
+                               uint8_t *tile);
+int or_container2_decode(const uint8_t *blob, uint64_t blob_bytes, uint8_t *q);
+
 /* ---- linear layer (Sec. 2.1): y[b][i] = sum_j w_hat[i][j] x[b][j] + bias[i] in fp64 ---- */
 void or_gemv(const uint16_t *w_hat, uint32_t M, uint32_t N, const uint16_t *x, uint32_t B,
              const uint16_t *bias, double *y);

@@ -96,6 +96,50 @@ int eqe_rd_lambda_search(const uint16_t *w_bf16, uint32_t M, uint32_t N, double 
                          uint32_t sample_rows, const eqe_rd_params *params, double *lambda,
                          double *h);
 
+/* ---- container version 2 (decoded by the same entry points of eq.h) ----
+ * Version 2 codes the same quantised codes with two choices of this library
+ * where the paper leaves the coder to a closed one (App. A.1):
+ *  - vec order: the M x N code matrix is cut into tiles of TR rows by TC
+ *    columns (the last tile row and column may be smaller); tile (b, t),
+ *    t < NT = ceil(N / TC), is chunk b * NT + t, and row s of a tile is the
+ *    segment of coder state s (TR states per chunk), in column order;
+ *  - alphabet: phrases.  A segment is parsed greedily from its start: the
+ *    four codes at the position if they are in the quad dictionary DQ, else
+ *    the two codes if they are in the pair dictionary DP, else one code.
+ *    The alphabet is DQ, then DP, then the codes emitted alone (DS), each in
+ *    ascending order of its codes read as a little-endian integer; the
+ *    frequencies are the symbols' counts normalised to 2^R as for version 1.
+ *    DP: the pairs at positions 0, 2, 4, ... of all segments whose count
+ *    times 2^(R+2) is at least the number of pairs counted, at most the
+ *    2^(R-2) most frequent (ties: lower value).  DQ: likewise for the quads
+ *    at positions 0, 4, 8, ..., with the threshold tau times the number of
+ *    quads counted and at most 2^(R-1) of them.  Entries the parse never
+ *    emits are dropped.  tau is the one of 8, 4, 2, 1 whose alphabet needs
+ *    the fewest bits, sum over symbols of count * log2(2^R / f) in fp64
+ *    summed in alphabet order (ties: the larger tau);
+ *  - coder: interleaved rANS with the state arithmetic at 2^16 and
+ *    frequencies F = f * 2^(16 - R); step t decodes the t-th symbol of every
+ *    state whose segment is not yet complete, then those states take a word
+ *    in ascending order when x < 2^16 (layout of the container: eq.h). */
+typedef struct eqe_params2 {
+  uint32_t res_bits;    /* R: frequency resolution, 10..12 (12 recommended)          */
+  uint32_t tile_rows;   /* TR: coder states per chunk, 64, 128 or 256                */
+  uint32_t tile_cols;   /* TC: a positive multiple of 4                              */
+  uint32_t threads;     /* worker threads; 0 = one per online CPU, at most 16       */
+  uint64_t seed;        /* recorded in the header, not used                         */
+  float target_bits;    /* recorded in the header, not used                         */
+  uint32_t base_format; /* 1 = E4M3FN (0 is read as 1), 2 = Int8                    */
+} eqe_params2;
+
+/* Quantise w (M x N BF16, host) with scales bf16(alpha * absmax / Qmax), or
+ * with the given BF16 scales when scale_bf16 is non-null (alpha is then
+ * recorded as 0), and write a version-2 container to *blob (malloc'd; free
+ * with eqe_free).  Returns 0, -1 (bad arguments, including TR * TC >= 2^32
+ * and an unusable given scale) or -5 (out of memory). */
+int eqe_encode2(const uint16_t *w_bf16, uint32_t M, uint32_t N, float alpha,
+                const uint16_t *scale_bf16, const eqe_params2 *params, uint8_t **blob,
+                uint64_t *blob_bytes);
+
 void eqe_free(void *p);
 
 #ifdef __cplusplus

@@ -45,6 +45,13 @@ class eqe_params(ctypes.Structure):
                 ("base_format", ctypes.c_uint32)]
 
 
+class eqe_params2(ctypes.Structure):
+    _fields_ = [("res_bits", ctypes.c_uint32), ("tile_rows", ctypes.c_uint32),
+                ("tile_cols", ctypes.c_uint32), ("threads", ctypes.c_uint32),
+                ("seed", ctypes.c_uint64), ("target_bits", ctypes.c_float),
+                ("base_format", ctypes.c_uint32)]
+
+
 class eqe_rd_params(ctypes.Structure):
     _fields_ = [("lambda_", ctypes.c_double), ("lr", ctypes.c_double),
                 ("iters", ctypes.c_uint32), ("history", ctypes.c_uint32),
@@ -80,6 +87,9 @@ SIGNATURES = {
     "eqe_encode": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float,
                                   ctypes.POINTER(eqe_params), ctypes.POINTER(ctypes.c_void_p),
                                   ctypes.POINTER(ctypes.c_uint64)]),
+    "eqe_encode2": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_float, _vp,
+                                   ctypes.POINTER(eqe_params2), ctypes.POINTER(ctypes.c_void_p),
+                                   ctypes.POINTER(ctypes.c_uint64)]),
     "eqe_encode_scaled": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32, _vp,
                                          ctypes.POINTER(eqe_params),
                                          ctypes.POINTER(ctypes.c_void_p),
@@ -333,6 +343,31 @@ def eqe_encode(w: np.ndarray, alpha: float, *, prob_bits: int = 12, chunk_syms: 
         rc = lib().eqe_encode_scaled(w.ctypes.data, w.shape[0], w.shape[1], sc.ctypes.data,
                                      ctypes.byref(prm), ctypes.byref(p), ctypes.byref(nb))
         _check("eqe_encode_scaled", rc)
+    try:
+        out = np.empty(nb.value, dtype=np.uint8)
+        ctypes.memmove(out.ctypes.data, p.value, nb.value)
+    finally:
+        lib().eqe_free(p)
+    return out
+
+
+def eqe_encode2(w: np.ndarray, alpha: float, *, tile_rows: int, tile_cols: int,
+                res_bits: int = 12, threads: int = 0, seed: int = 0, target_bits: float = 0.0,
+                base_format: int = FMT_E4M3, scale_bf16: np.ndarray | None = None) -> np.ndarray:
+    """A version-2 container (tile-ordered chunks, phrase alphabet)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    prm = eqe_params2(res_bits, tile_rows, tile_cols, threads, seed, target_bits, base_format)
+    sc = None
+    if scale_bf16 is not None:
+        sc = np.ascontiguousarray(scale_bf16, dtype=np.uint16)
+        if sc.size != w.shape[0]:
+            raise ValueError("one scale per row")
+    p = ctypes.c_void_p()
+    nb = ctypes.c_uint64()
+    rc = lib().eqe_encode2(w.ctypes.data, w.shape[0], w.shape[1], alpha,
+                           None if sc is None else sc.ctypes.data, ctypes.byref(prm),
+                           ctypes.byref(p), ctypes.byref(nb))
+    _check("eqe_encode2", rc)
     try:
         out = np.empty(nb.value, dtype=np.uint8)
         ctypes.memmove(out.ctypes.data, p.value, nb.value)

@@ -446,3 +446,447 @@ extern "C" int eqe_rd_lambda_search(const uint16_t *w, uint32_t M, uint32_t N,
 }
 
 extern "C" void eqe_free(void *ptr) { std::free(ptr); }
+
+// ---------------------------------------------------------------------------
+// Container version 2: tiles of TR rows x TC columns are the chunks (row s of
+// a tile is the segment of coder state s), each segment coded as a greedy
+// parse into quads, pairs and single codes from a per-layer dictionary, with
+// rANS at M = 2^16 and frequencies in multiples of 2^(16-R).  The rules
+// (dictionary shares, the choice among tau = 8, 4, 2, 1, the normalisation)
+// are stated in eq_encode.h.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr uint32_t kNoEntry = 0xFFFFFFFFu;
+
+// Open-addressing counter keyed by a 32-bit value.
+class Counter {
+ public:
+  Counter() : keys_(1024, 0), counts_(1024, 0), used_(1024, 0) {}
+  void add(uint32_t key, uint64_t n = 1) {
+    if (2 * (size_ + 1) > keys_.size()) grow();
+    size_t i = slot(key);
+    if (!used_[i]) {
+      used_[i] = 1;
+      keys_[i] = key;
+      ++size_;
+    }
+    counts_[i] += n;
+  }
+  void merge(const Counter &o) {
+    for (size_t i = 0; i < o.keys_.size(); ++i)
+      if (o.used_[i]) add(o.keys_[i], o.counts_[i]);
+  }
+  template <class Fn>
+  void each(Fn fn) const {
+    for (size_t i = 0; i < keys_.size(); ++i)
+      if (used_[i]) fn(keys_[i], counts_[i]);
+  }
+
+ private:
+  size_t slot(uint32_t key) const {
+    const size_t mask = keys_.size() - 1;
+    size_t i = (key * 0x9E3779B1u) & mask;
+    while (used_[i] && keys_[i] != key) i = (i + 1) & mask;
+    return i;
+  }
+  void grow() {
+    std::vector<uint32_t> k;
+    std::vector<uint64_t> c;
+    std::vector<uint8_t> u;
+    k.swap(keys_), c.swap(counts_), u.swap(used_);
+    keys_.assign(2 * k.size(), 0), counts_.assign(2 * k.size(), 0), used_.assign(2 * k.size(), 0);
+    size_ = 0;
+    for (size_t i = 0; i < k.size(); ++i)
+      if (u[i]) add(k[i], c[i]);
+  }
+  std::vector<uint32_t> keys_;
+  std::vector<uint64_t> counts_;
+  std::vector<uint8_t> used_;
+  size_t size_ = 0;
+};
+
+// Sorted set of dictionary values with their indices, looked up by hashing.
+class Lookup {
+ public:
+  explicit Lookup(const std::vector<uint32_t> &vals) {
+    size_t cap = 16;
+    while (cap < 4 * vals.size()) cap *= 2;
+    keys_.assign(cap, 0);
+    idx_.assign(cap, kNoEntry);
+    for (uint32_t k = 0; k < vals.size(); ++k) {
+      size_t i = (vals[k] * 0x9E3779B1u) & (cap - 1);
+      while (idx_[i] != kNoEntry) i = (i + 1) & (cap - 1);
+      keys_[i] = vals[k];
+      idx_[i] = k;
+    }
+  }
+  uint32_t find(uint32_t v) const {
+    const size_t mask = keys_.size() - 1;
+    for (size_t i = (v * 0x9E3779B1u) & mask;; i = (i + 1) & mask) {
+      if (idx_[i] == kNoEntry) return kNoEntry;
+      if (keys_[i] == v) return idx_[i];
+    }
+  }
+
+ private:
+  std::vector<uint32_t> keys_, idx_;
+};
+
+inline uint32_t quad_at(const uint8_t *u) {
+  uint32_t v;
+  std::memcpy(&v, u, 4);  // little-endian host: codes in position order
+  return v;
+}
+inline uint32_t pair_at(const uint8_t *u) { return uint32_t(u[0]) | uint32_t(u[1]) << 8; }
+
+struct Geometry {
+  uint32_t M, N, TR, TC, NT, n_chunks;
+  void tile(uint32_t c, uint32_t &r0, uint32_t &c0, uint32_t &rows, uint32_t &cols) const {
+    r0 = (c / NT) * TR;
+    c0 = (c % NT) * TC;
+    rows = std::min(TR, M - r0);
+    cols = std::min(TC, N - c0);
+  }
+};
+
+// Values passing count * 2^(R+2) >= tau * units, at most cap of them by
+// (count desc, value asc), returned ascending.
+std::vector<uint32_t> select_values(const Counter &h, uint64_t units, uint32_t R, uint32_t tau,
+                                    uint32_t cap) {
+  std::vector<std::pair<uint64_t, uint32_t>> cand;
+  h.each([&](uint32_t v, uint64_t c) {
+    if ((c << (R + 2)) >= uint64_t(tau) * units) cand.emplace_back(c, v);
+  });
+  std::sort(cand.begin(), cand.end(), [](const auto &a, const auto &b) {
+    return a.first != b.first ? a.first > b.first : a.second < b.second;
+  });
+  if (cand.size() > cap) cand.resize(cap);
+  std::vector<uint32_t> out;
+  for (auto &p : cand) out.push_back(p.second);
+  std::sort(out.begin(), out.end());
+  return out;
+}
+
+// Counts of the units of width 4 (positions 0, 4, ...) or 2 (0, 2, ...) of
+// every segment.
+Counter unit_counts(const uint8_t *q, const Geometry &g, uint32_t width, unsigned nt,
+                    uint64_t &units) {
+  std::vector<Counter> part(nt);
+  std::atomic<uint32_t> next_task{0};
+  const uint32_t tasks = g.M;  // one row at a time, all its tiles
+  auto body = [&](unsigned id) {
+    Counter &h = part[id];
+    for (uint32_t r; (r = next_task.fetch_add(1)) < tasks;) {
+      const uint8_t *row = q + uint64_t(r) * g.N;
+      for (uint32_t t = 0; t < g.NT; ++t) {
+        const uint32_t c0 = t * g.TC, w = std::min(g.TC, g.N - c0);
+        for (uint32_t j = 0; j + width <= w; j += width)
+          h.add(width == 4 ? quad_at(row + c0 + j) : pair_at(row + c0 + j));
+      }
+    }
+  };
+  std::vector<std::thread> pool;
+  for (unsigned t = 1; t < nt; ++t) pool.emplace_back(body, t);
+  body(0);
+  for (auto &t : pool) t.join();
+  units = 0;
+  for (uint32_t t = 0; t < g.NT; ++t) units += uint64_t(g.M) * (std::min(g.TC, g.N - t * g.TC) / width);
+  Counter all;
+  for (auto &p : part) all.merge(p);
+  return all;
+}
+
+// Greedy parse of one segment; emits raw symbol ids: quad k, pair nq + k,
+// single nq + np + code.
+template <class Emit>
+void parse(const uint8_t *u, uint32_t w, const Lookup &dq, const Lookup &dp, uint32_t nq,
+           uint32_t np, Emit emit) {
+  uint32_t j = 0;
+  while (j < w) {
+    if (j + 4 <= w) {
+      const uint32_t k = dq.find(quad_at(u + j));
+      if (k != kNoEntry) {
+        emit(k);
+        j += 4;
+        continue;
+      }
+    }
+    if (j + 2 <= w) {
+      const uint32_t k = dp.find(pair_at(u + j));
+      if (k != kNoEntry) {
+        emit(nq + k);
+        j += 2;
+        continue;
+      }
+    }
+    emit(nq + np + u[j]);
+    j += 1;
+  }
+}
+
+// Counts to frequencies >= 1 summing to 2^R: the rule of normalise() above
+// over an arbitrary alphabet (ties by lower index).
+bool normalise_counts(const std::vector<uint64_t> &cnt, uint32_t R, std::vector<uint16_t> &freq) {
+  const size_t K = cnt.size();
+  const int64_t M = int64_t(1) << R;
+  if (K == 0 || int64_t(K) > M) return false;
+  uint64_t n = 0;
+  for (uint64_t c : cnt) {
+    if (!c) return false;
+    n += c;
+  }
+  std::vector<int64_t> f(K);
+  std::vector<uint64_t> rem(K);
+  int64_t sum = 0;
+  for (size_t k = 0; k < K; ++k) {
+    const uint64_t num = cnt[k] * uint64_t(M);
+    f[k] = std::max<int64_t>(1, int64_t(num / n));
+    rem[k] = num % n;
+    sum += f[k];
+  }
+  int64_t deficit = M - sum;
+  if (deficit > 0) {
+    std::vector<size_t> order(K);
+    for (size_t k = 0; k < K; ++k) order[k] = k;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](size_t a, size_t b) { return rem[a] > rem[b]; });
+    for (size_t i = 0; deficit > 0; i = (i + 1) % K, --deficit) ++f[order[i]];
+  }
+  while (deficit < 0) {
+    size_t best = K;
+    for (size_t k = 0; k < K; ++k)
+      if (f[k] > 1 && (best == K || f[k] > f[best])) best = k;
+    if (best == K) return false;
+    --f[best];
+    ++deficit;
+  }
+  freq.resize(K);
+  for (size_t k = 0; k < K; ++k) freq[k] = static_cast<uint16_t>(f[k]);
+  return true;
+}
+
+// One candidate alphabet: its dictionaries after dropping unused entries,
+// the renumbering of raw symbol ids, counts, frequencies and coded bits.
+struct Alphabet {
+  std::vector<uint32_t> quads, pairs;  // as selected (before dropping)
+  std::vector<uint32_t> map;           // raw id -> final index
+  std::vector<uint32_t> phr;           // final phrases: codes as a little-endian u32
+  uint32_t nq = 0, np = 0, ns = 0;
+  std::vector<uint64_t> cnt;
+  std::vector<uint16_t> freq;
+  double bits = 0.0;
+};
+
+bool make_alphabet(const uint8_t *q, const Geometry &g, uint32_t R, uint32_t tau,
+                   const Counter &quad_h, uint64_t quad_units, const std::vector<uint32_t> &pairs,
+                   unsigned nt, Alphabet &a) {
+  a.quads = select_values(quad_h, quad_units, R, tau, 1u << (R - 1));
+  a.pairs = pairs;
+  const uint32_t nq = uint32_t(a.quads.size()), np = uint32_t(a.pairs.size());
+  const uint32_t raw = nq + np + 256;
+  const Lookup dq(a.quads), dp(a.pairs);
+  std::vector<std::vector<uint64_t>> part(nt, std::vector<uint64_t>(raw, 0));
+  std::atomic<uint32_t> next_task{0};
+  auto body = [&](unsigned id) {
+    uint64_t *h = part[id].data();
+    for (uint32_t r; (r = next_task.fetch_add(1)) < g.M;) {
+      const uint8_t *row = q + uint64_t(r) * g.N;
+      for (uint32_t t = 0; t < g.NT; ++t) {
+        const uint32_t c0 = t * g.TC, w = std::min(g.TC, g.N - c0);
+        parse(row + c0, w, dq, dp, nq, np, [&](uint32_t s) { ++h[s]; });
+      }
+    }
+  };
+  std::vector<std::thread> pool;
+  for (unsigned t = 1; t < nt; ++t) pool.emplace_back(body, t);
+  body(0);
+  for (auto &t : pool) t.join();
+  std::vector<uint64_t> seen(raw, 0);
+  for (auto &p : part)
+    for (uint32_t s = 0; s < raw; ++s) seen[s] += p[s];
+  a.map.assign(raw, kNoEntry);
+  a.phr.clear();
+  a.cnt.clear();
+  a.nq = a.np = a.ns = 0;
+  for (uint32_t k = 0; k < nq; ++k)
+    if (seen[k]) a.map[k] = uint32_t(a.phr.size()), a.phr.push_back(a.quads[k]),
+                 a.cnt.push_back(seen[k]), ++a.nq;
+  for (uint32_t k = 0; k < np; ++k)
+    if (seen[nq + k]) a.map[nq + k] = uint32_t(a.phr.size()), a.phr.push_back(a.pairs[k]),
+                      a.cnt.push_back(seen[nq + k]), ++a.np;
+  for (uint32_t c = 0; c < 256; ++c)
+    if (seen[nq + np + c]) a.map[nq + np + c] = uint32_t(a.phr.size()), a.phr.push_back(c),
+                           a.cnt.push_back(seen[nq + np + c]), ++a.ns;
+  if (a.phr.size() > (size_t(1) << R)) return false;
+  if (!normalise_counts(a.cnt, R, a.freq)) return false;
+  a.bits = 0.0;
+  for (size_t k = 0; k < a.cnt.size(); ++k)
+    a.bits += double(a.cnt[k]) * std::log2(double(1u << R) / double(a.freq[k]));
+  return true;
+}
+
+// Encode one chunk: the states' symbol sequences (sym[off[s] .. off[s] +
+// len[s])) back to front; words are produced into `out_end` backwards.
+uint64_t encode_chunk2(const uint16_t *sym, const uint32_t *off, const uint32_t *len, uint32_t W,
+                       const uint64_t *F, const uint64_t *CUM, uint16_t *out_end,
+                       uint32_t *states) {
+  std::vector<uint64_t> x(W, kStateLow);
+  uint32_t T = 0;
+  for (uint32_t s = 0; s < W; ++s) T = std::max(T, len[s]);
+  uint16_t *w = out_end;
+  for (uint32_t t = T; t-- > 0;)
+    for (uint32_t s = W; s-- > 0;) {
+      if (t >= len[s]) continue;
+      const uint32_t k = sym[off[s] + t];
+      uint64_t v = x[s];
+      if (v >= (F[k] << 16)) {
+        *--w = static_cast<uint16_t>(v & 0xFFFF);
+        v >>= 16;
+      }
+      x[s] = (v / F[k]) * 65536 + (v % F[k]) + CUM[k];
+    }
+  for (uint32_t s = 0; s < W; ++s) states[s] = static_cast<uint32_t>(x[s]);
+  return static_cast<uint64_t>(out_end - w);
+}
+
+int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const uint16_t *given,
+                 const eqe_params2 *p, uint8_t **blob_out, uint64_t *bytes_out) {
+  if (!w || !p || !blob_out || !bytes_out || !M || !N) return -1;
+  const uint64_t n = static_cast<uint64_t>(M) * N;
+  const uint32_t R = p->res_bits, TR = p->tile_rows, TC = p->tile_cols;
+  const uint32_t fmt = p->base_format ? p->base_format : kFmtE4M3;
+  if (n >= (uint64_t(1) << 32) || (TR != 64 && TR != 128 && TR != 256) || TC == 0 || TC % 4 ||
+      uint64_t(TR) * TC >= (uint64_t(1) << 32) || R < 10 || R > 12 ||
+      (!given && !(alpha > 0.0f)) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
+    return -1;
+  if (given)
+    for (uint32_t i = 0; i < M; ++i)
+      if (!scale_usable(given[i])) return -1;
+  Geometry g{M, N, TR, TC, (N + TC - 1) / TC, 0};
+  const uint64_t nchunks64 = uint64_t(g.NT) * ((M + TR - 1) / TR);
+  if (nchunks64 >= (uint64_t(1) << 32)) return -1;
+  g.n_chunks = uint32_t(nchunks64);
+  const unsigned nt = worker_count(p->threads);
+  try {
+    std::vector<uint16_t> scale(M);
+    std::vector<uint8_t> codes(n);
+    std::vector<uint32_t> rows(M);
+    for (uint32_t i = 0; i < M; ++i) rows[i] = i;
+    uint64_t hist[256];
+    quantize_rows(w, N, alpha, fmt, rows, nt, scale.data(), codes.data(), hist, given);
+
+    uint64_t quad_units = 0, pair_units = 0;
+    const Counter quad_h = unit_counts(codes.data(), g, 4, nt, quad_units);
+    const Counter pair_h = unit_counts(codes.data(), g, 2, nt, pair_units);
+    const std::vector<uint32_t> pairs = select_values(pair_h, pair_units, R, 1, 1u << (R - 2));
+    Alphabet best, cur;
+    uint32_t best_tau = 0;
+    for (uint32_t tau = 8; tau >= 1; tau /= 2) {
+      if (!make_alphabet(codes.data(), g, R, tau, quad_h, quad_units, pairs, nt, cur)) return -1;
+      if (best_tau == 0 || cur.bits < best.bits) {
+        best = cur;
+        best_tau = tau;
+      }
+    }
+    const uint32_t n_sym = uint32_t(best.phr.size());
+    std::vector<uint64_t> F(n_sym), CUM(n_sym);
+    for (uint32_t k = 0, acc = 0; k < n_sym; ++k) {
+      F[k] = uint64_t(best.freq[k]) << (16 - R);
+      CUM[k] = acc;
+      acc += uint32_t(F[k]);
+    }
+
+    // parse and encode every chunk
+    const Lookup dq(best.quads), dp(best.pairs);
+    const uint32_t nq_raw = uint32_t(best.quads.size()), np_raw = uint32_t(best.pairs.size());
+    std::vector<std::vector<uint16_t>> words(g.n_chunks);
+    std::vector<uint32_t> states(uint64_t(g.n_chunks) * TR);
+    parallel_for(g.n_chunks, nt, [&](uint64_t c) {
+      uint32_t r0, c0, rws, cols;
+      g.tile(uint32_t(c), r0, c0, rws, cols);
+      std::vector<uint16_t> sym;
+      sym.reserve(uint64_t(rws) * cols / 2);
+      std::vector<uint32_t> off(TR, 0), len(TR, 0);
+      for (uint32_t s = 0; s < rws; ++s) {
+        off[s] = uint32_t(sym.size());
+        parse(codes.data() + uint64_t(r0 + s) * N + c0, cols, dq, dp, nq_raw, np_raw,
+              [&](uint32_t raw) { sym.push_back(static_cast<uint16_t>(best.map[raw])); });
+        len[s] = uint32_t(sym.size()) - off[s];
+      }
+      for (uint32_t s = rws; s < TR; ++s) off[s] = uint32_t(sym.size());
+      std::vector<uint16_t> buf(sym.size() + 16);
+      const uint64_t nw = encode_chunk2(sym.data(), off.data(), len.data(), TR, F.data(),
+                                        CUM.data(), buf.data() + buf.size(),
+                                        states.data() + c * TR);
+      words[c].assign(buf.end() - nw, buf.end());
+    });
+    std::vector<uint64_t> off(uint64_t(g.n_chunks) + 1, 0);
+    for (uint32_t c = 0; c < g.n_chunks; ++c) off[c + 1] = off[c] + words[c].size();
+    const uint64_t total = off[g.n_chunks];
+    if (total >= (uint64_t(1) << 32)) return -1;
+    const uint64_t padded = round_up(total + 1024, 128);
+
+    const uint64_t o_scale = kHeaderBytes;
+    const uint64_t o_phr = round_up(o_scale + 2ull * M, 256);
+    const uint64_t o_freq = round_up(o_phr + 4ull * n_sym, 256);
+    const uint64_t o_off = round_up(o_freq + 2ull * n_sym, 256);
+    const uint64_t o_state = round_up(o_off + 4ull * (g.n_chunks + 1), 256);
+    const uint64_t o_words = round_up(o_state + 4ull * g.n_chunks * TR, 256);
+    const uint64_t bytes = round_up(o_words + 2 * padded, 256);
+    uint8_t *b = static_cast<uint8_t *>(std::calloc(1, bytes));
+    if (!b) return -5;
+    std::memcpy(b, "EQC1", 4);
+    put<uint32_t>(b, 4, 2);                  // version
+    put<uint32_t>(b, 8, kHeaderBytes);
+    put<uint32_t>(b, 12, fmt);
+    put<uint32_t>(b, 16, M);
+    put<uint32_t>(b, 20, N);
+    put<uint32_t>(b, 24, TR * TC);
+    put<uint32_t>(b, 28, g.n_chunks);
+    put<uint32_t>(b, 32, TR);
+    put<uint32_t>(b, 36, R);
+    put<uint32_t>(b, 40, n_sym);
+    put<uint32_t>(b, 44, 0);                 // flags
+    put<uint64_t>(b, 48, total);
+    put<uint64_t>(b, 56, padded);
+    put<uint64_t>(b, 64, p->seed);
+    put<float>(b, 72, given ? 0.0f : alpha);
+    put<float>(b, 76, p->target_bits);
+    put<float>(b, 80, static_cast<float>(entropy_bits(hist)));
+    put<uint32_t>(b, 84, TC);
+    put<uint64_t>(b, 88, o_scale);
+    put<uint64_t>(b, 96, o_phr);
+    put<uint64_t>(b, 104, o_freq);
+    put<uint64_t>(b, 112, o_off);
+    put<uint64_t>(b, 120, o_state);
+    put<uint64_t>(b, 128, o_words);
+    put<uint64_t>(b, 136, bytes);
+    put<uint32_t>(b, 144, best.nq);
+    put<uint32_t>(b, 148, best.np);
+    put<uint32_t>(b, 152, best.ns);
+    put<uint32_t>(b, 156, best_tau);
+    std::memcpy(b + o_scale, scale.data(), 2ull * M);
+    std::memcpy(b + o_phr, best.phr.data(), 4ull * n_sym);
+    std::memcpy(b + o_freq, best.freq.data(), 2ull * n_sym);
+    for (uint32_t c = 0; c <= g.n_chunks; ++c) put<uint32_t>(b, o_off + 4ull * c, uint32_t(off[c]));
+    std::memcpy(b + o_state, states.data(), 4ull * g.n_chunks * TR);
+    parallel_for(g.n_chunks, nt, [&](uint64_t c) {
+      if (!words[c].empty())
+        std::memcpy(b + o_words + 2 * off[c], words[c].data(), 2 * words[c].size());
+    });
+    *blob_out = b;
+    *bytes_out = bytes;
+    return 0;
+  } catch (const std::bad_alloc &) {
+    return -5;
+  }
+}
+
+}  // namespace
+
+extern "C" int eqe_encode2(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
+                           const uint16_t *scale_bf16, const eqe_params2 *p, uint8_t **blob_out,
+                           uint64_t *bytes_out) {
+  return encode2_impl(w, M, N, scale_bf16 ? 0.0f : alpha, scale_bf16, p, blob_out, bytes_out);
+}

@@ -109,3 +109,37 @@ def test_c3_gate_full_size_matches_oracle_quantiser():
         ref = oracle.quantize(w[rows.start:rows.stop], scale[rows.start:rows.stop]).ravel()
         off = k0 - rows.start * spec.cols
         assert (ref[off:off + q.size] == q).all()
+
+
+# ---- container version 2 ----
+
+@pytest.mark.parametrize("M,N,TR,TC,bits,fmt,outliers", [
+    (300, 1000, 64, 256, 2.0, 1, False),   # ragged tiles in both directions
+    (37, 1283, 128, 64, 3.0, 1, False),    # fewer rows than a tile, N odd
+    (5, 7, 64, 4, 2.0, 1, False),
+    (1, 1, 64, 4, 2.0, 1, False),
+    (64, 4096, 64, 64, 2.0, 2, False),     # Int8
+    (520, 2048, 256, 256, 4.0, 1, True),   # 4 bits: few quads pass
+    (96, 4096, 128, 512, 3.0, 2, True),
+])
+def test_v2_containers_identical_to_oracle(M, N, TR, TC, bits, fmt, outliers):
+    w = synth.weights(small_spec(M, N, seed=5 * M + N, outliers=outliers))
+    alpha, _ = oracle.alpha_search(w, bits, fmt)
+    a = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, threads=3, base_format=fmt)
+    b = oracle.container2_build(w, alpha, TR, TC, fmt=fmt)
+    assert a.size == b.size and (a == b).all()
+
+
+def test_v2_given_scales_identical_to_oracle():
+    w = synth.weights(small_spec(40, 512, seed=77))
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    scale = oracle.row_scales(w, alpha * 0.75)
+    a = eq.eqe_encode2(w, 0.0, tile_rows=64, tile_cols=128, scale_bf16=scale)
+    b = oracle.container2_build(w, 0.0, 64, 128, scale=scale)
+    assert (a == b).all() and oracle.container2_info(a).alpha == 0.0
+    with pytest.raises(eq.EqError):
+        eq.eqe_encode2(w, alpha, tile_rows=96, tile_cols=128)
+    with pytest.raises(eq.EqError):
+        eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=130)
+    with pytest.raises(eq.EqError):
+        eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=128, res_bits=13)

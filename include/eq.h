@@ -41,6 +41,25 @@
  * next word: x = (x << 16) | word.  After the last step every lane is at
  * 2^16 and the chunk's words are used up exactly.
  *
+ * Version 2 (written by eqe_encode2, eq_encode.h; header field 4 = 2) keeps
+ * the header and sections above with these differences:
+ *   36 prob_bits = R, the frequency resolution (10..12); 40 n_syms = the
+ *   size of the phrase alphabet; 84 tile_cols TC (a multiple of 4); 32 lanes
+ *   = tile rows TR; 24 chunk_syms = TR * TC; 144 n_quads, 148 n_pairs,
+ *   152 n_singles (their sum is n_syms); 156 the encoder's dictionary
+ *   threshold (informative).
+ *   Chunk c is the tile of rows [b TR, b TR + TR) and columns [t TC, t TC +
+ *   TC) (cut at the matrix edge), b = c div NT, t = c mod NT, NT =
+ *   ceil(N / TC); state s of the chunk codes row b TR + s of the tile.
+ *   sym section: u8[n_syms][4], symbol k's codes in position order (quads
+ *   first, then pairs, then single codes; unused bytes 0); freq: u16 f_k >= 1
+ *   summing to 2^R.  A step decodes, for every state whose row segment is not
+ *   yet complete, slot = x mod 2^16, the symbol k with 2^(16-R) cum_k <= slot
+ *   < 2^(16-R) (cum_k + f_k), x = F_k (x >> 16) + slot - 2^(16-R) cum_k with
+ *   F_k = 2^(16-R) f_k, and appends its 4, 2 or 1 codes to the segment; then
+ *   those states in ascending order take the next word when x < 2^16.
+ *   Decoding a version-2 layer to codes or BF16 needs 2 * TR * N < 2^31.
+ *
  * Conventions for every entry point below:
  *  - Device pointers are allocated and owned by the caller; the library never
  *    allocates, frees or synchronises (except eq_get_status, which waits on
@@ -88,9 +107,13 @@ typedef struct eq_layer {
   const uint16_t *words;
   uint32_t *lut;             /* device scratch, eq_lut_bytes() bytes, caller-owned */
   int32_t *status;           /* device int32, caller-owned                         */
+  uint32_t version;          /* container version, 1 or 2                          */
+  uint32_t tile_cols;        /* version 2: tile columns TC (tile rows = lanes)     */
+  uint32_t n_quads, n_pairs, n_singles; /* version 2: alphabet parts (sum n_syms) */
 } eq_layer;
 
-/* Bytes of device scratch the decode tables of a layer need. */
+/* Bytes of device scratch the decode tables of a layer need (either
+ * container version). */
 size_t eq_lut_bytes(void);
 
 /* Validate the container `host_blob` (blob_bytes long, host memory) and fill

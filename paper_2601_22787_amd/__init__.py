@@ -35,7 +35,10 @@ class eq_layer(ctypes.Structure):
                 ("n_syms", ctypes.c_uint32), ("base_format", ctypes.c_uint32),
                 ("total_words", ctypes.c_uint64), ("padded_words", ctypes.c_uint64),
                 ("scale", _vp), ("sym", _vp), ("freq", _vp), ("chunk_off", _vp),
-                ("chunk_state", _vp), ("words", _vp), ("lut", _vp), ("status", _vp)]
+                ("chunk_state", _vp), ("words", _vp), ("lut", _vp), ("status", _vp),
+                ("version", ctypes.c_uint32), ("tile_cols", ctypes.c_uint32),
+                ("n_quads", ctypes.c_uint32), ("n_pairs", ctypes.c_uint32),
+                ("n_singles", ctypes.c_uint32)]
 
 
 class eqe_params(ctypes.Structure):

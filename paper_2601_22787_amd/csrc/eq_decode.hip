@@ -13,19 +13,20 @@
 #include <type_traits>
 
 #include "eq.h"
+#include "eq_device.h"
 #include "eq_internal.h"
+#include "eq_v2.h"
 
 namespace {
 
 using namespace eq_detail;
+using namespace eq_dev;
 
-constexpr int kWave = 64;
 constexpr int kMaxWaves = 16;                 // wavefronts per block (one chunk each at a time)
 constexpr int kMaxBlock = kWave * kMaxWaves;
 constexpr int kMaxBatch = 8;
 constexpr uint32_t kHalf = 512;               // stream words per window half (1 KiB)
 constexpr uint32_t kWin = 2 * kHalf;          // per-wave LDS window of stream words
-constexpr int32_t kBufferFlags = 0x00020000;  // buffer resource word 3 (gfx9 family)
 constexpr uint32_t kMaxXLdsBytes = 64 * 1024; // activations staged whole up to this size
 constexpr uint32_t kTileBytes = 48 * 1024;    // one activation tile at most (two are in LDS)
 constexpr uint32_t kMinTileBytes = 32 * 1024; // tiles at least this large, or no tiling
@@ -63,36 +64,6 @@ struct Args {
   uint32_t tile_steps;          // steps per activation tile (tiled GEMV)
 };
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float float2v __attribute__((ext_vector_type(2)));
-typedef short short4v __attribute__((ext_vector_type(4)));
-typedef float float4v __attribute__((ext_vector_type(4)));
-
-__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
-
-// Two fp32 values to two nearest-even BF16 (low half: a).
-__device__ inline uint32_t pack_bf16(float a, float b) {
-  const float2v v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
-
-// acc + lo16(a) * lo16(b) + hi16(a) * hi16(b), operands as BF16 pairs.
-__device__ inline float dot2_bf16(uint32_t a, uint32_t b, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
-                                        __builtin_bit_cast(bf16x2, b), acc, false);
-}
-
-// E4M3FN value of a code: sign | exponent (bias 7) | 3-bit mantissa;
-// exponent 0 is subnormal (m * 2^-9).
-__device__ inline float e4m3_value(uint32_t c) {
-  const uint32_t e = (c >> 3) & 15u, m = c & 7u;
-  float mag;
-  if (e == 0) mag = static_cast<float>(m) * 0.001953125f;  // 2^-9, exact
-  else mag = __uint_as_float(((e + 120u) << 23) | (m << 20));
-  if ((c & 0x7Fu) == 0x7Fu) mag = __uint_as_float(0x7FC00000u);
-  return (c & 0x80u) ? -mag : mag;
-}
-
 // One v_mfma_f32_4x4x4_16b_bf16: 16 blocks of 4 lanes, C[i][j] += sum_k
 // A[i][k] B[k][j], where lane 4 blk + i holds row i of A (four BF16 in two
 // registers, low half first) and lane 4 blk + j holds column j of B and
@@ -113,92 +84,11 @@ __device__ inline float mfma_diag(float4v c, uint32_t lane) {
   return j == 0 ? c.x : j == 1 ? c.y : j == 2 ? c.z : c.w;
 }
 
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-__device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
-
-// Wave issue priority 3 - q (q = 0..3, wave-uniform).
-__device__ inline void set_prio_down(uint32_t q) {
-  switch (q) {
-    case 0: __builtin_amdgcn_s_setprio(3); break;
-    case 1: __builtin_amdgcn_s_setprio(2); break;
-    case 2: __builtin_amdgcn_s_setprio(1); break;
-    default: __builtin_amdgcn_s_setprio(0); break;
-  }
-}
-
-// LDS pointers as 32-bit byte addresses, so that wave-uniform positions can
-// live in scalar registers and be advanced by scalar arithmetic.
-typedef __attribute__((address_space(3))) const uint16_t lds_u16;
-__device__ inline uint32_t lds_addr(const void *p) {
-  return static_cast<uint32_t>(
-      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
-}
-__device__ inline uint32_t lds_read_u16(uint32_t addr) { return *(lds_u16 *)(addr); }
-__device__ inline void lds_write_u16(uint32_t addr, uint32_t v) {
-  *(__attribute__((address_space(3))) uint16_t *)(addr) = static_cast<uint16_t>(v);
-}
-
 // Byte address of the row-table entry of the code in bits 24..31 of a slot
 // entry e (bits 13..23 of e are zero, so e >> 23 is twice the code); tab is
 // the table's address over 512.
 __device__ inline uint32_t rowtab_addr(uint32_t tab, uint32_t e) {
   return __builtin_amdgcn_alignbit(tab, e, 23);
-}
-
-// a + 2 * b on the scalar unit in one instruction (both wave-uniform).  The
-// instruction writes SCC, which the compiler must not keep live across it.
-__device__ inline uint32_t add_twice(uint32_t a, uint32_t b) {
-  uint32_t r;
-  asm("s_lshl1_add_u32 %0, %1, %2" : "=s"(r) : "s"(b), "s"(a) : "scc");
-  return r;
-}
-
-// Per-lane select by a wave mask (bit l of m picks b for lane l), as one
-// v_cndmask.  Written out so that the compiler keeps it branch-free and does
-// not sink the loads feeding b into a branch.
-__device__ inline uint32_t select_by_mask(uint64_t m, uint32_t a, uint32_t b) {
-  uint32_t r;
-  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "s"(m));
-  return r;
-}
-
-// Renormalisation of the lanes whose bit is set in m: x = (x << 16) | w on
-// those lanes (x < 2^16 there; only the low 16 bits of w are used), x
-// unchanged on the others.  One v_perm_b32 under exec = exec & m instead of a
-// shift-or and a select: the two scalar instructions that narrow and restore
-// exec issue beside other waves' vector work.  They write SCC.
-__device__ inline uint32_t renorm_lanes(uint64_t m, uint32_t x, uint32_t w) {
-  uint64_t saved;
-  // result bytes 3..0 = x byte 1, x byte 0, w byte 1, w byte 0
-  asm("s_and_saveexec_b64 %1, %2\n\t"
-      "v_perm_b32 %0, %0, %3, %4\n\t"
-      "s_mov_b64 exec, %1"
-      : "+v"(x), "=&s"(saved)
-      : "s"(m), "v"(w), "s"(0x05040100u)
-      : "scc");
-  return x;
-}
-
-// Read-only inputs seen through the constant address space, so that loads
-// at wave-uniform addresses become scalar (SMEM) loads and never wait on the
-// vector memory counter.
-typedef const __attribute__((address_space(4))) uint32_t const_u32;
-
-__device__ inline const_u32 *as_const(const void *p) { return (const_u32 *)(p); }
-
-// BF16 element i of a read-only array (i wave-uniform), via the aligned dword
-// that holds it.  The array needs only 2-byte alignment (a bias may be a view
-// at an odd element): scalar loads ignore the low two address bits, so the
-// dword is addressed explicitly and the half picked by bit 1 of the address.
-__device__ inline float bf16_at(const uint16_t *base, uint32_t i) {
-  const uintptr_t at = reinterpret_cast<uintptr_t>(base) + 2 * uintptr_t(i);
-  const uint32_t w = *as_const(reinterpret_cast<const void *>(at & ~uintptr_t(3)));
-  return __uint_as_float((at & 2) ? (w & 0xFFFF0000u) : (w << 16));
 }
 
 // Two E4M3FN codes (bytes 0 and 1 of c) to the BF16 pair of their values
@@ -230,12 +120,6 @@ __device__ inline float code_f32(uint32_t e) {
 // of the entry are zero (f <= 2^12), so e >> 22 is already the byte offset.
 __device__ inline uint32_t code_value(const uint32_t *val_s, uint32_t e) {
   return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(val_s) + (e >> 22));
-}
-
-// 16 stream words starting at word index i (a multiple of 8), clamped to the
-// padded section so that a read ahead never leaves the container.
-__device__ inline uint4 load_words(const uint16_t *words, uint32_t i, uint32_t last8) {
-  return *reinterpret_cast<const uint4 *>(words + min(i, last8));
 }
 
 // Decode tables.  Slot s of symbol k (cum_k <= s < cum_k + f_k):
@@ -1280,7 +1164,7 @@ Args make_args(const eq_layer *L) {
 }
 
 bool layer_ok(const eq_layer *L) {
-  return L && L->lut && L->status && L->words && L->chunk_off && L->chunk_state && L->scale &&
+  return L && L->version == 1 && L->lut && L->status && L->words && L->chunk_off && L->chunk_state && L->scale &&
          (L->lanes == 64 || L->lanes == 128 || L->lanes == 256) &&
          L->prob_bits >= kMinProbBits && L->prob_bits <= 12 && L->n_chunks > 0 && L->cols > 0 &&
          L->rows > 0 && (L->base_format == kFmtE4M3 || L->base_format == kFmtInt8);
@@ -1568,6 +1452,7 @@ bool joint_ok(const eq_layer *const *L, uint32_t n) {
 }  // namespace
 
 extern "C" int eq_layer_prepare(const eq_layer *L, hipStream_t stream) {
+  if (L && L->version == 2) return v2_prepare(L, stream);
   if (!layer_ok(L) || !L->sym || !L->freq || L->n_syms < 1 || L->n_syms > 256) return EQ_EINVAL;
   hipLaunchKernelGGL(prepare_kernel, dim3(1), dim3(1024), 0, stream, L->sym, L->freq, L->n_syms,
                      1u << L->prob_bits, L->base_format, L->lut, L->status);
@@ -1575,6 +1460,7 @@ extern "C" int eq_layer_prepare(const eq_layer *L, hipStream_t stream) {
 }
 
 extern "C" int eq_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t stream) {
+  if (L && L->version == 2) return v2_decode_codes(L, codes, stream);
   if (!layer_ok(L) || !codes) return EQ_EINVAL;
   Args a = make_args(L);
   a.codes = codes;
@@ -1582,6 +1468,7 @@ extern "C" int eq_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t st
 }
 
 extern "C" int eq_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t stream) {
+  if (L && L->version == 2) return v2_decode_bf16(L, w, stream);
   if (!layer_ok(L) || !w) return EQ_EINVAL;
   Args a = make_args(L);
   a.wout = w;
@@ -1592,6 +1479,7 @@ extern "C" int eq_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t stream
 // column-paired activations; for rows that are not whole steps, the decoded
 // codes (one byte per weight).
 extern "C" size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
+  if (L && L->version == 2) return v2_gemv_workspace_bytes(L, B);
   if (!layer_ok(L) || B < 1 || B > kMaxBatch) return 0;
   if (L->cols % L->lanes != 0) return round256(size_t(L->rows) * L->cols);
   return round256(size_t(2) * L->n_chunks * B * sizeof(float)) +
@@ -1601,6 +1489,12 @@ extern "C" size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
 extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
                               const uint16_t *bias, float *y, void *ws, size_t ws_bytes,
                               hipStream_t stream) {
+  if (L && L->version == 2) {
+    if (uint64_t(B) * L->cols >= (uint64_t(1) << 32) ||
+        uint64_t(B) * L->rows >= (uint64_t(1) << 32))
+      return EQ_EINVAL;
+    return v2_decode_gemv(L, x, B, bias, y, ws, ws_bytes, stream);
+  }
   if (!layer_ok(L) || !x || !y || !ws || B < 1 || B > kMaxBatch) return EQ_EINVAL;
   if (ws_bytes < eq_gemv_workspace_bytes(L, B)) return EQ_EINVAL;
   if (uint64_t(B) * L->cols >= (uint64_t(1) << 32) || uint64_t(B) * L->rows >= (uint64_t(1) << 32))
@@ -1648,9 +1542,13 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
 extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
                                     hipStream_t stream) {
   if (!L || !w || n < 1 || n > kMaxLayers) return EQ_EINVAL;
-  for (uint32_t i = 0; i < n; ++i)
-    if (!layer_ok(L[i]) || !w[i]) return EQ_EINVAL;
-  if (n == 1 || !joint_ok(L, n)) {
+  bool v2 = false;
+  for (uint32_t i = 0; i < n; ++i) {
+    if (!L[i] || !w[i]) return EQ_EINVAL;
+    v2 |= L[i]->version == 2;
+    if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
+  }
+  if (n == 1 || v2 || !joint_ok(L, n)) {
     for (uint32_t i = 0; i < n; ++i) {
       const int rc = eq_decode_bf16(L[i], w[i], stream);
       if (rc != EQ_OK) return rc;
@@ -1682,8 +1580,12 @@ extern "C" int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const 
                                     void *ws, size_t ws_bytes, hipStream_t stream) {
   if (!L || !y || !x || !ws || n < 1 || n > kMaxLayers || B < 1 || B > kMaxBatch)
     return EQ_EINVAL;
-  for (uint32_t i = 0; i < n; ++i)
-    if (!layer_ok(L[i]) || !y[i] || L[i]->cols != L[0]->cols) return EQ_EINVAL;
+  bool v2 = false;
+  for (uint32_t i = 0; i < n; ++i) {
+    if (!L[i] || !y[i] || L[i]->cols != L[0]->cols) return EQ_EINVAL;
+    v2 |= L[i]->version == 2;
+    if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
+  }
   if (ws_bytes < eq_gemv_multi_workspace_bytes(L, n, B)) return EQ_EINVAL;
   // layer i's workspace follows those of layers 0 .. i-1
   size_t off[kMaxLayers];
@@ -1705,7 +1607,7 @@ extern "C" int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const 
   MultiArgs shaped;
   const uint32_t waves = multi_shape(m, f.cus, kMaxWaves, shaped);
   const size_t xbytes = xlds_bytes(m.a[0]);
-  const bool joint = n > 1 && joint_ok(L, n) && xbytes <= kMaxXLdsBytes &&
+  const bool joint = n > 1 && !v2 && joint_ok(L, n) && xbytes <= kMaxXLdsBytes &&
                      kStaticLds + dyn_lds_bytes(waves, xbytes, false) <= size_t(f.lds_per_block);
   if (!joint) {
     for (uint32_t i = 0; i < n; ++i) {

@@ -1,0 +1,537 @@
+// gfx950 kernels for version-2 containers (eq.h): tile-ordered chunks and a
+// phrase alphabet, rANS at 2^16.
+//
+// Alg. 2 of the paper with the coder of container version 2: one wavefront
+// decodes one chunk (a tile of TR rows x TC columns); lane l holds the coder
+// states of tile rows l, l + 64, ... (TR / 64 of them).  Every state walks its
+// row's TC columns, one phrase of 4, 2 or 1 codes per step, so one state
+// update yields 3-4 codes on the synthetic 2-bit layers.  The phrase table
+// (kBuckets entries of 16 bytes, indexed by the top 12 bits of the slot) sits
+// in LDS; an entry holds what the state update needs and the phrase's values:
+//   .x = (2^16 - F) | (2 * length) << 16      .y = 2^(16-R) * cum
+//   .z, .w = the four codes' values as BF16 pairs (zero past the length)
+// so that  x' = F (x >> 16) + (x mod 2^16) - cum  =  x - ((2^16 - F) (x >> 16) + cum)
+// is one 16 x 16-bit multiply-add (high half of x selected by op_sel) and one
+// subtraction.  Stream words are handed out with a wavefront ballot and a
+// masked bit count in ascending state order, as the coder reads them.
+//
+// GEMV: all states of a chunk walk the same TC columns, so the chunk's
+// activations (TC values per batch row) sit in the wavefront's LDS; a
+// phrase's four values meet the four activations at its column with one
+// (unaligned) 8-byte LDS read and two dot2 products per batch row.  A state's
+// sum is its row's partial over the tile; partials of the NT column tiles are
+// added in tile order by merge2_kernel (deterministic).
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+
+#include "eq.h"
+#include "eq_device.h"
+#include "eq_internal.h"
+#include "eq_v2.h"
+
+namespace {
+
+using namespace eq_detail;
+using namespace eq_dev;
+
+constexpr int kMaxWaves2 = 16;
+constexpr int kMaxBlock2 = kWave * kMaxWaves2;
+constexpr int kMaxBatch2 = 8;
+constexpr uint32_t kHalf2 = 512;           // stream words per window half
+constexpr uint32_t kWin2 = 2 * kHalf2;     // per-wave LDS window (2 KiB)
+constexpr uint32_t kXPad = 8;              // zero activations after a tile row
+
+enum Mode2 { kCodes2 = 0, kBf16_2 = 1, kGemv2 = 2 };
+
+struct Args2 {
+  const uint4 *lut;          // kBuckets phrase entries (see the file comment)
+  const uint32_t *codes4;    // kBuckets phrase codes, little-endian
+  const uint16_t *scale;
+  const uint32_t *chunk_off;
+  const uint32_t *chunk_state;
+  const uint16_t *words;
+  int32_t *status;
+  uint32_t rows, cols, TR, TC, NT, n_chunks, padded_words;
+  uint32_t wave_lds;         // bytes of dynamic LDS per wavefront after the table
+  uint32_t xrow;             // elements per activation row in LDS (TC + kXPad, rounded)
+  uint8_t *codes;
+  uint16_t *wout;
+  const uint16_t *x;
+  uint32_t batch;
+  const uint16_t *bias;
+  float *y;
+  float *ws;                 // partial row sums [batch][NT][rows] (NT > 1)
+};
+
+// x' = x - ((2^16 - F) * (x >> 16) + cum): the 16-bit multiply takes the low
+// half of e.x and the high half of x.
+__device__ inline uint32_t state_update(uint32_t x, uint32_t ex, uint32_t ey) {
+  uint32_t t;
+  asm("v_mad_u32_u16 %0, %1, %2, %3 op_sel:[0,1,0,0]" : "=v"(t) : "v"(ex), "v"(x), "v"(ey));
+  return x - t;
+}
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Phrase entry of state x (the table sits at LDS address 0: x & 0xFFF0 is the
+// byte offset of bucket (x mod 2^16) >> 4).
+__device__ inline u32x4 entry_of(uint32_t x) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(x & 0xFFF0u);
+}
+
+// 8 bytes of LDS at any 2-byte aligned address (the hardware splits
+// unaligned accesses; checked on gfx950).
+__device__ inline u32x2 lds_read_u64(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x2 *>(addr);
+}
+
+template <int G, int MODE, int NB>
+struct Tile {
+  static constexpr uint32_t TR = G * kWave;
+  const Args2 &a;
+  uint32_t lane, c, r0, c0, rows, cols, tcol;
+  int nb;
+  uint32_t x[G];
+  bool valid[G];
+  uint32_t pos[G];   // GEMV: LDS byte address of the state's column in batch row 0;
+                     // otherwise its column within the tile row
+  uint32_t end;      // pos at the end of a row segment
+  uint32_t obase[G]; // codes / BF16: the state's row offset (elements) from the tile origin
+  float srow[G];     // BF16: the state's row scale
+  float acc[G][NB ? NB : kMaxBatch2];
+  // stream
+  uint32_t p_end, wb, wa, ra, last8;
+  uint4 next;
+  uint4 *win4;
+  __amdgpu_buffer_rsrc_t out_rsrc;
+
+  __device__ __forceinline__ Tile(const Args2 &a_, uint32_t c_, uint32_t lane_, char *wave_lds)
+      : a(a_), lane(lane_), c(c_) {
+    const uint32_t b = c / a.NT;
+    tcol = c - b * a.NT;
+    r0 = b * TR;
+    c0 = tcol * a.TC;
+    rows = min(TR, a.rows - r0);
+    cols = min(a.TC, a.cols - c0);
+    nb = NB ? NB : int(a.batch);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint32_t s = g * kWave + lane;
+      valid[g] = s < rows;
+      x[g] = a.chunk_state[size_t(c) * TR + s];
+    }
+    const uint32_t p = as_const(a.chunk_off)[c];
+    p_end = as_const(a.chunk_off)[c + 1];
+    last8 = min(a.padded_words - 8, p_end & ~7u);
+    win4 = reinterpret_cast<uint4 *>(wave_lds);
+    wb = p & ~7u;
+    wa = uniform(lds_addr(win4));
+    ra = wa + 2 * (p - wb);
+    win4[lane] = load_words(a.words, wb + 8 * lane, last8);
+    win4[kHalf2 / 8 + lane] = load_words(a.words, wb + kHalf2 + 8 * lane, last8);
+    if (MODE == kGemv2) {
+      // the tile's activations, kXPad zeros after each row
+      uint16_t *xt = reinterpret_cast<uint16_t *>(wave_lds + kWin2 * 2);
+      for (int bb = 0; bb < nb; ++bb)
+        for (uint32_t j = lane; j < cols + kXPad; j += kWave)
+          xt[bb * a.xrow + j] = j < cols ? a.x[size_t(bb) * a.cols + c0 + j] : uint16_t(0);
+      const uint32_t x0 = uniform(lds_addr(xt));
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        pos[g] = x0;
+#pragma unroll
+        for (int bb = 0; bb < (NB ? NB : kMaxBatch2); ++bb) acc[g][bb] = 0.0f;
+      }
+      end = x0 + 2 * cols;
+    } else {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        pos[g] = 0;
+        obase[g] = (g * kWave + lane) * a.cols;
+        if (MODE == kBf16_2) srow[g] = valid[g] ? bf16_at(a.scale, r0 + g * kWave + lane) : 0.0f;
+      }
+      end = cols;
+      const uint32_t span = (rows - 1) * a.cols + cols;  // elements from the tile origin
+      if (MODE == kCodes2)
+        out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + size_t(r0) * a.cols + c0, 0,
+                                                     int(span), kBufferFlags);
+      else
+        out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.wout + size_t(r0) * a.cols + c0, 0,
+                                                     int(2 * span), kBufferFlags);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    next = load_words(a.words, wb + kWin2 + 8 * lane, last8);
+  }
+
+  __device__ __forceinline__ void slide() {
+    if (ra - wa >= 2 * kHalf2) {
+      const uint4 keep = win4[kHalf2 / 8 + lane];
+      win4[lane] = keep;
+      win4[kHalf2 / 8 + lane] = next;
+      wb += kHalf2;
+      ra -= 2 * kHalf2;
+      next = load_words(a.words, wb + kWin2 + 8 * lane, last8);
+    }
+  }
+
+  // Use state g's phrase e: WIDE stores the whole phrase slot (four codes,
+  // valid while the slot lies inside the row segment; later phrases of the
+  // same state overwrite what lies past this one), else exactly its length.
+  static constexpr int NX = MODE == kGemv2 ? (NB ? NB : kMaxBatch2) : 1;
+
+  // The activations at state g's column, four per batch row (GEMV).
+  __device__ __forceinline__ void read_x(int g, u32x2 (&xv)[NX]) {
+#pragma unroll
+    for (int bb = 0; bb < NX; ++bb)
+      if (bb < nb) xv[bb] = lds_read_u64(pos[g] + 2 * bb * a.xrow);
+  }
+
+  template <bool WIDE>
+  __device__ __forceinline__ void use(int g, u32x4 e, const u32x2 (&xv)[NX]) {
+    if (MODE == kGemv2) {
+#pragma unroll
+      for (int bb = 0; bb < NX; ++bb)
+        if (bb < nb) acc[g][bb] = dot2_bf16(e.w, xv[bb].y, dot2_bf16(e.z, xv[bb].x, acc[g][bb]));
+      pos[g] += e.x >> 16;
+    } else if (MODE == kBf16_2) {
+      const float s = srow[g];
+      const uint32_t lo = pack_bf16(s * __uint_as_float(e.z << 16),
+                                    s * __uint_as_float(e.z & 0xFFFF0000u));
+      const uint32_t hi = pack_bf16(s * __uint_as_float(e.w << 16),
+                                    s * __uint_as_float(e.w & 0xFFFF0000u));
+      const uint32_t off = 2 * (obase[g] + pos[g]);
+      const uint32_t len2 = e.x >> 16;  // bytes of the phrase's BF16 values / 2
+      if (WIDE) {
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, out_rsrc, off, 0, 0);
+      } else if (len2 == 8) {
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, out_rsrc, off, 0, 0);
+      } else if (len2 == 4) {
+        __builtin_amdgcn_raw_buffer_store_b32(lo, out_rsrc, off, 0, 0);
+      } else {
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(lo), out_rsrc, off, 0, 0);
+      }
+      pos[g] += len2 >> 1;
+    } else {
+      const uint32_t off = obase[g] + pos[g];
+      const uint32_t len2 = e.x >> 16;
+      if (WIDE || len2 == 8) {
+        __builtin_amdgcn_raw_buffer_store_b32(e.z, out_rsrc, off, 0, 0);
+      } else if (len2 == 4) {
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(e.z), out_rsrc, off, 0, 0);
+      } else {
+        __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(e.z), out_rsrc, off, 0, 0);
+      }
+      pos[g] += len2 >> 1;
+    }
+  }
+
+  // One step.  MASKED: only states whose segment is not complete take part
+  // (else every state does, with wide stores).
+  template <bool MASKED>
+  __device__ __forceinline__ void step(const bool (&act)[G]) {
+    slide();
+    u32x4 e[G];
+    u32x2 xv[G][NX];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (!MASKED || act[g]) e[g] = entry_of(x[g]);
+    if (MODE == kGemv2) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (!MASKED || act[g]) read_x(g, xv[g]);
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (!MASKED || act[g]) x[g] = state_update(x[g], e[g].x, e[g].y);
+    // renormalise in ascending state order (state g * 64 + lane)
+    uint64_t need[G];
+    uint32_t word[G];
+    uint32_t r = ra;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      need[g] = __builtin_amdgcn_ballot_w64((!MASKED || act[g]) && x[g] < 0x10000u);
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+          uint32_t(need[g] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(need[g]), 0u));
+      word[g] = lds_read_u16(r + 2 * below);
+      r = add_twice(r, static_cast<uint32_t>(__popcll(need[g])));
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (!MASKED || act[g]) use<!MASKED>(g, e[g], xv[g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g) x[g] = renorm_lanes(need[g], x[g], word[g]);
+    ra = r;
+  }
+
+  __device__ __forceinline__ void run() {
+    const bool all[G] = {};
+    bool full = rows == TR;
+    // Every state needs at least cols / 4 phrases; while each phrase slot lies
+    // inside the segment, stores may be wide.
+    const uint32_t t1 = full ? cols / 4 : 0;
+    for (uint32_t t = 0; t < t1; ++t) step<false>(all);
+    // every phrase holds at least one code: at most cols steps in all (the
+    // bound also ends the loop on a damaged table)
+    for (uint32_t t = t1; t < cols; ++t) {
+      bool act[G];
+      bool any = false;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        act[g] = valid[g] && pos[g] < end;
+        any |= act[g];
+      }
+      if (__builtin_amdgcn_ballot_w64(any) == 0) break;
+      step<true>(act);
+    }
+    finish();
+  }
+
+  __device__ __forceinline__ void finish() {
+    if (MODE == kGemv2) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        if (!valid[g]) continue;
+        const uint32_t row = r0 + g * kWave + lane;
+#pragma unroll
+        for (int bb = 0; bb < (NB ? NB : kMaxBatch2); ++bb) {
+          if (bb >= nb) continue;
+          if (a.NT == 1) {
+            const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
+            a.y[size_t(bb) * a.rows + row] = bf16_to_f32(a.scale[row]) * acc[g][bb] + bias;
+          } else {
+            a.ws[(size_t(bb) * a.NT + tcol) * a.rows + row] = acc[g][bb];
+          }
+        }
+      }
+    }
+    bool bad = wb + (ra - wa) / 2 != p_end;
+#pragma unroll
+    for (int g = 0; g < G; ++g) bad |= x[g] != 0x10000u || (valid[g] && pos[g] != end);
+    if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
+  }
+};
+
+template <int G, int MODE, int NB>
+__global__ __launch_bounds__(kMaxBlock2) void decode2_kernel(Args2 a) {
+  extern __shared__ uint4 dyn2[];
+  // the phrase table at LDS address 0 (no static LDS in this kernel)
+  for (uint32_t i = threadIdx.x; i < kBuckets; i += blockDim.x) {
+    uint4 e = a.lut[i];
+    if (MODE == kCodes2) e.z = a.codes4[i];
+    dyn2[i] = e;
+  }
+  __syncthreads();
+  const uint32_t nw = blockDim.x / kWave, wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  char *mine = reinterpret_cast<char *>(dyn2 + kBuckets) + size_t(wave) * a.wave_lds;
+  for (uint32_t c = uniform(blockIdx.x * nw + wave); c < a.n_chunks; c += gridDim.x * nw) {
+    Tile<G, MODE, NB> t(a, c, lane, mine);
+    t.run();
+  }
+}
+
+// Rows split over NT > 1 column tiles: y = s * (partials added in tile order)
+// + bias.
+__global__ void merge2_kernel(Args2 a) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.rows * a.batch) return;
+  const uint32_t bb = i / a.rows, row = i - bb * a.rows;
+  const float *p = a.ws + size_t(bb) * a.NT * a.rows + row;
+  float sum = 0.0f;
+  for (uint32_t t = 0; t < a.NT; ++t) sum += p[size_t(t) * a.rows];
+  const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
+  a.y[i] = bf16_to_f32(a.scale[row]) * sum + bias;
+}
+
+// Phrase table of a layer: bucket b (of kBuckets) belongs to symbol k when
+// 2^(12-R) cum_k <= b < 2^(12-R) (cum_k + f_k).
+__global__ __launch_bounds__(1024) void prepare2_kernel(const uint32_t *phr, const uint16_t *freq,
+                                                        uint32_t K, uint32_t nq, uint32_t np,
+                                                        uint32_t R, uint32_t fmt, uint4 *lut,
+                                                        uint32_t *codes4, int32_t *status) {
+  __shared__ uint32_t cum_s[kBuckets + 1];
+  const uint32_t t = threadIdx.x;
+  if (t == 0) {
+    uint32_t c = 0;
+    for (uint32_t k = 0; k < K; ++k) {
+      cum_s[k] = c;
+      c += freq[k];
+    }
+    cum_s[K] = c;
+  }
+  __syncthreads();
+  const uint32_t sh = 12 - R;
+  for (uint32_t bkt = t; bkt < kBuckets; bkt += blockDim.x) {
+    const uint32_t slot = bkt >> sh;  // in units of 2^-R
+    uint32_t lo = 0, hi = K - 1;      // largest k with cum_k <= slot
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) / 2;
+      if (cum_s[mid] <= slot) lo = mid;
+      else hi = mid - 1;
+    }
+    const uint32_t k = lo;
+    const uint32_t F = uint32_t(freq[k]) << (16 - R);
+    const uint32_t len = k < nq ? 4 : (k < nq + np ? 2 : 1);
+    const uint32_t codes = phr[k];
+    uint32_t v[4];
+    for (uint32_t j = 0; j < 4; ++j) {
+      const uint32_t code = (codes >> (8 * j)) & 0xFF;
+      const float val = fmt == kFmtInt8 ? static_cast<float>(static_cast<int8_t>(code))
+                                        : e4m3_value(code);
+      v[j] = j < len ? (__float_as_uint(val) >> 16) : 0u;  // exact in BF16
+    }
+    lut[bkt] = make_uint4((65536u - F) | ((2 * len) << 16), cum_s[k] << (16 - R),
+                          v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+    codes4[bkt] = codes;
+  }
+  if (t == 0) *status = 0;
+}
+
+Args2 make_args2(const eq_layer *L) {
+  Args2 a{};
+  a.lut = reinterpret_cast<const uint4 *>(L->lut);
+  a.codes4 = L->lut + 4 * kBuckets;
+  a.scale = L->scale;
+  a.chunk_off = L->chunk_off;
+  a.chunk_state = L->chunk_state;
+  a.words = L->words;
+  a.status = L->status;
+  a.rows = L->rows;
+  a.cols = L->cols;
+  a.TR = L->lanes;
+  a.TC = L->tile_cols;
+  a.NT = (L->cols + L->tile_cols - 1) / L->tile_cols;
+  a.n_chunks = L->n_chunks;
+  a.padded_words = static_cast<uint32_t>(L->padded_words);
+  return a;
+}
+
+struct Facts2 {
+  int lds = 160 * 1024;
+  int cus = 256;
+};
+
+Facts2 facts2() {
+  static std::atomic<int> lds[64], cus[64];
+  int dev = 0;
+  Facts2 f;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return f;
+  int l = lds[dev].load(std::memory_order_relaxed), c = cus[dev].load(std::memory_order_relaxed);
+  if (l == 0) {
+    if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+        l <= 0)
+      l = f.lds;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c <= 0)
+      c = f.cus;
+    lds[dev].store(l, std::memory_order_relaxed);
+    cus[dev].store(c, std::memory_order_relaxed);
+  }
+  f.lds = l;
+  f.cus = c;
+  return f;
+}
+
+constexpr size_t kTableBytes = size_t(kBuckets) * sizeof(uint4);
+
+// LDS per wavefront: the stream window, then (GEMV) the tile's activations.
+uint32_t wave_lds_bytes(int mode, const Args2 &a) {
+  uint32_t b = kWin2 * 2;
+  if (mode == kGemv2) b += (a.batch * a.xrow * 2 + 15) / 16 * 16;
+  return b;
+}
+
+// One block per compute unit (the table takes most of LDS), as many
+// wavefronts as the chunks need for one round, at most what LDS holds.
+template <int MODE, int NB>
+int launch2(Args2 a, hipStream_t s) {
+  // output offsets from a tile's origin are 32-bit byte offsets
+  if (MODE != kGemv2 && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+  const Facts2 f = facts2();
+  a.xrow = (a.TC + kXPad + 3) / 4 * 4;
+  a.wave_lds = wave_lds_bytes(MODE, a);
+  uint32_t waves = (a.n_chunks + f.cus - 1) / f.cus;
+  waves = waves < 1 ? 1 : (waves > kMaxWaves2 ? kMaxWaves2 : waves);
+  while (waves > 1 && kTableBytes + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
+  if (kTableBytes + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
+  uint32_t blocks = (a.n_chunks + waves - 1) / waves;
+  if (blocks > uint32_t(f.cus) * 4) blocks = uint32_t(f.cus) * 4;
+  const size_t shm = kTableBytes + size_t(waves) * a.wave_lds;
+  const dim3 grid(blocks), block(waves * kWave);
+  switch (a.TR) {
+    case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB>), grid, block, shm, s, a); break;
+    case 128: hipLaunchKernelGGL((decode2_kernel<2, MODE, NB>), grid, block, shm, s, a); break;
+    default: hipLaunchKernelGGL((decode2_kernel<4, MODE, NB>), grid, block, shm, s, a); break;
+  }
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+size_t round256(size_t v) { return (v + 255) / 256 * 256; }
+
+}  // namespace
+
+namespace eq_detail {
+
+bool v2_layer_ok(const eq_layer *L) {
+  return L && L->version == 2 && L->lut && L->status && L->words && L->chunk_off &&
+         L->chunk_state && L->scale && L->sym && L->freq &&
+         (L->lanes == 64 || L->lanes == 128 || L->lanes == 256) && L->tile_cols > 0 &&
+         L->tile_cols % 4 == 0 && L->prob_bits >= 10 && L->prob_bits <= 12 && L->n_syms >= 1 &&
+         L->n_syms <= (1u << L->prob_bits) && L->rows > 0 && L->cols > 0 && L->n_chunks > 0 &&
+         (L->base_format == kFmtE4M3 || L->base_format == kFmtInt8);
+}
+
+int v2_prepare(const eq_layer *L, hipStream_t s) {
+  if (!v2_layer_ok(L)) return EQ_EINVAL;
+  hipLaunchKernelGGL(prepare2_kernel, dim3(1), dim3(1024), 0, s,
+                     reinterpret_cast<const uint32_t *>(L->sym), L->freq, L->n_syms, L->n_quads,
+                     L->n_pairs, L->prob_bits, L->base_format, reinterpret_cast<uint4 *>(L->lut),
+                     L->lut + 4 * kBuckets, L->status);
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+int v2_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t s) {
+  if (!v2_layer_ok(L) || !codes) return EQ_EINVAL;
+  Args2 a = make_args2(L);
+  a.codes = codes;
+  return launch2<kCodes2, 1>(a, s);
+}
+
+int v2_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t s) {
+  if (!v2_layer_ok(L) || !w) return EQ_EINVAL;
+  Args2 a = make_args2(L);
+  a.wout = w;
+  return launch2<kBf16_2, 1>(a, s);
+}
+
+// Workspace: the partial row sums of every column tile (none when a tile
+// holds whole rows).
+size_t v2_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
+  if (!v2_layer_ok(L) || B < 1 || B > kMaxBatch2) return 0;
+  const size_t NT = (L->cols + L->tile_cols - 1) / L->tile_cols;
+  return NT > 1 ? round256(size_t(B) * NT * L->rows * sizeof(float)) : 256;
+}
+
+int v2_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
+                   float *y, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (!v2_layer_ok(L) || !x || !y || B < 1 || B > kMaxBatch2) return EQ_EINVAL;
+  if (!ws || ws_bytes < v2_gemv_workspace_bytes(L, B)) return EQ_EINVAL;
+  Args2 a = make_args2(L);
+  a.x = x;
+  a.batch = B;
+  a.bias = bias;
+  a.y = y;
+  a.ws = static_cast<float *>(ws);
+  const int rc = B == 1 ? launch2<kGemv2, 1>(a, s)
+                        : (B == kMaxBatch2 ? launch2<kGemv2, kMaxBatch2>(a, s)
+                                           : launch2<kGemv2, 0>(a, s));
+  if (rc != EQ_OK) return rc;
+  if (a.NT > 1) {
+    const uint32_t n = L->rows * B;
+    hipLaunchKernelGGL(merge2_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
+  }
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+}  // namespace eq_detail

@@ -27,6 +27,89 @@ bool scale_ok(uint16_t s) {
   return e >= 127 - 117 && e <= 127 + 119;
 }
 
+// A code valid in the base format: E4M3FN never NaN, Int8 never -128.
+bool code_ok(uint32_t fmt, uint8_t c) {
+  return fmt == eq_detail::kFmtE4M3 ? (c & 0x7F) != 0x7F : c != 0x80;
+}
+
+// Version 2: tile-ordered chunks and the phrase alphabet (layout in eq.h).
+int init_v2(eq_layer *L, const uint8_t *b, uint64_t bytes, const uint8_t *d) {
+  const uint32_t fmt = rd<uint32_t>(b, 12);
+  const uint32_t M = rd<uint32_t>(b, 16), N = rd<uint32_t>(b, 20), C = rd<uint32_t>(b, 24);
+  const uint32_t n_chunks = rd<uint32_t>(b, 28), TR = rd<uint32_t>(b, 32);
+  const uint32_t R = rd<uint32_t>(b, 36), K = rd<uint32_t>(b, 40), TC = rd<uint32_t>(b, 84);
+  const uint32_t nq = rd<uint32_t>(b, 144), np = rd<uint32_t>(b, 148), ns = rd<uint32_t>(b, 152);
+  const uint64_t total = rd<uint64_t>(b, 48), padded = rd<uint64_t>(b, 56);
+  const uint64_t o_scale = rd<uint64_t>(b, 88), o_phr = rd<uint64_t>(b, 96);
+  const uint64_t o_freq = rd<uint64_t>(b, 104), o_off = rd<uint64_t>(b, 112);
+  const uint64_t o_state = rd<uint64_t>(b, 120), o_words = rd<uint64_t>(b, 128);
+  const uint64_t file_bytes = rd<uint64_t>(b, 136);
+  const uint64_t n = static_cast<uint64_t>(M) * N;
+  if (file_bytes > bytes || n == 0 || n >= (uint64_t(1) << 32)) return EQ_EFORMAT;
+  if ((TR != 64 && TR != 128 && TR != 256) || TC == 0 || TC % 4 ||
+      uint64_t(TR) * TC != C || R < 10 || R > 12)
+    return EQ_EFORMAT;
+  if (uint64_t(n_chunks) != uint64_t((M + TR - 1) / TR) * ((N + TC - 1) / TC)) return EQ_EFORMAT;
+  if (K < 1 || K > (1u << R) || uint64_t(nq) + np + ns != K || ns > 256) return EQ_EFORMAT;
+  if (padded < total + 1024 || padded % 128 != 0 || padded + C >= (uint64_t(1) << 32))
+    return EQ_EFORMAT;
+  if (!section_ok(o_scale, 2ull * M, file_bytes) || !section_ok(o_phr, 4ull * K, file_bytes) ||
+      !section_ok(o_freq, 2ull * K, file_bytes) ||
+      !section_ok(o_off, 4ull * (n_chunks + 1), file_bytes) ||
+      !section_ok(o_state, 4ull * n_chunks * TR, file_bytes) ||
+      !section_ok(o_words, 2 * padded, file_bytes))
+    return EQ_EFORMAT;
+  // phrases: valid codes, unused bytes zero, each part strictly ascending
+  uint32_t fsum = 0;
+  for (uint32_t k = 0; k < K; ++k) {
+    const uint32_t len = k < nq ? 4 : (k < nq + np ? 2 : 1);
+    const uint32_t v = rd<uint32_t>(b, o_phr + 4ull * k);
+    for (uint32_t e = 0; e < 4; ++e) {
+      const uint8_t c = static_cast<uint8_t>(v >> (8 * e));
+      if (e < len ? !code_ok(fmt, c) : c != 0) return EQ_EFORMAT;
+    }
+    const bool part_start = k == 0 || k == nq || k == nq + np;
+    if (!part_start && v <= rd<uint32_t>(b, o_phr + 4ull * (k - 1))) return EQ_EFORMAT;
+    const uint16_t f = rd<uint16_t>(b, o_freq + 2ull * k);
+    if (f == 0) return EQ_EFORMAT;
+    fsum += f;
+  }
+  if (fsum != (1u << R)) return EQ_EFORMAT;
+  uint32_t prev = 0;
+  for (uint32_t c = 0; c <= n_chunks; ++c) {
+    const uint32_t o = rd<uint32_t>(b, o_off + 4ull * c);
+    if ((c == 0 && o != 0) || o < prev) return EQ_EFORMAT;
+    prev = o;
+  }
+  if (prev != total) return EQ_EFORMAT;
+  for (uint64_t s = 0; s < static_cast<uint64_t>(n_chunks) * TR; ++s)
+    if (rd<uint32_t>(b, o_state + 4 * s) < (1u << 16)) return EQ_EFORMAT;
+  for (uint32_t i = 0; i < M; ++i)
+    if (!scale_ok(rd<uint16_t>(b, o_scale + 2ull * i))) return EQ_EFORMAT;
+  L->rows = M;
+  L->cols = N;
+  L->chunk_syms = C;
+  L->n_chunks = n_chunks;
+  L->lanes = TR;
+  L->prob_bits = R;
+  L->n_syms = K;
+  L->base_format = fmt;
+  L->total_words = total;
+  L->padded_words = padded;
+  L->scale = reinterpret_cast<const uint16_t *>(d + o_scale);
+  L->sym = d + o_phr;
+  L->freq = reinterpret_cast<const uint16_t *>(d + o_freq);
+  L->chunk_off = reinterpret_cast<const uint32_t *>(d + o_off);
+  L->chunk_state = reinterpret_cast<const uint32_t *>(d + o_state);
+  L->words = reinterpret_cast<const uint16_t *>(d + o_words);
+  L->version = 2;
+  L->tile_cols = TC;
+  L->n_quads = nq;
+  L->n_pairs = np;
+  L->n_singles = ns;
+  return EQ_OK;
+}
+
 }  // namespace
 
 extern "C" size_t eq_lut_bytes(void) { return eq_detail::kLutBytes; }
@@ -40,10 +123,20 @@ extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
     return EQ_EINVAL;
   const uint8_t *b = static_cast<const uint8_t *>(host_blob);
   if (bytes < 256 || std::memcmp(b, "EQC1", 4) != 0) return EQ_EFORMAT;
-  const uint32_t fmt = rd<uint32_t>(b, 12);
-  if (rd<uint32_t>(b, 4) != 1 || rd<uint32_t>(b, 8) != 256 ||
+  const uint32_t fmt = rd<uint32_t>(b, 12), version = rd<uint32_t>(b, 4);
+  if ((version != 1 && version != 2) || rd<uint32_t>(b, 8) != 256 ||
       (fmt != eq_detail::kFmtE4M3 && fmt != eq_detail::kFmtInt8))
     return EQ_EFORMAT;
+  if (version == 2) {
+    eq_layer v;
+    std::memset(&v, 0, sizeof v);
+    const int rc = init_v2(&v, b, bytes, static_cast<const uint8_t *>(dev_blob));
+    if (rc != EQ_OK) return rc;
+    v.lut = static_cast<uint32_t *>(dev_lut);
+    v.status = dev_status;
+    *L = v;
+    return EQ_OK;
+  }
   const uint32_t M = rd<uint32_t>(b, 16), N = rd<uint32_t>(b, 20), C = rd<uint32_t>(b, 24);
   const uint32_t n_chunks = rd<uint32_t>(b, 28), W = rd<uint32_t>(b, 32);
   const uint32_t P = rd<uint32_t>(b, 36), K = rd<uint32_t>(b, 40);
@@ -113,6 +206,7 @@ extern "C" int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t bytes,
   v.words = reinterpret_cast<const uint16_t *>(d + o_words);
   v.lut = static_cast<uint32_t *>(dev_lut);
   v.status = dev_status;
+  v.version = 1;
   *L = v;
   return EQ_OK;
 }

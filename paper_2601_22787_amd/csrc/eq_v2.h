@@ -1,0 +1,14 @@
+// Version-2 containers (tile-ordered chunks, phrase alphabet): the entry
+// points of eq.h hand a version-2 layer to these (eq_decode2.hip).
+#pragma once
+#include "eq.h"
+
+namespace eq_detail {
+int v2_prepare(const eq_layer *L, hipStream_t s);
+int v2_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t s);
+int v2_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t s);
+size_t v2_gemv_workspace_bytes(const eq_layer *L, uint32_t B);
+int v2_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
+                   float *y, void *ws, size_t ws_bytes, hipStream_t s);
+bool v2_layer_ok(const eq_layer *L);
+}  // namespace eq_detail

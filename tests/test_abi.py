@@ -187,3 +187,32 @@ def test_probability_precision_below_range_rejected():
     with pytest.raises(ValueError):
         oracle.container_info(bad)
     assert _init(bad)[0] == eq.EQ_EFORMAT
+
+
+def test_layer_init_version2():
+    """A version-2 container validates and reports its tile shape and
+    alphabet; damaged headers and sections are rejected on the host."""
+    w = synth.weights(small_spec(70, 1000, seed=23))
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    b2 = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=256)
+    info = oracle.container2_info(b2)
+    rc, L = _init(b2)
+    assert rc == eq.EQ_OK and L.version == 2
+    assert (L.rows, L.cols, L.lanes, L.tile_cols, L.n_chunks, L.prob_bits, L.n_syms) == \
+        (70, 1000, 64, 256, info.n_chunks, 12, info.n_syms)
+    assert (L.n_quads, L.n_pairs, L.n_singles) == (info.n_quads, info.n_pairs, info.n_singles)
+    assert eq.lib().eq_gemv_workspace_bytes(ctypes.byref(L), 8) >= 8 * 4 * 70 * 4
+    bad = {
+        "tile_cols": _patch(b2, 84, 250, np.uint32),
+        "res_bits": _patch(b2, 36, 9, np.uint32),
+        "parts": _patch(b2, 144, info.n_quads + 1, np.uint32),
+        "chunks": _patch(b2, 28, info.n_chunks - 1, np.uint32),
+        "freq": _patch(b2, info.off_freq, 7, np.uint16),
+        "phrase_order": _patch(b2, info.off_phr, 0xFFFFFFF0, np.uint32),
+        "pair_byte": _patch(b2, info.off_phr + 4 * info.n_quads + 3, 1, np.uint8),
+        "nan_code": _patch(b2, info.off_phr + 4 * (info.n_syms - 1), 0x7F, np.uint8),
+        "state_low": _patch(b2, info.off_chunk_state + 4, 3, np.uint32),
+        "offsets": _patch(b2, info.off_chunk_off + 4, 0xFFFFFFF, np.uint32),
+    }
+    for name, b in bad.items():
+        assert _init(b)[0] == eq.EQ_EFORMAT, name

@@ -1,0 +1,248 @@
+"""GPU parity of container version 2 (tile-ordered chunks, phrase alphabet)
+against the oracle.
+
+Codes and BF16 weights bit-exact against the oracle's decode and
+dequantiser; the fused GEMV within max|y - y_ref| / max|y_ref| <= 1e-2 per
+batch row against the oracle's fp64 GEMV on the decoded BF16 weights; one-hot
+inputs exact.  Shapes cover partial tiles in both directions, fewer rows than
+a tile, N not a multiple of 4 (segments ending in pairs and single codes),
+every tile height, narrow and wide tiles, both base formats and a
+single-phrase layer.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import config_matrices, small_spec
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def eq():
+    import paper_2601_22787_amd as m
+    m.lib()
+    assert torch.cuda.is_available()
+    return m
+
+
+def _dev():
+    return torch.device("cuda:0")
+
+
+def gpu_codes(eq, L, off=0):
+    n = L.rows * L.cols
+    out = torch.full((n + off + 8,), 0xA5, dtype=torch.uint8, device=_dev())
+    eq.eq_decode_codes(L, out[off:off + n])
+    got = out.cpu().numpy()
+    assert (got[:off] == 0xA5).all() and (got[off + n:] == 0xA5).all()
+    return got[off:off + n].reshape(L.rows, L.cols)
+
+
+def gpu_bf16(eq, L, off=0):
+    n = L.rows * L.cols
+    out = torch.full((n + off + 8,), -1, dtype=torch.int16, device=_dev())
+    eq.eq_decode_bf16(L, out[off:off + n])
+    got = out.cpu().numpy().view(np.uint16)
+    assert (got[:off] == 0xFFFF).all() and (got[off + n:] == 0xFFFF).all()
+    return got[off:off + n].reshape(L.rows, L.cols)
+
+
+def gpu_gemv(eq, L, x_bits, bias_bits=None):
+    B = x_bits.shape[0]
+    x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+    bias = None if bias_bits is None else torch.from_numpy(bias_bits.view(np.int16)).to(_dev())
+    y = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+    eq.eq_decode_gemv(L, x, B, bias, y, L.workspace(B))
+    return y.cpu().numpy()
+
+
+def rel_err(y, y_ref):
+    return np.abs(y - y_ref).max(axis=1) / np.maximum(np.abs(y_ref).max(axis=1), 1e-30)
+
+
+def check_full(eq, blob, spec, batches=(1, 3, 8), with_bias=True, offsets=(0,)):
+    L = eq.Layer(blob, _dev())
+    assert L.raw.version == 2
+    rc, q_ref = oracle.container2_decode_par(blob)
+    assert rc == oracle.OK
+    w_ref = oracle.dequant_par(q_ref, oracle.container_scales(blob),
+                               oracle.container2_info(blob).base_format)
+    for off in offsets:
+        assert np.array_equal(gpu_codes(eq, L, off), q_ref), ("codes", off)
+        assert np.array_equal(gpu_bf16(eq, L, off), w_ref), ("bf16", off)
+    for B in batches:
+        x = synth.activations(spec, B)
+        bias = synth.bias(spec) if with_bias else None
+        y = gpu_gemv(eq, L, x, bias)
+        err = rel_err(y, oracle.gemv_par(w_ref, x, bias))
+        assert np.isfinite(y).all() and (err <= TOL).all(), (B, err)
+    assert eq.eq_get_status(L) == eq.EQ_OK
+    return L, q_ref, w_ref
+
+
+def build(eq, spec, TR, TC, bits, fmt=1):
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, bits, base_format=fmt)
+    return w, eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, base_format=fmt)
+
+
+EDGE = [
+    # M, N, TR, TC, bits, outliers
+    (1, 4, 64, 4, 2.0, False),           # one phrase slot
+    (1, 1, 64, 4, 2.0, False),           # one code
+    (3, 77, 64, 64, 3.0, False),         # N odd: pairs and singles at segment ends
+    (5, 100, 256, 32, 2.0, False),       # rows far below a tile
+    (40, 640, 64, 256, 2.0, False),      # partial last column tile
+    (300, 1000, 64, 256, 2.5, False),    # partial tiles both ways
+    (130, 4096, 128, 512, 4.0, True),    # 4 bits, outliers, wide tiles
+    (37, 1283, 128, 64, 3.0, False),
+    (520, 2048, 256, 256, 2.0, False),   # the config-4 tile, partial last tile row
+    (24, 1024, 64, 1024, 6.0, False),    # near-flat distribution, long segments
+    (777, 260, 256, 4, 2.0, True),       # the narrowest tiles
+]
+
+
+@pytest.mark.parametrize("M,N,TR,TC,bits,outliers", EDGE)
+def test_v2_edge_shapes(eq, M, N, TR, TC, bits, outliers):
+    say("v2 edge", M, N, TR, TC, bits)
+    spec = small_spec(M, N, bits=bits, seed=2000 + 7 * M + N, outliers=outliers)
+    _, blob = build(eq, spec, TR, TC, bits)
+    check_full(eq, blob, spec)
+
+
+def test_v2_output_offsets(eq):
+    """Phrases are stored with 8-byte (BF16) and 4-byte (codes) stores at any
+    element offset: outputs that start 1-3 elements into a buffer are
+    bit-exact and nothing outside them is written."""
+    spec = small_spec(70, 1000, bits=2.0, seed=2100)
+    _, blob = build(eq, spec, 64, 256, 2.0)
+    check_full(eq, blob, spec, batches=(1,), offsets=(0, 1, 2, 3))
+
+
+def test_v2_single_phrase_and_oracle_built(eq):
+    spec = small_spec(70, 512, seed=2200)
+    w = np.zeros((70, 512), dtype=np.uint16)
+    blob = eq.eqe_encode2(w, 1.0, tile_rows=64, tile_cols=256)
+    assert oracle.container2_info(blob).n_syms == 1
+    check_full(eq, blob, spec, batches=(1, 2))
+    # a container written by the oracle's own encoder
+    spec = small_spec(200, 768, bits=2.0, seed=2201)
+    w = synth.weights(spec)
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    check_full(eq, oracle.container2_build(w, alpha, 128, 128), spec, batches=(1, 8))
+
+
+@pytest.mark.parametrize("TR", [64, 256])
+def test_v2_every_code_and_one_hot(eq, TR):
+    """All 253 finite E4M3FN codes in one layer (each row holds s * v(q) for
+    every q, so AbsMax with alpha = 1 reproduces each code), and one-hot
+    inputs: y_i = s_i * v(q_ij) exactly, for every column."""
+    codes = [c for c in range(256) if (c & 0x7F) != 0x7F and c != 0x80]
+    vals = np.array([oracle.e4m3_value(c) for c in codes])
+    M, N = 6, 512
+    w = np.zeros((M, N), dtype=np.uint16)
+    for i in range(M):
+        row = np.resize(np.roll(vals, 37 * i), N) * (2.0 ** (i - 2))
+        w[i] = [synth.to_bf16(float(v)) for v in row]
+    blob = eq.eqe_encode2(w, 1.0, tile_rows=TR, tile_cols=128)
+    spec = small_spec(M, N, seed=2300)
+    L, q_ref, _ = check_full(eq, blob, spec, batches=(1, 2))
+    assert len(np.unique(q_ref)) == len(codes)
+    scale = synth.bf16_to_f32(oracle.container_scales(blob)).astype(np.float64)
+    for j0 in range(0, N, 8):
+        x = np.zeros((8, N), dtype=np.uint16)
+        for b in range(8):
+            x[b, j0 + b] = 0x3F80
+        y = gpu_gemv(eq, L, x)
+        for b in range(8):
+            exact = scale * np.array([oracle.e4m3_value(int(c)) for c in q_ref[:, j0 + b]])
+            assert np.array_equal(y[b].astype(np.float64), exact), (j0 + b)
+
+
+def test_v2_int8(eq):
+    for (M, N, TR, TC) in ((96, 1000, 64, 256), (300, 2048, 256, 256)):
+        say("v2 int8", M, N)
+        spec = small_spec(M, N, bits=2.0, seed=2400 + M)
+        _, blob = build(eq, spec, TR, TC, 2.0, fmt=eq.FMT_INT8)
+        assert oracle.container2_info(blob).base_format == eq.FMT_INT8
+        check_full(eq, blob, spec, batches=(1, 8))
+
+
+def test_v2_zero_input_and_bias_view(eq):
+    spec = small_spec(300, 1024, bits=2.0, seed=2500)
+    _, blob = build(eq, spec, 64, 256, 2.0)
+    L = eq.Layer(blob, _dev())
+    bias_bits = synth.bias(spec)
+    backing = torch.zeros(302, dtype=torch.int16, device=_dev())
+    backing[1:301] = torch.from_numpy(bias_bits.view(np.int16)).to(_dev())
+    for B in (1, 8):
+        y = torch.full((B, 300), float("nan"), dtype=torch.float32, device=_dev())
+        eq.eq_decode_gemv(L, torch.zeros((B, 1024), dtype=torch.int16, device=_dev()), B,
+                          backing[1:301], y, L.workspace(B))
+        assert np.array_equal(y.cpu().numpy(), np.stack([synth.bf16_to_f32(bias_bits)] * B))
+
+
+def test_v2_deterministic(eq):
+    spec = small_spec(256, 4096, bits=2.0, seed=2600)
+    _, blob = build(eq, spec, 64, 256, 2.0)
+    L = eq.Layer(blob, _dev())
+    x = synth.activations(spec, 3)
+    y0 = gpu_gemv(eq, L, x)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y1 = torch.full((3, 256), float("nan"), dtype=torch.float32, device=_dev())
+        xt = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(_dev())
+        eq.eq_decode_gemv(L, xt, 3, None, y1, L.workspace(3), s)
+    torch.cuda.synchronize()
+    assert np.array_equal(y0, y1.cpu().numpy()) and np.array_equal(y0, gpu_gemv(eq, L, x))
+
+
+def test_v2_corrupted_stream_flagged(eq):
+    spec = small_spec(64, 1024, bits=2.0, seed=2700)
+    _, blob = build(eq, spec, 64, 256, 2.0)
+    info = oracle.container2_info(blob)
+    r = np.random.default_rng(5)
+    flagged = 0
+    for trial in range(6):
+        bad = blob.copy()
+        word = int(r.integers(info.total_words))
+        bad[info.off_words + 2 * word + int(r.integers(2))] ^= np.uint8(1 << int(r.integers(8)))
+        L = eq.Layer(bad, _dev())
+        out = torch.empty(L.rows * L.cols, dtype=torch.uint8, device=_dev())
+        eq.eq_decode_codes(L, out)
+        q = out.cpu().numpy().reshape(L.rows, L.cols)
+        rc_gpu = eq.eq_get_status(L)
+        rc_ref, q_ref = oracle.container2_decode(bad)
+        if rc_ref == oracle.ECORRUPT:
+            assert rc_gpu == eq.EQ_ECORRUPT
+            flagged += 1
+        else:
+            assert rc_gpu == eq.EQ_OK and np.array_equal(q, q_ref)
+        eq.eq_layer_prepare(L)
+        assert eq.eq_get_status(L) == eq.EQ_OK
+    assert flagged >= 1
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_v2_configs_1_to_3(eq, cfg):
+    for spec in config_matrices(cfg):
+        TR = 64
+        TC = spec.chunk_syms // TR
+        say("v2 config", cfg, spec.name, spec.rows, spec.cols, TR, TC)
+        w = synth.weights(spec)
+        alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=1024)
+        blob = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, seed=spec.seed,
+                              target_bits=spec.target_bits)
+        check_full(eq, blob, spec, batches=(1, 8) if cfg < 3 else (1,))

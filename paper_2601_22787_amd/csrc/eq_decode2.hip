@@ -12,7 +12,12 @@
 //   .z, .w = the four codes' values as BF16 pairs (zero past the length)
 // so that  x' = F (x >> 16) + (x mod 2^16) - cum  =  x - ((2^16 - F) (x >> 16) + cum)
 // is one 16 x 16-bit multiply-add (high half of x selected by op_sel) and one
-// subtraction.  Stream words are handed out with a wavefront ballot and a
+// subtraction.  In LDS the entry is split in two 8-byte halves read by two
+// 8-byte loads (a 16-byte LDS read at a random address costs about three
+// times as much as an 8-byte one on gfx950): the state half (.x with the
+// step of the state's position in the kernel's units, .y) at bucket * 8, and
+// the value half (.z, .w, or the codes) at kValHalf + bucket * 8, an offset
+// that keeps the two loads from being merged.  Stream words are handed out with a wavefront ballot and a
 // masked bit count in ascending state order, as the coder reads them.
 //
 // GEMV: all states of a chunk walk the same TC columns, so the chunk's
@@ -41,6 +46,12 @@ constexpr int kMaxBatch2 = 8;
 constexpr uint32_t kHalf2 = 512;           // stream words per window half
 constexpr uint32_t kWin2 = 2 * kHalf2;     // per-wave LDS window (2 KiB)
 constexpr uint32_t kXPad = 8;              // zero activations after a tile row
+// LDS table: state halves at [0, 32 KiB), value halves from kValHalf on.
+constexpr uint32_t kValHalf = kBuckets * 8 + 8;
+constexpr uint32_t kTableBytes2 = (kValHalf + kBuckets * 8 + 8 + 15) / 16 * 16;
+// One more entry after the kBuckets: the identity (2^16 - F = 0, cum = 0,
+// step 0, values 0), the step taken by states whose row segment is done.
+constexpr uint32_t kIdentity2 = kBuckets * 8;
 
 enum Mode2 { kCodes2 = 0, kBf16_2 = 1, kGemv2 = 2 };
 
@@ -75,11 +86,13 @@ __device__ inline uint32_t state_update(uint32_t x, uint32_t ex, uint32_t ey) {
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Phrase entry of state x (the table sits at LDS address 0: x & 0xFFF0 is the
-// byte offset of bucket (x mod 2^16) >> 4).
-__device__ inline u32x4 entry_of(uint32_t x) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(x & 0xFFF0u);
-}
+typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
+
+// LDS byte offset of the state half of the bucket of state x (the table
+// sits at LDS address 0): ((x mod 2^16) >> 4) * 8.
+__device__ inline uint32_t bucket_addr(uint32_t x) { return (x >> 1) & 0x7FF8u; }
+__device__ inline u32x2 state_half(uint32_t addr) { return *(lds_u32x2 *)(addr); }
+__device__ inline u32x2 value_half(uint32_t addr) { return *(lds_u32x2 *)(addr + kValHalf); }
 
 // 8 bytes of LDS at any 2-byte aligned address (the hardware splits
 // unaligned accesses; checked on gfx950).
@@ -95,10 +108,11 @@ struct Tile {
   int nb;
   uint32_t x[G];
   bool valid[G];
-  uint32_t pos[G];   // GEMV: LDS byte address of the state's column in batch row 0;
-                     // otherwise its column within the tile row
+  uint32_t pos[G];   // GEMV: LDS byte address of the state's column (its
+                     // activation record at batch 1, else in batch row 0);
+                     // codes / BF16: byte offset of its column in the output row
   uint32_t end;      // pos at the end of a row segment
-  uint32_t obase[G]; // codes / BF16: the state's row offset (elements) from the tile origin
+  uint32_t obase[G]; // codes / BF16: the state's row offset (bytes) from the tile origin
   float srow[G];     // BF16: the state's row scale
   float acc[G][NB ? NB : kMaxBatch2];
   // stream
@@ -131,7 +145,26 @@ struct Tile {
     ra = wa + 2 * (p - wb);
     win4[lane] = load_words(a.words, wb + 8 * lane, last8);
     win4[kHalf2 / 8 + lane] = load_words(a.words, wb + kHalf2 + 8 * lane, last8);
-    if (MODE == kGemv2) {
+    if (MODE == kGemv2 && NB == 1) {
+      // batch 1: record j holds the activations of columns j .. j + 3 (zero
+      // past the tile row), so a phrase at column j reads 8 aligned bytes at
+      // 8 j; record cols (all zero) is read by states whose segment is done
+      u32x2 *rec = reinterpret_cast<u32x2 *>(wave_lds + kWin2 * 2);
+      const uint16_t *xr = a.x + c0;
+      for (uint32_t j = lane; j <= cols; j += kWave) {
+        uint32_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = j + e < cols ? xr[j + e] : 0u;
+        rec[j] = u32x2{v[0] | (v[1] << 16), v[2] | (v[3] << 16)};
+      }
+      const uint32_t x0 = uniform(lds_addr(rec));
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        pos[g] = x0;
+        acc[g][0] = 0.0f;
+      }
+      end = x0 + 8 * cols;
+    } else if (MODE == kGemv2) {
       // the tile's activations, kXPad zeros after each row
       uint16_t *xt = reinterpret_cast<uint16_t *>(wave_lds + kWin2 * 2);
       for (int bb = 0; bb < nb; ++bb)
@@ -148,11 +181,11 @@ struct Tile {
     } else {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        pos[g] = 0;
-        obase[g] = (g * kWave + lane) * a.cols;
+        pos[g] = 0;  // byte offset within the state's row segment
+        obase[g] = (g * kWave + lane) * a.cols * (MODE == kBf16_2 ? 2 : 1);
         if (MODE == kBf16_2) srow[g] = valid[g] ? bf16_at(a.scale, r0 + g * kWave + lane) : 0.0f;
       }
-      end = cols;
+      end = cols * (MODE == kBf16_2 ? 2 : 1);
       const uint32_t span = (rows - 1) * a.cols + cols;  // elements from the tile origin
       if (MODE == kCodes2)
         out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + size_t(r0) * a.cols + c0, 0,
@@ -183,48 +216,49 @@ struct Tile {
 
   // The activations at state g's column, four per batch row (GEMV).
   __device__ __forceinline__ void read_x(int g, u32x2 (&xv)[NX]) {
+    if (NB == 1) {
+      xv[0] = *(lds_u32x2 *)(pos[g]);  // the column's record, 8-byte aligned
+      return;
+    }
 #pragma unroll
     for (int bb = 0; bb < NX; ++bb)
       if (bb < nb) xv[bb] = lds_read_u64(pos[g] + 2 * bb * a.xrow);
   }
 
+  // es: state half (.x high half = the position step in this kernel's units),
+  // ev: value half (BF16 pairs, or the codes).
   template <bool WIDE>
-  __device__ __forceinline__ void use(int g, u32x4 e, const u32x2 (&xv)[NX]) {
+  __device__ __forceinline__ void use(int g, u32x2 es, u32x2 ev, const u32x2 (&xv)[NX]) {
+    const uint32_t step = es.x >> 16;
     if (MODE == kGemv2) {
 #pragma unroll
       for (int bb = 0; bb < NX; ++bb)
-        if (bb < nb) acc[g][bb] = dot2_bf16(e.w, xv[bb].y, dot2_bf16(e.z, xv[bb].x, acc[g][bb]));
-      pos[g] += e.x >> 16;
+        if (bb < nb) acc[g][bb] = dot2_bf16(ev.y, xv[bb].y, dot2_bf16(ev.x, xv[bb].x, acc[g][bb]));
     } else if (MODE == kBf16_2) {
       const float s = srow[g];
-      const uint32_t lo = pack_bf16(s * __uint_as_float(e.z << 16),
-                                    s * __uint_as_float(e.z & 0xFFFF0000u));
-      const uint32_t hi = pack_bf16(s * __uint_as_float(e.w << 16),
-                                    s * __uint_as_float(e.w & 0xFFFF0000u));
-      const uint32_t off = 2 * (obase[g] + pos[g]);
-      const uint32_t len2 = e.x >> 16;  // bytes of the phrase's BF16 values / 2
-      if (WIDE) {
+      const uint32_t lo = pack_bf16(s * __uint_as_float(ev.x << 16),
+                                    s * __uint_as_float(ev.x & 0xFFFF0000u));
+      const uint32_t hi = pack_bf16(s * __uint_as_float(ev.y << 16),
+                                    s * __uint_as_float(ev.y & 0xFFFF0000u));
+      const uint32_t off = obase[g] + pos[g];
+      if (WIDE || step == 8) {
         __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, out_rsrc, off, 0, 0);
-      } else if (len2 == 8) {
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, out_rsrc, off, 0, 0);
-      } else if (len2 == 4) {
+      } else if (step == 4) {
         __builtin_amdgcn_raw_buffer_store_b32(lo, out_rsrc, off, 0, 0);
       } else {
         __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(lo), out_rsrc, off, 0, 0);
       }
-      pos[g] += len2 >> 1;
     } else {
       const uint32_t off = obase[g] + pos[g];
-      const uint32_t len2 = e.x >> 16;
-      if (WIDE || len2 == 8) {
-        __builtin_amdgcn_raw_buffer_store_b32(e.z, out_rsrc, off, 0, 0);
-      } else if (len2 == 4) {
-        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(e.z), out_rsrc, off, 0, 0);
+      if (WIDE || step == 4) {
+        __builtin_amdgcn_raw_buffer_store_b32(ev.x, out_rsrc, off, 0, 0);
+      } else if (step == 2) {
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(ev.x), out_rsrc, off, 0, 0);
       } else {
-        __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(e.z), out_rsrc, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(ev.x), out_rsrc, off, 0, 0);
       }
-      pos[g] += len2 >> 1;
     }
+    pos[g] += step;
   }
 
   // One step.  MASKED: only states whose segment is not complete take part
@@ -232,11 +266,15 @@ struct Tile {
   template <bool MASKED>
   __device__ __forceinline__ void step(const bool (&act)[G]) {
     slide();
-    u32x4 e[G];
+    u32x2 es[G], ev[G];
+    uint32_t ba[G];
     u32x2 xv[G][NX];
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      if (!MASKED || act[g]) e[g] = entry_of(x[g]);
+      if (!MASKED || act[g]) {
+        ba[g] = bucket_addr(x[g]);
+        es[g] = state_half(ba[g]);
+      }
     if (MODE == kGemv2) {
 #pragma unroll
       for (int g = 0; g < G; ++g)
@@ -244,7 +282,10 @@ struct Tile {
     }
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      if (!MASKED || act[g]) x[g] = state_update(x[g], e[g].x, e[g].y);
+      if (!MASKED || act[g]) ev[g] = value_half(ba[g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (!MASKED || act[g]) x[g] = state_update(x[g], es[g].x, es[g].y);
     // renormalise in ascending state order (state g * 64 + lane)
     uint64_t need[G];
     uint32_t word[G];
@@ -259,10 +300,131 @@ struct Tile {
     }
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      if (!MASKED || act[g]) use<!MASKED>(g, e[g], xv[g]);
+      if (!MASKED || act[g]) use<!MASKED>(g, es[g], ev[g], xv[g]);
 #pragma unroll
     for (int g = 0; g < G; ++g) x[g] = renorm_lanes(need[g], x[g], word[g]);
     ra = r;
+  }
+
+  // --- pipelined full steps -------------------------------------------------
+  // A state's step has three parts: I (read its table entry and activations),
+  // U (update, ballot, read its stream word) and F (use the phrase, merge the
+  // word).  The lane's G states are offset by fractions of a step so that
+  // every I -> U and U -> F latency is covered by other states' work, while
+  // the words are still taken in the coder's order (step t: states 0..G-1,
+  // then step t + 1).  With G = 4 a step is
+  //   F0 I0' U2 | F1 I1' U3 | F2 I2' U0' | F3 I3' U1'      (' = step t + 1)
+  // and with G = 2   F0 I0' U1 | F1 I1' U0'.
+  u32x2 pes[G], pev[G];
+  u32x2 pxv[G][NX];
+  uint64_t pneed[G];
+  uint32_t pword[G];
+  bool pact[G];
+
+  // MASK: a state whose segment is done (or whose row lies past the layer)
+  // takes the identity entry: its state, position and sum stay as they are
+  // and it reads no word (GEMV at batch 1 only: its activation read stays
+  // inside the records).
+  template <int g, bool MASK>
+  __device__ __forceinline__ void p_issue() {
+    uint32_t ba = bucket_addr(x[g]);
+    if (MASK) {
+      pact[g] = valid[g] && pos[g] < end;
+      ba = pact[g] ? ba : kIdentity2;
+    }
+    pes[g] = state_half(ba);
+    if (MODE == kGemv2) read_x(g, pxv[g]);
+    pev[g] = value_half(ba);
+  }
+  template <int g>
+  __device__ __forceinline__ void p_update() {
+    x[g] = state_update(x[g], pes[g].x, pes[g].y);
+    pneed[g] = __builtin_amdgcn_ballot_w64(x[g] < 0x10000u);
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+        uint32_t(pneed[g] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(pneed[g]), 0u));
+    pword[g] = lds_read_u16(ra + 2 * below);
+    ra = add_twice(ra, static_cast<uint32_t>(__popcll(pneed[g])));
+  }
+  template <int g>
+  __device__ __forceinline__ void p_finish() {
+    use<true>(g, pes[g], pev[g], pxv[g]);
+    x[g] = renorm_lanes(pneed[g], x[g], pword[g]);
+  }
+
+  // One pipelined step: F(t) of every state, I(t + 1) after it, U of the
+  // next in the coder's order.
+  template <bool MASK>
+  __device__ __forceinline__ void p_step() {
+    constexpr int H = G / 2;
+    // the window moves between steps (a step reads at most TR words, half a
+    // window)
+    slide();
+    p_finish<0>();
+    p_issue<0, MASK>();
+    p_update<H>();
+    p_finish<1 % G>();
+    p_issue<1 % G, MASK>();
+    if (G == 4) {
+      p_update<3 % G>();
+      p_finish<2 % G>();
+      p_issue<2 % G, MASK>();
+      p_update<0>();
+      p_finish<3 % G>();
+      p_issue<3 % G, MASK>();
+      p_update<1 % G>();
+    } else {
+      p_update<0>();
+    }
+  }
+
+  // T steps, G = 2 or 4.  Without MASK every state takes part in all T (and
+  // the wave lowers its issue priority through the steps so that waves that
+  // are behind catch up); with MASK, T bounds the steps and the loop ends once
+  // every segment is done.
+  template <bool MASK>
+  __device__ __forceinline__ void run_pipelined(uint32_t T) {
+    if (T == 0) return;
+    constexpr int H = G / 2;
+    slide();
+    p_issue<0, MASK>();
+    p_issue<1 % G, MASK>();
+    if (G == 4) {
+      p_issue<2 % G, MASK>();
+      p_issue<3 % G, MASK>();
+    }
+    p_update<0>();
+    if (G == 4) p_update<1 % G>();
+    const uint32_t n = T - 1;
+    if (MASK) {
+      for (uint32_t t = 0; t < n; ++t) {
+        p_step<true>();
+        bool any = false;
+#pragma unroll
+        for (int g = 0; g < G; ++g) any |= pact[g];
+        // nothing of step t + 1 is pending but identity steps
+        if (__builtin_amdgcn_ballot_w64(any) == 0) return;
+      }
+    } else {
+      uint32_t t = 0;
+#pragma unroll 1
+      for (uint32_t q = 0; q < 4; ++q) {
+        set_prio_down(q);
+        const uint32_t stop = q == 0 ? n / 2 : q == 1 ? n - n / 4 : q == 2 ? n - n / 16 : n;
+        for (; t < stop; ++t) {
+          asm("" : "+s"(t));
+          p_step<false>();
+        }
+      }
+    }
+    slide();
+    p_finish<0>();
+    p_update<H>();
+    p_finish<1 % G>();
+    if (G == 4) {
+      p_update<3 % G>();
+      p_finish<2 % G>();
+      p_finish<3 % G>();
+    }
   }
 
   __device__ __forceinline__ void run() {
@@ -271,7 +433,18 @@ struct Tile {
     // Every state needs at least cols / 4 phrases; while each phrase slot lies
     // inside the segment, stores may be wide.
     const uint32_t t1 = full ? cols / 4 : 0;
-    for (uint32_t t = 0; t < t1; ++t) step<false>(all);
+    if (G >= 2) {
+      run_pipelined<false>(t1);
+      if (MODE == kGemv2 && NB == 1) {
+        // every phrase holds at least one code: at most cols steps in all
+        // (the bound also ends the loop on a damaged stream)
+        run_pipelined<true>(cols - t1);
+        finish();
+        return;
+      }
+    } else {
+      for (uint32_t t = 0; t < t1; ++t) step<false>(all);
+    }
     // every phrase holds at least one code: at most cols steps in all (the
     // bound also ends the loop on a damaged table)
     for (uint32_t t = t1; t < cols; ++t) {
@@ -316,32 +489,60 @@ struct Tile {
 template <int G, int MODE, int NB>
 __global__ __launch_bounds__(kMaxBlock2) void decode2_kernel(Args2 a) {
   extern __shared__ uint4 dyn2[];
-  // the phrase table at LDS address 0 (no static LDS in this kernel)
+  // the phrase table at LDS address 0 (no static LDS in this kernel), the
+  // position step in this kernel's units: record bytes (GEMV at batch 1),
+  // activation bytes (GEMV), BF16 bytes, code bytes
+  char *tab = reinterpret_cast<char *>(dyn2);
   for (uint32_t i = threadIdx.x; i < kBuckets; i += blockDim.x) {
-    uint4 e = a.lut[i];
-    if (MODE == kCodes2) e.z = a.codes4[i];
-    dyn2[i] = e;
+    const uint4 e = a.lut[i];
+    const uint32_t len = e.x >> 17;
+    const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 2 * len)
+                                         : (MODE == kBf16_2 ? 2 * len : len);
+    *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{(e.x & 0xFFFFu) | (step << 16), e.y};
+    *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) =
+        MODE == kCodes2 ? u32x2{a.codes4[i], 0u} : u32x2{e.z, e.w};
+  }
+  if (threadIdx.x == 0) {
+    *reinterpret_cast<u32x2 *>(tab + kIdentity2) = u32x2{0u, 0u};
+    *reinterpret_cast<u32x2 *>(tab + kValHalf + kIdentity2) = u32x2{0u, 0u};
   }
   __syncthreads();
   const uint32_t nw = blockDim.x / kWave, wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  char *mine = reinterpret_cast<char *>(dyn2 + kBuckets) + size_t(wave) * a.wave_lds;
+  char *mine = tab + kTableBytes2 + size_t(wave) * a.wave_lds;
   for (uint32_t c = uniform(blockIdx.x * nw + wave); c < a.n_chunks; c += gridDim.x * nw) {
     Tile<G, MODE, NB> t(a, c, lane, mine);
     t.run();
   }
 }
 
-// Rows split over NT > 1 column tiles: y = s * (partials added in tile order)
-// + bias.
-__global__ void merge2_kernel(Args2 a) {
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= a.rows * a.batch) return;
-  const uint32_t bb = i / a.rows, row = i - bb * a.rows;
+// Rows split over NT > 1 column tiles: y = s * (partials added in tile
+// order) + bias.  Four threads per output: thread p sums tiles [p NT / 4,
+// (p + 1) NT / 4) in order (independent loads, so their latencies overlap),
+// then the four sums are added in order p = 0..3.
+constexpr int kMergeSplit = 4;
+__global__ __launch_bounds__(256) void merge2_kernel(Args2 a) {
+  const uint32_t i = (blockIdx.x * blockDim.x + threadIdx.x) / kMergeSplit;
+  const uint32_t part = threadIdx.x % kMergeSplit;
+  const uint32_t n = a.rows * a.batch;
+  const uint32_t ii = i < n ? i : n - 1;  // idle threads take part in the shuffles
+  const uint32_t bb = ii / a.rows, row = ii - bb * a.rows;
   const float *p = a.ws + size_t(bb) * a.NT * a.rows + row;
+  const uint32_t t0 = part * a.NT / kMergeSplit, t1 = (part + 1) * a.NT / kMergeSplit;
   float sum = 0.0f;
-  for (uint32_t t = 0; t < a.NT; ++t) sum += p[size_t(t) * a.rows];
-  const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
-  a.y[i] = bf16_to_f32(a.scale[row]) * sum + bias;
+  uint32_t t = t0;
+  for (; t + 4 <= t1; t += 4) {
+    const float v0 = p[size_t(t) * a.rows], v1 = p[size_t(t + 1) * a.rows];
+    const float v2 = p[size_t(t + 2) * a.rows], v3 = p[size_t(t + 3) * a.rows];
+    sum = (((sum + v0) + v1) + v2) + v3;
+  }
+  for (; t < t1; ++t) sum += p[size_t(t) * a.rows];
+  const uint32_t lane = threadIdx.x % kWave, base = lane & ~uint32_t(kMergeSplit - 1);
+  const float s0 = __shfl(sum, base), s1 = __shfl(sum, base + 1);
+  const float s2 = __shfl(sum, base + 2), s3 = __shfl(sum, base + 3);
+  if (part == 0 && i < n) {
+    const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
+    a.y[i] = bf16_to_f32(a.scale[row]) * (((s0 + s1) + s2) + s3) + bias;
+  }
 }
 
 // Phrase table of a layer: bucket b (of kBuckets) belongs to symbol k when
@@ -433,12 +634,13 @@ Facts2 facts2() {
   return f;
 }
 
-constexpr size_t kTableBytes = size_t(kBuckets) * sizeof(uint4);
 
-// LDS per wavefront: the stream window, then (GEMV) the tile's activations.
+// LDS per wavefront: the stream window, then (GEMV) the tile's activations:
+// one 8-byte record per column at batch 1, else the rows.
 uint32_t wave_lds_bytes(int mode, const Args2 &a) {
   uint32_t b = kWin2 * 2;
-  if (mode == kGemv2) b += (a.batch * a.xrow * 2 + 15) / 16 * 16;
+  if (mode == kGemv2)
+    b += a.batch == 1 ? ((a.TC + 1) * 8 + 15) / 16 * 16 : (a.batch * a.xrow * 2 + 15) / 16 * 16;
   return b;
 }
 
@@ -453,11 +655,11 @@ int launch2(Args2 a, hipStream_t s) {
   a.wave_lds = wave_lds_bytes(MODE, a);
   uint32_t waves = (a.n_chunks + f.cus - 1) / f.cus;
   waves = waves < 1 ? 1 : (waves > kMaxWaves2 ? kMaxWaves2 : waves);
-  while (waves > 1 && kTableBytes + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
-  if (kTableBytes + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
+  while (waves > 1 && kTableBytes2 + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
+  if (kTableBytes2 + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
   uint32_t blocks = (a.n_chunks + waves - 1) / waves;
   if (blocks > uint32_t(f.cus) * 4) blocks = uint32_t(f.cus) * 4;
-  const size_t shm = kTableBytes + size_t(waves) * a.wave_lds;
+  const size_t shm = kTableBytes2 + size_t(waves) * a.wave_lds;
   const dim3 grid(blocks), block(waves * kWave);
   switch (a.TR) {
     case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB>), grid, block, shm, s, a); break;
@@ -528,7 +730,7 @@ int v2_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint1
                                            : launch2<kGemv2, 0>(a, s));
   if (rc != EQ_OK) return rc;
   if (a.NT > 1) {
-    const uint32_t n = L->rows * B;
+    const uint32_t n = L->rows * B * kMergeSplit;
     hipLaunchKernelGGL(merge2_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;

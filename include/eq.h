@@ -63,12 +63,14 @@
  * Conventions for every entry point below:
  *  - Device pointers are allocated and owned by the caller; the library never
  *    allocates, frees or synchronises (except eq_get_status, which waits on
- *    the given stream).
+ *    the given stream).  The one piece of device memory it holds itself is
+ *    eq_decode_gemv_noalloc's static scratch, part of its code object.
  *  - Calls are asynchronous on `stream` and reentrant; different layers or
  *    outputs may be processed on several streams at once.
  *  - Return codes: EQ_OK, EQ_EINVAL (null pointer, size or range),
  *    EQ_EFORMAT (container header or sections inconsistent), EQ_EHIP (a HIP
- *    launch or runtime call failed).  Stream corruption found while decoding
+ *    launch or runtime call failed), EQ_ESCRATCH (eq_decode_gemv_noalloc
+ *    only: the call needs more than the library's static scratch).  Stream corruption found while decoding
  *    on the device is recorded in the layer's status word (EQ_ECORRUPT via
  *    eq_get_status); outputs of a corrupted chunk are then unspecified, but
  *    no access ever leaves the container or the output buffers.
@@ -88,6 +90,7 @@ extern "C" {
 #define EQ_EFORMAT (-2)
 #define EQ_EHIP (-3)
 #define EQ_ECORRUPT (-4)
+#define EQ_ESCRATCH (-5)
 
 /* A validated view of one container in device memory (filled by eq_layer_init). */
 typedef struct eq_layer {
@@ -160,6 +163,21 @@ size_t eq_gemv_workspace_bytes(const eq_layer *L, uint32_t B);
  * ws/ws_bytes: device workspace of at least eq_gemv_workspace_bytes(L, B). */
 int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
                    float *y, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * eq_decode_gemv with the workspace taken from a static array of
+ * EQ_NOALLOC_SCRATCH_BYTES in the library's code object instead of `ws`.
+ * The call allocates nothing.  Each device holds one such array from the
+ * first call on it until the process ends, and every call on that device
+ * uses it: calls that overlap on one device (several streams or threads)
+ * race and must be serialised by the caller.  Returns EQ_ESCRATCH when
+ * eq_gemv_workspace_bytes(L, B) exceeds EQ_NOALLOC_SCRATCH_BYTES (checked on
+ * the host before any device work), otherwise what eq_decode_gemv returns;
+ * results are identical to eq_decode_gemv's. */
+#define EQ_NOALLOC_SCRATCH_BYTES (32u << 20)
+int eq_decode_gemv_noalloc(const eq_layer *L, const uint16_t *x, uint32_t B,
+                           const uint16_t *bias, float *y, hipStream_t stream);
 
 /* Block-wise decompression (Sec. 2.2, paragraph "Block-Wise Decompression
  * Pipeline": all compressed matrices of a transformer block are decoded

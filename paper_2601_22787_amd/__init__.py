@@ -15,7 +15,8 @@ import numpy as np
 from ._build import LIB as _LIB_PATH
 from ._build import build as _build_lib
 
-EQ_OK, EQ_EINVAL, EQ_EFORMAT, EQ_EHIP, EQ_ECORRUPT = 0, -1, -2, -3, -4
+EQ_OK, EQ_EINVAL, EQ_EFORMAT, EQ_EHIP, EQ_ECORRUPT, EQ_ESCRATCH = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 32 << 20
 FMT_E4M3, FMT_INT8 = 1, 2  # base formats of the codes (container field base_format)
 
 _lib = None
@@ -72,6 +73,8 @@ SIGNATURES = {
     "eq_gemv_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(eq_layer), ctypes.c_uint32]),
     "eq_decode_gemv": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp, _vp,
                                       _vp, ctypes.c_size_t, _vp]),
+    "eq_decode_gemv_noalloc": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp,
+                                              _vp, _vp]),
     "eq_decode_bf16_multi": (ctypes.c_int, [_vp, _vp, ctypes.c_uint32, _vp]),
     "eq_gemv_multi_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_uint32, ctypes.c_uint32]),
     "eq_decode_gemv_multi": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp, _vp,
@@ -212,6 +215,19 @@ def eq_decode_gemv(L, x, B: int, bias, y, ws, stream=None) -> None:
     nbytes = ws.numel() * ws.element_size()
     _check("eq_decode_gemv", lib().eq_decode_gemv(ctypes.byref(r), px, B, pb, py, pw, nbytes,
                                                   _stream(stream)))
+
+
+def eq_decode_gemv_noalloc(L, x, B: int, bias, y, stream=None) -> None:
+    """eq_decode_gemv with the library's static per-device scratch as workspace."""
+    import torch
+    r = _raw(L)
+    if x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError("x must hold 16-bit BF16 patterns")
+    px = _dptr(x, None, B * r.cols)
+    pb = _dptr(bias, None, r.rows) if bias is not None else None
+    py = _dptr(y, torch.float32, B * r.rows)
+    _check("eq_decode_gemv_noalloc",
+           lib().eq_decode_gemv_noalloc(ctypes.byref(r), px, B, pb, py, _stream(stream)))
 
 
 def _layer_array(layers):

@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "eq.h"
@@ -1537,6 +1538,43 @@ extern "C" int eq_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B,
     hipLaunchKernelGGL(merge_rows_kernel, dim3((L->n_chunks + 254) / 256), dim3(256), 0, stream,
                        a);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+// eq_decode_gemv_noalloc's workspace: one array per device, in the code
+// object (no allocation call at any time).  Its device address comes from
+// hipGetSymbolAddress on each device's first call, with that device current;
+// the array's name is not a device address in host code.  Every call on a
+// device shares it, so calls that overlap on one device race.  No kernel
+// needs it cleared: each call writes every partial, activation pair or code
+// before it reads it.
+static __device__ __align__(256) unsigned char scratch[EQ_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+static void *scratch_on_current_device() {
+  static std::atomic<void *> ptr[kMaxDevices];
+  static std::mutex mu;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void *p = ptr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(mu);
+  p = ptr[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    ptr[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
+extern "C" int eq_decode_gemv_noalloc(const eq_layer *L, const uint16_t *x, uint32_t B,
+                                      const uint16_t *bias, float *y, hipStream_t stream) {
+  const size_t need = eq_gemv_workspace_bytes(L, B);
+  if (need == 0) return EQ_EINVAL;
+  if (need > EQ_NOALLOC_SCRATCH_BYTES) return EQ_ESCRATCH;
+  void *ws = scratch_on_current_device();
+  if (!ws) return EQ_EHIP;
+  return eq_decode_gemv(L, x, B, bias, y, ws, EQ_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,

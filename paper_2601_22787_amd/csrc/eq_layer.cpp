@@ -218,6 +218,7 @@ extern "C" const char *eq_strerror(int code) {
     case EQ_EFORMAT: return "container header or sections inconsistent";
     case EQ_EHIP: return "HIP launch or runtime call failed";
     case EQ_ECORRUPT: return "entropy-coded stream failed its end-of-chunk check";
+    case EQ_ESCRATCH: return "workspace needed exceeds the static scratch (EQ_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown error code";
   }
 }

@@ -52,6 +52,16 @@ constexpr uint32_t kTableBytes2 = (kValHalf + kBuckets * 8 + 8 + 15) / 16 * 16;
 // One more entry after the kBuckets: the identity (2^16 - F = 0, cum = 0,
 // step 0, values 0), the step taken by states whose row segment is done.
 constexpr uint32_t kIdentity2 = kBuckets * 8;
+// Codes and BF16 output: the value half is the phrase's four codes, 4 bytes
+// at kCodesHalf + bucket * 4 (the identity's after the kBuckets).
+constexpr uint32_t kCodesHalf = kBuckets * 8 + 8;
+constexpr uint32_t kTableCodes2 = (kCodesHalf + kBuckets * 4 + 4 + 15) / 16 * 16;
+// Codes and BF16 output leave the wavefront as whole 64-code segments of a
+// row (a 128-byte line of BF16): each tile row has an LDS ring holding its
+// current segment and 4 bytes more, where a phrase that crosses the
+// segment's end spills (8-byte aligned rows).
+constexpr uint32_t kSeg = 64;
+constexpr uint32_t kRing = 72;
 
 enum Mode2 { kCodes2 = 0, kBf16_2 = 1, kGemv2 = 2 };
 
@@ -70,6 +80,7 @@ struct Args2 {
   uint16_t *wout;
   const uint16_t *x;
   uint32_t batch;
+  uint32_t fmt;              // base format (codes to values at BF16 output)
   const uint16_t *bias;
   float *y;
   float *ws;                 // partial row sums [batch][NT][rows] (NT > 1)
@@ -110,10 +121,12 @@ struct Tile {
   bool valid[G];
   uint32_t pos[G];   // GEMV: LDS byte address of the state's column (its
                      // activation record at batch 1, else in batch row 0);
-                     // codes / BF16: byte offset of its column in the output row
+                     // codes / BF16: its column in the tile
   uint32_t end;      // pos at the end of a row segment
-  uint32_t obase[G]; // codes / BF16: the state's row offset (bytes) from the tile origin
   float srow[G];     // BF16: the state's row scale
+  uint32_t rr[G];    // codes / BF16: LDS address of the state's ring
+  bool cr[G];        // codes / BF16: the last phrase completed a segment
+  uint32_t ring, list;  // codes / BF16: LDS addresses of the rings, the flush list
   float acc[G][NB ? NB : kMaxBatch2];
   // stream
   uint32_t p_end, wb, wa, ra, last8;
@@ -179,13 +192,16 @@ struct Tile {
       }
       end = x0 + 2 * cols;
     } else {
+      ring = uniform(lds_addr(wave_lds + kWin2 * 2));
+      list = ring + TR * kRing;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        pos[g] = 0;  // byte offset within the state's row segment
-        obase[g] = (g * kWave + lane) * a.cols * (MODE == kBf16_2 ? 2 : 1);
-        if (MODE == kBf16_2) srow[g] = valid[g] ? bf16_at(a.scale, r0 + g * kWave + lane) : 0.0f;
+        pos[g] = 0;
+        rr[g] = ring + (g * kWave + lane) * kRing;
+        cr[g] = false;
+        srow[g] = MODE == kBf16_2 && valid[g] ? bf16_at(a.scale, r0 + g * kWave + lane) : 0.0f;
       }
-      end = cols * (MODE == kBf16_2 ? 2 : 1);
+      end = cols;
       const uint32_t span = (rows - 1) * a.cols + cols;  // elements from the tile origin
       if (MODE == kCodes2)
         out_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + size_t(r0) * a.cols + c0, 0,
@@ -234,29 +250,13 @@ struct Tile {
 #pragma unroll
       for (int bb = 0; bb < NX; ++bb)
         if (bb < nb) acc[g][bb] = dot2_bf16(ev.y, xv[bb].y, dot2_bf16(ev.x, xv[bb].x, acc[g][bb]));
-    } else if (MODE == kBf16_2) {
-      const float s = srow[g];
-      const uint32_t lo = pack_bf16(s * __uint_as_float(ev.x << 16),
-                                    s * __uint_as_float(ev.x & 0xFFFF0000u));
-      const uint32_t hi = pack_bf16(s * __uint_as_float(ev.y << 16),
-                                    s * __uint_as_float(ev.y & 0xFFFF0000u));
-      const uint32_t off = obase[g] + pos[g];
-      if (WIDE || step == 8) {
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, out_rsrc, off, 0, 0);
-      } else if (step == 4) {
-        __builtin_amdgcn_raw_buffer_store_b32(lo, out_rsrc, off, 0, 0);
-      } else {
-        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(lo), out_rsrc, off, 0, 0);
-      }
     } else {
-      const uint32_t off = obase[g] + pos[g];
-      if (WIDE || step == 4) {
-        __builtin_amdgcn_raw_buffer_store_b32(ev.x, out_rsrc, off, 0, 0);
-      } else if (step == 2) {
-        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(ev.x), out_rsrc, off, 0, 0);
-      } else {
-        __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(ev.x), out_rsrc, off, 0, 0);
-      }
+      // the phrase's four codes into the row's ring (an unaligned 4-byte
+      // write; bytes past the phrase are overwritten by the next one or lie
+      // past the segment), and whether it completed the segment
+      const uint32_t q = pos[g] & (kSeg - 1);
+      *(__attribute__((address_space(3))) uint32_t *)(rr[g] + q) = ev.x;
+      cr[g] = q + step >= kSeg;
     }
     pos[g] += step;
   }
@@ -282,7 +282,7 @@ struct Tile {
     }
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      if (!MASKED || act[g]) ev[g] = value_half(ba[g]);
+      if (!MASKED || act[g]) ev[g] = value_of(ba[g]);
 #pragma unroll
     for (int g = 0; g < G; ++g)
       if (!MASKED || act[g]) x[g] = state_update(x[g], es[g].x, es[g].y);
@@ -299,11 +299,135 @@ struct Tile {
       r = add_twice(r, static_cast<uint32_t>(__popcll(need[g])));
     }
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+    for (int g = 0; g < G; ++g) {
       if (!MASKED || act[g]) use<!MASKED>(g, es[g], ev[g], xv[g]);
+      else cr[g] = false;
+    }
 #pragma unroll
     for (int g = 0; g < G; ++g) x[g] = renorm_lanes(need[g], x[g], word[g]);
     ra = r;
+    flush();
+  }
+
+  // The value half of a bucket: BF16 values (GEMV) or the four codes.
+  __device__ __forceinline__ u32x2 value_of(uint32_t ba) {
+    if (MODE == kGemv2) return value_half(ba);
+    return u32x2{*(__attribute__((address_space(3))) const uint32_t *)((ba >> 1) + kCodesHalf),
+                 0u};
+  }
+
+  // --- codes / BF16 output --------------------------------------------------
+  // Store n (<= 16) codes of tile row `row` from column col0 on: `d` holds
+  // 16 codes (from the row's ring).  Whole 16-code pieces go out as one
+  // (codes) or two (BF16) 16-byte stores; a shorter piece, which only a
+  // row's last segment has, element by element.
+  __device__ __forceinline__ void store_piece(uint32_t row, uint32_t col0, u32x4 d, uint32_t n,
+                                              float sc) {
+    const uint32_t idx = row * a.cols + col0;  // < 2^31 (checked at launch)
+    if (MODE == kCodes2) {
+      if (n >= 16) {
+        __builtin_amdgcn_raw_buffer_store_b128(d, out_rsrc, idx, 0, 0);
+      } else {
+        for (uint32_t e = 0; e < n; ++e)
+          __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(d[e / 4] >> (8 * (e % 4))),
+                                               out_rsrc, idx + e, 0, 0);
+      }
+      return;
+    }
+    uint32_t o[8];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      float v0, v1, v2, v3;
+      if (a.fmt == kFmtInt8) {
+        v0 = static_cast<float>(static_cast<int8_t>(d[w]));
+        v1 = static_cast<float>(static_cast<int8_t>(d[w] >> 8));
+        v2 = static_cast<float>(static_cast<int8_t>(d[w] >> 16));
+        v3 = static_cast<float>(static_cast<int8_t>(d[w] >> 24));
+      } else {
+        // E4M3FN to fp32 in hardware, two codes at a time
+        const float2v lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(d[w]), false);
+        const float2v hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(d[w]), true);
+        v0 = lo.x; v1 = lo.y; v2 = hi.x; v3 = hi.y;
+      }
+      // s * v is exact in fp32; one rounding to BF16
+      o[2 * w] = pack_bf16(sc * v0, sc * v1);
+      o[2 * w + 1] = pack_bf16(sc * v2, sc * v3);
+    }
+    if (n >= 16) {
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4{o[0], o[1], o[2], o[3]}, out_rsrc, 2 * idx, 0,
+                                             0);
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4{o[4], o[5], o[6], o[7]}, out_rsrc,
+                                             2 * idx + 16, 0, 0);
+    } else {
+      for (uint32_t e = 0; e < n; ++e)
+        __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(o[e / 2] >> (16 * (e % 2))),
+                                              out_rsrc, 2 * (idx + e), 0, 0);
+    }
+  }
+
+  // Write the list's n segments (entries: tile row | segment << 16, the row
+  // scale), four lanes per segment; then the rows listed with `spill` move
+  // the codes past their segment to the ring's start.
+  __device__ __forceinline__ void write_list(uint32_t n) {
+    for (uint32_t k = 0; k < n; k += kWave / 4) {
+      const uint32_t e = k + lane / 4, part = lane % 4;
+      if (e < n) {
+        const u32x2 ent = *(lds_u32x2 *)(list + 8 * e);
+        const uint32_t row = ent.x & 0xFFFFu, col0 = (ent.x >> 16) * kSeg + 16 * part;
+        const uint32_t src = ring + row * kRing + 16 * part;
+        const u32x2 d0 = *(lds_u32x2 *)(src), d1 = *(lds_u32x2 *)(src + 8);
+        const uint32_t lim = end > col0 ? end - col0 : 0u;
+        store_piece(row, col0, u32x4{d0.x, d0.y, d1.x, d1.y}, min(lim, 16u),
+                    __uint_as_float(ent.y));
+      }
+    }
+  }
+
+  // After a step: the segments its phrases completed go out.
+  __device__ __forceinline__ void flush() {
+    if (MODE == kGemv2) return;
+    uint32_t n = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint64_t m = __builtin_amdgcn_ballot_w64(cr[g]);
+      if (m == 0) continue;
+      if (cr[g]) {
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
+            uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+        // the segment just completed: the one before pos
+        const uint32_t seg = (pos[g] >> 6) - 1;
+        *(__attribute__((address_space(3))) u32x2 *)(list + 8 * (n + rank)) =
+            u32x2{(g * kWave + lane) | (seg << 16), __float_as_uint(srow[g])};
+      }
+      n += static_cast<uint32_t>(__popcll(m));
+    }
+    if (n == 0) return;
+    write_list(n);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (cr[g]) {
+        const uint32_t spill = *(__attribute__((address_space(3))) const uint32_t *)(rr[g] + kSeg);
+        *(__attribute__((address_space(3))) uint32_t *)(rr[g]) = spill;
+        cr[g] = false;
+      }
+  }
+
+  // At the end of the tile: every row's last, partial segment.
+  __device__ __forceinline__ void flush_tail() {
+    if (MODE == kGemv2 || (end & (kSeg - 1)) == 0) return;
+    uint32_t n = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint64_t m = __builtin_amdgcn_ballot_w64(valid[g]);
+      if (valid[g]) {
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
+            uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+        *(__attribute__((address_space(3))) u32x2 *)(list + 8 * (n + rank)) =
+            u32x2{(g * kWave + lane) | ((end >> 6) << 16), __float_as_uint(srow[g])};
+      }
+      n += static_cast<uint32_t>(__popcll(m));
+    }
+    write_list(n);
   }
 
   // --- pipelined full steps -------------------------------------------------
@@ -334,7 +458,7 @@ struct Tile {
     }
     pes[g] = state_half(ba);
     if (MODE == kGemv2) read_x(g, pxv[g]);
-    pev[g] = value_half(ba);
+    pev[g] = value_of(ba);
   }
   template <int g>
   __device__ __forceinline__ void p_update() {
@@ -375,6 +499,7 @@ struct Tile {
     } else {
       p_update<0>();
     }
+    flush();
   }
 
   // T steps, G = 2 or 4.  Without MASK every state takes part in all T (and
@@ -425,6 +550,7 @@ struct Tile {
       p_finish<2 % G>();
       p_finish<3 % G>();
     }
+    flush();
   }
 
   __device__ __forceinline__ void run() {
@@ -435,10 +561,11 @@ struct Tile {
     const uint32_t t1 = full ? cols / 4 : 0;
     if (G >= 2) {
       run_pipelined<false>(t1);
-      if (MODE == kGemv2 && NB == 1) {
+      if (MODE != kGemv2 || NB == 1) {
         // every phrase holds at least one code: at most cols steps in all
         // (the bound also ends the loop on a damaged stream)
         run_pipelined<true>(cols - t1);
+        flush_tail();
         finish();
         return;
       }
@@ -458,6 +585,7 @@ struct Tile {
       if (__builtin_amdgcn_ballot_w64(any) == 0) break;
       step<true>(act);
     }
+    flush_tail();
     finish();
   }
 
@@ -486,29 +614,35 @@ struct Tile {
   }
 };
 
+constexpr uint32_t table_bytes2(int mode) { return mode == kGemv2 ? kTableBytes2 : kTableCodes2; }
+
 template <int G, int MODE, int NB>
 __global__ __launch_bounds__(kMaxBlock2) void decode2_kernel(Args2 a) {
   extern __shared__ uint4 dyn2[];
   // the phrase table at LDS address 0 (no static LDS in this kernel), the
   // position step in this kernel's units: record bytes (GEMV at batch 1),
-  // activation bytes (GEMV), BF16 bytes, code bytes
+  // activation bytes (GEMV), codes (codes and BF16 output)
   char *tab = reinterpret_cast<char *>(dyn2);
   for (uint32_t i = threadIdx.x; i < kBuckets; i += blockDim.x) {
     const uint4 e = a.lut[i];
     const uint32_t len = e.x >> 17;
-    const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 2 * len)
-                                         : (MODE == kBf16_2 ? 2 * len : len);
+    const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 2 * len) : len;
     *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{(e.x & 0xFFFFu) | (step << 16), e.y};
-    *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) =
-        MODE == kCodes2 ? u32x2{a.codes4[i], 0u} : u32x2{e.z, e.w};
+    if (MODE == kGemv2)
+      *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) = u32x2{e.z, e.w};
+    else
+      *reinterpret_cast<uint32_t *>(tab + kCodesHalf + 4 * i) = a.codes4[i];
   }
   if (threadIdx.x == 0) {
     *reinterpret_cast<u32x2 *>(tab + kIdentity2) = u32x2{0u, 0u};
-    *reinterpret_cast<u32x2 *>(tab + kValHalf + kIdentity2) = u32x2{0u, 0u};
+    if (MODE == kGemv2)
+      *reinterpret_cast<u32x2 *>(tab + kValHalf + kIdentity2) = u32x2{0u, 0u};
+    else
+      *reinterpret_cast<uint32_t *>(tab + kCodesHalf + kIdentity2 / 2) = 0u;
   }
   __syncthreads();
   const uint32_t nw = blockDim.x / kWave, wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  char *mine = tab + kTableBytes2 + size_t(wave) * a.wave_lds;
+  char *mine = tab + table_bytes2(MODE) + size_t(wave) * a.wave_lds;
   for (uint32_t c = uniform(blockIdx.x * nw + wave); c < a.n_chunks; c += gridDim.x * nw) {
     Tile<G, MODE, NB> t(a, c, lane, mine);
     t.run();
@@ -605,6 +739,7 @@ Args2 make_args2(const eq_layer *L) {
   a.NT = (L->cols + L->tile_cols - 1) / L->tile_cols;
   a.n_chunks = L->n_chunks;
   a.padded_words = static_cast<uint32_t>(L->padded_words);
+  a.fmt = L->base_format;
   return a;
 }
 
@@ -636,9 +771,11 @@ Facts2 facts2() {
 
 
 // LDS per wavefront: the stream window, then (GEMV) the tile's activations:
-// one 8-byte record per column at batch 1, else the rows.
+// one 8-byte record per column at batch 1, else the rows; (codes, BF16) the
+// rows' rings and the flush list.
 uint32_t wave_lds_bytes(int mode, const Args2 &a) {
   uint32_t b = kWin2 * 2;
+  if (mode != kGemv2) b += a.TR * (kRing + 8);
   if (mode == kGemv2)
     b += a.batch == 1 ? ((a.TC + 1) * 8 + 15) / 16 * 16 : (a.batch * a.xrow * 2 + 15) / 16 * 16;
   return b;
@@ -655,11 +792,12 @@ int launch2(Args2 a, hipStream_t s) {
   a.wave_lds = wave_lds_bytes(MODE, a);
   uint32_t waves = (a.n_chunks + f.cus - 1) / f.cus;
   waves = waves < 1 ? 1 : (waves > kMaxWaves2 ? kMaxWaves2 : waves);
-  while (waves > 1 && kTableBytes2 + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
-  if (kTableBytes2 + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
+  const size_t tb = table_bytes2(MODE);
+  while (waves > 1 && tb + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
+  if (tb + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
   uint32_t blocks = (a.n_chunks + waves - 1) / waves;
   if (blocks > uint32_t(f.cus) * 4) blocks = uint32_t(f.cus) * 4;
-  const size_t shm = kTableBytes2 + size_t(waves) * a.wave_lds;
+  const size_t shm = tb + size_t(waves) * a.wave_lds;
   const dim3 grid(blocks), block(waves * kWave);
   switch (a.TR) {
     case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB>), grid, block, shm, s, a); break;

@@ -42,10 +42,12 @@ using namespace eq_dev;
 
 constexpr int kMaxWaves2 = 16;
 constexpr int kMaxBlock2 = kWave * kMaxWaves2;
+// GEMV at 4 or 8 batch rows: at most 8 wavefronts per block (LDS allows about
+// that many), so that a wavefront may hold up to 256 VGPRs (no spills).
+constexpr int max_waves2(int mode, int nb) { return mode == 2 && nb >= 4 ? 8 : kMaxWaves2; }
 constexpr int kMaxBatch2 = 8;
 constexpr uint32_t kHalf2 = 512;           // stream words per window half
 constexpr uint32_t kWin2 = 2 * kHalf2;     // per-wave LDS window (2 KiB)
-constexpr uint32_t kXPad = 8;              // zero activations after a tile row
 // LDS table: state halves at [0, 32 KiB), value halves from kValHalf on.
 constexpr uint32_t kValHalf = kBuckets * 8 + 8;
 constexpr uint32_t kTableBytes2 = (kValHalf + kBuckets * 8 + 8 + 15) / 16 * 16;
@@ -75,7 +77,6 @@ struct Args2 {
   int32_t *status;
   uint32_t rows, cols, TR, TC, NT, n_chunks, padded_words;
   uint32_t wave_lds;         // bytes of dynamic LDS per wavefront after the table
-  uint32_t xrow;             // elements per activation row in LDS (TC + kXPad, rounded)
   uint8_t *codes;
   uint16_t *wout;
   const uint16_t *x;
@@ -105,12 +106,6 @@ __device__ inline uint32_t bucket_addr(uint32_t x) { return (x >> 1) & 0x7FF8u; 
 __device__ inline u32x2 state_half(uint32_t addr) { return *(lds_u32x2 *)(addr); }
 __device__ inline u32x2 value_half(uint32_t addr) { return *(lds_u32x2 *)(addr + kValHalf); }
 
-// 8 bytes of LDS at any 2-byte aligned address (the hardware splits
-// unaligned accesses; checked on gfx950).
-__device__ inline u32x2 lds_read_u64(uint32_t addr) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) u32x2 *>(addr);
-}
-
 template <int G, int MODE, int NB>
 struct Tile {
   static constexpr uint32_t TR = G * kWave;
@@ -127,7 +122,7 @@ struct Tile {
   uint32_t rr[G];    // codes / BF16: LDS address of the state's ring
   bool cr[G];        // codes / BF16: the last phrase completed a segment
   uint32_t ring, list;  // codes / BF16: LDS addresses of the rings, the flush list
-  float acc[G][NB ? NB : kMaxBatch2];
+  float acc[G][NB];
   // stream
   uint32_t p_end, wb, wa, ra, last8;
   uint4 next;
@@ -142,7 +137,7 @@ struct Tile {
     c0 = tcol * a.TC;
     rows = min(TR, a.rows - r0);
     cols = min(a.TC, a.cols - c0);
-    nb = NB ? NB : int(a.batch);
+    nb = int(a.batch);  // <= NB; rows nb .. NB - 1 are zero activations
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const uint32_t s = g * kWave + lane;
@@ -161,10 +156,11 @@ struct Tile {
     if (MODE == kGemv2 && NB == 1) {
       // batch 1: record j holds the activations of columns j .. j + 3 (zero
       // past the tile row), so a phrase at column j reads 8 aligned bytes at
-      // 8 j; record cols (all zero) is read by states whose segment is done
+      // 8 j; records cols .. cols + 3 (all zero) are read by states whose
+      // segment is done (or, on a damaged stream, overshot by up to 3)
       u32x2 *rec = reinterpret_cast<u32x2 *>(wave_lds + kWin2 * 2);
       const uint16_t *xr = a.x + c0;
-      for (uint32_t j = lane; j <= cols; j += kWave) {
+      for (uint32_t j = lane; j < cols + 4; j += kWave) {
         uint32_t v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = j + e < cols ? xr[j + e] : 0u;
@@ -178,19 +174,29 @@ struct Tile {
       }
       end = x0 + 8 * cols;
     } else if (MODE == kGemv2) {
-      // the tile's activations, kXPad zeros after each row
-      uint16_t *xt = reinterpret_cast<uint16_t *>(wave_lds + kWin2 * 2);
-      for (int bb = 0; bb < nb; ++bb)
-        for (uint32_t j = lane; j < cols + kXPad; j += kWave)
-          xt[bb * a.xrow + j] = j < cols ? a.x[size_t(bb) * a.cols + c0 + j] : uint16_t(0);
-      const uint32_t x0 = uniform(lds_addr(xt));
+      // batch NB >= 2: pair table T[p] (4 NB bytes at 4 NB p), T[p][b] =
+      // (x[b][p], x[b][p + 1]) as a BF16 pair, zero past the tile row and
+      // for padded batch rows; a phrase at column p reads T[p] and T[p + 2]
+      // (aligned 4 NB-byte reads), and finished states read from T[cols]
+      // on (up to T[cols + 6] on a damaged stream)
+      uint32_t *tp = reinterpret_cast<uint32_t *>(wave_lds + kWin2 * 2);
+      for (uint32_t e = lane; e < (a.TC + 8) * NB; e += kWave) {
+        const uint32_t p = e / NB, bb = e % NB;
+        uint32_t v = 0;
+        if (bb < uint32_t(nb)) {
+          const uint16_t *xr = a.x + size_t(bb) * a.cols + c0;
+          v = (p < cols ? xr[p] : 0u) | ((p + 1 < cols ? uint32_t(xr[p + 1]) : 0u) << 16);
+        }
+        tp[e] = v;
+      }
+      const uint32_t x0 = uniform(lds_addr(tp));
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         pos[g] = x0;
 #pragma unroll
-        for (int bb = 0; bb < (NB ? NB : kMaxBatch2); ++bb) acc[g][bb] = 0.0f;
+        for (int bb = 0; bb < NB; ++bb) acc[g][bb] = 0.0f;
       }
-      end = x0 + 2 * cols;
+      end = x0 + 4 * NB * cols;
     } else {
       ring = uniform(lds_addr(wave_lds + kWin2 * 2));
       list = ring + TR * kRing;
@@ -228,7 +234,7 @@ struct Tile {
   // Use state g's phrase e: WIDE stores the whole phrase slot (four codes,
   // valid while the slot lies inside the row segment; later phrases of the
   // same state overwrite what lies past this one), else exactly its length.
-  static constexpr int NX = MODE == kGemv2 ? (NB ? NB : kMaxBatch2) : 1;
+  static constexpr int NX = MODE == kGemv2 ? NB : 1;
 
   // The activations at state g's column, four per batch row (GEMV).
   __device__ __forceinline__ void read_x(int g, u32x2 (&xv)[NX]) {
@@ -236,9 +242,25 @@ struct Tile {
       xv[0] = *(lds_u32x2 *)(pos[g]);  // the column's record, 8-byte aligned
       return;
     }
+    // T[p] and T[p + 2]: xv[b] = {pair (p, p + 1), pair (p + 2, p + 3)} of row b
+    uint32_t lo[NB], hi[NB];
+    if (NB == 2) {
+      const u32x2 v0 = *(lds_u32x2 *)(pos[g]), v1 = *(lds_u32x2 *)(pos[g] + 16);
+      lo[0] = v0.x; lo[1 % NB] = v0.y; hi[0] = v1.x; hi[1 % NB] = v1.y;
+    } else {
 #pragma unroll
-    for (int bb = 0; bb < NX; ++bb)
-      if (bb < nb) xv[bb] = lds_read_u64(pos[g] + 2 * bb * a.xrow);
+      for (int q = 0; q < NB / 4; ++q) {
+        const u32x4 v0 = *(__attribute__((address_space(3))) const u32x4 *)(pos[g] + 16 * q);
+        const u32x4 v1 =
+            *(__attribute__((address_space(3))) const u32x4 *)(pos[g] + 8 * NB + 16 * q);
+        lo[(4 * q) % NB] = v0.x; lo[(4 * q + 1) % NB] = v0.y;
+        lo[(4 * q + 2) % NB] = v0.z; lo[(4 * q + 3) % NB] = v0.w;
+        hi[(4 * q) % NB] = v1.x; hi[(4 * q + 1) % NB] = v1.y;
+        hi[(4 * q + 2) % NB] = v1.z; hi[(4 * q + 3) % NB] = v1.w;
+      }
+    }
+#pragma unroll
+    for (int bb = 0; bb < NX; ++bb) xv[bb] = u32x2{lo[bb], hi[bb]};
   }
 
   // es: state half (.x high half = the position step in this kernel's units),
@@ -249,7 +271,7 @@ struct Tile {
     if (MODE == kGemv2) {
 #pragma unroll
       for (int bb = 0; bb < NX; ++bb)
-        if (bb < nb) acc[g][bb] = dot2_bf16(ev.y, xv[bb].y, dot2_bf16(ev.x, xv[bb].x, acc[g][bb]));
+        acc[g][bb] = dot2_bf16(ev.y, xv[bb].y, dot2_bf16(ev.x, xv[bb].x, acc[g][bb]));
     } else {
       // the phrase's four codes into the row's ring (an unaligned 4-byte
       // write; bytes past the phrase are overwritten by the next one or lie
@@ -561,7 +583,7 @@ struct Tile {
     const uint32_t t1 = full ? cols / 4 : 0;
     if (G >= 2) {
       run_pipelined<false>(t1);
-      if (MODE != kGemv2 || NB == 1) {
+      {
         // every phrase holds at least one code: at most cols steps in all
         // (the bound also ends the loop on a damaged stream)
         run_pipelined<true>(cols - t1);
@@ -596,7 +618,7 @@ struct Tile {
         if (!valid[g]) continue;
         const uint32_t row = r0 + g * kWave + lane;
 #pragma unroll
-        for (int bb = 0; bb < (NB ? NB : kMaxBatch2); ++bb) {
+        for (int bb = 0; bb < NB; ++bb) {
           if (bb >= nb) continue;
           if (a.NT == 1) {
             const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
@@ -617,7 +639,7 @@ struct Tile {
 constexpr uint32_t table_bytes2(int mode) { return mode == kGemv2 ? kTableBytes2 : kTableCodes2; }
 
 template <int G, int MODE, int NB>
-__global__ __launch_bounds__(kMaxBlock2) void decode2_kernel(Args2 a) {
+__global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(Args2 a) {
   extern __shared__ uint4 dyn2[];
   // the phrase table at LDS address 0 (no static LDS in this kernel), the
   // position step in this kernel's units: record bytes (GEMV at batch 1),
@@ -626,7 +648,7 @@ __global__ __launch_bounds__(kMaxBlock2) void decode2_kernel(Args2 a) {
   for (uint32_t i = threadIdx.x; i < kBuckets; i += blockDim.x) {
     const uint4 e = a.lut[i];
     const uint32_t len = e.x >> 17;
-    const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 2 * len) : len;
+    const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 4 * NB * len) : len;
     *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{(e.x & 0xFFFFu) | (step << 16), e.y};
     if (MODE == kGemv2)
       *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) = u32x2{e.z, e.w};
@@ -776,8 +798,10 @@ Facts2 facts2() {
 uint32_t wave_lds_bytes(int mode, const Args2 &a) {
   uint32_t b = kWin2 * 2;
   if (mode != kGemv2) b += a.TR * (kRing + 8);
-  if (mode == kGemv2)
-    b += a.batch == 1 ? ((a.TC + 1) * 8 + 15) / 16 * 16 : (a.batch * a.xrow * 2 + 15) / 16 * 16;
+  if (mode == kGemv2) {
+    const uint32_t nbp = a.batch == 1 ? 1 : a.batch == 2 ? 2 : a.batch <= 4 ? 4 : 8;
+    b += nbp == 1 ? ((a.TC + 4) * 8 + 15) / 16 * 16 : (a.TC + 8) * 4 * nbp;
+  }
   return b;
 }
 
@@ -788,10 +812,10 @@ int launch2(Args2 a, hipStream_t s) {
   // output offsets from a tile's origin are 32-bit byte offsets
   if (MODE != kGemv2 && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
   const Facts2 f = facts2();
-  a.xrow = (a.TC + kXPad + 3) / 4 * 4;
   a.wave_lds = wave_lds_bytes(MODE, a);
   uint32_t waves = (a.n_chunks + f.cus - 1) / f.cus;
-  waves = waves < 1 ? 1 : (waves > kMaxWaves2 ? kMaxWaves2 : waves);
+  constexpr uint32_t wmax = max_waves2(MODE, NB);
+  waves = waves < 1 ? 1 : (waves > wmax ? wmax : waves);
   const size_t tb = table_bytes2(MODE);
   while (waves > 1 && tb + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
   if (tb + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
@@ -863,9 +887,11 @@ int v2_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint1
   a.bias = bias;
   a.y = y;
   a.ws = static_cast<float *>(ws);
-  const int rc = B == 1 ? launch2<kGemv2, 1>(a, s)
-                        : (B == kMaxBatch2 ? launch2<kGemv2, kMaxBatch2>(a, s)
-                                           : launch2<kGemv2, 0>(a, s));
+  // batch padded to 1, 2, 4 or 8 rows
+  const int rc = B == 1   ? launch2<kGemv2, 1>(a, s)
+                 : B == 2 ? launch2<kGemv2, 2>(a, s)
+                 : B <= 4 ? launch2<kGemv2, 4>(a, s)
+                          : launch2<kGemv2, 8>(a, s);
   if (rc != EQ_OK) return rc;
   if (a.NT > 1) {
     const uint32_t n = L->rows * B * kMergeSplit;

@@ -72,7 +72,7 @@ def rel_err(y, y_ref):
     return np.abs(y - y_ref).max(axis=1) / np.maximum(np.abs(y_ref).max(axis=1), 1e-30)
 
 
-def check_full(eq, blob, spec, batches=(1, 3, 8), with_bias=True, offsets=(0,)):
+def check_full(eq, blob, spec, batches=(1, 2, 3, 5, 8), with_bias=True, offsets=(0,)):
     L = eq.Layer(blob, _dev())
     assert L.raw.version == 2
     rc, q_ref = oracle.container2_decode_par(blob)

@@ -5,15 +5,20 @@ Workload: the Llama-70B-shaped MLP pair, an 8192x28672 and a 28672x8192 BF16
 matrix (Student-t(4) entries, log-normal(0, 0.5) row scales), quantised to
 E4M3 at ~2.0 bits/param entropy and entropy-coded in 65536-symbol chunks.
 One step runs the whole decode path on both matrices: decode to BF16, fused
-decode-GEMV at batch 1 and fused decode-GEMV at batch 8 (6 launches).
-Containers are resident in HBM before timing starts; several copies are
-rotated so that compressed reads are not served from the 256 MB MALL.
+decode-GEMV at batch 1 and fused decode-GEMV at batch 8 (5 launches), on
+containers of version 1.  Containers are resident in HBM before timing
+starts; every read of a matrix takes the next of several device copies, so
+that no launch finds its compressed bytes in the 256 MB MALL.
 
 Prints one JSON line: the decode throughput of the whole step, per-kernel
-times (mean and p10/p50/p90), the HBM fraction of every kernel, the ALU
-roofline of the dominant kernel and the oracle's CPU throughput.
+times (mean and p10/p50/p90) and HBM fractions, the HBM roofline of the
+dominant kernel, the target row (fused decode-GEMV at batch 1 on the
+8192x28672 matrix, compressed bytes over time against the HBM peak) on both
+container versions, every op on container version 2 (256 x 256 tiles of the
+same codes), and the oracle's CPU throughput.
 --base-format int8 runs the same workload coded with the Int8 base format
-(the paper's alternative to Float8) instead of E4M3.
+(the paper's alternative to Float8) instead of E4M3.  --workload selects
+configs 1-3, the 80-layer stack or prefill instead.
 """
 from __future__ import annotations
 
@@ -32,30 +37,17 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 # Vector ALU: 256 CUs x 4 SIMDs x 16 lanes, one 32-bit lane-op per lane and
 # clock at 2.4 GHz (packed FP32 not counted: the path is integer work).
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
-# Algorithmic issue slots of the vector-ALU port per decoded symbol (32-bit
-# lane-ops; a matrix-core instruction also takes one slot): the decode step
-# (slot mask, slot index, x >> P, multiply-add, renormalisation compare,
-# two-part lane prefix count, word address, and the renormalising merge as one
-# byte permute under a narrowed exec mask = 9) plus the use of the symbol:
-# BF16 output 2.5 (code conversion, scale multiply, half a pack of two
-# values); GEMV 1 (byte pick and conversion, per symbol pair) plus, at batch
-# 1, one dot2 per pair (0.5) and, at batch 8, one 4x4x4 MFMA per batch row
-# and four symbols (2).
-# Int8 codes: one conversion per symbol and one pack per pair instead of the
-# byte pick and pair conversion (+0.5 per symbol on the GEMV).
-ALG_OPS = {"bf16": 9.0 + 1.0 + 1.0 + 0.5, "gemv1": 9.0 + 0.5 + 0.5 + 0.5,
-           "gemv8": 9.0 + 0.5 + 0.5 + 2.0}
-ALG_OPS_INT8 = {"bf16": 11.5, "gemv1": 11.0, "gemv8": 12.5}
-# Kernel (function) name of each op family's decode launch on these shapes.
-# (template arguments: lanes / 64, op, [whole-row steps,] activation source,
-# batch, base format)
+# Kernel (function) name of each op family's decode launch on these shapes,
+# container version 1 (template arguments: lanes / 64, op, [whole-row
+# steps,] activation source, batch, base format).
 KERNEL = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 1>",
           "gemv1": "decode_kernel<4, 2, true, 1, 1, 1>", "gemv8": "gemv_tiled_kernel<4, 8, 1>"}
 KERNEL_INT8 = {"bf16": "multi_decode_kernel<4, 1, 0, 1, 2>",
                "gemv1": "decode_kernel<4, 2, true, 1, 1, 2>", "gemv8": "gemv_tiled_kernel<4, 8, 2>"}
 FORMATS = {"e4m3": 1, "int8": 2}
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_config4.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2601_22787_amd", "csrc", "eq_decode.hip")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_config4.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2601_22787_amd", "csrc", f)
+                  for f in ("eq_decode.hip", "eq_decode2.hip", "eq_device.h")]
 
 
 def parse():
@@ -81,11 +73,18 @@ def parse():
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
     ap.add_argument("--base-format", choices=tuple(FORMATS), default="e4m3",
                     help="base format of the codes (c4 workload): E4M3 (default) or Int8")
+    ap.add_argument("--counters-from", nargs="+", metavar="DIR",
+                    help="no benchmark: summarise rocprofv3 --pmc output directories (FETCH_SIZE; "
+                         "WRITE_SIZE + SQ_INSTS_VALU) of a run of this script into the counter "
+                         "file the HBM traffic and VALU figures are read from")
     return ap.parse_args()
 
 
-def build_layers(eq, synth, specs, copies, dev, fmt=1):
-    """Encode each matrix once (product encoder), upload `copies` copies."""
+def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0):
+    """Encode each matrix (product encoder) and upload `copies` device copies;
+    with v2_copies > 0 also the same codes (same alpha) in container version
+    2, tiles of `lanes` rows x chunk_syms / lanes columns (the same symbols
+    per chunk)."""
     out = []
     for spec in specs:
         t0 = time.time()
@@ -94,9 +93,19 @@ def build_layers(eq, synth, specs, copies, dev, fmt=1):
         blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
                              seed=spec.seed, target_bits=spec.target_bits, base_format=fmt)
         layers = [eq.Layer(blob, dev) for _ in range(copies)]
-        print(f"[bench] {spec.name} {spec.rows}x{spec.cols}: container {blob.size / 1e6:.1f} MB "
-              f"built in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
-        out.append((spec, w, blob, layers))
+        item = {"spec": spec, "w": w, "blob": blob, "layers": layers}
+        msg = f"container {blob.size / 1e6:.1f} MB"
+        if v2_copies:
+            blob2 = eq.eqe_encode2(w, alpha, tile_rows=spec.lanes,
+                                   tile_cols=spec.chunk_syms // spec.lanes,
+                                   seed=spec.seed, target_bits=spec.target_bits,
+                                   base_format=fmt)
+            item["blob2"] = blob2
+            item["layers2"] = [eq.Layer(blob2, dev) for _ in range(v2_copies)]
+            msg += f", version 2 {blob2.size / 1e6:.1f} MB"
+        print(f"[bench] {spec.name} {spec.rows}x{spec.cols}: {msg} built in "
+              f"{time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+        out.append(item)
     return out
 
 
@@ -122,61 +131,175 @@ def algorithmic_bytes(info, op, B):
 
 
 def cpu_baseline(layers, target_s, threads, fmt=1):
-    """The oracle, as written, on a bounded sample: the first R rows of the
-    8192x28672 matrix decoded from its container chunk by chunk, dequantised
-    to BF16 and multiplied by one activation row in fp64.  Timed on one
-    thread, then with `threads` threads over independent chunks and row
-    blocks (the oracle's C routines release the interpreter lock)."""
+    """The oracle, as written, on bounded samples, on `threads` host threads
+    over independent chunks and row blocks (its C routines release the
+    interpreter lock), median of three runs:
+    - value: the first R rows of the 8192x28672 matrix decoded from its
+      container chunk by chunk, dequantised to BF16 and multiplied by one
+      activation row in fp64 (decode-GEMV, B = 1); also on one thread;
+    - bf16: the same rows decoded and dequantised (decode to BF16);
+    - config 5: one 1024x8192 row block per entropy class (2, 3, 4 bits,
+      65536-symbol chunks) decoded, dequantised and multiplied; the seconds
+      of an 80-layer pass extrapolated from the per-parameter times."""
     import numpy as np
 
     import oracle
+    import paper_2601_22787_amd as eq
     import synth
-    spec, w, blob, _ = layers[0]
-    info = oracle.container_info(blob)
-    N, C = info.cols, info.chunk_syms
-    scale = oracle.container_scales(blob)
-    x = synth.activations(spec, 1)
+    from synth.configs import MatrixSpec, STUDENT_T, matrix_seed
 
-    def run(R, T):
-        t0 = time.perf_counter()
-        nchunks = (R * N + C - 1) // C
-        q = np.empty(nchunks * C, dtype=np.uint8)
+    def timer(blob, spec, gemv):
+        info = oracle.container_info(blob)
+        N, C = info.cols, info.chunk_syms
+        scale = oracle.container_scales(blob)
+        x = synth.activations(spec, 1)
 
-        def dec(c):
-            rc, qc = oracle.container_decode_chunk(blob, c)
-            assert rc == oracle.OK
-            q[c * C:c * C + qc.size] = qc
+        def run(R, T):
+            t0 = time.perf_counter()
+            nchunks = (R * N + C - 1) // C
+            q = np.empty(nchunks * C, dtype=np.uint8)
 
-        def rows(r0, r1):
-            w_hat = oracle.dequant(q[r0 * N:r1 * N].reshape(r1 - r0, N), scale[r0:r1], fmt)
-            oracle.gemv(w_hat, x)
+            def dec(c):
+                rc, qc = oracle.container_decode_chunk(blob, c)
+                assert rc == oracle.OK
+                q[c * C:c * C + qc.size] = qc
 
-        if T == 1:
-            for c in range(nchunks):
-                dec(c)
-            rows(0, R)
-        else:
-            with ThreadPoolExecutor(T) as ex:
-                list(ex.map(dec, range(nchunks)))
-                step = (R + T - 1) // T
-                list(ex.map(lambda r0: rows(r0, min(R, r0 + step)), range(0, R, step)))
-        return time.perf_counter() - t0
+            def rows(r0, r1):
+                w_hat = oracle.dequant(q[r0 * N:r1 * N].reshape(r1 - r0, N), scale[r0:r1], fmt)
+                if gemv:
+                    oracle.gemv(w_hat, x)
 
-    def sample(T):
-        # rows sized from a short probe run; then the median of three runs
-        R0 = 8 * T
-        t0 = run(R0, T)
-        R = int(min(info.rows, max(R0, R0 * target_s / max(t0, 1e-6))))
-        return R, sorted(run(R, T) for _ in range(3))[1]
+            if T == 1:
+                for c in range(nchunks):
+                    dec(c)
+                rows(0, R)
+            else:
+                with ThreadPoolExecutor(T) as ex:
+                    list(ex.map(dec, range(nchunks)))
+                    step = (R + T - 1) // T
+                    list(ex.map(lambda r0: rows(r0, min(R, r0 + step)), range(0, R, step)))
+            return time.perf_counter() - t0
 
-    R1, t1 = sample(1)
-    RT, tT = sample(threads)
+        def sample(T, seconds):
+            # rows sized from a short probe run; then the median of three runs
+            R0 = 8 * T
+            t0 = run(R0, T)
+            R = int(min(info.rows, max(R0, R0 * seconds / max(t0, 1e-6))))
+            return R, N, sorted(run(R, T) for _ in range(3))[1]
+        return sample
+
+    spec, blob = layers[0]["spec"], layers[0]["blob"]
+    R1, N, t1 = timer(blob, spec, True)(1, target_s)
+    RT, _, tT = timer(blob, spec, True)(threads, target_s)
+    RB, _, tB = timer(blob, spec, False)(threads, target_s / 2)
+    # config 5, one row block per entropy class
+    per_param = {}
+    for cls, bits in enumerate((2.0, 3.0, 4.0)):
+        sp = MatrixSpec(f"c5.class{cls}", 1024, 8192, STUDENT_T, 5, 0.5, 0.0, 0.0, bits, 65536,
+                        256, matrix_seed(5, cls, 4))
+        w = synth.weights(sp)
+        alpha, _ = eq.eqe_alpha_search(w, bits, sample_rows=256, base_format=fmt)
+        b5 = eq.eqe_encode(w, alpha, chunk_syms=65536, lanes=256, seed=sp.seed, target_bits=bits,
+                           base_format=fmt)
+        R5, N5, t5 = timer(b5, sp, True)(threads, target_s / 4)
+        per_param[bits] = t5 / (R5 * N5)
+    stack = {"q": (8192, 8192), "k": (1024, 8192), "v": (1024, 8192), "o": (8192, 8192),
+             "gate": (28672, 8192), "up": (28672, 8192), "down": (8192, 28672)}
+    layer_params = sum(m * n for m, n in stack.values())
+    c5_seconds = sum(layer_params * per_param[(2.0, 3.0, 4.0)[l % 3]] for l in range(80))
     return {"value": RT * N / tT / 1e9, "unit": "Gparams/s", "cores": threads, "kind": "oracle",
             "sample": f"first {RT} rows ({RT * N} params) of the 8192x28672 matrix: oracle rANS "
                       f"decode per chunk + BF16 dequantisation + fp64 GEMV (B=1) on {threads} "
                       f"threads over chunks and row blocks, median of 3 runs, {tT:.1f}s each",
             "single_thread_value": R1 * N / t1 / 1e9,
-            "single_thread_sample": f"first {R1} rows, one thread, median of 3 runs, {t1:.1f}s each"}
+            "single_thread_sample": f"first {R1} rows, one thread, median of 3 runs, {t1:.1f}s each",
+            "bf16_value": RB * N / tB / 1e9,
+            "bf16_sample": f"first {RB} rows of the 8192x28672 matrix: oracle decode + BF16 "
+                           f"dequantisation (no GEMV) on {threads} threads, median of 3 runs, "
+                           f"{tB:.1f}s each",
+            "config5_seconds_per_pass": round(c5_seconds, 2),
+            "config5_sample": "extrapolated: one 1024x8192 row block per entropy class (2, 3, 4 "
+                              "bits) timed (oracle decode + dequantisation + fp64 GEMV B=1, "
+                              f"{threads} threads); seconds per parameter of each class times "
+                              "the parameters of the 80 layers (layer l in class l mod 3)"}
+
+
+def kernel_counters(kernel):
+    """HBM bytes (FETCH_SIZE + WRITE_SIZE, each scaled by the counters'
+    readings for a copy of known size) and SQ_INSTS_VALU of one launch of
+    `kernel`, from the committed counter summary; None if that summary was
+    taken on other kernel sources."""
+    try:
+        with open(COUNTERS_FILE) as f:
+            t = json.load(f)
+    except OSError:
+        return None
+    if t.get("source_sha256") != kernel_source_sha():
+        return None
+    return t.get("kernels", {}).get(kernel)
+
+
+def short_kernel_name(full):
+    """'void (anonymous namespace)::decode_kernel<4, 2, true, 1, 1, 1>(...)'
+    -> 'decode_kernel<4, 2, true, 1, 1, 1>'."""
+    s = full.replace("(anonymous namespace)::", "").strip()
+    if s.startswith("void "):
+        s = s[5:]
+    s = s.split("(")[0].strip()
+    base, _, targs = s.partition("<")
+    return base.split("::")[-1] + ("<" + targs if targs else "")
+
+
+def summarise_counters(dirs):
+    """Per-dispatch means of FETCH_SIZE, WRITE_SIZE (KiB) and SQ_INSTS_VALU per
+    kernel over rocprofv3 counter-collection CSVs; HBM bytes scaled by the
+    readings for the bench's 256 MiB device-to-device copy (read and written
+    once: 2^28 bytes each way)."""
+    import csv
+    import glob
+    import statistics
+    vals = {}
+    for d in dirs:
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                for r in csv.DictReader(f):
+                    key = (short_kernel_name(r["Kernel_Name"]), r["Counter_Name"])
+                    vals.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
+                    vals[key][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    per = {}
+    for (k, c), d in vals.items():
+        per.setdefault(k, {})[c] = (statistics.mean(d.values()), len(d))
+    # the copy: the kernel whose fetch per dispatch is closest to 256 MiB
+    copies = [(abs(v["FETCH_SIZE"][0] - 262144.0), k) for k, v in per.items()
+              if "FETCH_SIZE" in v and "WRITE_SIZE" in v]
+    ref = min(copies)[1]
+    f_fetch = 262144.0 / per[ref]["FETCH_SIZE"][0]
+    f_write = 262144.0 / per[ref]["WRITE_SIZE"][0]
+    out = {"source_sha256": kernel_source_sha(), "copy_kernel": ref,
+           "copy_fetch_kib": round(per[ref]["FETCH_SIZE"][0], 1),
+           "copy_write_kib": round(per[ref]["WRITE_SIZE"][0], 1),
+           "scale_fetch": round(f_fetch, 5), "scale_write": round(f_write, 5), "kernels": {}}
+    for k, v in sorted(per.items()):
+        if "FETCH_SIZE" not in v or "WRITE_SIZE" not in v:
+            continue
+        e = {"fetch_kib": round(v["FETCH_SIZE"][0], 1), "write_kib": round(v["WRITE_SIZE"][0], 1),
+             "dispatches": v["FETCH_SIZE"][1],
+             "hbm_bytes": round(1024.0 * (f_fetch * v["FETCH_SIZE"][0] +
+                                          f_write * v["WRITE_SIZE"][0]))}
+        if "SQ_INSTS_VALU" in v:
+            e["valu_insts"] = round(v["SQ_INSTS_VALU"][0])
+        out["kernels"][k] = e
+    with open(COUNTERS_FILE, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    print(json.dumps(out, indent=1, sort_keys=True))
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def run_env():
@@ -217,24 +340,6 @@ def gpu_clocks():
                 out[key] = levels  # a trailing '*' marks the current level
                 break
     return out
-
-
-def traffic_per_launch(op, fmt_name="e4m3"):
-    """HBM bytes of one launch of `op`'s decode kernel, from the committed
-    FETCH_SIZE / WRITE_SIZE counter summary, scaled by the counters' readings
-    for a copy of known size; None if that summary was taken on another
-    version of the kernel source."""
-    try:
-        with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-        with open(KERNEL_SOURCE, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
-    except OSError:
-        return None
-    key = op if fmt_name == "e4m3" else f"{fmt_name}.{op}"
-    if t.get("source_sha256") != sha or key not in t.get("kernels", {}):
-        return None
-    return t["kernels"][key]["hbm_bytes"]
 
 
 def run_stack(args):
@@ -378,52 +483,66 @@ def run_small(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     rows = []
+
+    def time_op(fn, lays):
+        for i in range(args.warmup):
+            fn(lays[i % len(lays)])
+        ev = []
+        for i in range(args.steps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn(lays[i % len(lays)])
+            e1.record()
+            ev.append((e0, e1))
+        torch.cuda.synchronize()
+        return [1000.0 * a.elapsed_time(b) for a, b in ev]
+
     for cfg in (1, 2, 3):
         specs = config_matrices(cfg)
-        for spec, w, blob, lays in build_layers(eq, synth, specs, args.copies, dev):
-            del w
-            info = blob_info(blob)
+        for item in build_layers(eq, synth, specs, args.copies, dev, v2_copies=args.copies):
+            spec = item["spec"]
             out = torch.empty(spec.params, dtype=torch.int16, device=dev)
             x = torch.from_numpy(synth.activations(spec, 1).view(np.int16)).to(dev)
             y = torch.empty(1, spec.rows, dtype=torch.float32, device=dev)
-            ws = lays[0].workspace(1)
-            fns = {"bf16": lambda L: eq.eq_decode_bf16(L, out),
-                   "gemv1": lambda L: eq.eq_decode_gemv(L, x, 1, None, y, ws)}
-            for op, fn in fns.items():
-                for i in range(args.warmup):
-                    fn(lays[i % len(lays)])
-                ev = []
-                for i in range(args.steps):
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record()
-                    fn(lays[i % len(lays)])
-                    e1.record()
-                    ev.append((e0, e1))
-                torch.cuda.synchronize()
-                ts = [1000.0 * a.elapsed_time(b) for a, b in ev]
-                us = sum(ts) / len(ts)
-                nbytes = algorithmic_bytes(info, op, 1)
-                rows.append({"config": cfg, "matrix": spec.name, "shape": [spec.rows, spec.cols],
-                             "chunk_syms": spec.chunk_syms, "lanes": spec.lanes,
-                             "entropy_bits": round(info["entropy"], 4),
-                             "container_mb": round(info["file_bytes"] / 1e6, 3), "op": op,
-                             "us": round(us, 2),
-                             "us_p50": round(float(np.percentile(ts, 50)), 2),
-                             "gparams_per_s": round(spec.params / us / 1e3, 1),
-                             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)})
-                print(f"[bench] config {cfg} {spec.name} {op}: {us:.1f} us", file=sys.stderr,
-                      flush=True)
-            for L in lays:
-                if eq.eq_get_status(L) != eq.EQ_OK:
-                    raise RuntimeError("decode status not OK")
-            del lays, out
+            for version, blob, lays in ((1, item["blob"], item["layers"]),
+                                        (2, item["blob2"], item["layers2"])):
+                info = blob_info(blob)
+                ws = lays[0].workspace(1)
+                fns = {"bf16": lambda L: eq.eq_decode_bf16(L, out),
+                       "gemv1": lambda L, ws=ws: eq.eq_decode_gemv(L, x, 1, None, y, ws)}
+                for op, fn in fns.items():
+                    ts = time_op(fn, lays)
+                    us = sum(ts) / len(ts)
+                    nbytes = algorithmic_bytes(info, op, 1)
+                    rows.append({"config": cfg, "matrix": spec.name,
+                                 "shape": [spec.rows, spec.cols], "container": version,
+                                 "chunk_syms": spec.chunk_syms, "lanes": spec.lanes,
+                                 "entropy_bits": round(info["entropy"], 4),
+                                 "container_mb": round(info["file_bytes"] / 1e6, 3), "op": op,
+                                 "us": round(us, 2),
+                                 "us_p50": round(float(np.percentile(ts, 50)), 2),
+                                 "gparams_per_s": round(spec.params / us / 1e3, 1),
+                                 "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)})
+                    print(f"[bench] config {cfg} {spec.name} v{version} {op}: {us:.1f} us",
+                          file=sys.stderr, flush=True)
+                for L in lays:
+                    if eq.eq_get_status(L) != eq.EQ_OK:
+                        raise RuntimeError("decode status not OK")
+            del item, out
             torch.cuda.empty_cache()
-    params = sum(r["shape"][0] * r["shape"][1] for r in rows if r["op"] == "gemv1")
-    us_gemv = sum(r["us"] for r in rows if r["op"] == "gemv1")
+    # headline: the faster container per matrix for the batch-1 GEMV
+    best = {}
+    for r in rows:
+        if r["op"] == "gemv1":
+            k = (r["config"], r["matrix"])
+            if k not in best or r["us"] < best[k]["us"]:
+                best[k] = r
+    params = sum(r["shape"][0] * r["shape"][1] for r in best.values())
+    us_gemv = sum(r["us"] for r in best.values())
     print(json.dumps({
         "metric": "decoded Gparams/s, configs 1-3, fused decode-GEMV B=1 over every matrix "
-                  "(launches timed one by one)",
+                  "(launches timed one by one; the faster container version per matrix)",
         "value": round(params / us_gemv / 1e3, 1), "unit": "Gparams/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
         "vs_baseline": None, "dtype": "u32", "data": "synthetic",
@@ -457,7 +576,8 @@ def run_prefill(args):
     layers = build_layers(eq, synth, specs, 1, dev, fmt)
     B = args.tokens
     bufs = []
-    for spec, w, blob, lays in layers:
+    for item in layers:
+        spec, lays = item["spec"], item["layers"]
         x = torch.from_numpy(np.stack([synth.vector(spec.seed, 100 + t % 64, spec.cols)
                                        for t in range(B)]).view(np.int16)).to(dev)
         y = torch.empty(B, spec.rows, dtype=torch.float32, device=dev)
@@ -531,22 +651,36 @@ def run_prefill(args):
         "kernels": kernels}), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py: runs on one GPU only; --gpus {args.gpus} is not supported (several "
-              f"GPUs would each hold and decode their own output rows of every layer)",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.workload == "c5":
-        run_stack(args)
-        return
-    if args.workload == "prefill":
-        run_prefill(args)
-        return
-    if args.workload == "c123":
-        run_small(args)
-        return
+V2_KERNEL = {"gemv1": "decode2_kernel<4, 2, 1>", "gemv8": "decode2_kernel<4, 2, 8>",
+             "bf16": "decode2_kernel<4, 1, 1>", "codes": "decode2_kernel<4, 0, 1>"}
+TARGET_FRAC = 0.60  # fused decode-GEMV B=1 on 8192x28672, compressed bytes / HBM peak
+
+
+def time_eager(fn, n, reps):
+    """Mean, p50 and all per-launch times (us) of fn(i) for i < reps, each
+    bracketed by HIP events on the current stream (the library's stream)."""
+    import numpy as np
+    import torch
+    ev = []
+    for i in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn(i)
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ts = [1000.0 * e0.elapsed_time(e1) for e0, e1 in ev]
+    return float(np.mean(ts)), float(np.median(ts)), ts
+
+
+def compressed_bytes(info):
+    return info["file_bytes"] - 2 * (info["padded_words"] - info["total_words"])
+
+
+def run_c4(args):
+    import math
+
     import numpy as np
     import torch
 
@@ -559,35 +693,46 @@ def main():
     torch.cuda.set_device(dev)
     specs = config_matrices(4)
     fmt = FORMATS[args.base_format]
-    alg_ops = ALG_OPS if fmt == 1 else ALG_OPS_INT8
     kernel_names = KERNEL if fmt == 1 else KERNEL_INT8
-    layers = build_layers(eq, synth, specs, args.copies, dev, fmt)
+    layers = build_layers(eq, synth, specs, args.copies, dev, fmt, v2_copies=args.copies)
     ops = ["bf16", "gemv1", "gemv8"]
+    copies = args.copies
 
     # device buffers shared by all steps
     wouts = [torch.empty(spec.params, dtype=torch.int16, device=dev) for spec in specs]
+    codes_out = torch.empty(max(s.params for s in specs), dtype=torch.uint8, device=dev)
     bufs = []
-    for spec, w, blob, lays in layers:
+    for item in layers:
+        spec = item["spec"]
         d = {}
         for B in (1, 8):
             x = torch.from_numpy(synth.activations(spec, B).view(np.int16)).to(dev)
             y = torch.empty(B, spec.rows, dtype=torch.float32, device=dev)
-            d[B] = (x, y, lays[0].workspace(B))
+            d[B] = (x, y, item["layers"][0].workspace(B), item["layers2"][0].workspace(B))
         bufs.append(d)
-    infos = [blob_info(blob) for _, _, blob, _ in layers]
+    infos = [blob_info(item["blob"]) for item in layers]
+    infos2 = [blob_info(item["blob2"]) for item in layers]
     ALL = -1  # launch covering both matrices
 
     # One step: the layer's two matrices decoded to BF16 by one block-wise
     # launch (they are decompressed together, as a block's weights are),
     # then the fused GEMVs of each matrix at B = 1 and B = 8 (the two
-    # matrices read different inputs, so they are separate launches).
+    # matrices read different inputs, so they are separate launches).  Every
+    # read of a matrix takes the next of its device copies (read k of step s:
+    # copy (3 s + k) mod copies), so no launch finds its container in the
+    # MALL from the launch before.
+    reads = 3
+    period = copies // math.gcd(reads, copies)
+
     def launches(s):
-        Ls = [lays[s % len(lays)] for _, _, _, lays in layers]
-        yield ALL, "bf16", lambda: eq.eq_decode_bf16_multi(Ls, wouts)
-        for mi, L in enumerate(Ls):
-            for op in ("gemv1", "gemv8"):
+        def lay(item, k):
+            return item["layers"][(reads * s + k) % copies]
+        yield ALL, "bf16", lambda: eq.eq_decode_bf16_multi([lay(it, 0) for it in layers], wouts)
+        for mi, item in enumerate(layers):
+            for k, op in ((1, "gemv1"), (2, "gemv8")):
                 B = 1 if op == "gemv1" else 8
-                x, y, ws = bufs[mi][B]
+                x, y, ws, _ = bufs[mi][B]
+                L = lay(item, k)
                 yield mi, op, (lambda L=L, x=x, B=B, y=y, ws=ws:
                                eq.eq_decode_gemv(L, x, B, None, y, ws))
 
@@ -617,28 +762,31 @@ def main():
     copy_gbs = 2 * ref_src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del ref_src, ref_dst
 
+    def check_status():
+        for item in layers:
+            for L in item["layers"] + item["layers2"]:
+                rc = eq.eq_get_status(L)
+                if rc != eq.EQ_OK:
+                    raise RuntimeError(f"decode status {eq.eq_strerror(rc)}")
+
     for s in range(args.warmup):
         one_step(s)
     torch.cuda.synchronize()
-    for _, _, _, lays in layers:
-        for L in lays:
-            rc = eq.eq_get_status(L)
-            if rc != eq.EQ_OK:
-                raise RuntimeError(f"decode status {eq.eq_strerror(rc)}")
+    check_status()
 
-    # The step as a serving loop would run it: one HIP graph per container
-    # copy (the library's calls only launch kernels, so they capture), replayed
-    # in rotation.  Per-launch figures come from an eager pass afterwards.
-    copies = len(layers[0][3])
+    # The step as a serving loop would run it: one HIP graph per position in
+    # the copy rotation (the library's calls only launch kernels, so they
+    # capture), replayed in order.  Per-launch figures come from an eager
+    # pass afterwards.
     graphs = []
     if not args.eager:
-        for c in range(copies):
+        for c in range(period):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 one_step(c)
             graphs.append(g)
-        for s in range(copies):
-            graphs[s].replay()
+        for c in range(period):
+            graphs[c].replay()
     timers = []
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
@@ -647,7 +795,7 @@ def main():
     t_start.record()
     for s in range(args.steps):
         if graphs:
-            graphs[(args.warmup + s) % copies].replay()
+            graphs[(args.warmup + s) % period].replay()
         else:
             one_step(args.warmup + s, timers)
     t_end.record()
@@ -659,11 +807,7 @@ def main():
         for s in range(args.steps):
             one_step(args.warmup + s, timers)
         torch.cuda.synchronize()
-    for _, _, _, lays in layers:
-        for L in lays:
-            rc = eq.eq_get_status(L)
-            if rc != eq.EQ_OK:
-                raise RuntimeError(f"decode status {eq.eq_strerror(rc)}")
+    check_status()
 
     per = {}
     for mi, op, e0, e1 in timers:
@@ -678,24 +822,19 @@ def main():
         q10, q50, q90 = (1000.0 * float(v) for v in np.percentile(ts, [10, 50, 90]))
         params = sum(specs[m].params for m in covered)
         nbytes = sum(algorithmic_bytes(infos[m], op, B) for m in covered)
-        comp = sum(infos[m]["file_bytes"] - 2 * (infos[m]["padded_words"] - infos[m]["total_words"])
-                   for m in covered)
-        ops_alg = alg_ops[op] * params
-        tops = ops_alg / us / 1e6
+        comp = sum(compressed_bytes(infos[m]) for m in covered)
         kernels[f"{name}.{op}"] = {
-            "us": round(us, 2), "us_p10": round(q10, 2), "us_p50": round(q50, 2),
-            "us_p90": round(q90, 2), "params": params,
+            "kernel": kernel_names[op], "us": round(us, 2), "us_p10": round(q10, 2),
+            "us_p50": round(q50, 2), "us_p90": round(q90, 2), "params": params,
             "gparams_per_s": round(params / us / 1e3, 1),
             "alg_bytes": nbytes, "gbs": round(nbytes / us / 1e3, 1),
             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
-            "hbm_frac_compressed": round(comp / us / 1e3 / HBM_PEAK_GBS, 4),
-            "alg_ops_per_param": alg_ops[op], "tops": round(tops, 2),
-            "alu_frac": round(tops / ALU_PEAK_TOPS, 4)}
-        f = fam.setdefault(op, {"us": 0.0, "launches": 0, "bytes": 0, "ops": 0.0})
+            "hbm_frac_compressed": round(comp / us / 1e3 / HBM_PEAK_GBS, 4)}
+        f = fam.setdefault(op, {"us": 0.0, "launches": 0, "bytes": 0, "params": 0})
         f["us"] += us
         f["launches"] += 1
         f["bytes"] += nbytes
-        f["ops"] += ops_alg
+        f["params"] += params
     # dominant kernel: the op family with the largest share of the step;
     # figures per launch (mean over the family's launches)
     dom = max(fam, key=lambda k: fam[k]["us"])
@@ -703,11 +842,61 @@ def main():
     dom_us = fd["us"] / fd["launches"]
     dom_bytes = fd["bytes"] / fd["launches"]
     achieved_gbs = fd["bytes"] / fd["us"] / 1e3
-    achieved_tops = fd["ops"] / fd["us"] / 1e6
+
+    # Container version 2 (tiles of 256 x 256, one phrase of 1-4 codes per
+    # state update) of the same codes: every op timed launch by launch over
+    # the rotated copies.
+    v2 = {}
+    for mi, item in enumerate(layers):
+        spec, L2 = item["spec"], item["layers2"]
+        out = wouts[mi]
+        fns = {"gemv1": lambda i, mi=mi, L2=L2: eq.eq_decode_gemv(
+                   L2[i % copies], bufs[mi][1][0], 1, None, bufs[mi][1][1], bufs[mi][1][3]),
+               "gemv8": lambda i, mi=mi, L2=L2: eq.eq_decode_gemv(
+                   L2[i % copies], bufs[mi][8][0], 8, None, bufs[mi][8][1], bufs[mi][8][3]),
+               "bf16": lambda i, L2=L2, out=out: eq.eq_decode_bf16(L2[i % copies], out),
+               "codes": lambda i, L2=L2, n=spec.params: eq.eq_decode_codes(
+                   L2[i % copies], codes_out[:n])}
+        for op, fn in fns.items():
+            for i in range(args.warmup):
+                fn(i)
+            us, p50, _ = time_eager(fn, copies, max(args.steps, 20))
+            B = 8 if op == "gemv8" else 1
+            nbytes = (algorithmic_bytes(infos2[mi], op, B) if op != "codes"
+                      else compressed_bytes(infos2[mi]) + spec.params)
+            v2[f"{spec.name}.{op}"] = {
+                "kernel": V2_KERNEL[op], "us": round(us, 2), "us_p50": round(p50, 2),
+                "gparams_per_s": round(spec.params / us / 1e3, 1), "alg_bytes": nbytes,
+                "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+                "hbm_frac_compressed": round(compressed_bytes(infos2[mi]) / us / 1e3 /
+                                             HBM_PEAK_GBS, 4)}
+    check_status()
+
+    # The target row: fused decode-GEMV at batch 1 on the 8192x28672 matrix,
+    # compressed bytes over the launch time against the HBM peak.
+    tr = {}
+    for version, info, us in ((1, infos[0], kernels["down.gemv1"]["us"]),
+                              (2, infos2[0], v2["down.gemv1"]["us"])):
+        cb = compressed_bytes(info)
+        tr[str(version)] = {"us": us, "compressed_bytes": cb,
+                            "bits_per_param": round(8 * info["file_bytes"] / specs[0].params, 4),
+                            "gbs": round(cb / us / 1e3, 1),
+                            "frac": round(cb / us / 1e3 / HBM_PEAK_GBS, 4)}
+    best = min(tr, key=lambda k: tr[k]["us"])
+    target_row = {"shape": [specs[0].rows, specs[0].cols], "op": "fused decode-GEMV, batch 1",
+                  "container": int(best), "kernel": (V2_KERNEL["gemv1"] if best == "2"
+                                                     else kernel_names["gemv1"]),
+                  "us": tr[best]["us"], "frac": tr[best]["frac"], "target_frac": TARGET_FRAC,
+                  "entropy_bits": round(infos[0]["entropy"], 4), "by_container": tr}
+    tc = kernel_counters(target_row["kernel"])
+    target_row["traffic"] = tc.get("hbm_bytes") if tc else None
+    if tc and "valu_insts" in tc:
+        target_row["valu_lane_ops_per_param"] = round(64.0 * tc["valu_insts"] / specs[0].params,
+                                                      2)
 
     params_per_step = sum(s.params for s in specs) * len(ops)
     value = params_per_step / (ms_per_step * 1e-3) / 1e9
-
+    counters = kernel_counters(kernel_names[dom])
     result = {
         "metric": "decoded Gparams/s (decode->BF16 + fused decode-GEMV B=1,8 over the "
                   "8192x28672 and 28672x8192 layers); per-kernel us/layer and % HBM roofline",
@@ -716,30 +905,59 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
         "config": {"workload": f"Llama-70B MLP layers 8192x28672 + 28672x8192, "
                                f"{args.base_format.upper()} at ~2.0 "
-                               "bits/param, 65536-symbol chunks, 256 rANS lanes/chunk; per step: "
-                               "both matrices decoded to BF16 by one block-wise launch, then "
-                               "fused decode-GEMV B=1 and B=8 per matrix",
+                               "bits/param, 65536-symbol chunks, 256 rANS lanes/chunk "
+                               "(container version 1); per step: both matrices decoded to BF16 "
+                               "by one block-wise launch, then fused decode-GEMV B=1 and B=8 per "
+                               "matrix",
                    "base_format": args.base_format,
                    "entropy_bits": [round(i["entropy"], 4) for i in infos],
                    "container_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos],
-                   "copies_rotated": args.copies,
-                   "launch": "eager" if args.eager else "HIP graph of the step, one per container copy"},
-        "roofline": {"bound": "alu", "kernel": kernel_names[dom], "op": dom,
-                     "achieved": round(achieved_tops, 2), "peak": round(ALU_PEAK_TOPS, 2),
-                     "unit": "Tops/s", "frac": round(achieved_tops / ALU_PEAK_TOPS, 4),
-                     "traffic": traffic_per_launch(dom, args.base_format),
-                     "alg_bytes": round(dom_bytes), "us_per_launch": round(dom_us, 2),
-                     "hbm": {"achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS,
-                             "unit": "GB/s", "frac": round(achieved_gbs / HBM_PEAK_GBS, 4)}},
+                   "container_v2_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos2],
+                   "copies_rotated": copies,
+                   "launch": "eager" if args.eager else "HIP graphs of the step"},
+        "roofline": {"bound": "hbm", "kernel": kernel_names[dom], "op": dom,
+                     "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": counters.get("hbm_bytes") if counters else None,
+                     "alg_bytes": round(dom_bytes), "us_per_launch": round(dom_us, 2)},
+        "target_row": target_row,
         "kernels": kernels,
+        "container_v2": v2,
         "copy_reference_gbs": round(copy_gbs, 1),
         "wall_s_timed": round(wall, 3),
         "env": run_env(),
     }
+    if counters and "valu_insts" in counters:
+        # secondary: vector-ALU issue of the dominant kernel from its measured
+        # SQ_INSTS_VALU (wave instructions, 64 lanes each) per launch
+        lane_ops = 64.0 * counters["valu_insts"]
+        result["roofline"]["alu"] = {
+            "lane_ops_per_param": round(lane_ops / (fd["params"] / fd["launches"]), 2),
+            "achieved_tops": round(lane_ops / dom_us / 1e6, 2), "peak_tops": round(ALU_PEAK_TOPS, 2),
+            "frac": round(lane_ops / dom_us / 1e6 / ALU_PEAK_TOPS, 4)}
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
         result["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds, threads, fmt)
     print(json.dumps(result), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: runs on one GPU only; --gpus {args.gpus} is not supported (several "
+              f"GPUs would each hold and decode their own output rows of every layer)",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.counters_from:
+        summarise_counters(args.counters_from)
+    elif args.workload == "c5":
+        run_stack(args)
+    elif args.workload == "prefill":
+        run_prefill(args)
+    elif args.workload == "c123":
+        run_small(args)
+    else:
+        run_c4(args)
 
 
 if __name__ == "__main__":

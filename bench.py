@@ -258,20 +258,22 @@ def summarise_counters(dirs):
     import csv
     import glob
     import statistics
-    vals = {}
+    vals, full = {}, {}
     for d in dirs:
         for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             with open(path) as f:
                 for r in csv.DictReader(f):
-                    key = (short_kernel_name(r["Kernel_Name"]), r["Counter_Name"])
+                    short = short_kernel_name(r["Kernel_Name"])
+                    full[short] = r["Kernel_Name"]
+                    key = (short, r["Counter_Name"])
                     vals.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
                     vals[key][r["Dispatch_Id"]] += float(r["Counter_Value"])
     per = {}
     for (k, c), d in vals.items():
         per.setdefault(k, {})[c] = (statistics.mean(d.values()), len(d))
-    # the copy: the kernel whose fetch per dispatch is closest to 256 MiB
+    # the copy: torch's elementwise copy kernel, 256 MiB each way
     copies = [(abs(v["FETCH_SIZE"][0] - 262144.0), k) for k, v in per.items()
-              if "FETCH_SIZE" in v and "WRITE_SIZE" in v]
+              if "FETCH_SIZE" in v and "WRITE_SIZE" in v and "copy_kernel" in full[k]]
     ref = min(copies)[1]
     f_fetch = 262144.0 / per[ref]["FETCH_SIZE"][0]
     f_write = 262144.0 / per[ref]["WRITE_SIZE"][0]
@@ -748,10 +750,12 @@ def run_c4(args):
                 e1.record()
                 timers.append((mi, op, e0, e1))
 
-    # Reference: a plain device-to-device copy of 256 MiB, the known-size
-    # kernel against which HBM byte counters are calibrated.
+    # Reference: a plain elementwise copy of 256 MiB (uint8 to int8, so that
+    # it runs as torch's copy kernel rather than a runtime blit shared with
+    # the uploads), the known-size kernel against which HBM byte counters are
+    # calibrated.
     ref_src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-    ref_dst = torch.empty_like(ref_src)
+    ref_dst = torch.empty(256 << 20, dtype=torch.int8, device=dev)
     ref_dst.copy_(ref_src)
     c0 = torch.cuda.Event(enable_timing=True)
     c1 = torch.cuda.Event(enable_timing=True)

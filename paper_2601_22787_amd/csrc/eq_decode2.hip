@@ -58,6 +58,10 @@ constexpr uint32_t kIdentity2 = kBuckets * 8;
 // at kCodesHalf + bucket * 4 (the identity's after the kBuckets).
 constexpr uint32_t kCodesHalf = kBuckets * 8 + 8;
 constexpr uint32_t kTableCodes2 = (kCodesHalf + kBuckets * 4 + 4 + 15) / 16 * 16;
+// Packed table (layers of more than one phrase; GEMV on E4M3 codes): one
+// 8-byte entry per bucket, {F | (cum + length) << 16, the four codes}, and
+// the identity {0, 0} after them.
+constexpr uint32_t kTablePacked2 = kBuckets * 8 + 16;
 // Codes and BF16 output leave the wavefront as whole 64-code segments of a
 // row (a 128-byte line of BF16): each tile row has an LDS ring holding its
 // current segment and 4 bytes more, where a phrase that crosses the
@@ -82,6 +86,7 @@ struct Args2 {
   const uint16_t *x;
   uint32_t batch;
   uint32_t fmt;              // base format (codes to values at BF16 output)
+  uint32_t n_syms;           // phrases in the alphabet
   const uint16_t *bias;
   float *y;
   float *ws;                 // partial row sums [batch][NT][rows] (NT > 1)
@@ -95,6 +100,20 @@ __device__ inline uint32_t state_update(uint32_t x, uint32_t ex, uint32_t ey) {
   return x - t;
 }
 
+// Packed entry w = F | (cum + length) << 16 (cum has its low 16 - R >= 4
+// bits zero, so the length 1, 2 or 4 sits there):
+//   t = (x mod 2^16) - (cum + length)     one subtraction of selected halves
+//   x' = F (x >> 16) + t + length         multiply-add, then the length back
+__device__ inline uint32_t state_update_pk(uint32_t x, uint32_t w) {
+  uint32_t t, y;
+  asm("v_sub_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
+      "src1_sel:WORD_1"
+      : "=v"(t)
+      : "v"(x), "v"(w));
+  asm("v_mad_u32_u16 %0, %1, %2, %3 op_sel:[0,1,0,0]" : "=v"(y) : "v"(w), "v"(x), "v"(t));
+  return y + ((w >> 16) & 7u);
+}
+
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -106,9 +125,12 @@ __device__ inline uint32_t bucket_addr(uint32_t x) { return (x >> 1) & 0x7FF8u; 
 __device__ inline u32x2 state_half(uint32_t addr) { return *(lds_u32x2 *)(addr); }
 __device__ inline u32x2 value_half(uint32_t addr) { return *(lds_u32x2 *)(addr + kValHalf); }
 
-template <int G, int MODE, int NB>
+template <int G, int MODE, int NB, bool PK>
 struct Tile {
   static constexpr uint32_t TR = G * kWave;
+  // log2 of the position step per code (packed entries hold the length)
+  static constexpr uint32_t kUnitShift =
+      MODE != kGemv2 ? 0 : (NB == 1 ? 3 : (NB == 2 ? 3 : (NB == 4 ? 4 : 5)));
   const Args2 &a;
   uint32_t lane, c, r0, c0, rows, cols, tcol;
   int nb;
@@ -265,9 +287,28 @@ struct Tile {
 
   // es: state half (.x high half = the position step in this kernel's units),
   // ev: value half (BF16 pairs, or the codes).
+  // The entry of bucket address ba (state half; the value half unless PK).
+  __device__ __forceinline__ void fetch(uint32_t ba, u32x2 &es, u32x2 &ev) {
+    es = state_half(ba);
+    if (!PK) ev = value_of(ba);
+  }
+  __device__ __forceinline__ uint32_t update(uint32_t xs, u32x2 es) {
+    return PK ? state_update_pk(xs, es.x) : state_update(xs, es.x, es.y);
+  }
+  // The phrase's values from a packed entry: BF16 pairs (GEMV; E4M3 codes
+  // converted in hardware, whose fp32 values are exact in BF16) or the codes.
+  __device__ __forceinline__ u32x2 values(u32x2 es, u32x2 ev) {
+    if (!PK) return ev;
+    if (MODE != kGemv2) return u32x2{es.y, 0u};
+    const float2v lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(es.y), false);
+    const float2v hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(es.y), true);
+    return u32x2{__builtin_amdgcn_perm(__float_as_uint(lo.y), __float_as_uint(lo.x), 0x07060302u),
+                 __builtin_amdgcn_perm(__float_as_uint(hi.y), __float_as_uint(hi.x), 0x07060302u)};
+  }
+
   template <bool WIDE>
   __device__ __forceinline__ void use(int g, u32x2 es, u32x2 ev, const u32x2 (&xv)[NX]) {
-    const uint32_t step = es.x >> 16;
+    const uint32_t step = PK ? ((es.x >> 16) & 7u) << kUnitShift : es.x >> 16;
     if (MODE == kGemv2) {
 #pragma unroll
       for (int bb = 0; bb < NX; ++bb)
@@ -302,12 +343,14 @@ struct Tile {
       for (int g = 0; g < G; ++g)
         if (!MASKED || act[g]) read_x(g, xv[g]);
     }
+    if (!PK) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (!MASKED || act[g]) ev[g] = value_of(ba[g]);
+    }
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      if (!MASKED || act[g]) ev[g] = value_of(ba[g]);
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      if (!MASKED || act[g]) x[g] = state_update(x[g], es[g].x, es[g].y);
+      if (!MASKED || act[g]) x[g] = update(x[g], es[g]);
     // renormalise in ascending state order (state g * 64 + lane)
     uint64_t need[G];
     uint32_t word[G];
@@ -322,7 +365,7 @@ struct Tile {
     }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      if (!MASKED || act[g]) use<!MASKED>(g, es[g], ev[g], xv[g]);
+      if (!MASKED || act[g]) use<!MASKED>(g, es[g], values(es[g], ev[g]), xv[g]);
       else cr[g] = false;
     }
 #pragma unroll
@@ -480,11 +523,14 @@ struct Tile {
     }
     pes[g] = state_half(ba);
     if (MODE == kGemv2) read_x(g, pxv[g]);
-    pev[g] = value_of(ba);
+    if (!PK) pev[g] = value_of(ba);
   }
-  template <int g>
+  template <int g, bool MASK>
   __device__ __forceinline__ void p_update() {
-    x[g] = state_update(x[g], pes[g].x, pes[g].y);
+    // a packed identity entry does not leave the state as it is: a finished
+    // state keeps its value
+    const uint32_t xn = update(x[g], pes[g]);
+    x[g] = PK && MASK ? (pact[g] ? xn : x[g]) : xn;
     pneed[g] = __builtin_amdgcn_ballot_w64(x[g] < 0x10000u);
     const uint32_t below = __builtin_amdgcn_mbcnt_hi(
         uint32_t(pneed[g] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(pneed[g]), 0u));
@@ -493,7 +539,7 @@ struct Tile {
   }
   template <int g>
   __device__ __forceinline__ void p_finish() {
-    use<true>(g, pes[g], pev[g], pxv[g]);
+    use<true>(g, pes[g], values(pes[g], pev[g]), pxv[g]);
     x[g] = renorm_lanes(pneed[g], x[g], pword[g]);
   }
 
@@ -507,19 +553,19 @@ struct Tile {
     slide();
     p_finish<0>();
     p_issue<0, MASK>();
-    p_update<H>();
+    p_update<H, MASK>();
     p_finish<1 % G>();
     p_issue<1 % G, MASK>();
     if (G == 4) {
-      p_update<3 % G>();
+      p_update<3 % G, MASK>();
       p_finish<2 % G>();
       p_issue<2 % G, MASK>();
-      p_update<0>();
+      p_update<0, MASK>();
       p_finish<3 % G>();
       p_issue<3 % G, MASK>();
-      p_update<1 % G>();
+      p_update<1 % G, MASK>();
     } else {
-      p_update<0>();
+      p_update<0, MASK>();
     }
     flush();
   }
@@ -539,8 +585,8 @@ struct Tile {
       p_issue<2 % G, MASK>();
       p_issue<3 % G, MASK>();
     }
-    p_update<0>();
-    if (G == 4) p_update<1 % G>();
+    p_update<0, MASK>();
+    if (G == 4) p_update<1 % G, MASK>();
     const uint32_t n = T - 1;
     if (MASK) {
       for (uint32_t t = 0; t < n; ++t) {
@@ -565,10 +611,10 @@ struct Tile {
     }
     slide();
     p_finish<0>();
-    p_update<H>();
+    p_update<H, MASK>();
     p_finish<1 % G>();
     if (G == 4) {
-      p_update<3 % G>();
+      p_update<3 % G, MASK>();
       p_finish<2 % G>();
       p_finish<3 % G>();
     }
@@ -636,16 +682,23 @@ struct Tile {
   }
 };
 
-constexpr uint32_t table_bytes2(int mode) { return mode == kGemv2 ? kTableBytes2 : kTableCodes2; }
+constexpr uint32_t table_bytes2(int mode, bool pk) {
+  return pk ? kTablePacked2 : (mode == kGemv2 ? kTableBytes2 : kTableCodes2);
+}
 
-template <int G, int MODE, int NB>
+template <int G, int MODE, int NB, bool PK>
 __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(Args2 a) {
   extern __shared__ uint4 dyn2[];
   // the phrase table at LDS address 0 (no static LDS in this kernel), the
   // position step in this kernel's units: record bytes (GEMV at batch 1),
   // activation bytes (GEMV), codes (codes and BF16 output)
   char *tab = reinterpret_cast<char *>(dyn2);
-  for (uint32_t i = threadIdx.x; i < kBuckets; i += blockDim.x) {
+  for (uint32_t i = threadIdx.x; PK && i < kBuckets; i += blockDim.x) {
+    const uint4 e = a.lut[i];
+    const uint32_t len = e.x >> 17, F = 65536u - (e.x & 0xFFFFu);  // F < 2^16: K > 1
+    *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{F | ((e.y | len) << 16), a.codes4[i]};
+  }
+  for (uint32_t i = threadIdx.x; !PK && i < kBuckets; i += blockDim.x) {
     const uint4 e = a.lut[i];
     const uint32_t len = e.x >> 17;
     const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 4 * NB * len) : len;
@@ -657,25 +710,27 @@ __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(A
   }
   if (threadIdx.x == 0) {
     *reinterpret_cast<u32x2 *>(tab + kIdentity2) = u32x2{0u, 0u};
-    if (MODE == kGemv2)
+    if (PK) {
+    } else if (MODE == kGemv2)
       *reinterpret_cast<u32x2 *>(tab + kValHalf + kIdentity2) = u32x2{0u, 0u};
     else
       *reinterpret_cast<uint32_t *>(tab + kCodesHalf + kIdentity2 / 2) = 0u;
   }
   __syncthreads();
   const uint32_t nw = blockDim.x / kWave, wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  char *mine = tab + table_bytes2(MODE) + size_t(wave) * a.wave_lds;
+  char *mine = tab + table_bytes2(MODE, PK) + size_t(wave) * a.wave_lds;
   for (uint32_t c = uniform(blockIdx.x * nw + wave); c < a.n_chunks; c += gridDim.x * nw) {
-    Tile<G, MODE, NB> t(a, c, lane, mine);
+    Tile<G, MODE, NB, PK> t(a, c, lane, mine);
     t.run();
   }
 }
 
 // Rows split over NT > 1 column tiles: y = s * (partials added in tile
-// order) + bias.  Four threads per output: thread p sums tiles [p NT / 4,
-// (p + 1) NT / 4) in order (independent loads, so their latencies overlap),
-// then the four sums are added in order p = 0..3.
-constexpr int kMergeSplit = 4;
+// order) + bias.  kMergeSplit threads per output: thread p sums tiles
+// [p NT / kMergeSplit, (p + 1) NT / kMergeSplit) in order (independent loads,
+// so their latencies overlap), then the parts are added pairwise in a fixed
+// tree (deterministic).
+constexpr int kMergeSplit = 16;
 __global__ __launch_bounds__(256) void merge2_kernel(Args2 a) {
   const uint32_t i = (blockIdx.x * blockDim.x + threadIdx.x) / kMergeSplit;
   const uint32_t part = threadIdx.x % kMergeSplit;
@@ -692,12 +747,12 @@ __global__ __launch_bounds__(256) void merge2_kernel(Args2 a) {
     sum = (((sum + v0) + v1) + v2) + v3;
   }
   for (; t < t1; ++t) sum += p[size_t(t) * a.rows];
-  const uint32_t lane = threadIdx.x % kWave, base = lane & ~uint32_t(kMergeSplit - 1);
-  const float s0 = __shfl(sum, base), s1 = __shfl(sum, base + 1);
-  const float s2 = __shfl(sum, base + 2), s3 = __shfl(sum, base + 3);
+  // parts p and p + h for h = 1, 2, 4, 8 (within each group of kMergeSplit lanes)
+#pragma unroll
+  for (int h = 1; h < kMergeSplit; h *= 2) sum += __shfl_xor(sum, h);
   if (part == 0 && i < n) {
     const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
-    a.y[i] = bf16_to_f32(a.scale[row]) * (((s0 + s1) + s2) + s3) + bias;
+    a.y[i] = bf16_to_f32(a.scale[row]) * sum + bias;
   }
 }
 
@@ -762,6 +817,7 @@ Args2 make_args2(const eq_layer *L) {
   a.n_chunks = L->n_chunks;
   a.padded_words = static_cast<uint32_t>(L->padded_words);
   a.fmt = L->base_format;
+  a.n_syms = L->n_syms;
   return a;
 }
 
@@ -807,16 +863,14 @@ uint32_t wave_lds_bytes(int mode, const Args2 &a) {
 
 // One block per compute unit (the table takes most of LDS), as many
 // wavefronts as the chunks need for one round, at most what LDS holds.
-template <int MODE, int NB>
-int launch2(Args2 a, hipStream_t s) {
-  // output offsets from a tile's origin are 32-bit byte offsets
-  if (MODE != kGemv2 && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+template <int MODE, int NB, bool PK>
+int launch2_pk(Args2 a, hipStream_t s) {
   const Facts2 f = facts2();
   a.wave_lds = wave_lds_bytes(MODE, a);
   uint32_t waves = (a.n_chunks + f.cus - 1) / f.cus;
   constexpr uint32_t wmax = max_waves2(MODE, NB);
   waves = waves < 1 ? 1 : (waves > wmax ? wmax : waves);
-  const size_t tb = table_bytes2(MODE);
+  const size_t tb = table_bytes2(MODE, PK);
   while (waves > 1 && tb + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
   if (tb + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
   uint32_t blocks = (a.n_chunks + waves - 1) / waves;
@@ -824,11 +878,25 @@ int launch2(Args2 a, hipStream_t s) {
   const size_t shm = tb + size_t(waves) * a.wave_lds;
   const dim3 grid(blocks), block(waves * kWave);
   switch (a.TR) {
-    case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB>), grid, block, shm, s, a); break;
-    case 128: hipLaunchKernelGGL((decode2_kernel<2, MODE, NB>), grid, block, shm, s, a); break;
-    default: hipLaunchKernelGGL((decode2_kernel<4, MODE, NB>), grid, block, shm, s, a); break;
+    case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB, PK>), grid, block, shm, s, a); break;
+    case 128: hipLaunchKernelGGL((decode2_kernel<2, MODE, NB, PK>), grid, block, shm, s, a); break;
+    default: hipLaunchKernelGGL((decode2_kernel<4, MODE, NB, PK>), grid, block, shm, s, a); break;
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+// Packed table entries for codes and BF16 output of layers of more than one
+// phrase (one phrase has F = 2^16, which does not fit the entry's 16 bits).
+// The GEMV keeps the split table: its phrase values as BF16 pairs cost no
+// conversion, and its update two instructions less, which on gfx950
+// outweighs the third LDS read per phrase (measured: 66 against 75 us on
+// the 8192 x 28672 matrix at batch 1).
+template <int MODE, int NB>
+int launch2(Args2 a, hipStream_t s) {
+  // output offsets from a tile's origin are 32-bit byte offsets
+  if (MODE != kGemv2 && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+  if (MODE != kGemv2 && a.n_syms > 1) return launch2_pk<MODE, NB, true>(a, s);
+  return launch2_pk<MODE, NB, false>(a, s);
 }
 
 size_t round256(size_t v) { return (v + 255) / 256 * 256; }

@@ -190,6 +190,18 @@ int eq_decode_gemv_noalloc(const eq_layer *L, const uint16_t *x, uint32_t B,
 int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
                          hipStream_t stream);
 
+/* Block-wise decompression to the base format (Sec. 2.2, "Block-Wise
+ * Decompression Pipeline": the paper decodes a block's weights into one
+ * Float8 buffer per device, which its W8A16 GEMM reads).  Decodes layers
+ * L[0..n-1] (host array of n views, 1 <= n <= 8) to one-byte codes: layer i
+ * to codes[i] (device, its M*N codes, as eq_decode_codes writes them), with
+ * identical results.  Layers of container version 1 whose rows are whole
+ * steps and that share one lane count and base format are decoded by one
+ * launch; otherwise each layer gets its own launch, in order.  The codes
+ * feed eq_gemm_codes. */
+int eq_decode_codes_multi(const eq_layer *const *L, uint8_t *const *codes, uint32_t n,
+                          hipStream_t stream);
+
 /* Workspace bytes eq_decode_gemv_multi needs: the sum of the layers'
  * eq_gemv_workspace_bytes(L[i], B); 0 if an argument is invalid. */
 size_t eq_gemv_multi_workspace_bytes(const eq_layer *const *L, uint32_t n, uint32_t B);

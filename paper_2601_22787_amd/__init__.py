@@ -76,6 +76,7 @@ SIGNATURES = {
     "eq_decode_gemv_noalloc": (ctypes.c_int, [ctypes.POINTER(eq_layer), _vp, ctypes.c_uint32, _vp,
                                               _vp, _vp]),
     "eq_decode_bf16_multi": (ctypes.c_int, [_vp, _vp, ctypes.c_uint32, _vp]),
+    "eq_decode_codes_multi": (ctypes.c_int, [_vp, _vp, ctypes.c_uint32, _vp]),
     "eq_gemv_multi_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_uint32, ctypes.c_uint32]),
     "eq_decode_gemv_multi": (ctypes.c_int, [_vp, ctypes.c_uint32, _vp, ctypes.c_uint32, _vp, _vp,
                                             _vp, ctypes.c_size_t, _vp]),
@@ -253,6 +254,17 @@ def eq_decode_bf16_multi(layers, outs, stream=None) -> None:
     ptrs = _ptr_array([_dptr(w, None, r.rows * r.cols) for w, r in zip(outs, raws)])
     _check("eq_decode_bf16_multi",
            lib().eq_decode_bf16_multi(arr, ptrs, len(raws), _stream(stream)))
+
+
+def eq_decode_codes_multi(layers, outs, stream=None) -> None:
+    """Block-wise decode of several layers to one-byte codes: layer i to outs[i]."""
+    import torch
+    if len(layers) != len(outs):
+        raise ValueError("one output per layer")
+    arr, raws = _layer_array(layers)
+    ptrs = _ptr_array([_dptr(c, torch.uint8, r.rows * r.cols) for c, r in zip(outs, raws)])
+    _check("eq_decode_codes_multi",
+           lib().eq_decode_codes_multi(arr, ptrs, len(raws), _stream(stream)))
 
 
 def eq_gemv_multi_workspace_bytes(layers, B: int) -> int:

@@ -1602,6 +1602,31 @@ extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w
   return launch_multi<kBf16, kXGlobal, 1>(m, 0, stream, device_facts());
 }
 
+extern "C" int eq_decode_codes_multi(const eq_layer *const *L, uint8_t *const *codes, uint32_t n,
+                                     hipStream_t stream) {
+  if (!L || !codes || n < 1 || n > kMaxLayers) return EQ_EINVAL;
+  bool v2 = false;
+  for (uint32_t i = 0; i < n; ++i) {
+    if (!L[i] || !codes[i]) return EQ_EINVAL;
+    v2 |= L[i]->version == 2;
+    if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
+  }
+  if (n == 1 || v2 || !joint_ok(L, n)) {
+    for (uint32_t i = 0; i < n; ++i) {
+      const int rc = eq_decode_codes(L[i], codes[i], stream);
+      if (rc != EQ_OK) return rc;
+    }
+    return EQ_OK;
+  }
+  MultiArgs m{};
+  m.n = n;
+  for (uint32_t i = 0; i < n; ++i) {
+    m.a[i] = make_args(L[i]);
+    m.a[i].codes = codes[i];
+  }
+  return launch_multi<kCodes, kXGlobal, 1>(m, 0, stream, device_facts());
+}
+
 extern "C" size_t eq_gemv_multi_workspace_bytes(const eq_layer *const *L, uint32_t n, uint32_t B) {
   if (!L || n < 1 || n > kMaxLayers) return 0;
   size_t total = 0;

@@ -5,8 +5,8 @@ of the config-5 stack (one per entropy class, all seven matrices) are
 compared element by element against the oracle, with no sampling:
   - codes (Alg. 2 lines 1-2) and BF16 weights (plus the dequantiser of
     Sec. 2.1) bit-exact, through the single-layer entry points and through
-    the block-wise launches the benchmark times (Sec. 2.2 block-wise
-    decompression);
+    the block-wise launches (Sec. 2.2 block-wise decompression: to BF16 as
+    the benchmark times it, and to one code buffer for the whole block);
   - the codes also equal the oracle quantiser applied to the generated
     weights;
   - every output of the fused GEMV (Alg. 2 line 3) within the normwise bar
@@ -116,10 +116,17 @@ def test_config4_whole_matrices(eq):
     Ls = [L for _, _, _, L in layers]
     outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev()) for L in Ls]
     eq.eq_decode_bf16_multi(Ls, outs)
-    for (spec, w, blob, L), out in zip(layers, outs):
+    # the pair's codes into one block buffer (one launch), as the prefill reads them
+    sizes = [L.rows * L.cols for L in Ls]
+    block = torch.full((sum(sizes) + 64,), 0xA5, dtype=torch.uint8, device=_dev())
+    views = [block[:sizes[0]], block[sizes[0]:sizes[0] + sizes[1]]]
+    eq.eq_decode_codes_multi(Ls, views)
+    assert (block[sum(sizes):] == 0xA5).all()
+    for (spec, w, blob, L), out, cv in zip(layers, outs, views):
         say("config 4 parity", spec.name)
         q_ref, w_ref = reference(w, blob)
         assert np.array_equal(gpu_codes(eq, L), q_ref), spec.name
+        assert np.array_equal(cv.cpu().numpy().reshape(L.rows, L.cols), q_ref), spec.name
         assert np.array_equal(to_np_bf16(out, L), w_ref), spec.name
         one = torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev())
         eq.eq_decode_bf16(L, one)
@@ -154,6 +161,13 @@ def test_config5_layer_whole(eq, layer):
     Ls = [built[n][2] for n in names]
     outs = [torch.full((L.rows * L.cols,), -1, dtype=torch.int16, device=_dev()) for L in Ls]
     eq.eq_decode_bf16_multi(Ls, outs)
+    # the whole layer's codes into one block buffer by one launch
+    sizes = [L.rows * L.cols for L in Ls]
+    block = torch.full((sum(sizes) + 64,), 0xA5, dtype=torch.uint8, device=_dev())
+    starts = np.cumsum([0] + sizes)
+    code_views = [block[starts[i]:starts[i + 1]] for i in range(len(Ls))]
+    eq.eq_decode_codes_multi(Ls, code_views)
+    assert (block[sum(sizes):] == 0xA5).all()
     ys = {}
     for i, (g, ncols) in enumerate(GROUPS):
         x_bits = synth.vector(0x5EED, 16 + i, ncols).reshape(1, ncols)
@@ -164,11 +178,12 @@ def test_config5_layer_whole(eq, layer):
         eq.eq_decode_gemv_multi(gl, x, 1, None, gy, eq.multi_workspace(gl, 1))
         for n, y in zip(g, gy):
             ys[n] = (x_bits, y.cpu().numpy())
-    for n, out in zip(names, outs):
+    for n, out, cv in zip(names, outs, code_views):
         w, blob, L = built[n]
         say("config 5 parity", layer, n)
         q_ref, w_ref = reference(w, blob)
         assert np.array_equal(gpu_codes(eq, L), q_ref), n
+        assert np.array_equal(cv.cpu().numpy().reshape(L.rows, L.cols), q_ref), n
         assert np.array_equal(to_np_bf16(out, L), w_ref), n
         one = torch.empty(L.rows * L.cols, dtype=torch.int16, device=_dev())
         eq.eq_decode_bf16(L, one)

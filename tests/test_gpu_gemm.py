@@ -238,3 +238,40 @@ def test_gemm_large_tiles_ragged(eq):
     blob = encode(eq, w, 3.0, 16384, 64, 1)
     L = eq.Layer(blob, _dev())
     _sampled(eq, spec, w, blob, L, 4100, 1, 99)
+
+
+def test_block_codes_buffer_feeds_gemm(eq):
+    """Sec. 2.2 block-wise pipeline: the codes of three layers into one block
+    buffer by one launch of eq_decode_codes_multi, then eq_gemm_codes from
+    that buffer:
+    codes bit-exact against the oracle, outputs equal to eq_decode_gemm's and
+    within the bar against the oracle's fp64 GEMM."""
+    shapes = [(200, 512, 4096, 64, 4200), (96, 512, 2048, 64, 4201), (64, 1024, 8192, 64, 4202)]
+    layers = []
+    for M, N, C, lanes, seed in shapes:
+        spec = small_spec(M, N, bits=2.5, chunk=C, lanes=lanes, seed=seed)
+        w = synth.weights(spec)
+        blob = encode(eq, w, 2.5, C, lanes, 1)
+        layers.append((spec, blob, eq.Layer(blob, _dev())))
+    sizes = [s.params for s, _, _ in layers]
+    block = torch.full((sum(sizes) + 64,), 0xA5, dtype=torch.uint8, device=_dev())
+    starts = np.cumsum([0] + sizes)
+    views = [block[starts[i]:starts[i + 1]] for i in range(len(layers))]
+    eq.eq_decode_codes_multi([L for _, _, L in layers], views)
+    assert (block[sum(sizes):] == 0xA5).all()
+    B = 24
+    for (spec, blob, L), cv in zip(layers, views):
+        rc, q_ref = oracle.container_decode(blob)
+        assert rc == oracle.OK
+        assert np.array_equal(cv.cpu().numpy().reshape(spec.rows, spec.cols), q_ref)
+        x_bits = tokens(spec, B)
+        x = torch.from_numpy(x_bits.view(np.int16)).to(_dev())
+        y = torch.full((B, spec.rows), float("nan"), dtype=torch.float32, device=_dev())
+        nws = eq.eq_gemm_codes_workspace_bytes(L, B)
+        ws = torch.empty(nws, dtype=torch.uint8, device=_dev()) if nws else None
+        eq.eq_gemm_codes(L, cv, x, B, None, y, ws)
+        yn = y.cpu().numpy()
+        assert np.array_equal(yn, gpu_gemm(eq, L, x_bits))
+        w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
+        assert (rel_err(yn, oracle.gemv(w_ref, x_bits)) <= TOL).all()
+        assert eq.eq_get_status(L) == eq.EQ_OK

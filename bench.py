@@ -69,6 +69,8 @@ def parse():
                          "every matrix of configs 1-3, decode to BF16 and decode-GEMV B=1; "
                          "prefill: the c4 pair at --tokens tokens, decode to codes + MFMA GEMM")
     ap.add_argument("--tokens", type=int, default=2048, help="prefill batch (tokens)")
+    ap.add_argument("--container", type=int, choices=(1, 2), default=1,
+                    help="c5 workload: container version of the stack's layers")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
     ap.add_argument("--base-format", choices=tuple(FORMATS), default="e4m3",
@@ -80,10 +82,18 @@ def parse():
     return ap.parse_args()
 
 
+def v2_tile_rows(chunk_syms):
+    """Tile rows of the version-2 containers for C-symbol chunks: 256 for
+    65536-symbol chunks (256 x 256 tiles), else 128 (two pipelined coder
+    states per lane; measured faster than 64 for the batch-1 GEMV on the
+    16384-symbol chunks of configs 2 and 3)."""
+    return 256 if chunk_syms >= 65536 else 128
+
+
 def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0):
     """Encode each matrix (product encoder) and upload `copies` device copies;
     with v2_copies > 0 also the same codes (same alpha) in container version
-    2, tiles of `lanes` rows x chunk_syms / lanes columns (the same symbols
+    2, tiles of v2_tile_rows(C) rows x C / rows columns (the same C symbols
     per chunk)."""
     out = []
     for spec in specs:
@@ -96,8 +106,8 @@ def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0):
         item = {"spec": spec, "w": w, "blob": blob, "layers": layers}
         msg = f"container {blob.size / 1e6:.1f} MB"
         if v2_copies:
-            blob2 = eq.eqe_encode2(w, alpha, tile_rows=spec.lanes,
-                                   tile_cols=spec.chunk_syms // spec.lanes,
+            tr = v2_tile_rows(spec.chunk_syms)
+            blob2 = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=spec.chunk_syms // tr,
                                    seed=spec.seed, target_bits=spec.target_bits,
                                    base_format=fmt)
             item["blob2"] = blob2
@@ -372,9 +382,14 @@ def run_stack(args):
         for spec in config_matrices(5, layers=[layer]):
             w = synth.weights(spec)
             alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
-            d[spec.name.split(".")[-1]] = (spec, eq.eqe_encode(
-                w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes, seed=spec.seed,
-                target_bits=spec.target_bits))
+            if args.container == 2:
+                tr = v2_tile_rows(spec.chunk_syms)
+                blob = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=spec.chunk_syms // tr,
+                                      seed=spec.seed, target_bits=spec.target_bits)
+            else:
+                blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
+                                     seed=spec.seed, target_bits=spec.target_bits)
+            d[spec.name.split(".")[-1]] = (spec, blob)
         proto.append(d)
         mb = sum(b.size for _, b in d.values()) / 1e6
         print(f"[bench] stack class {layer}: {mb:.0f} MB in {time.time() - t0:.1f}s",
@@ -460,7 +475,8 @@ def run_stack(args):
         "dtype": "u32", "data": "synthetic", "env": run_env(),
         "config": {"workload": "config 5: 80 layers x {q 8192x8192, k/v 1024x8192, o 8192x8192, "
                                "gate/up 28672x8192, down 8192x28672}, (2,3,4)[l mod 3] bits, "
-                               "65536-symbol chunks, 256 lanes; 3 distinct layers, 80 device copies",
+                               "65536-symbol chunks; 3 distinct layers, 80 device copies",
+                   "container": args.container,
                    "launch": "eager" if args.eager else "HIP graph of each 80-layer pass",
                    "params": params, "container_gb": round(cont_bytes / 1e9, 3),
                    "hbm_frac_compressed_block_gemv": round(

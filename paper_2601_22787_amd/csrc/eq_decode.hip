@@ -1656,6 +1656,11 @@ extern "C" int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const 
     off[i] = o;
     o += eq_gemv_workspace_bytes(L[i], B);
   }
+  if (v2 && v2_joint_ok(L, n)) {
+    void *wsi[kMaxLayers];
+    for (uint32_t i = 0; i < n; ++i) wsi[i] = static_cast<char *>(ws) + off[i];
+    return v2_decode_gemv_multi(L, n, x, B, bias, y, wsi, stream);
+  }
   const DeviceFacts f = device_facts();
   MultiArgs m{};
   m.n = n;

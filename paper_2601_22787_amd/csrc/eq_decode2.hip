@@ -28,6 +28,7 @@
 // added in tile order by merge2_kernel (deterministic).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "eq.h"
@@ -686,8 +687,10 @@ constexpr uint32_t table_bytes2(int mode, bool pk) {
   return pk ? kTablePacked2 : (mode == kGemv2 ? kTableBytes2 : kTableCodes2);
 }
 
+// The work of block `bid` of `nblocks` on layer a: stage the phrase table,
+// then each wavefront decodes chunks bid * nw + wave, + nblocks * nw, ...
 template <int G, int MODE, int NB, bool PK>
-__global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(Args2 a) {
+__device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint32_t nblocks) {
   extern __shared__ uint4 dyn2[];
   // the phrase table at LDS address 0 (no static LDS in this kernel), the
   // position step in this kernel's units: record bytes (GEMV at batch 1),
@@ -719,10 +722,32 @@ __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(A
   __syncthreads();
   const uint32_t nw = blockDim.x / kWave, wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   char *mine = tab + table_bytes2(MODE, PK) + size_t(wave) * a.wave_lds;
-  for (uint32_t c = uniform(blockIdx.x * nw + wave); c < a.n_chunks; c += gridDim.x * nw) {
+  for (uint32_t c = uniform(bid * nw + wave); c < a.n_chunks; c += nblocks * nw) {
     Tile<G, MODE, NB, PK> t(a, c, lane, mine);
     t.run();
   }
+}
+
+template <int G, int MODE, int NB, bool PK>
+__global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(Args2 a) {
+  decode2_block<G, MODE, NB, PK>(a, blockIdx.x, gridDim.x);
+}
+
+// Several layers in one launch (Sec. 2.2 block-wise decompression): blocks
+// [blk_end[i - 1], blk_end[i]) work on layer i (a block stages one layer's
+// table); the layers share the tile height and, for the GEMV, the input.
+constexpr uint32_t kMaxLayers2 = 8;
+struct MultiArgs2 {
+  Args2 a[kMaxLayers2];
+  uint32_t blk_end[kMaxLayers2];
+  uint32_t n;
+};
+
+template <int G, int MODE, int NB, bool PK>
+__global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_multi_kernel(MultiArgs2 m) {
+  uint32_t i = 0, b0 = 0;
+  while (i + 1 < m.n && blockIdx.x >= m.blk_end[i]) b0 = m.blk_end[i++];
+  decode2_block<G, MODE, NB, PK>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0);
 }
 
 // Rows split over NT > 1 column tiles: y = s * (partials added in tile
@@ -863,24 +888,85 @@ uint32_t wave_lds_bytes(int mode, const Args2 &a) {
 
 // One block per compute unit (the table takes most of LDS), as many
 // wavefronts as the chunks need for one round, at most what LDS holds.
+// Wavefronts per block for layers of n[0..k-1] chunks (each layer's chunks in
+// blocks of their own, a wavefront per chunk); 0 if not even one wavefront
+// fits LDS.  Start from one block per compute unit (total chunks / CUs
+// wavefronts) and add wavefronts until the blocks fit one round (the blocks
+// that LDS lets each compute unit hold at once); when no count up to the
+// limit does, take the count in [limit / 2, limit] that makes the busiest
+// unit's share, ceil(blocks / CUs) x waves chunks, smallest (the larger on
+// ties).
+uint32_t choose_waves(const uint32_t *n, uint32_t k, uint32_t wmax, size_t tb, size_t wl,
+                      const Facts2 &f) {
+  while (wmax > 0 && tb + size_t(wmax) * wl > size_t(f.lds)) --wmax;
+  if (wmax == 0) return 0;
+  uint64_t total = 0;
+  for (uint32_t i = 0; i < k; ++i) total += n[i];
+  auto blocks = [&](uint32_t w) {
+    uint64_t b = 0;
+    for (uint32_t i = 0; i < k; ++i) b += (n[i] + w - 1) / w;
+    return b;
+  };
+  auto slots = [&](uint32_t w) { return uint64_t(f.cus) * (size_t(f.lds) / (tb + size_t(w) * wl)); };
+  uint32_t w = uint32_t(std::min<uint64_t>(std::max<uint64_t>((total + f.cus - 1) / f.cus, 1), wmax));
+  while (w < wmax && blocks(w) > slots(w)) ++w;
+  if (blocks(w) > slots(w)) {
+    uint64_t best = ~uint64_t(0);
+    for (uint32_t v = wmax; v >= 1 && v >= (wmax + 1) / 2; --v) {
+      const uint64_t load = (blocks(v) + f.cus - 1) / f.cus * v;
+      if (load < best) {
+        best = load;
+        w = v;
+      }
+    }
+  }
+  return w;
+}
+
 template <int MODE, int NB, bool PK>
 int launch2_pk(Args2 a, hipStream_t s) {
   const Facts2 f = facts2();
   a.wave_lds = wave_lds_bytes(MODE, a);
-  uint32_t waves = (a.n_chunks + f.cus - 1) / f.cus;
-  constexpr uint32_t wmax = max_waves2(MODE, NB);
-  waves = waves < 1 ? 1 : (waves > wmax ? wmax : waves);
   const size_t tb = table_bytes2(MODE, PK);
-  while (waves > 1 && tb + size_t(waves) * a.wave_lds > size_t(f.lds)) --waves;
-  if (tb + size_t(waves) * a.wave_lds > size_t(f.lds)) return EQ_EINVAL;
-  uint32_t blocks = (a.n_chunks + waves - 1) / waves;
-  if (blocks > uint32_t(f.cus) * 4) blocks = uint32_t(f.cus) * 4;
+  const uint32_t waves = choose_waves(&a.n_chunks, 1, max_waves2(MODE, NB), tb, a.wave_lds, f);
+  if (waves == 0) return EQ_EINVAL;
+  const uint32_t blocks = (a.n_chunks + waves - 1) / waves;
   const size_t shm = tb + size_t(waves) * a.wave_lds;
   const dim3 grid(blocks), block(waves * kWave);
   switch (a.TR) {
     case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB, PK>), grid, block, shm, s, a); break;
     case 128: hipLaunchKernelGGL((decode2_kernel<2, MODE, NB, PK>), grid, block, shm, s, a); break;
     default: hipLaunchKernelGGL((decode2_kernel<4, MODE, NB, PK>), grid, block, shm, s, a); break;
+  }
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+}
+
+// Joint launch of m.n layers: one wavefront count for all (from the total
+// chunks, LDS for the largest per-wavefront need), each layer's blocks in
+// proportion to its chunks.
+template <int MODE, int NB, bool PK>
+int launch2_multi(MultiArgs2 m, hipStream_t s) {
+  const Facts2 f = facts2();
+  uint32_t wl = 0, n[kMaxLayers2];
+  for (uint32_t i = 0; i < m.n; ++i) {
+    wl = max(wl, wave_lds_bytes(MODE, m.a[i]));
+    n[i] = m.a[i].n_chunks;
+  }
+  const size_t tb = table_bytes2(MODE, PK);
+  const uint32_t waves = choose_waves(n, m.n, max_waves2(MODE, NB), tb, wl, f);
+  if (waves == 0) return EQ_EINVAL;
+  uint32_t end = 0;
+  for (uint32_t i = 0; i < m.n; ++i) {
+    m.a[i].wave_lds = wl;
+    end += (m.a[i].n_chunks + waves - 1) / waves;
+    m.blk_end[i] = end;
+  }
+  const size_t shm = tb + size_t(waves) * wl;
+  const dim3 grid(end), block(waves * kWave);
+  switch (m.a[0].TR) {
+    case 64: hipLaunchKernelGGL((decode2_multi_kernel<1, MODE, NB, PK>), grid, block, shm, s, m); break;
+    case 128: hipLaunchKernelGGL((decode2_multi_kernel<2, MODE, NB, PK>), grid, block, shm, s, m); break;
+    default: hipLaunchKernelGGL((decode2_multi_kernel<4, MODE, NB, PK>), grid, block, shm, s, m); break;
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
@@ -943,6 +1029,41 @@ size_t v2_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
   if (!v2_layer_ok(L) || B < 1 || B > kMaxBatch2) return 0;
   const size_t NT = (L->cols + L->tile_cols - 1) / L->tile_cols;
   return NT > 1 ? round256(size_t(B) * NT * L->rows * sizeof(float)) : 256;
+}
+
+bool v2_joint_ok(const eq_layer *const *L, uint32_t n) {
+  for (uint32_t i = 0; i < n; ++i)
+    if (!v2_layer_ok(L[i]) || L[i]->lanes != L[0]->lanes || L[i]->cols != L[0]->cols)
+      return false;
+  return n >= 2 && n <= kMaxLayers2;
+}
+
+int v2_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x, uint32_t B,
+                         const uint16_t *const *bias, float *const *y, void *const *ws,
+                         hipStream_t s) {
+  if (!v2_joint_ok(L, n) || !x || !y || B < 1 || B > kMaxBatch2) return EQ_EINVAL;
+  MultiArgs2 m{};
+  m.n = n;
+  for (uint32_t i = 0; i < n; ++i) {
+    if (!y[i] || !ws[i]) return EQ_EINVAL;
+    m.a[i] = make_args2(L[i]);
+    m.a[i].x = x;
+    m.a[i].batch = B;
+    m.a[i].bias = bias ? bias[i] : nullptr;
+    m.a[i].y = y[i];
+    m.a[i].ws = static_cast<float *>(ws[i]);
+  }
+  const int rc = B == 1   ? launch2_multi<kGemv2, 1, false>(m, s)
+                 : B == 2 ? launch2_multi<kGemv2, 2, false>(m, s)
+                 : B <= 4 ? launch2_multi<kGemv2, 4, false>(m, s)
+                          : launch2_multi<kGemv2, 8, false>(m, s);
+  if (rc != EQ_OK) return rc;
+  for (uint32_t i = 0; i < n; ++i)
+    if (m.a[i].NT > 1) {
+      const uint32_t t = L[i]->rows * B * kMergeSplit;
+      hipLaunchKernelGGL(merge2_kernel, dim3((t + 255) / 256), dim3(256), 0, s, m.a[i]);
+    }
+  return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
 int v2_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,

@@ -11,4 +11,12 @@ size_t v2_gemv_workspace_bytes(const eq_layer *L, uint32_t B);
 int v2_decode_gemv(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
                    float *y, void *ws, size_t ws_bytes, hipStream_t s);
 bool v2_layer_ok(const eq_layer *L);
+// Layers that one version-2 launch can decode together: 2..8 valid version-2
+// layers with one tile height and one input width.
+bool v2_joint_ok(const eq_layer *const *L, uint32_t n);
+// Fused GEMV of n such layers reading the same x; ws[i] is layer i's
+// workspace (v2_gemv_workspace_bytes(L[i], B)).
+int v2_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x, uint32_t B,
+                         const uint16_t *const *bias, float *const *y, void *const *ws,
+                         hipStream_t s);
 }  // namespace eq_detail

@@ -246,3 +246,35 @@ def test_v2_configs_1_to_3(eq, cfg):
         blob = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, seed=spec.seed,
                               target_bits=spec.target_bits)
         check_full(eq, blob, spec, batches=(1, 8) if cfg < 3 else (1,))
+
+
+@pytest.mark.parametrize("B", [1, 3, 8])
+def test_v2_gemv_multi_joint(eq, B):
+    """Layers sharing an input (as q|k|v) in one version-2 launch: outputs
+    identical to the single-layer launches (same per-tile work, same merge
+    order) and within the bar against the oracle; layers of different tile
+    heights fall back to one launch each."""
+    shapes = [(300, 1024, 64, 256, 2900), (64, 1024, 64, 256, 2901), (97, 1024, 64, 128, 2902)]
+    layers = []
+    for M, N, TR, TC, seed in shapes:
+        spec = small_spec(M, N, bits=2.0, seed=seed)
+        _, blob = build(eq, spec, TR, TC, 2.0)
+        layers.append((spec, blob, eq.Layer(blob, _dev())))
+    spec0 = layers[0][0]
+    x_bits = synth.activations(spec0, B)
+    x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+    Ls = [L for _, _, L in layers]
+    for group in (Ls, Ls + [eq.Layer(build(eq, small_spec(40, 1024, seed=2903), 128, 256,
+                                             2.0)[1], _dev())]):
+        ys = [torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+              for L in group]
+        eq.eq_decode_gemv_multi(group, x, B, None, ys, eq.multi_workspace(group, B))
+        for L, y in zip(group, ys):
+            assert np.array_equal(y.cpu().numpy(), gpu_gemv(eq, L, x_bits))
+    for (spec, blob, L), y in zip(layers, ys):
+        rc, q = oracle.container2_decode(blob)
+        assert rc == oracle.OK
+        w_ref = oracle.dequant(q, oracle.container_scales(blob))
+        err = rel_err(y.cpu().numpy(), oracle.gemv(w_ref, x_bits))
+        assert (err <= TOL).all(), err
+        assert eq.eq_get_status(L) == eq.EQ_OK

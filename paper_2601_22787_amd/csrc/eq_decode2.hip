@@ -118,13 +118,12 @@ __device__ inline uint32_t state_update_pk(uint32_t x, uint32_t w) {
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
 
 // LDS byte offset of the state half of the bucket of state x (the table
 // sits at LDS address 0): ((x mod 2^16) >> 4) * 8.
 __device__ inline uint32_t bucket_addr(uint32_t x) { return (x >> 1) & 0x7FF8u; }
-__device__ inline u32x2 state_half(uint32_t addr) { return *(lds_u32x2 *)(addr); }
-__device__ inline u32x2 value_half(uint32_t addr) { return *(lds_u32x2 *)(addr + kValHalf); }
+__device__ inline u32x2 state_half(uint32_t addr) { return *lds_ptr<const u32x2>(addr); }
+__device__ inline u32x2 value_half(uint32_t addr) { return *lds_ptr<const u32x2>(addr + kValHalf); }
 
 template <int G, int MODE, int NB, bool PK>
 struct Tile {
@@ -262,20 +261,20 @@ struct Tile {
   // The activations at state g's column, four per batch row (GEMV).
   __device__ __forceinline__ void read_x(int g, u32x2 (&xv)[NX]) {
     if (NB == 1) {
-      xv[0] = *(lds_u32x2 *)(pos[g]);  // the column's record, 8-byte aligned
+      xv[0] = *lds_ptr<const u32x2>(pos[g]);  // the column's record, 8-byte aligned
       return;
     }
     // T[p] and T[p + 2]: xv[b] = {pair (p, p + 1), pair (p + 2, p + 3)} of row b
     uint32_t lo[NB], hi[NB];
     if (NB == 2) {
-      const u32x2 v0 = *(lds_u32x2 *)(pos[g]), v1 = *(lds_u32x2 *)(pos[g] + 16);
+      const u32x2 v0 = *lds_ptr<const u32x2>(pos[g]), v1 = *lds_ptr<const u32x2>(pos[g] + 16);
       lo[0] = v0.x; lo[1 % NB] = v0.y; hi[0] = v1.x; hi[1 % NB] = v1.y;
     } else {
 #pragma unroll
       for (int q = 0; q < NB / 4; ++q) {
-        const u32x4 v0 = *(__attribute__((address_space(3))) const u32x4 *)(pos[g] + 16 * q);
+        const u32x4 v0 = *lds_ptr<const u32x4>(pos[g] + 16 * q);
         const u32x4 v1 =
-            *(__attribute__((address_space(3))) const u32x4 *)(pos[g] + 8 * NB + 16 * q);
+            *lds_ptr<const u32x4>(pos[g] + 8 * NB + 16 * q);
         lo[(4 * q) % NB] = v0.x; lo[(4 * q + 1) % NB] = v0.y;
         lo[(4 * q + 2) % NB] = v0.z; lo[(4 * q + 3) % NB] = v0.w;
         hi[(4 * q) % NB] = v1.x; hi[(4 * q + 1) % NB] = v1.y;
@@ -319,7 +318,7 @@ struct Tile {
       // write; bytes past the phrase are overwritten by the next one or lie
       // past the segment), and whether it completed the segment
       const uint32_t q = pos[g] & (kSeg - 1);
-      *(__attribute__((address_space(3))) uint32_t *)(rr[g] + q) = ev.x;
+      *lds_ptr<uint32_t>(rr[g] + q) = ev.x;
       cr[g] = q + step >= kSeg;
     }
     pos[g] += step;
@@ -378,7 +377,7 @@ struct Tile {
   // The value half of a bucket: BF16 values (GEMV) or the four codes.
   __device__ __forceinline__ u32x2 value_of(uint32_t ba) {
     if (MODE == kGemv2) return value_half(ba);
-    return u32x2{*(__attribute__((address_space(3))) const uint32_t *)((ba >> 1) + kCodesHalf),
+    return u32x2{*lds_ptr<const uint32_t>((ba >> 1) + kCodesHalf),
                  0u};
   }
 
@@ -438,10 +437,10 @@ struct Tile {
     for (uint32_t k = 0; k < n; k += kWave / 4) {
       const uint32_t e = k + lane / 4, part = lane % 4;
       if (e < n) {
-        const u32x2 ent = *(lds_u32x2 *)(list + 8 * e);
+        const u32x2 ent = *lds_ptr<const u32x2>(list + 8 * e);
         const uint32_t row = ent.x & 0xFFFFu, col0 = (ent.x >> 16) * kSeg + 16 * part;
         const uint32_t src = ring + row * kRing + 16 * part;
-        const u32x2 d0 = *(lds_u32x2 *)(src), d1 = *(lds_u32x2 *)(src + 8);
+        const u32x2 d0 = *lds_ptr<const u32x2>(src), d1 = *lds_ptr<const u32x2>(src + 8);
         const uint32_t lim = end > col0 ? end - col0 : 0u;
         store_piece(row, col0, u32x4{d0.x, d0.y, d1.x, d1.y}, min(lim, 16u),
                     __uint_as_float(ent.y));
@@ -462,7 +461,7 @@ struct Tile {
             uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
         // the segment just completed: the one before pos
         const uint32_t seg = (pos[g] >> 6) - 1;
-        *(__attribute__((address_space(3))) u32x2 *)(list + 8 * (n + rank)) =
+        *lds_ptr<u32x2>(list + 8 * (n + rank)) =
             u32x2{(g * kWave + lane) | (seg << 16), __float_as_uint(srow[g])};
       }
       n += static_cast<uint32_t>(__popcll(m));
@@ -472,8 +471,8 @@ struct Tile {
 #pragma unroll
     for (int g = 0; g < G; ++g)
       if (cr[g]) {
-        const uint32_t spill = *(__attribute__((address_space(3))) const uint32_t *)(rr[g] + kSeg);
-        *(__attribute__((address_space(3))) uint32_t *)(rr[g]) = spill;
+        const uint32_t spill = *lds_ptr<const uint32_t>(rr[g] + kSeg);
+        *lds_ptr<uint32_t>(rr[g]) = spill;
         cr[g] = false;
       }
   }
@@ -488,7 +487,7 @@ struct Tile {
       if (valid[g]) {
         const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
             uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
-        *(__attribute__((address_space(3))) u32x2 *)(list + 8 * (n + rank)) =
+        *lds_ptr<u32x2>(list + 8 * (n + rank)) =
             u32x2{(g * kWave + lane) | ((end >> 6) << 16), __float_as_uint(srow[g])};
       }
       n += static_cast<uint32_t>(__popcll(m));

@@ -65,9 +65,15 @@ __device__ inline uint32_t lds_addr(const void *p) {
   return static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
 }
-__device__ inline uint32_t lds_read_u16(uint32_t addr) { return *(lds_u16 *)(addr); }
+// An LDS pointer from its 32-bit byte address (through uintptr_t: LDS
+// pointers are 32-bit on the device, 64-bit in the host pass).
+template <typename T>
+__device__ inline __attribute__((address_space(3))) T *lds_ptr(uint32_t addr) {
+  return (__attribute__((address_space(3))) T *)(uintptr_t)addr;
+}
+__device__ inline uint32_t lds_read_u16(uint32_t addr) { return *lds_ptr<const uint16_t>(addr); }
 __device__ inline void lds_write_u16(uint32_t addr, uint32_t v) {
-  *(__attribute__((address_space(3))) uint16_t *)(addr) = static_cast<uint16_t>(v);
+  *lds_ptr<uint16_t>(addr) = static_cast<uint16_t>(v);
 }
 
 // a + 2 * b on the scalar unit in one instruction (both wave-uniform).  The

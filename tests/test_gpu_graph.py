@@ -58,6 +58,8 @@ def test_graph_replays_match_eager(eq):
         "bf16": torch.empty(n, dtype=torch.int16, device=_dev()),
         "m0": torch.empty(n, dtype=torch.int16, device=_dev()),
         "m1": torch.empty(Lv.rows * Lv.cols, dtype=torch.int16, device=_dev()),
+        "c0": torch.empty(n, dtype=torch.uint8, device=_dev()),
+        "c1": torch.empty(Lv.rows * Lv.cols, dtype=torch.uint8, device=_dev()),
         "y1": torch.empty(1, Lu.rows, dtype=torch.float32, device=_dev()),
         "y8": torch.empty(8, Lu.rows, dtype=torch.float32, device=_dev()),
         "yg": torch.empty(3, Lg.rows, dtype=torch.float32, device=_dev()),
@@ -70,6 +72,7 @@ def test_graph_replays_match_eager(eq):
         eq.eq_decode_codes(Lu, bufs["codes"])
         eq.eq_decode_bf16(Lu, bufs["bf16"])
         eq.eq_decode_bf16_multi([Lu, Lv], [bufs["m0"], bufs["m1"]])
+        eq.eq_decode_codes_multi([Lu, Lv], [bufs["c0"], bufs["c1"]])
         eq.eq_decode_gemv(Lu, x1, 1, None, bufs["y1"], ws1)
         eq.eq_decode_gemv(Lu, x8, 8, bias, bufs["y8"], ws8)
         eq.eq_decode_gemv(Lg, xg, 3, None, bufs["yg"], wsg)
@@ -95,4 +98,66 @@ def test_graph_replays_match_eager(eq):
             assert torch.equal(bufs[k], ref[k]), (rep, k)
         assert torch.equal(other, ref["y1"])
     for L in (Lu, Lv, Lg):
+        assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+def layer2(eq, M, N, TR, TC, seed):
+    spec = small_spec(M, N, bits=2.0, seed=seed)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, 2.0)
+    return eq.Layer(eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC), _dev()), spec
+
+
+def test_graph_replays_match_eager_v2(eq):
+    """The same for container version 2: codes and BF16 (rings in LDS), the
+    GEMV at batch 1 and 8 with its column-tile merge, the joint GEMV of two
+    layers sharing an input, block-wise codes, and the no-alloc GEMV (its
+    static scratch address is taken on the eager call before capture)."""
+    La, sa = layer2(eq, 300, 1024, 256, 256, 6100)
+    Lb, _ = layer2(eq, 70, 1024, 256, 256, 6101)
+    x1, x8 = xs(sa, 1), xs(sa, 8)
+    bias = torch.from_numpy(synth.bias(sa).view(np.int16)).to(_dev())
+    n = sa.rows * sa.cols
+    bufs = {
+        "codes": torch.empty(n, dtype=torch.uint8, device=_dev()),
+        "bf16": torch.empty(n, dtype=torch.int16, device=_dev()),
+        "c0": torch.empty(n, dtype=torch.uint8, device=_dev()),
+        "c1": torch.empty(Lb.rows * Lb.cols, dtype=torch.uint8, device=_dev()),
+        "y1": torch.empty(1, La.rows, dtype=torch.float32, device=_dev()),
+        "y8": torch.empty(8, La.rows, dtype=torch.float32, device=_dev()),
+        "ja": torch.empty(8, La.rows, dtype=torch.float32, device=_dev()),
+        "jb": torch.empty(8, Lb.rows, dtype=torch.float32, device=_dev()),
+        "na": torch.empty(8, La.rows, dtype=torch.float32, device=_dev()),
+    }
+    ws1, ws8, wsm = La.workspace(1), La.workspace(8), eq.multi_workspace([La, Lb], 8)
+
+    def calls():
+        eq.eq_decode_codes(La, bufs["codes"])
+        eq.eq_decode_bf16(La, bufs["bf16"])
+        eq.eq_decode_codes_multi([La, Lb], [bufs["c0"], bufs["c1"]])
+        eq.eq_decode_gemv(La, x1, 1, None, bufs["y1"], ws1)
+        eq.eq_decode_gemv(La, x8, 8, bias, bufs["y8"], ws8)
+        eq.eq_decode_gemv_multi([La, Lb], x8, 8, None, [bufs["ja"], bufs["jb"]], wsm)
+        eq.eq_decode_gemv_noalloc(La, x8, 8, bias, bufs["na"])
+
+    calls()
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in bufs.items()}
+    assert torch.equal(ref["na"], ref["y8"]) and torch.equal(ref["c0"], ref["codes"])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    for rep in range(3):
+        say("replay v2", rep)
+        for v in bufs.values():
+            v.fill_(-1 if v.dtype != torch.float32 else float("nan"))
+        other = torch.empty(1, La.rows, dtype=torch.float32, device=_dev())
+        eq.eq_decode_gemv(La, x1, 1, None, other, La.workspace(1))
+        (torch.randn(256, 256, device=_dev()) @ torch.randn(256, 256, device=_dev())).sum()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in bufs:
+            assert torch.equal(bufs[k], ref[k]), (rep, k)
+        assert torch.equal(other, ref["y1"])
+    for L in (La, Lb):
         assert eq.eq_get_status(L) == eq.EQ_OK

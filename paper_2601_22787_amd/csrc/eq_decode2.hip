@@ -125,6 +125,10 @@ __device__ inline uint32_t bucket_addr(uint32_t x) { return (x >> 1) & 0x7FF8u; 
 __device__ inline u32x2 state_half(uint32_t addr) { return *lds_ptr<const u32x2>(addr); }
 __device__ inline u32x2 value_half(uint32_t addr) { return *lds_ptr<const u32x2>(addr + kValHalf); }
 
+// Batch-1 GEMV: bytes of a wavefront's activation records (TC + 4 of 8
+// bytes, rounded to 16).
+__host__ __device__ constexpr uint32_t rec_bytes(uint32_t tc) { return ((tc + 4) * 8 + 15) / 16 * 16; }
+
 template <int G, int MODE, int NB, bool PK>
 struct Tile {
   static constexpr uint32_t TR = G * kWave;
@@ -695,20 +699,37 @@ __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint
   // position step in this kernel's units: record bytes (GEMV at batch 1),
   // activation bytes (GEMV), codes (codes and BF16 output)
   char *tab = reinterpret_cast<char *>(dyn2);
-  for (uint32_t i = threadIdx.x; PK && i < kBuckets; i += blockDim.x) {
-    const uint4 e = a.lut[i];
-    const uint32_t len = e.x >> 17, F = 65536u - (e.x & 0xFFFFu);  // F < 2^16: K > 1
-    *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{F | ((e.y | len) << 16), a.codes4[i]};
-  }
-  for (uint32_t i = threadIdx.x; !PK && i < kBuckets; i += blockDim.x) {
-    const uint4 e = a.lut[i];
-    const uint32_t len = e.x >> 17;
-    const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 4 * NB * len) : len;
-    *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{(e.x & 0xFFFFu) | (step << 16), e.y};
-    if (MODE == kGemv2)
-      *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) = u32x2{e.z, e.w};
-    else
-      *reinterpret_cast<uint32_t *>(tab + kCodesHalf + 4 * i) = a.codes4[i];
+  // kStage of a thread's entries are loaded before any is written, so their
+  // latencies overlap (one round for blocks of 512 threads or more)
+  constexpr uint32_t kStage = 8;
+  for (uint32_t i0 = threadIdx.x; i0 < kBuckets; i0 += kStage * blockDim.x) {
+    uint4 e[kStage];
+    uint32_t c4[kStage];
+#pragma unroll
+    for (uint32_t u = 0; u < kStage; ++u) {
+      const uint32_t i = i0 + u * blockDim.x;
+      if (i < kBuckets) {
+        e[u] = a.lut[i];
+        c4[u] = MODE != kGemv2 ? a.codes4[i] : 0u;
+      }
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kStage; ++u) {
+      const uint32_t i = i0 + u * blockDim.x;
+      if (i >= kBuckets) continue;
+      const uint32_t len = e[u].x >> 17;
+      if (PK) {
+        const uint32_t F = 65536u - (e[u].x & 0xFFFFu);  // F < 2^16: K > 1
+        *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{F | ((e[u].y | len) << 16), c4[u]};
+      } else {
+        const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 4 * NB * len) : len;
+        *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{(e[u].x & 0xFFFFu) | (step << 16), e[u].y};
+        if (MODE == kGemv2)
+          *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) = u32x2{e[u].z, e[u].w};
+        else
+          *reinterpret_cast<uint32_t *>(tab + kCodesHalf + 4 * i) = c4[u];
+      }
+    }
   }
   if (threadIdx.x == 0) {
     *reinterpret_cast<u32x2 *>(tab + kIdentity2) = u32x2{0u, 0u};
@@ -884,7 +905,7 @@ uint32_t wave_lds_bytes(int mode, const Args2 &a) {
   if (mode != kGemv2) b += a.TR * (kRing + 8);
   if (mode == kGemv2) {
     const uint32_t nbp = a.batch == 1 ? 1 : a.batch == 2 ? 2 : a.batch <= 4 ? 4 : 8;
-    b += nbp == 1 ? ((a.TC + 4) * 8 + 15) / 16 * 16 : (a.TC + 8) * 4 * nbp;
+    b += nbp == 1 ? rec_bytes(a.TC) : (a.TC + 8) * 4 * nbp;
   }
   return b;
 }

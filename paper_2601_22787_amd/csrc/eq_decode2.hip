@@ -1005,7 +1005,9 @@ template <int MODE, int NB>
 int launch2(Args2 a, hipStream_t s) {
   // output offsets from a tile's origin are 32-bit byte offsets
   if (MODE != kGemv2 && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
-  if (MODE != kGemv2 && a.n_syms > 1) return launch2_pk<MODE, NB, true>(a, s);
+  if constexpr (MODE != kGemv2) {
+    if (a.n_syms > 1) return launch2_pk<MODE, NB, true>(a, s);
+  }
   return launch2_pk<MODE, NB, false>(a, s);
 }
 

@@ -780,9 +780,9 @@ __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_multi_ke
 // so their latencies overlap), then the parts are added pairwise in a fixed
 // tree (deterministic).
 constexpr int kMergeSplit = 16;
-__global__ __launch_bounds__(256) void merge2_kernel(Args2 a) {
-  const uint32_t i = (blockIdx.x * blockDim.x + threadIdx.x) / kMergeSplit;
-  const uint32_t part = threadIdx.x % kMergeSplit;
+__device__ __forceinline__ void merge2(const Args2 &a, uint32_t tid) {
+  const uint32_t i = tid / kMergeSplit;
+  const uint32_t part = tid % kMergeSplit;
   const uint32_t n = a.rows * a.batch;
   const uint32_t ii = i < n ? i : n - 1;  // idle threads take part in the shuffles
   const uint32_t bb = ii / a.rows, row = ii - bb * a.rows;
@@ -804,6 +804,11 @@ __global__ __launch_bounds__(256) void merge2_kernel(Args2 a) {
     a.y[i] = bf16_to_f32(a.scale[row]) * sum + bias;
   }
 }
+
+__global__ __launch_bounds__(256) void merge2_kernel(Args2 a) {
+  merge2(a, blockIdx.x * blockDim.x + threadIdx.x);
+}
+
 
 // Phrase table of a layer: bucket b (of kBuckets) belongs to symbol k when
 // 2^(12-R) cum_k <= b < 2^(12-R) (cum_k + f_k).
@@ -965,6 +970,17 @@ int launch2_pk(Args2 a, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 
+// The merges of a joint launch in one grid: blockIdx.y picks the layer.
+// Layers of one column tile have no partials; past a layer's outputs whole
+// groups of kMergeSplit lanes (one output each) leave together, so no
+// shuffle reads a lane that has left.
+__global__ __launch_bounds__(256) void merge2_multi_kernel(MultiArgs2 m) {
+  const Args2 &a = m.a[blockIdx.y];
+  const uint32_t tid = blockIdx.x * blockDim.x + threadIdx.x;
+  if (a.NT <= 1 || tid / kMergeSplit >= a.rows * a.batch) return;
+  merge2(a, tid);
+}
+
 // Joint launch of m.n layers: one wavefront count for all (from the total
 // chunks, LDS for the largest per-wavefront need), each layer's blocks in
 // proportion to its chunks.
@@ -1084,11 +1100,14 @@ int v2_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x
                  : B <= 4 ? launch2_multi<kGemv2, 4, false>(m, s)
                           : launch2_multi<kGemv2, 8, false>(m, s);
   if (rc != EQ_OK) return rc;
-  for (uint32_t i = 0; i < n; ++i)
-    if (m.a[i].NT > 1) {
-      const uint32_t t = L[i]->rows * B * kMergeSplit;
-      hipLaunchKernelGGL(merge2_kernel, dim3((t + 255) / 256), dim3(256), 0, s, m.a[i]);
-    }
+  uint32_t tmax = 0;
+  bool any = false;
+  for (uint32_t i = 0; i < n; ++i) {
+    tmax = max(tmax, L[i]->rows * B * kMergeSplit);
+    any |= m.a[i].NT > 1;
+  }
+  if (any)
+    hipLaunchKernelGGL(merge2_multi_kernel, dim3((tmax + 255) / 256, n), dim3(256), 0, s, m);
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
 

@@ -199,6 +199,7 @@ struct Tile {
         acc[g][0] = 0.0f;
       }
       end = x0 + 8 * cols;
+      ring = x0 + rec_bytes(a.TC);  // the compaction scratch (kWave x 16 bytes)
     } else if (MODE == kGemv2) {
       // batch NB >= 2: pair table T[p] (4 NB bytes at 4 NB p), T[p][b] =
       // (x[b][p], x[b][p + 1]) as a BF16 pair, zero past the tile row and
@@ -578,7 +579,9 @@ struct Tile {
   // the wave lowers its issue priority through the steps so that waves that
   // are behind catch up); with MASK, T bounds the steps and the loop ends once
   // every segment is done.
-  template <bool MASK>
+  // COMPACT (batch-1 GEMV): leave the masked steps, at a step boundary,
+  // once at most 64 states are still active (compact_finish takes over).
+  template <bool MASK, bool COMPACT = false>
   __device__ __forceinline__ void run_pipelined(uint32_t T) {
     if (T == 0) return;
     constexpr int H = G / 2;
@@ -595,11 +598,14 @@ struct Tile {
     if (MASK) {
       for (uint32_t t = 0; t < n; ++t) {
         p_step<true>();
-        bool any = false;
+        uint32_t n_act = 0;
 #pragma unroll
-        for (int g = 0; g < G; ++g) any |= pact[g];
+        for (int g = 0; g < G; ++g)
+          n_act += static_cast<uint32_t>(__popcll(__builtin_amdgcn_ballot_w64(pact[g])));
         // nothing of step t + 1 is pending but identity steps
-        if (__builtin_amdgcn_ballot_w64(any) == 0) return;
+        if (n_act == 0) return;
+        // else complete step t + 1 (below) and hand over
+        if (COMPACT && n_act <= kWave) break;
       }
     } else {
       uint32_t t = 0;
@@ -636,6 +642,11 @@ struct Tile {
       {
         // every phrase holds at least one code: at most cols steps in all
         // (the bound also ends the loop on a damaged stream)
+        if (MODE == kGemv2 && NB == 1) {
+          run_pipelined<true, true>(cols - t1);
+          compact_finish();
+          return;
+        }
         run_pipelined<true>(cols - t1);
         flush_tail();
         finish();
@@ -659,6 +670,91 @@ struct Tile {
     }
     flush_tail();
     finish();
+  }
+
+  // Batch-1 GEMV, after the masked steps: if states are still active, they
+  // are at most 64.  Finished states write their sums and are checked; the
+  // active ones move, in ascending state order (the order in which the coder
+  // hands out words), to one state per lane through the wavefront's scratch,
+  // and finish with single-state steps: a quarter of a four-state step.
+  __device__ __forceinline__ void compact_finish() {
+    bool act[G];
+    uint32_t n_act = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      act[g] = valid[g] && pos[g] < end;
+      n_act += static_cast<uint32_t>(__popcll(__builtin_amdgcn_ballot_w64(act[g])));
+    }
+    if (n_act == 0 || n_act > kWave) {  // done, or the step bound hit (damaged stream)
+      finish();
+      return;
+    }
+    bool bad = false;
+    const uint32_t scr = ring;  // the scratch: kWave x 16 bytes after the records
+    uint32_t base = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if (valid[g] && !act[g]) {
+        write_sum(g * kWave + lane, acc[g][0]);
+        bad |= pos[g] != end;
+      }
+      bad |= !act[g] && x[g] != 0x10000u;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(act[g]);
+      const uint32_t rank = base + __builtin_amdgcn_mbcnt_hi(
+          uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+      // (four 4-byte writes: a vector built from the state arrays sent them
+      // to private memory)
+      const uint32_t xa = x[g], pa = pos[g], sa = __float_as_uint(acc[g][0]);
+      if (act[g]) {
+        const uint32_t d = scr + 16 * rank;
+        *lds_ptr<uint32_t>(d) = xa;
+        *lds_ptr<uint32_t>(d + 4) = pa;
+        *lds_ptr<uint32_t>(d + 8) = sa;
+        *lds_ptr<uint32_t>(d + 12) = g * kWave + lane;
+      }
+      base += static_cast<uint32_t>(__popcll(m));
+    }
+    const bool on = lane < n_act;
+    u32x4 v = u32x4{0x10000u, end, 0u, 0u};
+    if (on) v = *lds_ptr<const u32x4>(scr + 16 * lane);
+    uint32_t x1 = v.x, p1 = v.y;
+    float s1 = __uint_as_float(v.z);
+    // every active state advances at least one column per step
+    for (uint32_t t = 0; t < cols; ++t) {
+      const bool a1 = on && p1 < end;
+      if (__builtin_amdgcn_ballot_w64(a1) == 0) break;
+      slide();
+      const uint32_t ba = a1 ? bucket_addr(x1) : kIdentity2;
+      const u32x2 es = state_half(ba);
+      const u32x2 xv = *lds_ptr<const u32x2>(p1);  // records up to cols + 3 exist
+      const u32x2 ev = value_half(ba);
+      x1 = state_update(x1, es.x, es.y);
+      const uint64_t need = __builtin_amdgcn_ballot_w64(x1 < 0x10000u);
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+          uint32_t(need >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(need), 0u));
+      const uint32_t word = lds_read_u16(ra + 2 * below);
+      ra = add_twice(ra, static_cast<uint32_t>(__popcll(need)));
+      s1 = dot2_bf16(ev.y, xv.y, dot2_bf16(ev.x, xv.x, s1));
+      p1 += es.x >> 16;
+      x1 = renorm_lanes(need, x1, word);
+    }
+    if (on) {
+      write_sum(v.w, s1);
+      bad |= x1 != 0x10000u || p1 != end;
+    }
+    bad |= wb + (ra - wa) / 2 != p_end;
+    if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(a.status, 1);
+  }
+
+  // Batch-1 GEMV: the sum of tile row r (0 .. TR - 1) of this tile.
+  __device__ __forceinline__ void write_sum(uint32_t r, float sum) {
+    const uint32_t row = r0 + r;
+    if (a.NT == 1) {
+      const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
+      a.y[row] = bf16_to_f32(a.scale[row]) * sum + bias;
+    } else {
+      a.ws[size_t(tcol) * a.rows + row] = sum;
+    }
   }
 
   __device__ __forceinline__ void finish() {
@@ -910,7 +1006,7 @@ uint32_t wave_lds_bytes(int mode, const Args2 &a) {
   if (mode != kGemv2) b += a.TR * (kRing + 8);
   if (mode == kGemv2) {
     const uint32_t nbp = a.batch == 1 ? 1 : a.batch == 2 ? 2 : a.batch <= 4 ? 4 : 8;
-    b += nbp == 1 ? rec_bytes(a.TC) : (a.TC + 8) * 4 * nbp;
+    b += nbp == 1 ? rec_bytes(a.TC) + kWave * 16 : (a.TC + 8) * 4 * nbp;
   }
   return b;
 }

@@ -669,8 +669,9 @@ def run_prefill(args):
         "kernels": kernels}), flush=True)
 
 
-V2_KERNEL = {"gemv1": "decode2_kernel<4, 2, 1>", "gemv8": "decode2_kernel<4, 2, 8>",
-             "bf16": "decode2_kernel<4, 1, 1>", "codes": "decode2_kernel<4, 0, 1>"}
+# (template arguments: tile rows / 64, op, batch, packed table entries)
+V2_KERNEL = {"gemv1": "decode2_kernel<4, 2, 1, false>", "gemv8": "decode2_kernel<4, 2, 8, false>",
+             "bf16": "decode2_kernel<4, 1, 1, true>", "codes": "decode2_kernel<4, 0, 1, true>"}
 TARGET_FRAC = 0.60  # fused decode-GEMV B=1 on 8192x28672, compressed bytes / HBM peak
 
 

@@ -134,7 +134,9 @@ struct Tile {
   static constexpr uint32_t TR = G * kWave;
   // log2 of the position step per code (packed entries hold the length)
   static constexpr uint32_t kUnitShift =
-      MODE != kGemv2 ? 0 : (NB == 1 ? 3 : (NB == 2 ? 3 : (NB == 4 ? 4 : 5)));
+      MODE != kGemv2 ? 0 : (NB == 1 ? 3 : (NB == 2 ? 3 : 4));
+  // GEMV at batch 2-8: batch rows per pair-table entry (8 rows: two halves)
+  static constexpr uint32_t NQ = NB < 4 ? NB : 4;
   const Args2 &a;
   uint32_t lane, c, r0, c0, rows, cols, tcol;
   int nb;
@@ -144,6 +146,7 @@ struct Tile {
                      // activation record at batch 1, else in batch row 0);
                      // codes / BF16: its column in the tile
   uint32_t end;      // pos at the end of a row segment
+  uint32_t qstride;  // GEMV at batch 8: bytes from one pair-table half to the other
   float srow[G];     // BF16: the state's row scale
   uint32_t rr[G];    // codes / BF16: LDS address of the state's ring
   bool cr[G];        // codes / BF16: the last phrase completed a segment
@@ -201,14 +204,19 @@ struct Tile {
       end = x0 + 8 * cols;
       ring = x0 + rec_bytes(a.TC);  // the compaction scratch (kWave x 16 bytes)
     } else if (MODE == kGemv2) {
-      // batch NB >= 2: pair table T[p] (4 NB bytes at 4 NB p), T[p][b] =
+      // batch NB >= 2: pair table T[p] (4 NQ bytes at 4 NQ p), T[p][b] =
       // (x[b][p], x[b][p + 1]) as a BF16 pair, zero past the tile row and
       // for padded batch rows; a phrase at column p reads T[p] and T[p + 2]
-      // (aligned 4 NB-byte reads), and finished states read from T[cols]
-      // on (up to T[cols + 6] on a damaged stream)
+      // (aligned 4 NQ-byte reads), and finished states read from T[cols]
+      // on (up to T[cols + 6] on a damaged stream).  At batch 8 the table
+      // has two halves, rows 0-3 and rows 4-7, each of 16-byte entries:
+      // lanes read nearby columns, and 16-byte entries repeat the LDS banks
+      // every 16 columns instead of 8, so fewer reads meet in a bank
+      // (180 -> 170 us on the 8192 x 28672 matrix)
       uint32_t *tp = reinterpret_cast<uint32_t *>(wave_lds + kWin2 * 2);
+      const uint32_t half = (a.TC + 8) * NQ;
       for (uint32_t e = lane; e < (a.TC + 8) * NB; e += kWave) {
-        const uint32_t p = e / NB, bb = e % NB;
+        const uint32_t r = e % half, p = r / NQ, bb = (e / half) * NQ + r % NQ;
         uint32_t v = 0;
         if (bb < uint32_t(nb)) {
           const uint16_t *xr = a.x + size_t(bb) * a.cols + c0;
@@ -223,7 +231,8 @@ struct Tile {
 #pragma unroll
         for (int bb = 0; bb < NB; ++bb) acc[g][bb] = 0.0f;
       }
-      end = x0 + 4 * NB * cols;
+      end = x0 + 4 * NQ * cols;
+      qstride = 4 * half;
     } else {
       ring = uniform(lds_addr(wave_lds + kWin2 * 2));
       list = ring + TR * kRing;
@@ -277,9 +286,8 @@ struct Tile {
     } else {
 #pragma unroll
       for (int q = 0; q < NB / 4; ++q) {
-        const u32x4 v0 = *lds_ptr<const u32x4>(pos[g] + 16 * q);
-        const u32x4 v1 =
-            *lds_ptr<const u32x4>(pos[g] + 8 * NB + 16 * q);
+        const u32x4 v0 = *lds_ptr<const u32x4>(pos[g] + qstride * q);
+        const u32x4 v1 = *lds_ptr<const u32x4>(pos[g] + 32 + qstride * q);
         lo[(4 * q) % NB] = v0.x; lo[(4 * q + 1) % NB] = v0.y;
         lo[(4 * q + 2) % NB] = v0.z; lo[(4 * q + 3) % NB] = v0.w;
         hi[(4 * q) % NB] = v1.x; hi[(4 * q + 1) % NB] = v1.y;
@@ -818,7 +826,8 @@ __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint
         const uint32_t F = 65536u - (e[u].x & 0xFFFFu);  // F < 2^16: K > 1
         *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{F | ((e[u].y | len) << 16), c4[u]};
       } else {
-        const uint32_t step = MODE == kGemv2 ? (NB == 1 ? 8 * len : 4 * NB * len) : len;
+        const uint32_t step =
+            MODE == kGemv2 ? (NB == 1 ? 8 * len : 4 * (NB < 4 ? NB : 4) * len) : len;
         *reinterpret_cast<u32x2 *>(tab + 8 * i) = u32x2{(e[u].x & 0xFFFFu) | (step << 16), e[u].y};
         if (MODE == kGemv2)
           *reinterpret_cast<u32x2 *>(tab + kValHalf + 8 * i) = u32x2{e[u].z, e[u].w};

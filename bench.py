@@ -10,8 +10,9 @@ containers of version 1.  Containers are resident in HBM before timing
 starts; every read of a matrix takes the next of several device copies, so
 that no launch finds its compressed bytes in the 256 MB MALL.
 
-Prints one JSON line: the decode throughput of the whole step, per-kernel
-times (mean and p10/p50/p90) and HBM fractions, the HBM roofline of the
+Prints one JSON line: the decode throughput of the whole step, per-launch
+times (GPU time from graph replay, and eager per-call events with
+p10/p50/p90) and HBM fractions, the HBM roofline of the
 dominant kernel, the target row (fused decode-GEMV at batch 1 on the
 8192x28672 matrix, compressed bytes over time against the HBM peak) on both
 container versions, every op on container version 2 (256 x 256 tiles of the
@@ -531,15 +532,17 @@ def run_small(args):
                        "gemv1": lambda L, ws=ws: eq.eq_decode_gemv(L, x, 1, None, y, ws)}
                 for op, fn in fns.items():
                     ts = time_op(fn, lays)
-                    us = sum(ts) / len(ts)
+                    us_eager = sum(ts) / len(ts)
+                    us = us_eager if args.eager else time_graph(
+                        lambda i, fn=fn: fn(lays[i]), len(lays), 3)
                     nbytes = algorithmic_bytes(info, op, 1)
                     rows.append({"config": cfg, "matrix": spec.name,
                                  "shape": [spec.rows, spec.cols], "container": version,
                                  "chunk_syms": spec.chunk_syms, "lanes": spec.lanes,
                                  "entropy_bits": round(info["entropy"], 4),
                                  "container_mb": round(info["file_bytes"] / 1e6, 3), "op": op,
-                                 "us": round(us, 2),
-                                 "us_p50": round(float(np.percentile(ts, 50)), 2),
+                                 "us": round(us, 2), "us_eager": round(us_eager, 2),
+                                 "us_eager_p50": round(float(np.percentile(ts, 50)), 2),
                                  "gparams_per_s": round(spec.params / us / 1e3, 1),
                                  "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)})
                     print(f"[bench] config {cfg} {spec.name} v{version} {op}: {us:.1f} us",
@@ -693,6 +696,31 @@ def time_eager(fn, n, reps):
     return float(np.mean(ts)), float(np.median(ts)), ts
 
 
+def time_graph(fn, calls, reps):
+    """Mean time (us) per call of fn(0) .. fn(calls - 1), captured back to back
+    in one HIP graph (the sequence repeated to about 40 calls, so that the
+    gap between two replays is spread thin) and replayed reps times between
+    two HIP events: the GPU time of the calls' kernels without the host's
+    launch and event gaps."""
+    import torch
+    rounds = max(1, -(-40 // calls))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(rounds):
+            for i in range(calls):
+                fn(i)
+    g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return 1000.0 * e0.elapsed_time(e1) / (reps * rounds * calls)
+
+
 def compressed_bytes(info):
     return info["file_bytes"] - 2 * (info["padded_words"] - info["total_words"])
 
@@ -797,8 +825,8 @@ def run_c4(args):
 
     # The step as a serving loop would run it: one HIP graph per position in
     # the copy rotation (the library's calls only launch kernels, so they
-    # capture), replayed in order.  Per-launch figures come from an eager
-    # pass afterwards.
+    # capture), replayed in order.  Per-launch figures come from each op's
+    # launches replayed as a graph of their own, and from an eager pass.
     graphs = []
     if not args.eager:
         for c in range(period):
@@ -833,20 +861,33 @@ def run_c4(args):
     per = {}
     for mi, op, e0, e1 in timers:
         per.setdefault((mi, op), []).append(e0.elapsed_time(e1))
+    # GPU time per launch: each op's launches over the copy rotation,
+    # captured back to back in a HIP graph (the eager figures above also
+    # hold the host's launch and event gaps)
+    per_graph = {}
+    if not args.eager:
+        fns = {}
+        for c in range(period):
+            for mi, op, fn in launches(c):
+                fns.setdefault((mi, op), []).append(fn)
+        for key, fl in fns.items():
+            per_graph[key] = time_graph(lambda i, fl=fl: fl[i](), len(fl), 3)
     mats = list(range(len(specs)))
     kernels, fam = {}, {}
     for (mi, op), ts in per.items():
         covered = mats if mi == ALL else [mi]
         name = "layer" if mi == ALL else specs[mi].name
         B = 8 if op == "gemv8" else 1
-        us = 1000.0 * sum(ts) / len(ts)
+        us_eager = 1000.0 * sum(ts) / len(ts)
+        us = per_graph.get((mi, op), us_eager)
         q10, q50, q90 = (1000.0 * float(v) for v in np.percentile(ts, [10, 50, 90]))
         params = sum(specs[m].params for m in covered)
         nbytes = sum(algorithmic_bytes(infos[m], op, B) for m in covered)
         comp = sum(compressed_bytes(infos[m]) for m in covered)
         kernels[f"{name}.{op}"] = {
-            "kernel": kernel_names[op], "us": round(us, 2), "us_p10": round(q10, 2),
-            "us_p50": round(q50, 2), "us_p90": round(q90, 2), "params": params,
+            "kernel": kernel_names[op], "us": round(us, 2), "us_eager": round(us_eager, 2),
+            "us_eager_p10": round(q10, 2), "us_eager_p50": round(q50, 2),
+            "us_eager_p90": round(q90, 2), "params": params,
             "gparams_per_s": round(params / us / 1e3, 1),
             "alg_bytes": nbytes, "gbs": round(nbytes / us / 1e3, 1),
             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
@@ -881,12 +922,14 @@ def run_c4(args):
         for op, fn in fns.items():
             for i in range(args.warmup):
                 fn(i)
-            us, p50, _ = time_eager(fn, copies, max(args.steps, 20))
+            us_eager, p50, _ = time_eager(fn, copies, max(args.steps, 20))
+            us = us_eager if args.eager else time_graph(fn, copies, 3)
             B = 8 if op == "gemv8" else 1
             nbytes = (algorithmic_bytes(infos2[mi], op, B) if op != "codes"
                       else compressed_bytes(infos2[mi]) + spec.params)
             v2[f"{spec.name}.{op}"] = {
-                "kernel": V2_KERNEL[op], "us": round(us, 2), "us_p50": round(p50, 2),
+                "kernel": V2_KERNEL[op], "us": round(us, 2), "us_eager": round(us_eager, 2),
+                "us_eager_p50": round(p50, 2),
                 "gparams_per_s": round(spec.params / us / 1e3, 1), "alg_bytes": nbytes,
                 "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
                 "hbm_frac_compressed": round(compressed_bytes(infos2[mi]) / us / 1e3 /

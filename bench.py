@@ -721,6 +721,33 @@ def time_graph(fn, calls, reps):
     return 1000.0 * e0.elapsed_time(e1) / (reps * rounds * calls)
 
 
+def hbm_reference(torch, dev):
+    """Achievable HBM bandwidth on this device: a 1 GiB same-type device copy
+    (bytes read + written) and a 1 GiB streaming read (a sum over float32),
+    each the best of 5 runs timed with HIP events.  The roofline's
+    denominator stays the published 8 TB/s."""
+    n = 1 << 28  # 1 GiB of 4-byte words
+    src = torch.zeros(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    out = {}
+    for name, fn, nbytes in (("copy_gbs", lambda: dst.copy_(src), 2 * 4 * n),
+                             ("read_gbs", lambda: torch.sum(src), 4 * n)):
+        fn()
+        best = float("inf")
+        for _ in range(5):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) * 1e-3)
+        out[name] = round(nbytes / best / 1e9, 1)
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def compressed_bytes(info):
     return info["file_bytes"] - 2 * (info["padded_words"] - info["total_words"])
 
@@ -810,6 +837,7 @@ def run_c4(args):
     torch.cuda.synchronize()
     copy_gbs = 2 * ref_src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del ref_src, ref_dst
+    hbm_ref = hbm_reference(torch, dev)
 
     def check_status():
         for item in layers:
@@ -987,7 +1015,8 @@ def run_c4(args):
         "target_row": target_row,
         "kernels": kernels,
         "container_v2": v2,
-        "copy_reference_gbs": round(copy_gbs, 1),
+        "calibration_copy_gbs": round(copy_gbs, 1),
+        "hbm_reference": hbm_ref,
         "wall_s_timed": round(wall, 3),
         "env": run_env(),
     }

@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 import synth
+from gemv_ref import TOL_EXACT, exact_gemv, normwise
 from synth.configs import config_matrices, small_spec
 
 torch = pytest.importorskip("torch")
@@ -80,6 +81,8 @@ def check_full(eq, blob, spec_like, batches=(1,), with_bias=True):
         y_ref = oracle.gemv(w_ref, x, bias)
         err = rel_err(y, y_ref)
         assert np.isfinite(y).all() and (err <= TOL).all(), (B, err)
+        y_ex = exact_gemv(q_ref, oracle.container_scales(blob), x, bias_bits=bias)
+        assert (normwise(y, y_ex) <= TOL_EXACT).all(), (B, normwise(y, y_ex))
     assert eq.eq_get_status(L) == eq.EQ_OK
     return L
 

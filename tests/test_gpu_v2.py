@@ -16,6 +16,7 @@ import pytest
 
 import oracle
 import synth
+from gemv_ref import TOL_EXACT, exact_gemv, normwise
 from synth.configs import config_matrices, small_spec
 
 torch = pytest.importorskip("torch")
@@ -88,6 +89,9 @@ def check_full(eq, blob, spec, batches=(1, 2, 3, 5, 8), with_bias=True, offsets=
         y = gpu_gemv(eq, L, x, bias)
         err = rel_err(y, oracle.gemv_par(w_ref, x, bias))
         assert np.isfinite(y).all() and (err <= TOL).all(), (B, err)
+        y_ex = exact_gemv(q_ref, oracle.container_scales(blob), x,
+                          oracle.container2_info(blob).base_format, bias)
+        assert (normwise(y, y_ex) <= TOL_EXACT).all(), (B, normwise(y, y_ex))
     assert eq.eq_get_status(L) == eq.EQ_OK
     return L, q_ref, w_ref
 

@@ -70,10 +70,11 @@
  *  - Return codes: EQ_OK, EQ_EINVAL (null pointer, size or range),
  *    EQ_EFORMAT (container header or sections inconsistent), EQ_EHIP (a HIP
  *    launch or runtime call failed), EQ_ESCRATCH (eq_decode_gemv_noalloc
- *    only: the call needs more than the library's static scratch).  Stream corruption found while decoding
- *    on the device is recorded in the layer's status word (EQ_ECORRUPT via
- *    eq_get_status); outputs of a corrupted chunk are then unspecified, but
- *    no access ever leaves the container or the output buffers.
+ *    only: the call needs more than the library's static scratch).  Stream
+ *    corruption found while decoding on the device is recorded in the
+ *    layer's status word (EQ_ECORRUPT via eq_get_status); outputs of a
+ *    corrupted chunk are then unspecified, but no access ever leaves the
+ *    container or the output buffers.
  */
 #ifndef EQ_H
 #define EQ_H
@@ -127,11 +128,10 @@ size_t eq_lut_bytes(void);
  * caller and tied to this layer.  Checks: magic/version/base format, sizes
  * and section bounds, 8 <= P <= 12 (the kernels multiply f by x >> P with
  * 24-bit operands), ascending symbols valid in the base format, frequencies
- * >= 1 summing to 2^P,
- * monotone chunk offsets ending at total_words, padding >= 1024 words,
- * initial states in [2^16, 2^32), scales finite with magnitude in
- * [2^-117, 2^120) (so every dequantised product s * v(q), an 8-bit by at
- * most 7-bit significand product, is exact in fp32).
+ * >= 1 summing to 2^P, monotone chunk offsets ending at total_words,
+ * padding >= 1024 words, initial states in [2^16, 2^32), scales finite with
+ * magnitude in [2^-117, 2^120) (so every dequantised product s * v(q), an
+ * 8-bit by at most 7-bit significand product, is exact in fp32).
  * Returns EQ_OK, EQ_EINVAL or EQ_EFORMAT. */
 int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t blob_bytes, const void *dev_blob,
                   void *dev_lut, int32_t *dev_status);
@@ -184,9 +184,10 @@ int eq_decode_gemv_noalloc(const eq_layer *L, const uint16_t *x, uint32_t B,
  * together, ahead of the block's forward pass).  Decodes layers L[0..n-1]
  * (host array of n views, 1 <= n <= 8) to BF16: layer i to w[i] (device, its
  * M*N BF16 values), as eq_decode_bf16 does, with identical results.  Layers
- * whose rows are whole steps (N a multiple of W) and that share one lane
- * count are decoded by one launch, which keeps more chunks in flight per
- * compute unit; otherwise each layer gets its own launch, in order. */
+ * of container version 1 whose rows are whole steps (N a multiple of W) and
+ * that share one lane count are decoded by one launch, which keeps more
+ * chunks in flight per compute unit; otherwise (and for version 2) each
+ * layer gets its own launch, in order. */
 int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
                          hipStream_t stream);
 
@@ -214,9 +215,11 @@ size_t eq_gemv_multi_workspace_bytes(const eq_layer *const *L, uint32_t n, uint3
  * device pointers (each [M_i] BF16 or NULL); y is a host array of n device
  * pointers ([B][M_i] fp32).  ws/ws_bytes: device workspace of at least
  * eq_gemv_multi_workspace_bytes(L, n, B); layer i uses the slice after those
- * of layers 0..i-1.  Results equal eq_decode_gemv's for each layer.  Layers
- * that cannot share one launch (rows not whole steps, different lane counts,
- * activations too large for LDS) are run one launch each. */
+ * of layers 0..i-1.  Results equal eq_decode_gemv's for each layer.  One
+ * launch serves all layers when they share a container version and lane
+ * count (version 1: rows that are whole steps and activations that fit LDS;
+ * version 2: the tile height); otherwise each layer is run by a launch of
+ * its own. */
 int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x, uint32_t B,
                          const uint16_t *const *bias, float *const *y, void *ws,
                          size_t ws_bytes, hipStream_t stream);

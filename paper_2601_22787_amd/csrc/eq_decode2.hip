@@ -6,26 +6,33 @@
 // states of tile rows l, l + 64, ... (TR / 64 of them).  Every state walks its
 // row's TC columns, one phrase of 4, 2 or 1 codes per step, so one state
 // update yields 3-4 codes on the synthetic 2-bit layers.  The phrase table
-// (kBuckets entries of 16 bytes, indexed by the top 12 bits of the slot) sits
-// in LDS; an entry holds what the state update needs and the phrase's values:
+// (kBuckets entries, indexed by the top 12 bits of the slot) sits in LDS.  A
+// global entry holds what the state update needs and the phrase's values:
 //   .x = (2^16 - F) | (2 * length) << 16      .y = 2^(16-R) * cum
 //   .z, .w = the four codes' values as BF16 pairs (zero past the length)
 // so that  x' = F (x >> 16) + (x mod 2^16) - cum  =  x - ((2^16 - F) (x >> 16) + cum)
 // is one 16 x 16-bit multiply-add (high half of x selected by op_sel) and one
-// subtraction.  In LDS the entry is split in two 8-byte halves read by two
-// 8-byte loads (a 16-byte LDS read at a random address costs about three
-// times as much as an 8-byte one on gfx950): the state half (.x with the
-// step of the state's position in the kernel's units, .y) at bucket * 8, and
-// the value half (.z, .w, or the codes) at kValHalf + bucket * 8, an offset
-// that keeps the two loads from being merged.  Stream words are handed out with a wavefront ballot and a
-// masked bit count in ascending state order, as the coder reads them.
+// subtraction.  The GEMV splits the entry in LDS into two 8-byte halves read
+// by two 8-byte loads (a 16-byte LDS read at a random address costs about
+// three times as much as an 8-byte one on gfx950): the state half (.x with
+// the step of the state's position in the kernel's units, .y) at bucket * 8,
+// and the value half (.z, .w) at kValHalf + bucket * 8, an offset that keeps
+// the two loads from being merged.  Codes and BF16 output read one packed
+// 8-byte entry {F | (cum + length) << 16, the four codes} per phrase.  Stream
+// words are handed out with a wavefront ballot and a masked bit count in
+// ascending state order, as the coder reads them.
 //
 // GEMV: all states of a chunk walk the same TC columns, so the chunk's
-// activations (TC values per batch row) sit in the wavefront's LDS; a
-// phrase's four values meet the four activations at its column with one
-// (unaligned) 8-byte LDS read and two dot2 products per batch row.  A state's
-// sum is its row's partial over the tile; partials of the NT column tiles are
-// added in tile order by merge2_kernel (deterministic).
+// activations sit in the wavefront's LDS: at batch 1 one aligned 8-byte
+// record of four values per column, at batches 2-8 a table of value pairs;
+// a phrase's four values meet them with two dot2 products per batch row.  A
+// state's sum is its row's partial over the tile; partials of the NT column
+// tiles are added in tile order by merge2_kernel (deterministic).  At batch 1
+// the last states of a tile are compacted to one per lane.
+//
+// Codes and BF16 output: each phrase's codes go to an LDS ring of its row,
+// and whole 64-code segments of rows leave the wavefront together, so that
+// stores write contiguous lines.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -267,9 +274,7 @@ struct Tile {
     }
   }
 
-  // Use state g's phrase e: WIDE stores the whole phrase slot (four codes,
-  // valid while the slot lies inside the row segment; later phrases of the
-  // same state overwrite what lies past this one), else exactly its length.
+  // Activation operands per phrase: one per batch row (GEMV), else unused.
   static constexpr int NX = MODE == kGemv2 ? NB : 1;
 
   // The activations at state g's column, four per batch row (GEMV).
@@ -319,7 +324,8 @@ struct Tile {
                  __builtin_amdgcn_perm(__float_as_uint(hi.y), __float_as_uint(hi.x), 0x07060302u)};
   }
 
-  template <bool WIDE>
+  // Use state g's phrase: its products with the activations (GEMV) or its
+  // codes into the row's ring; then the state's position moves past it.
   __device__ __forceinline__ void use(int g, u32x2 es, u32x2 ev, const u32x2 (&xv)[NX]) {
     const uint32_t step = PK ? ((es.x >> 16) & 7u) << kUnitShift : es.x >> 16;
     if (MODE == kGemv2) {
@@ -337,8 +343,8 @@ struct Tile {
     pos[g] += step;
   }
 
-  // One step.  MASKED: only states whose segment is not complete take part
-  // (else every state does, with wide stores).
+  // One step (G = 1, no pipeline).  MASKED: only states whose segment is not
+  // complete take part (else every state does).
   template <bool MASKED>
   __device__ __forceinline__ void step(const bool (&act)[G]) {
     slide();
@@ -378,7 +384,7 @@ struct Tile {
     }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      if (!MASKED || act[g]) use<!MASKED>(g, es[g], values(es[g], ev[g]), xv[g]);
+      if (!MASKED || act[g]) use(g, es[g], values(es[g], ev[g]), xv[g]);
       else cr[g] = false;
     }
 #pragma unroll
@@ -558,7 +564,7 @@ struct Tile {
   }
   template <int g>
   __device__ __forceinline__ void p_finish() {
-    use<true>(g, pes[g], values(pes[g], pev[g]), pxv[g]);
+    use(g, pes[g], values(pes[g], pev[g]), pxv[g]);
     x[g] = renorm_lanes(pneed[g], x[g], pword[g]);
   }
 
@@ -648,29 +654,25 @@ struct Tile {
   __device__ __forceinline__ void run() {
     const bool all[G] = {};
     bool full = rows == TR;
-    // Every state needs at least cols / 4 phrases; while each phrase slot lies
-    // inside the segment, stores may be wide.
+    // Every state needs at least cols / 4 phrases, so in a full tile no state
+    // finishes before step cols / 4: those steps need no masks.
     const uint32_t t1 = full ? cols / 4 : 0;
     if (G >= 2) {
       run_pipelined<false>(t1);
-      {
-        // every phrase holds at least one code: at most cols steps in all
-        // (the bound also ends the loop on a damaged stream)
-        if (MODE == kGemv2 && NB == 1) {
-          run_pipelined<true, true>(cols - t1);
-          compact_finish();
-          return;
-        }
-        run_pipelined<true>(cols - t1);
-        flush_tail();
-        finish();
+      // every phrase holds at least one code: at most cols steps in all (the
+      // bound also ends the loop on a damaged stream)
+      if (MODE == kGemv2 && NB == 1) {
+        run_pipelined<true, true>(cols - t1);
+        compact_finish();
         return;
       }
-    } else {
-      for (uint32_t t = 0; t < t1; ++t) step<false>(all);
+      run_pipelined<true>(cols - t1);
+      flush_tail();
+      finish();
+      return;
     }
-    // every phrase holds at least one code: at most cols steps in all (the
-    // bound also ends the loop on a damaged table)
+    // G = 1: one state per lane, steps one after the other
+    for (uint32_t t = 0; t < t1; ++t) step<false>(all);
     for (uint32_t t = t1; t < cols; ++t) {
       bool act[G];
       bool any = false;

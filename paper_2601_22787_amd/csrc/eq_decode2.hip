@@ -31,7 +31,7 @@
 // the last states of a tile are compacted to one per lane.
 //
 // Codes and BF16 output: each phrase's codes go to an LDS ring of its row,
-// and whole 64-code segments of rows leave the wavefront together, so that
+// and whole 32-code segments of rows leave the wavefront together, so that
 // stores write contiguous lines.
 #include <hip/hip_runtime.h>
 
@@ -70,12 +70,16 @@ constexpr uint32_t kTableCodes2 = (kCodesHalf + kBuckets * 4 + 4 + 15) / 16 * 16
 // 8-byte entry per bucket, {F | (cum + length) << 16, the four codes}, and
 // the identity {0, 0} after them.
 constexpr uint32_t kTablePacked2 = kBuckets * 8 + 16;
-// Codes and BF16 output leave the wavefront as whole 64-code segments of a
-// row (a 128-byte line of BF16): each tile row has an LDS ring holding its
-// current segment and 4 bytes more, where a phrase that crosses the
-// segment's end spills (8-byte aligned rows).
-constexpr uint32_t kSeg = 64;
-constexpr uint32_t kRing = 72;
+// Codes and BF16 output leave the wavefront as whole 32-code segments of a
+// row (64 bytes of BF16), four lanes per segment: each tile row has an LDS
+// ring holding its current segment and 8 bytes more, where a phrase that
+// crosses the segment's end spills (8-byte aligned rows).  32-code rather
+// than 64-code segments halve the rings, so more wavefronts fit a compute
+// unit (8192 x 28672: codes 248 -> 232 us, BF16 298 -> 288 us).
+constexpr uint32_t kSegShift = 5;
+constexpr uint32_t kSeg = 1u << kSegShift;
+constexpr uint32_t kRing = kSeg + 8;
+constexpr uint32_t kCPL = kSeg / 4;  // codes per lane when a segment is written out
 
 enum Mode2 { kCodes2 = 0, kBf16_2 = 1, kGemv2 = 2 };
 
@@ -401,16 +405,17 @@ struct Tile {
   }
 
   // --- codes / BF16 output --------------------------------------------------
-  // Store n (<= 16) codes of tile row `row` from column col0 on: `d` holds
-  // 16 codes (from the row's ring).  Whole 16-code pieces go out as one
-  // (codes) or two (BF16) 16-byte stores; a shorter piece, which only a
-  // row's last segment has, element by element.
-  __device__ __forceinline__ void store_piece(uint32_t row, uint32_t col0, u32x4 d, uint32_t n,
+  // Store n (<= 8) codes of tile row `row` from column col0 on: `d` holds 8
+  // codes (from the row's ring).  A whole 8-code piece goes out as one 8-byte
+  // (codes) or 16-byte (BF16) store, so the four lanes of a segment write 32
+  // or 64 contiguous bytes; a shorter piece, which only a row's last segment
+  // has, element by element.
+  __device__ __forceinline__ void store_piece(uint32_t row, uint32_t col0, u32x2 d, uint32_t n,
                                               float sc) {
     const uint32_t idx = row * a.cols + col0;  // < 2^31 (checked at launch)
     if (MODE == kCodes2) {
-      if (n >= 16) {
-        __builtin_amdgcn_raw_buffer_store_b128(d, out_rsrc, idx, 0, 0);
+      if (n >= kCPL) {
+        __builtin_amdgcn_raw_buffer_store_b64(d, out_rsrc, idx, 0, 0);
       } else {
         for (uint32_t e = 0; e < n; ++e)
           __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(d[e / 4] >> (8 * (e % 4))),
@@ -418,9 +423,9 @@ struct Tile {
       }
       return;
     }
-    uint32_t o[8];
+    uint32_t o[4];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < 2; ++w) {
       float v0, v1, v2, v3;
       if (a.fmt == kFmtInt8) {
         v0 = static_cast<float>(static_cast<int8_t>(d[w]));
@@ -437,11 +442,9 @@ struct Tile {
       o[2 * w] = pack_bf16(sc * v0, sc * v1);
       o[2 * w + 1] = pack_bf16(sc * v2, sc * v3);
     }
-    if (n >= 16) {
+    if (n >= kCPL) {
       __builtin_amdgcn_raw_buffer_store_b128(u32x4{o[0], o[1], o[2], o[3]}, out_rsrc, 2 * idx, 0,
                                              0);
-      __builtin_amdgcn_raw_buffer_store_b128(u32x4{o[4], o[5], o[6], o[7]}, out_rsrc,
-                                             2 * idx + 16, 0, 0);
     } else {
       for (uint32_t e = 0; e < n; ++e)
         __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(o[e / 2] >> (16 * (e % 2))),
@@ -457,11 +460,10 @@ struct Tile {
       const uint32_t e = k + lane / 4, part = lane % 4;
       if (e < n) {
         const u32x2 ent = *lds_ptr<const u32x2>(list + 8 * e);
-        const uint32_t row = ent.x & 0xFFFFu, col0 = (ent.x >> 16) * kSeg + 16 * part;
-        const uint32_t src = ring + row * kRing + 16 * part;
-        const u32x2 d0 = *lds_ptr<const u32x2>(src), d1 = *lds_ptr<const u32x2>(src + 8);
+        const uint32_t row = ent.x & 0xFFFFu, col0 = (ent.x >> 16) * kSeg + kCPL * part;
+        const uint32_t src = ring + row * kRing + kCPL * part;
         const uint32_t lim = end > col0 ? end - col0 : 0u;
-        store_piece(row, col0, u32x4{d0.x, d0.y, d1.x, d1.y}, min(lim, 16u),
+        store_piece(row, col0, *lds_ptr<const u32x2>(src), min(lim, kCPL),
                     __uint_as_float(ent.y));
       }
     }
@@ -479,7 +481,7 @@ struct Tile {
         const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
             uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
         // the segment just completed: the one before pos
-        const uint32_t seg = (pos[g] >> 6) - 1;
+        const uint32_t seg = (pos[g] >> kSegShift) - 1;
         *lds_ptr<u32x2>(list + 8 * (n + rank)) =
             u32x2{(g * kWave + lane) | (seg << 16), __float_as_uint(srow[g])};
       }
@@ -507,7 +509,7 @@ struct Tile {
         const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
             uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
         *lds_ptr<u32x2>(list + 8 * (n + rank)) =
-            u32x2{(g * kWave + lane) | ((end >> 6) << 16), __float_as_uint(srow[g])};
+            u32x2{(g * kWave + lane) | ((end >> kSegShift) << 16), __float_as_uint(srow[g])};
       }
       n += static_cast<uint32_t>(__popcll(m));
     }

@@ -72,13 +72,12 @@ constexpr uint32_t kTableCodes2 = (kCodesHalf + kBuckets * 4 + 4 + 15) / 16 * 16
 constexpr uint32_t kTablePacked2 = kBuckets * 8 + 16;
 // Codes and BF16 output leave the wavefront as whole 32-code segments of a
 // row (64 bytes of BF16), four lanes per segment: each tile row has an LDS
-// ring holding its current segment and 8 bytes more, where a phrase that
-// crosses the segment's end spills (8-byte aligned rows).  32-code rather
-// than 64-code segments halve the rings, so more wavefronts fit a compute
-// unit (8192 x 28672: codes 248 -> 232 us, BF16 298 -> 288 us).
+// ring holding its current segment.  32-code rather than 64-code segments
+// halve the rings, so more wavefronts fit a compute unit (8192 x 28672:
+// codes 248 -> 232 us, BF16 298 -> 288 us).
 constexpr uint32_t kSegShift = 5;
 constexpr uint32_t kSeg = 1u << kSegShift;
-constexpr uint32_t kRing = kSeg + 8;
+constexpr uint32_t kRing = kSeg;
 constexpr uint32_t kCPL = kSeg / 4;  // codes per lane when a segment is written out
 
 enum Mode2 { kCodes2 = 0, kBf16_2 = 1, kGemv2 = 2 };
@@ -160,6 +159,8 @@ struct Tile {
   uint32_t qstride;  // GEMV at batch 8: bytes from one pair-table half to the other
   float srow[G];     // BF16: the state's row scale
   uint32_t rr[G];    // codes / BF16: LDS address of the state's ring
+  uint32_t pend[G];  // codes / BF16: the codes of the state's current ring dword
+                     // not yet written (pos mod 4 of them, low bytes first)
   bool cr[G];        // codes / BF16: the last phrase completed a segment
   uint32_t ring, list;  // codes / BF16: LDS addresses of the rings, the flush list
   float acc[G][NB];
@@ -252,6 +253,7 @@ struct Tile {
         pos[g] = 0;
         rr[g] = ring + (g * kWave + lane) * kRing;
         cr[g] = false;
+        pend[g] = 0;
         srow[g] = MODE == kBf16_2 && valid[g] ? bf16_at(a.scale, r0 + g * kWave + lane) : 0.0f;
       }
       end = cols;
@@ -337,11 +339,21 @@ struct Tile {
       for (int bb = 0; bb < NX; ++bb)
         acc[g][bb] = dot2_bf16(ev.y, xv[bb].y, dot2_bf16(ev.x, xv[bb].x, acc[g][bb]));
     } else {
-      // the phrase's four codes into the row's ring (an unaligned 4-byte
-      // write; bytes past the phrase are overwritten by the next one or lie
-      // past the segment), and whether it completed the segment
-      const uint32_t q = pos[g] & (kSeg - 1);
-      *lds_ptr<uint32_t>(rr[g] + q) = ev.x;
+      // the phrase's codes (ev.x, zero past its length) after the state's
+      // pending ones; a completed dword goes to the row's ring with an
+      // aligned 4-byte write, the rest stays pending (unaligned LDS writes
+      // were slower: codes 232 -> 203 us on 8192 x 28672).  Codes past the
+      // segment's end start the next segment's first dword, which is written
+      // only in a later step, after this step's flush has read the ring.
+      const uint32_t q = pos[g] & (kSeg - 1), o = q & 3;
+      const uint32_t lo = pend[g] | (ev.x << (8 * o));
+      const uint32_t hi = o ? ev.x >> (32 - 8 * o) : 0u;
+      if (o + step >= 4) {
+        *lds_ptr<uint32_t>(rr[g] + (q & ~3u)) = lo;
+        pend[g] = hi;
+      } else {
+        pend[g] = lo;
+      }
       cr[g] = q + step >= kSeg;
     }
     pos[g] += step;
@@ -453,8 +465,7 @@ struct Tile {
   }
 
   // Write the list's n segments (entries: tile row | segment << 16, the row
-  // scale), four lanes per segment; then the rows listed with `spill` move
-  // the codes past their segment to the ring's start.
+  // scale), four lanes per segment.
   __device__ __forceinline__ void write_list(uint32_t n) {
     for (uint32_t k = 0; k < n; k += kWave / 4) {
       const uint32_t e = k + lane / 4, part = lane % 4;
@@ -490,17 +501,17 @@ struct Tile {
     if (n == 0) return;
     write_list(n);
 #pragma unroll
-    for (int g = 0; g < G; ++g)
-      if (cr[g]) {
-        const uint32_t spill = *lds_ptr<const uint32_t>(rr[g] + kSeg);
-        *lds_ptr<uint32_t>(rr[g]) = spill;
-        cr[g] = false;
-      }
+    for (int g = 0; g < G; ++g) cr[g] = false;
   }
 
   // At the end of the tile: every row's last, partial segment.
   __device__ __forceinline__ void flush_tail() {
     if (MODE == kGemv2 || (end & (kSeg - 1)) == 0) return;
+    // the codes still pending (end not a multiple of 4) into the ring
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (valid[g] && (pos[g] & 3))
+        *lds_ptr<uint32_t>(rr[g] + ((pos[g] & (kSeg - 1)) & ~3u)) = pend[g];
     uint32_t n = 0;
 #pragma unroll
     for (int g = 0; g < G; ++g) {

@@ -227,14 +227,45 @@ struct Tile {
       // (180 -> 170 us on the 8192 x 28672 matrix)
       uint32_t *tp = reinterpret_cast<uint32_t *>(wave_lds + kWin2 * 2);
       const uint32_t half = (a.TC + 8) * NQ;
-      for (uint32_t e = lane; e < (a.TC + 8) * NB; e += kWave) {
-        const uint32_t r = e % half, p = r / NQ, bb = (e / half) * NQ + r % NQ;
-        uint32_t v = 0;
-        if (bb < uint32_t(nb)) {
-          const uint16_t *xr = a.x + size_t(bb) * a.cols + c0;
-          v = (p < cols ? xr[p] : 0u) | ((p + 1 < cols ? uint32_t(xr[p + 1]) : 0u) << 16);
+      if (((reinterpret_cast<uintptr_t>(a.x) | (size_t(a.cols) * 2) | (size_t(c0) * 2)) & 15) ==
+          0) {
+        // 16-byte aligned rows: an item is 8 columns of one batch row, one
+        // 16-byte load and the next column's value giving the 8 columns'
+        // pairs (batch 8 on 8192 x 28672: 159 -> 157 us against one 2-byte
+        // load per value)
+        const uint32_t groups = (a.TC + 8 + 7) / 8;
+        for (uint32_t it = lane; it < groups * NB; it += kWave) {
+          const uint32_t bb = it / groups, p0 = 8 * (it % groups);
+          uint32_t w[9];
+#pragma unroll
+          for (int k = 0; k < 9; ++k) w[k] = 0;
+          if (bb < uint32_t(nb)) {
+            const uint16_t *xr = a.x + size_t(bb) * a.cols + c0;
+            if (p0 + 8 <= cols) {
+              const uint4 v = *reinterpret_cast<const uint4 *>(xr + p0);
+              w[0] = v.x & 0xFFFFu; w[1] = v.x >> 16; w[2] = v.y & 0xFFFFu; w[3] = v.y >> 16;
+              w[4] = v.z & 0xFFFFu; w[5] = v.z >> 16; w[6] = v.w & 0xFFFFu; w[7] = v.w >> 16;
+              w[8] = p0 + 8 < cols ? xr[p0 + 8] : 0u;
+            } else {
+#pragma unroll
+              for (int k = 0; k < 9; ++k) w[k] = p0 + k < cols ? xr[p0 + k] : 0u;
+            }
+          }
+          const uint32_t base = (bb / NQ) * half + bb % NQ;
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (p0 + k < a.TC + 8) tp[base + (p0 + k) * NQ] = w[k] | (w[k + 1] << 16);
         }
-        tp[e] = v;
+      } else {
+        for (uint32_t e = lane; e < (a.TC + 8) * NB; e += kWave) {
+          const uint32_t r = e % half, p = r / NQ, bb = (e / half) * NQ + r % NQ;
+          uint32_t v = 0;
+          if (bb < uint32_t(nb)) {
+            const uint16_t *xr = a.x + size_t(bb) * a.cols + c0;
+            v = (p < cols ? xr[p] : 0u) | ((p + 1 < cols ? uint32_t(xr[p + 1]) : 0u) << 16);
+          }
+          tp[e] = v;
+        }
       }
       const uint32_t x0 = uniform(lds_addr(tp));
 #pragma unroll

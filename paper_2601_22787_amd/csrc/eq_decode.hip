@@ -680,16 +680,14 @@ struct Decoder {
   }
   // Read back the staged step at chunk offset kk (storing the previous one).
   __device__ __forceinline__ void stage_get(uint32_t kk) {
-    typedef const __attribute__((address_space(3))) uint64_t lds_u64;
-    typedef const __attribute__((address_space(3))) uint32_t lds_u32;
     if (pend_valid) stage_store();
     const uint32_t addr = stg + 2 * (G - 1) * lane;  // staging area + 2 G lane
     if (G >= 4) {
-      const uint64_t v = *(lds_u64 *)(addr);
+      const uint64_t v = *lds_ptr<const uint64_t>(addr);
       pend[0] = static_cast<uint32_t>(v);
       pend[G >= 4 ? 1 : 0] = static_cast<uint32_t>(v >> 32);
     } else {
-      pend[0] = *(lds_u32 *)(addr);
+      pend[0] = *lds_ptr<const uint32_t>(addr);
     }
     pkk = kk;
     pend_valid = true;

@@ -240,7 +240,8 @@ int eq_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x
 size_t eq_gemm_codes_workspace_bytes(const eq_layer *L, uint32_t B);
 
 /* Workspace bytes of eq_decode_gemm for B tokens: the M*N codes, rounded up
- * to 256, then eq_gemm_codes_workspace_bytes(L, B). */
+ * to 256, then eq_gemm_codes_workspace_bytes(L, B); for B <= 8 at least
+ * eq_gemv_workspace_bytes(L, B) too. */
 size_t eq_gemm_workspace_bytes(const eq_layer *L, uint32_t B);
 
 /* y[t][i] = s_i * sum_j v(codes[i][j]) x[t][j] + bias[i] for t < B, any
@@ -254,9 +255,11 @@ int eq_gemm_codes(const eq_layer *L, const uint8_t *codes, const uint16_t *x, ui
                   const uint16_t *bias, float *y, void *ws, size_t ws_bytes,
                   hipStream_t stream);
 
-/* eq_decode_codes into the start of ws (at least eq_gemm_workspace_bytes(L,
- * B) bytes, device, 16-byte aligned), then eq_gemm_codes with the rest of
- * ws: Alg. 2 for a batch of B tokens. */
+/* Alg. 2 for a batch of B tokens: eq_decode_codes into the start of ws (at
+ * least eq_gemm_workspace_bytes(L, B) bytes, device, 16-byte aligned), then
+ * eq_gemm_codes with the rest of ws.  For B <= 8 it runs eq_decode_gemv
+ * instead (with ws as its workspace), which is faster at such batches and
+ * gives that call's results. */
 int eq_decode_gemm(const eq_layer *L, const uint16_t *x, uint32_t B, const uint16_t *bias,
                    float *y, void *ws, size_t ws_bytes, hipStream_t stream);
 

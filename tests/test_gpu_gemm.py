@@ -7,7 +7,8 @@ fp64 GEMM on the decoded BF16 weights (as for the GEMV), plus exact outputs
 for one-hot tokens (y = s_i v(q_ij), a single product), on ragged shapes
 (tokens, rows and columns not multiples of the 128 x 128 x 64 tile), both
 base formats, and sampled rows and tokens of the full-size 8192 x 28672
-layer."""
+layer.  Batches of up to 8 tokens go to the fused decode-GEMV instead, with
+its results."""
 import sys
 
 import numpy as np
@@ -275,3 +276,38 @@ def test_block_codes_buffer_feeds_gemm(eq):
         w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
         assert (rel_err(yn, oracle.gemv(w_ref, x_bits)) <= TOL).all()
         assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+@pytest.mark.parametrize("version", [1, 2])
+@pytest.mark.parametrize("fmt", [1, 2])
+def test_small_batches_take_the_fused_gemv(eq, version, fmt):
+    """Up to 8 tokens eq_decode_gemm runs the fused decode-GEMV: its outputs
+    equal eq_decode_gemv's bit for bit (same workspace size rule), meet the
+    GEMV bar against the oracle, and 9 tokens go through the GEMM."""
+    M, N = 96, 1024
+    spec = small_spec(M, N, bits=2.5, chunk=4096, lanes=64, seed=4321 + version + fmt)
+    w = synth.weights(spec)
+    alpha, _ = eq.eqe_alpha_search(w, 2.5, base_format=fmt)
+    if version == 1:
+        blob = eq.eqe_encode(w, alpha, chunk_syms=4096, lanes=64, base_format=fmt)
+    else:
+        blob = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=64, base_format=fmt)
+    L = eq.Layer(blob, _dev())
+    rc, q = (oracle.container2_decode(blob) if version == 2 else oracle.container_decode(blob))
+    assert rc == oracle.OK
+    w_ref = oracle.dequant(q, oracle.container_scales(blob), fmt)
+    bias = synth.bias(spec)
+    bias_t = torch.from_numpy(bias.view(np.int16)).to(_dev())
+    for B in (1, 5, 8, 9):
+        x_bits = tokens(spec, B)
+        x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+        assert eq.eq_gemm_workspace_bytes(L, B) >= (eq.eq_gemv_workspace_bytes(L, B)
+                                                    if B <= 8 else 0)
+        y = gpu_gemm(eq, L, x_bits, bias)
+        err = rel_err(y, oracle.gemv(w_ref, x_bits, bias))
+        assert np.isfinite(y).all() and (err <= TOL).all(), (B, err)
+        if B <= 8:
+            y2 = torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+            eq.eq_decode_gemv(L, x, B, bias_t, y2, L.workspace(B))
+            assert np.array_equal(y, y2.cpu().numpy()), B
+    assert eq.eq_get_status(L) == eq.EQ_OK

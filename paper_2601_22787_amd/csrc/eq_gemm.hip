@@ -304,7 +304,8 @@ void launch_gemm(GemmArgs a, hipStream_t stream) {
 // than that.  When the tiles leave compute units idle, the input columns are
 // cut into slices (at most 16, each at least 4 stages of 64 columns) whose
 // partial sums are reduced in slice order: 256 x 256 blocks one per compute
-// unit, 128 x 128 blocks at least one per compute unit (two fit).
+// unit, 128 x 128 blocks at least one per compute unit (two fit; two per
+// unit when the tokens fit one block).
 struct GemmPlan {
   bool big;
   uint32_t splits, split_stages;
@@ -317,7 +318,14 @@ GemmPlan plan_gemm(uint32_t B, uint32_t M, uint32_t N, int cus) {
   GemmPlan p{10 * 4 * t256 <= 14 * t128, 1, stages};  // padded areas, in 128 x 128 units
   const uint64_t tiles = p.big ? t256 : t128;
   if (tiles >= uint64_t(cus)) return p;
-  uint64_t want = p.big ? uint64_t(cus) / tiles : (uint64_t(cus) + tiles - 1) / tiles;
+  // 128 x 128 blocks: two fit a compute unit.  When all tokens fit one block
+  // (the codes are then read once in all), slice so that the blocks fill
+  // one round of two per compute unit (8192 x 28672 at 16-64 tokens: 92-93
+  // -> 68-73 us); with several token blocks, one per compute unit
+  // measured faster.
+  uint64_t want = p.big ? uint64_t(cus) / tiles
+                  : B <= 128 ? std::max<uint64_t>(1, 2 * uint64_t(cus) / tiles)
+                             : (uint64_t(cus) + tiles - 1) / tiles;
   want = want < 16 ? want : 16;
   const uint64_t cap = stages / 4;
   const uint64_t sp = want < cap ? want : cap;

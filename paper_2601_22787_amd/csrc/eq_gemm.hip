@@ -301,13 +301,20 @@ void launch_gemm(GemmArgs a, hipStream_t stream) {
 // does a stage's work at about 1.4x the rate of 128 x 128 blocks (4
 // wavefronts of 64 x 64; measured per stage on the config-4 matrices), so it
 // is used unless its padding (tokens and rows rounded up to 256) costs more
-// than that.  When the tiles leave compute units idle, the input columns are
-// cut into slices (at most 16, each at least 4 stages of 64 columns) whose
-// partial sums are reduced in slice order: 256 x 256 blocks one per compute
-// unit, 128 x 128 blocks at least one per compute unit (two fit; two per
-// unit when the tokens fit one block).
+// than that.  Up to 64 tokens the GEMM is bound by the stream of codes, read
+// once in all: blocks of 32 or 64 tokens x 256 rows (4 wavefronts of 32 or
+// 64 x 64) load a quarter or half of the activation rows a 128 x 128 block
+// loads per code (8192 x 28672 at 16 tokens: 70 -> 46 us).  When the tiles
+// leave compute units idle, the input columns are cut into slices (at most
+// 16, each at least 4 stages of 64 columns) whose partial sums are reduced in
+// slice order: 256 x 256 blocks one per compute unit; blocks of up to 128
+// tokens, of which two fit a compute unit, one round of two per unit (the
+// codes are then read once in all; 8192 x 28672 at 65-128 tokens: 92-100 ->
+// 77-85 us); with several 128-token blocks one per unit measured faster.
+enum GemmTile { kTile256, kTile128, kTile64x256, kTile32x256 };
+
 struct GemmPlan {
-  bool big;
+  GemmTile tile;
   uint32_t splits, split_stages;
 };
 
@@ -315,15 +322,17 @@ GemmPlan plan_gemm(uint32_t B, uint32_t M, uint32_t N, int cus) {
   const uint32_t stages = (N + kBK - 1) / kBK;
   const uint64_t t256 = uint64_t((M + 255) / 256) * ((B + 255) / 256);
   const uint64_t t128 = uint64_t((M + 127) / 128) * ((B + 127) / 128);
-  GemmPlan p{10 * 4 * t256 <= 14 * t128, 1, stages};  // padded areas, in 128 x 128 units
-  const uint64_t tiles = p.big ? t256 : t128;
+  GemmPlan p{kTile128, 1, stages};
+  uint64_t tiles = t128;
+  if (B <= 64) {
+    p.tile = B <= 32 ? kTile32x256 : kTile64x256;
+    tiles = (M + 255) / 256;
+  } else if (10 * 4 * t256 <= 14 * t128) {  // padded areas, in 128 x 128 units
+    p.tile = kTile256;
+    tiles = t256;
+  }
   if (tiles >= uint64_t(cus)) return p;
-  // 128 x 128 blocks: two fit a compute unit.  When all tokens fit one block
-  // (the codes are then read once in all), slice so that the blocks fill
-  // one round of two per compute unit (8192 x 28672 at 16-64 tokens: 92-93
-  // -> 68-73 us); with several token blocks, one per compute unit
-  // measured faster.
-  uint64_t want = p.big ? uint64_t(cus) / tiles
+  uint64_t want = p.tile == kTile256 ? uint64_t(cus) / tiles
                   : B <= 128 ? std::max<uint64_t>(1, 2 * uint64_t(cus) / tiles)
                              : (uint64_t(cus) + tiles - 1) / tiles;
   want = want < 16 ? want : 16;
@@ -339,8 +348,12 @@ template <int FMT>
 void launch_gemm_fmt(GemmArgs a, const GemmPlan &p, hipStream_t stream) {
   a.splits = p.splits;
   a.split_stages = p.split_stages;
-  if (p.big) launch_gemm<FMT, 256, 256, 128, 64>(a, stream);
-  else launch_gemm<FMT, 128, 128, 64, 64>(a, stream);
+  switch (p.tile) {
+    case kTile256: launch_gemm<FMT, 256, 256, 128, 64>(a, stream); break;
+    case kTile64x256: launch_gemm<FMT, 64, 256, 64, 64>(a, stream); break;
+    case kTile32x256: launch_gemm<FMT, 32, 256, 32, 64>(a, stream); break;
+    default: launch_gemm<FMT, 128, 128, 64, 64>(a, stream); break;
+  }
   if (p.splits > 1) {
     const size_t n = size_t(a.B) * a.M;
     hipLaunchKernelGGL(reduce_splits_kernel, dim3(uint32_t((n + 255) / 256)), dim3(256), 0, stream,

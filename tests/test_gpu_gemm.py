@@ -152,12 +152,13 @@ def test_gemm_codes_entry_and_checks(eq):
                           torch.empty(256, dtype=torch.uint8, device=_dev()))
 
 
-@pytest.mark.parametrize("N,B", [(4096, 20), (4112, 9), (2048, 128)])
+@pytest.mark.parametrize("N,B", [(4096, 20), (4112, 9), (4096, 48), (2048, 128)])
 def test_gemm_split_k(eq, N, B):
     """Few output tiles and long rows: the input columns are cut into slices
-    (16 slices of 4 stages; 13 uneven slices of 5 of 65 stages; 8 of 4), the
-    partial sums reduced in slice order.  Within the bar, deterministic, and
-    the workspace is required."""
+    (32-token blocks: 16 slices of 4 stages, 13 uneven slices of 5 of 65
+    stages; 64-token blocks: 16 of 4; 128 x 128 blocks: 8 of 4), the partial
+    sums reduced in slice order.  Within the bar, deterministic, and the
+    workspace is required."""
     say("split-K", N, B)
     spec = small_spec(100, N, bits=2.0, chunk=8192, lanes=64, seed=4300 + N + B)
     w = synth.weights(spec)

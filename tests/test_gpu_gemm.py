@@ -115,10 +115,13 @@ def test_gemm_one_hot_exact(eq, fmt):
     cols = np.arange(0, N, 3)
     x = np.zeros((cols.size, N), dtype=np.uint16)
     x[np.arange(cols.size), cols] = 0x3F80
-    y = gpu_gemm(eq, L, x)
-    for t, j in enumerate(cols):
-        exact = scale * np.array([oracle.code_value(fmt, int(c)) for c in q[:, j]])
-        assert np.array_equal(y[t].astype(np.float64), exact), j
+    exact = {j: scale * np.array([oracle.code_value(fmt, int(c)) for c in q[:, j]])
+             for j in cols}
+    # 171 tokens: 128 x 128 blocks; 50 and 20: the 64- and 32-token blocks
+    for n in (cols.size, 50, 20):
+        y = gpu_gemm(eq, L, x[:n])
+        for t, j in enumerate(cols[:n]):
+            assert np.array_equal(y[t].astype(np.float64), exact[j]), (n, j)
 
 
 def test_gemm_codes_entry_and_checks(eq):

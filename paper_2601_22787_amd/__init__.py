@@ -497,7 +497,8 @@ def _raw(L) -> eq_layer:
 
 def smoke() -> None:
     """One small decode (codes, BF16), fused GEMV (B = 3) and prefill (24
-    tokens) on cuda:0, checked against the CPU oracle."""
+    tokens) on cuda:0, and the same codes in a version-2 container (codes and
+    the batch-1 GEMV), checked against the CPU oracle."""
     import sys
 
     import torch
@@ -545,5 +546,22 @@ def smoke() -> None:
     yt_ref = oracle.gemv(w_ref, xt_bits)
     err_t = np.abs(yt.cpu().numpy() - yt_ref).max(axis=1) / np.abs(yt_ref).max(axis=1)
     assert (err_t <= 1e-2).all(), f"prefill error {err_t}"
+    # version 2: tiles of 64 x 64, codes and the batch-1 GEMV
+    blob2 = eqe_encode2(w, alpha, tile_rows=64, tile_cols=64)
+    L2 = Layer(blob2, dev)
+    codes2 = torch.empty(spec.params, dtype=torch.uint8, device=dev)
+    eq_decode_codes(L2, codes2)
+    x1 = x[:1].contiguous()
+    y1 = torch.empty(1, spec.rows, dtype=torch.float32, device=dev)
+    eq_decode_gemv(L2, x1, 1, None, y1, L2.workspace(1))
+    _check("eq_get_status", eq_get_status(L2))
+    rc, q2_ref = oracle.container2_decode(blob2)
+    assert rc == oracle.OK
+    assert np.array_equal(codes2.cpu().numpy().reshape(q2_ref.shape), q2_ref), "v2 codes differ"
+    w2_ref = oracle.dequant(q2_ref, oracle.container_scales(blob2))
+    y1_ref = oracle.gemv(w2_ref, synth.activations(spec, B)[:1])
+    err2 = np.abs(y1.cpu().numpy() - y1_ref).max() / np.abs(y1_ref).max()
+    assert err2 <= 1e-2, f"version-2 gemv error {err2}"
     print(f"smoke ok: codes/bf16 bit-exact, gemv max rel err {err.max():.2e}, "
-          f"prefill max rel err {err_t.max():.2e}")
+          f"prefill max rel err {err_t.max():.2e}; version 2: codes bit-exact, "
+          f"gemv rel err {err2:.2e}")

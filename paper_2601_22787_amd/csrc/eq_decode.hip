@@ -1584,6 +1584,7 @@ extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w
     v2 |= L[i]->version == 2;
     if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
   }
+  if (v2 && v2_joint_out_ok(L, n)) return v2_decode_bf16_multi(L, w, n, stream);
   if (n == 1 || v2 || !joint_ok(L, n)) {
     for (uint32_t i = 0; i < n; ++i) {
       const int rc = eq_decode_bf16(L[i], w[i], stream);
@@ -1609,6 +1610,7 @@ extern "C" int eq_decode_codes_multi(const eq_layer *const *L, uint8_t *const *c
     v2 |= L[i]->version == 2;
     if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
   }
+  if (v2 && v2_joint_out_ok(L, n)) return v2_decode_codes_multi(L, codes, n, stream);
   if (n == 1 || v2 || !joint_ok(L, n)) {
     for (uint32_t i = 0; i < n; ++i) {
       const int rc = eq_decode_codes(L[i], codes[i], stream);

@@ -1237,6 +1237,50 @@ size_t v2_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
   return NT > 1 ? round256(size_t(B) * NT * L->rows * sizeof(float)) : 256;
 }
 
+// Block-wise decode of version-2 layers of one tile height to codes or BF16
+// (Sec. 2.2, block-wise decompression), each layer to its own output: one
+// launch, blocks per layer in proportion to its tiles, so that small layers
+// (the key and value projections of a block) run beside large ones instead
+// of leaving most compute units idle in launches of their own.  Packed table
+// entries when every layer allows them.
+bool v2_joint_out_ok(const eq_layer *const *L, uint32_t n) {
+  for (uint32_t i = 0; i < n; ++i)
+    if (!v2_layer_ok(L[i]) || L[i]->lanes != L[0]->lanes) return false;
+  return n >= 2 && n <= kMaxLayers2;
+}
+
+template <int MODE>
+int v2_decode_out_multi(const eq_layer *const *L, uint32_t n, void *const *out, hipStream_t s) {
+  if (!v2_joint_out_ok(L, n)) return EQ_EINVAL;
+  MultiArgs2 m{};
+  m.n = n;
+  bool pk = true;
+  for (uint32_t i = 0; i < n; ++i) {
+    if (!out[i]) return EQ_EINVAL;
+    // output offsets from a tile's origin are 32-bit byte offsets
+    if (uint64_t(2) * L[i]->lanes * L[i]->cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+    m.a[i] = make_args2(L[i]);
+    if (MODE == kCodes2) m.a[i].codes = static_cast<uint8_t *>(out[i]);
+    else m.a[i].wout = static_cast<uint16_t *>(out[i]);
+    pk &= m.a[i].n_syms > 1;
+  }
+  return pk ? launch2_multi<MODE, 1, true>(m, s) : launch2_multi<MODE, 1, false>(m, s);
+}
+
+int v2_decode_codes_multi(const eq_layer *const *L, uint8_t *const *codes, uint32_t n,
+                          hipStream_t s) {
+  void *out[kMaxLayers2] = {};
+  for (uint32_t i = 0; i < n && i < kMaxLayers2; ++i) out[i] = codes[i];
+  return v2_decode_out_multi<kCodes2>(L, n, out, s);
+}
+
+int v2_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
+                         hipStream_t s) {
+  void *out[kMaxLayers2] = {};
+  for (uint32_t i = 0; i < n && i < kMaxLayers2; ++i) out[i] = w[i];
+  return v2_decode_out_multi<kBf16_2>(L, n, out, s);
+}
+
 bool v2_joint_ok(const eq_layer *const *L, uint32_t n) {
   for (uint32_t i = 0; i < n; ++i)
     if (!v2_layer_ok(L[i]) || L[i]->lanes != L[0]->lanes || L[i]->cols != L[0]->cols)

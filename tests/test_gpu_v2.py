@@ -282,3 +282,52 @@ def test_v2_gemv_multi_joint(eq, B):
         err = rel_err(y.cpu().numpy(), oracle.gemv(w_ref, x_bits))
         assert (err <= TOL).all(), err
         assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+@pytest.mark.parametrize("single_phrase", [False, True])
+def test_v2_block_wise_codes_and_bf16(eq, single_phrase):
+    """Block-wise decode of version-2 layers of one tile height (Sec. 2.2):
+    one launch over ragged layers of different widths, tile widths and base
+    formats (with a single-phrase layer: the split table for all), each
+    layer's codes and BF16 bit-exact against the oracle and nothing written
+    outside its output; layers of different tile heights fall back to one
+    launch each, with the same results."""
+    shapes = [(130, 512, 64, 2.0, 1), (40, 640, 256, 3.0, 2), (5, 100, 32, 2.0, 1),
+              (300, 1000, 256, 2.5, 1)]
+    blobs, specs = [], []
+    for i, (M, N, TC, bits, fmt) in enumerate(shapes):
+        spec = small_spec(M, N, bits=bits, seed=2600 + i)
+        w = synth.weights(spec)
+        if single_phrase and i == 2:
+            w = np.zeros_like(w)
+        alpha, _ = eq.eqe_alpha_search(w, bits, base_format=fmt) if w.any() else (1.0, 0)
+        blobs.append(eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=TC, base_format=fmt))
+        specs.append(spec)
+    Ls = [eq.Layer(b, _dev()) for b in blobs]
+    sizes = [L.rows * L.cols for L in Ls]
+    for heights in ("one", "mixed"):
+        layers, bl = list(Ls), list(blobs)
+        if heights == "mixed":
+            spec = small_spec(200, 768, bits=2.0, seed=2650)
+            w = synth.weights(spec)
+            alpha, _ = eq.eqe_alpha_search(w, 2.0)
+            bl.append(eq.eqe_encode2(w, alpha, tile_rows=128, tile_cols=128))
+            layers.append(eq.Layer(bl[-1], _dev()))
+        n = [L.rows * L.cols for L in layers]
+        codes = torch.full((sum(n) + 64,), 0xA5, dtype=torch.uint8, device=_dev())
+        starts = np.cumsum([0] + n)
+        cviews = [codes[starts[i]:starts[i + 1]] for i in range(len(layers))]
+        eq.eq_decode_codes_multi(layers, cviews)
+        bufs = [torch.full((k + 8,), -1, dtype=torch.int16, device=_dev()) for k in n]
+        eq.eq_decode_bf16_multi(layers, [b[:k] for b, k in zip(bufs, n)])
+        assert (codes[sum(n):] == 0xA5).all()
+        for L, blob, cv, b, k in zip(layers, bl, cviews, bufs, n):
+            rc, q_ref = oracle.container2_decode(blob)
+            assert rc == oracle.OK
+            fmt = oracle.container2_info(blob).base_format
+            w_ref = oracle.dequant(q_ref, oracle.container_scales(blob), fmt)
+            assert np.array_equal(cv.cpu().numpy().reshape(q_ref.shape), q_ref), heights
+            got = b.cpu().numpy().view(np.uint16)
+            assert np.array_equal(got[:k].reshape(w_ref.shape), w_ref), heights
+            assert (got[k:] == 0xFFFF).all()
+            assert eq.eq_get_status(L) == eq.EQ_OK

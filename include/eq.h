@@ -141,14 +141,14 @@ int eq_layer_init(eq_layer *L, const void *host_blob, uint64_t blob_bytes, const
  * word.  Must run (on the same stream, or be complete) before any decode. */
 int eq_layer_prepare(const eq_layer *L, hipStream_t stream);
 
-/* Alg. 2 lines 1-2: entropy-decode every chunk; codes[k] is the code (E4M3FN
- * or Int8 byte) of element k of the row-major M x N matrix (M*N bytes,
- * device). */
+/* Alg. 2, entropy decoding and view: decode every chunk; codes[k] is the
+ * code (E4M3FN or Int8 byte) of element k of the row-major M x N matrix
+ * (M*N bytes, device). */
 int eq_decode_codes(const eq_layer *L, uint8_t *codes, hipStream_t stream);
 
-/* Alg. 2 lines 1-2 plus the dequantiser of Sec. 2.1: w[i*N + j] =
- * bf16(s_i * v(q_ij)), the exact product rounded once to nearest-even
- * (M*N BF16 bit patterns, device). */
+/* Alg. 2's entropy decoding and view plus the dequantiser of Sec. 2.1:
+ * w[i*N + j] = bf16(s_i * v(q_ij)), the exact product rounded once to
+ * nearest-even (M*N BF16 bit patterns, device). */
 int eq_decode_bf16(const eq_layer *L, uint16_t *w, hipStream_t stream);
 
 /* Workspace bytes eq_decode_gemv needs for batch B (1..8). */

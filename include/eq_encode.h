@@ -60,7 +60,7 @@ int eqe_encode(const uint16_t *w_bf16, uint32_t M, uint32_t N, float alpha,
 int eqe_encode_scaled(const uint16_t *w_bf16, uint32_t M, uint32_t N, const uint16_t *scale_bf16,
                       const eqe_params *params, uint8_t **blob, uint64_t *blob_bytes);
 
-/* ---- scale optimisation: Sec. 2.2, eq. optimization (Alg. 1 line 2) ----
+/* ---- scale optimisation: Sec. 2.2, eq. optimization (Alg. 1) ----
  * F(S) = ||W - S W_q||_1 / ||W||_1 + lambda * ||W_q||_1 / (M N),  W_q = Q(W / S),
  * minimised over the per-row scales S from the AbsMax start (eq. absmax)
  * with L-BFGS and the straight-through estimator for Q's rounding. */

@@ -631,7 +631,7 @@ int or_container_info(const uint8_t *b, uint64_t bytes, or_info *h) {
   return OR_OK;
 }
 
-/* Alg. 2 line 1 for one chunk. */
+/* Alg. 2, entropy decoding for one chunk. */
 int or_container_decode_chunk(const uint8_t *b, uint64_t bytes, uint32_t c, uint8_t *q) {
   or_info h;
   int rc = or_container_info(b, bytes, &h);
@@ -681,7 +681,7 @@ int or_container_decode(const uint8_t *b, uint64_t bytes, uint8_t *q) {
 }
 
 /* ------------------------------------------------------------------ */
-/* Scale optimisation, Sec. 2.2 eq. optimization (Alg. 1 line 2)        */
+/* Scale optimisation, Sec. 2.2 eq. optimization (Alg. 1)                */
 /* ------------------------------------------------------------------ */
 
 static double sign_of(double v) { return v > 0.0 ? 1.0 : (v < 0.0 ? -1.0 : 0.0); }

@@ -114,7 +114,7 @@ int or_container_decode_chunk(const uint8_t *blob, uint64_t blob_bytes, uint32_t
                               uint8_t *q);
 int or_container_decode(const uint8_t *blob, uint64_t blob_bytes, uint8_t *q);
 
-/* ---- scale optimisation (Sec. 2.2 eq. optimization; Alg. 1 line 2) ----
+/* ---- scale optimisation (Sec. 2.2 eq. optimization; Alg. 1) ----
  * F(S) = sum|W - S*W_q| / sum|W| + lambda * sum|W_q| / (M N), W_q = Q(W/S)
  * (u = W/S in fp32, as the quantiser), with the straight-through gradient
  * dQ/du = 1 where |u| <= Qmax and 0 where the clamp acts. */

@@ -747,7 +747,7 @@ int or_container2_info(const uint8_t *b, uint64_t bytes, or_info2 *h) {
   return OR_OK;
 }
 
-/* Alg. 2 line 1 for one chunk: the tile's codes, row-major (rows x cols of
+/* Alg. 2, entropy decoding for one chunk: the tile's codes, row-major (rows x cols of
  * the tile as or_tile_geometry gives them). */
 int or_container2_decode_chunk(const uint8_t *b, uint64_t bytes, uint32_t c, uint8_t *tile) {
   or_info2 h;

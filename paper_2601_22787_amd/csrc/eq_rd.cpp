@@ -7,7 +7,7 @@
 // with R the entry-wise l1 norm of the quantised values (taken per entry,
 // i.e. divided by M*N, so that lambda is independent of the layer size),
 // starting from the AbsMax scales (eq. absmax), with L-BFGS and the
-// straight-through estimator for the rounding of Q (Alg. 1 line 2).  The
+// straight-through estimator for the rounding of Q (Alg. 1, the scale optimisation).  The
 // objective separates over rows, so one evaluation is one pass over W with
 // rows spread over threads.
 #include <algorithm>

@@ -3,13 +3,13 @@
 Config 4 (the 8192x28672 / 28672x8192 MLP pair) and the three distinct layers
 of the config-5 stack (one per entropy class, all seven matrices) are
 compared element by element against the oracle, with no sampling:
-  - codes (Alg. 2 lines 1-2) and BF16 weights (plus the dequantiser of
+  - codes (Alg. 2, entropy decoding and view) and BF16 weights (plus the dequantiser of
     Sec. 2.1) bit-exact, through the single-layer entry points and through
     the block-wise launches (Sec. 2.2 block-wise decompression: to BF16 as
     the benchmark times it, and to one code buffer for the whole block);
   - the codes also equal the oracle quantiser applied to the generated
     weights;
-  - every output of the fused GEMV (Alg. 2 line 3) within the normwise bar
+  - every output of the fused GEMV (Alg. 2, QMatMul) within the normwise bar
     max|y - y_ref| / max|y_ref| <= 1e-2 per batch row against the oracle's
     fp64 GEMV on the decoded BF16 weights; the elementwise error over the
     entries with |y_ref| >= 1e-3 max|y_ref| is printed beside it.  That

@@ -1,4 +1,4 @@
-"""Oracle container (Alg. 1 end to end, Alg. 2 line 1) and linear layer.
+"""Oracle container (Alg. 1 end to end, Alg. 2, entropy decoding) and linear layer.
 
 Pins: decoded codes equal the quantiser's codes (lossless, Sec. 2.2), the
 header's entropy equals the codes' empirical entropy, payload bits/param is

@@ -1,4 +1,5 @@
-"""Oracle quantiser / dequantiser / scale choice (Sec. 2.1, Alg. 1 lines 1-3).
+"""Oracle quantiser / dequantiser / scale choice (Sec. 2.1; Alg. 1: AbsMax
+initialisation, scale choice, quantisation).
 
 Pins: torch's float32 -> float8_e4m3fn cast (round to nearest even) for Q,
 torch's float32 -> bfloat16 cast of the exact product for the dequantiser,

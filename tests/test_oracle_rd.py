@@ -1,4 +1,4 @@
-"""Scale optimisation of the encoder (Sec. 2.2, eq. optimization; Alg. 1 line 2).
+"""Scale optimisation of the encoder (Sec. 2.2, eq. optimization; Alg. 1, scale optimisation).
 
 Oracle pins: hand-worked objective and straight-through gradient values for
 single weights (E4M3 and Int8, inside and outside the clamp, both signs);

@@ -45,7 +45,8 @@ class Info2(ctypes.Structure):
                [(n, ctypes.c_float) for n in ("alpha", "target_bits", "entropy_bits")] + \
                [(n, ctypes.c_uint64) for n in
                 ("off_scale", "off_phr", "off_freq", "off_chunk_off", "off_chunk_state",
-                 "off_words")]
+                 "off_words")] + \
+               [("flags", ctypes.c_uint32), ("off_order", ctypes.c_uint64)]
 
 
 def build() -> str:
@@ -137,8 +138,9 @@ def lib():
             "or_container2_build": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.c_uint32,
                                                    ctypes.c_float, _vp, ctypes.c_uint32,
                                                    ctypes.c_uint32, ctypes.c_uint32,
-                                                   ctypes.c_uint32, ctypes.c_uint64,
-                                                   ctypes.c_float, ctypes.POINTER(ctypes.c_void_p),
+                                                   ctypes.c_uint32, ctypes.c_uint32,
+                                                   ctypes.c_uint64, ctypes.c_float,
+                                                   ctypes.POINTER(ctypes.c_void_p),
                                                    ctypes.POINTER(ctypes.c_uint64)]),
             "or_container2_info": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.POINTER(Info2)]),
             "or_container2_decode_chunk": (ctypes.c_int, [_vp, ctypes.c_uint64, ctypes.c_uint32,
@@ -594,15 +596,18 @@ def prans_decode(words, states, need, freq, plen, R: int):
 
 def container2_build(w: np.ndarray, alpha: float, TR: int, TC: int, R: int = V2_RES,
                      seed: int = 0, target_bits: float = 0.0, fmt: int = E4M3,
-                     scale: np.ndarray | None = None) -> np.ndarray:
+                     scale: np.ndarray | None = None, row_order: bool = False) -> np.ndarray:
+    """Version-2 container; row_order: tiles cut over the rows sorted by their
+    phrase count (eq_phrase.c, item 4)."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     M, N = w.shape
     if scale is not None:
         scale = np.ascontiguousarray(scale, dtype=np.uint16)
     p = ctypes.c_void_p()
     nb = ctypes.c_uint64()
-    rc = lib().or_container2_build(_ptr(w), M, N, alpha, _ptr(scale), fmt, R, TR, TC, seed,
-                                   target_bits, ctypes.byref(p), ctypes.byref(nb))
+    rc = lib().or_container2_build(_ptr(w), M, N, alpha, _ptr(scale), fmt, R, TR, TC,
+                                   int(bool(row_order)), seed, target_bits, ctypes.byref(p),
+                                   ctypes.byref(nb))
     if rc != OK:
         raise ValueError(f"or_container2_build: {rc}")
     try:
@@ -643,17 +648,29 @@ def container2_decode(blob: np.ndarray):
     return rc, q
 
 
+def container2_row_order(blob: np.ndarray) -> np.ndarray:
+    """order[k]: the matrix row of stored row k (the identity without a row
+    order section)."""
+    info = container2_info(blob)
+    if not info.flags & 1:
+        return np.arange(info.rows, dtype=np.uint32)
+    o = info.off_order
+    return np.frombuffer(np.ascontiguousarray(blob[o:o + 4 * info.rows]).tobytes(),
+                         dtype=np.uint32).copy()
+
+
 def container2_decode_par(blob: np.ndarray, threads: int = 0):
     """container2_decode, tile by tile on several host threads."""
     from concurrent.futures import ThreadPoolExecutor
     blob = np.ascontiguousarray(blob, dtype=np.uint8)
     info = container2_info(blob)
+    order = container2_row_order(blob)
     q = np.zeros((info.rows, info.cols), dtype=np.uint8)
 
     def one(c):
         rc, t = container2_decode_chunk(blob, c)
         r0, c0, rows, cols = tile_geometry(info.rows, info.cols, info.lanes, info.tile_cols, c)
-        q[r0:r0 + rows, c0:c0 + cols] = t
+        q[order[r0:r0 + rows], c0:c0 + cols] = t
         return rc
 
     with ThreadPoolExecutor(_threads(threads)) as ex:

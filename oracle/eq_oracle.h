@@ -149,6 +149,8 @@ typedef struct or_info2 {
   uint64_t total_words, padded_words, seed, file_bytes;
   float alpha, target_bits, entropy_bits;
   uint64_t off_scale, off_phr, off_freq, off_chunk_off, off_chunk_state, off_words;
+  uint32_t flags;      /* bit 0: the rows are tiled in a stored order       */
+  uint64_t off_order;  /* the order section (M uint32), 0 without one       */
 } or_info2;
 
 /* counts of n symbols (each >= 1) to frequencies >= 1 summing to 2^R, by the
@@ -172,11 +174,15 @@ int or_prans_decode(const uint16_t *words, uint64_t n_words, const uint32_t *sta
                     const uint32_t *need, uint32_t W, const uint16_t *freq, const uint8_t *plen,
                     uint32_t n_sym, uint32_t R, uint32_t *tok, const uint64_t *off,
                     uint32_t *got);
+/* row_order 1: tiles cut over the rows by ascending phrase count (eq_phrase.c,
+ * item 4); 0: matrix order */
 int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
                         const uint16_t *given_scale, uint32_t fmt, uint32_t R, uint32_t TR,
-                        uint32_t TC, uint64_t seed, float target_bits, uint8_t **blob,
-                        uint64_t *blob_bytes);
+                        uint32_t TC, uint32_t row_order, uint64_t seed, float target_bits,
+                        uint8_t **blob, uint64_t *blob_bytes);
 int or_container2_info(const uint8_t *blob, uint64_t blob_bytes, or_info2 *info);
+/* the matrix row of stored row k (info from or_container2_info) */
+uint32_t or_container2_row(const uint8_t *blob, const or_info2 *info, uint32_t k);
 int or_container2_decode_chunk(const uint8_t *blob, uint64_t blob_bytes, uint32_t chunk,
                                uint8_t *tile);
 int or_container2_decode(const uint8_t *blob, uint64_t blob_bytes, uint8_t *q);

@@ -44,6 +44,19 @@
  *    order, take the next word if x < 2^16.  States finish at different
  *    steps (segments hold different numbers of symbols).  After the last
  *    step every state is back at 2^16 and the words are used up.
+ *
+ * 4. Row order (optional, flag bit 0): the tiles of item 1 are cut over the
+ *    rows taken in a stored order, row k of the stored matrix being matrix
+ *    row order[k] (a permutation, kept in its own section; the scales stay
+ *    in matrix order).  A state's segment is then a stretch of matrix row
+ *    order[b TR + s].  Encoder rule: the rows by ascending number of
+ *    phrases of their parse (item 2, summed over the row's segments), ties
+ *    by lower row index.  The alphabet does not depend on the row order (its
+ *    counts are sums over segments), so the container equals, section for
+ *    section, the matrix-order container of the row-permuted codes, apart
+ *    from the scales and the order section.  A tile lasts as long as its
+ *    longest segment (the decoder's steps), so rows of like length in one
+ *    tile shorten the tiles.
  */
 #include <math.h>
 #include <stdint.h>
@@ -543,17 +556,30 @@ enum {
   H_TOTAL_WORDS = 48, H_PADDED_WORDS = 56, H_SEED = 64, H_ALPHA = 72, H_TARGET = 76,
   H_ENTROPY = 80, H_TILE_COLS = 84, H_OFF_SCALE = 88, H_OFF_PHR = 96, H_OFF_FREQ = 104,
   H_OFF_CHUNK_OFF = 112, H_OFF_CHUNK_STATE = 120, H_OFF_WORDS = 128, H_FILE_BYTES = 136,
-  H_NQUAD = 144, H_NPAIR = 148, H_NSINGLE = 152, H_TAU = 156, HEADER_BYTES = 256
+  H_NQUAD = 144, H_NPAIR = 148, H_NSINGLE = 152, H_TAU = 156, H_OFF_ORDER = 160,
+  HEADER_BYTES = 256
 };
+enum { FLAG_ROW_ORDER = 1u };
 
 static uint64_t padded_words_for(uint64_t total) { return (total + 1024 + 127) & ~(uint64_t)127; }
 
+/* rows by ascending phrase count, ties by lower row index (item 4) */
+typedef struct {
+  uint64_t cost;
+  uint32_t row;
+} row_cost_t;
+static int row_cost_cmp(const void *pa, const void *pb) {
+  const row_cost_t *a = (const row_cost_t *)pa, *b = (const row_cost_t *)pb;
+  if (a->cost != b->cost) return a->cost < b->cost ? -1 : 1;
+  return a->row < b->row ? -1 : (a->row > b->row);
+}
+
 int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
                         const uint16_t *given_scale, uint32_t fmt, uint32_t R, uint32_t TR,
-                        uint32_t TC, uint64_t seed, float target_bits, uint8_t **blob_out,
-                        uint64_t *blob_bytes) {
+                        uint32_t TC, uint32_t row_order, uint64_t seed, float target_bits,
+                        uint8_t **blob_out, uint64_t *blob_bytes) {
   if (!w || M == 0 || N == 0 || R < 10 || R > 12 || (TR != 64 && TR != 128 && TR != 256) ||
-      TC == 0 || TC % 4 || (fmt != OR_FMT_E4M3 && fmt != OR_FMT_INT8))
+      TC == 0 || TC % 4 || (fmt != OR_FMT_E4M3 && fmt != OR_FMT_INT8) || row_order > 1)
     return OR_EINVAL;
   uint64_t n = (uint64_t)M * N;
   if (n >= (1ull << 32) || (uint64_t)TR * TC >= (1ull << 32)) return OR_EINVAL;
@@ -569,6 +595,9 @@ int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
   uint16_t *words = (uint16_t *)malloc(sizeof(uint16_t) * ((size_t)n + 16));
   uint32_t *chunk_off = (uint32_t *)malloc(sizeof(uint32_t) * ((size_t)n_chunks + 1));
   uint32_t *states = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)n_chunks * TR);
+  uint32_t *order = NULL;
+  uint8_t *qs = NULL;
+  row_cost_t *rc_rows = NULL;
   alphabet_t best, cur;
   memset(&best, 0, sizeof best);
   memset(&cur, 0, sizeof cur);
@@ -601,6 +630,39 @@ int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
     if (rc != OR_OK) goto done;
     alphabet_free(&cur);
   }
+  if (row_order) {
+    /* item 4: each row's phrase count over its segments, the rows sorted by
+     * it, and the parse of the codes with their rows in that order (the
+     * same alphabet: its counts do not depend on the order of the rows) */
+    order = (uint32_t *)malloc(sizeof(uint32_t) * M);
+    qs = (uint8_t *)malloc((size_t)n);
+    rc_rows = (row_cost_t *)malloc(sizeof(row_cost_t) * M);
+    if (!order || !qs || !rc_rows) {
+      rc = OR_ENOMEM;
+      goto done;
+    }
+    for (uint32_t i = 0; i < M; ++i) {
+      uint64_t cost = 0;
+      for (uint32_t t = 0; t < NT; ++t) cost += tok_len[((uint64_t)(i / TR) * NT + t) * TR + i % TR];
+      rc_rows[i].cost = cost;
+      rc_rows[i].row = i;
+    }
+    qsort(rc_rows, M, sizeof(row_cost_t), row_cost_cmp);
+    for (uint32_t k = 0; k < M; ++k) {
+      order[k] = rc_rows[k].row;
+      memcpy(qs + (uint64_t)k * N, q + (uint64_t)order[k] * N, N);
+    }
+    rc = build_alphabet(qs, M, N, TR, TC, R, best_tau, n_chunks, tok, tok_off, tok_len, &cur);
+    if (rc != OR_OK) goto done;
+    int same = cur.n_sym == best.n_sym && cur.nq == best.nq && cur.np == best.np &&
+               cur.ns == best.ns;
+    for (uint32_t k = 0; same && k < best.n_sym; ++k) same = cur.freq[k] == best.freq[k];
+    alphabet_free(&cur);
+    if (!same) {
+      rc = OR_EINVAL;
+      goto done;
+    }
+  }
   uint32_t nq = best.nq, np = best.np, ns = best.ns, n_sym = best.n_sym;
   uint64_t total = 0;
   for (uint32_t c = 0; c < n_chunks; ++c) {
@@ -626,7 +688,8 @@ int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
   uint64_t o_freq = align256(o_phr + 4ull * n_sym);
   uint64_t o_coff = align256(o_freq + 2ull * n_sym);
   uint64_t o_cst = align256(o_coff + 4ull * (n_chunks + 1));
-  uint64_t o_words = align256(o_cst + 4ull * n_chunks * TR);
+  uint64_t o_order = row_order ? align256(o_cst + 4ull * n_chunks * TR) : 0;
+  uint64_t o_words = row_order ? align256(o_order + 4ull * M) : align256(o_cst + 4ull * n_chunks * TR);
   uint64_t bytes = align256(o_words + 2ull * padded);
   uint8_t *b = (uint8_t *)calloc(1, bytes);
   if (!b) {
@@ -644,7 +707,7 @@ int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
   put32(b, H_LANES, TR);
   put32(b, H_PBITS, R);
   put32(b, H_NSYMS, n_sym);
-  put32(b, H_FLAGS, 0);
+  put32(b, H_FLAGS, row_order ? FLAG_ROW_ORDER : 0);
   put64(b, H_TOTAL_WORDS, total);
   put64(b, H_PADDED_WORDS, padded);
   put64(b, H_SEED, seed);
@@ -670,6 +733,9 @@ int or_container2_build(const uint16_t *w, uint32_t M, uint32_t N, float alpha,
   put32(b, H_NPAIR, np);
   put32(b, H_NSINGLE, ns);
   put32(b, H_TAU, best_tau);
+  put64(b, H_OFF_ORDER, o_order);
+  if (row_order)
+    for (uint32_t k = 0; k < M; ++k) put32(b, o_order + 4ull * k, order[k]);
   for (uint32_t i = 0; i < M; ++i) {
     b[o_scale + 2ull * i] = (uint8_t)scale[i];
     b[o_scale + 2ull * i + 1] = (uint8_t)(scale[i] >> 8);
@@ -693,7 +759,7 @@ done:
   alphabet_free(&best);
   alphabet_free(&cur);
   free(scale), free(q), free(tok), free(tok_off), free(tok_len);
-  free(words), free(chunk_off), free(states);
+  free(words), free(chunk_off), free(states), free(order), free(qs), free(rc_rows);
   return rc;
 }
 
@@ -727,6 +793,8 @@ int or_container2_info(const uint8_t *b, uint64_t bytes, or_info2 *h) {
   h->off_chunk_state = get64(b, H_OFF_CHUNK_STATE);
   h->off_words = get64(b, H_OFF_WORDS);
   h->file_bytes = get64(b, H_FILE_BYTES);
+  h->flags = get32(b, H_FLAGS);
+  h->off_order = get64(b, H_OFF_ORDER);
   uint64_t n = (uint64_t)h->rows * h->cols;
   uint32_t TR = h->lanes, TC = h->tile_cols;
   if ((h->base_format != OR_FMT_E4M3 && h->base_format != OR_FMT_INT8) || n == 0 ||
@@ -744,11 +812,31 @@ int or_container2_info(const uint8_t *b, uint64_t bytes, or_info2 *h) {
       h->off_chunk_state + 4ull * h->n_chunks * TR > h->file_bytes ||
       h->off_words + 2ull * h->padded_words > h->file_bytes)
     return OR_EFORMAT;
-  return OR_OK;
+  /* item 4: the order section, a permutation of the rows */
+  if (h->flags & ~(uint32_t)FLAG_ROW_ORDER) return OR_EFORMAT;
+  if (!(h->flags & FLAG_ROW_ORDER)) return h->off_order == 0 ? OR_OK : OR_EFORMAT;
+  if (h->off_order < HEADER_BYTES || h->off_order + 4ull * h->rows > h->file_bytes)
+    return OR_EFORMAT;
+  uint8_t *seen = (uint8_t *)calloc(h->rows, 1);
+  if (!seen) return OR_ENOMEM;
+  int rc = OR_OK;
+  for (uint32_t k = 0; k < h->rows && rc == OR_OK; ++k) {
+    uint32_t r = get32(b, h->off_order + 4ull * k);
+    if (r >= h->rows || seen[r]) rc = OR_EFORMAT;
+    else seen[r] = 1;
+  }
+  free(seen);
+  return rc;
+}
+
+/* Matrix row of stored row k (item 4; the identity without a row order). */
+uint32_t or_container2_row(const uint8_t *b, const or_info2 *h, uint32_t k) {
+  return (h->flags & FLAG_ROW_ORDER) ? get32(b, h->off_order + 4ull * k) : k;
 }
 
 /* Alg. 2, entropy decoding for one chunk: the tile's codes, row-major (rows x cols of
- * the tile as or_tile_geometry gives them). */
+ * the tile as or_tile_geometry gives them; tile row s is stored row r0 + s, which
+ * or_container2_row maps to its matrix row). */
 int or_container2_decode_chunk(const uint8_t *b, uint64_t bytes, uint32_t c, uint8_t *tile) {
   or_info2 h;
   int rc = or_container2_info(b, bytes, &h);
@@ -815,7 +903,8 @@ int or_container2_decode(const uint8_t *b, uint64_t bytes, uint8_t *q) {
     rc = or_container2_decode_chunk(b, bytes, c, tile);
     if (rc != OR_OK && worst == OR_OK) worst = rc;
     for (uint32_t s = 0; s < rows; ++s)
-      memcpy(q + (uint64_t)(r0 + s) * h.cols + c0, tile + (uint64_t)s * cols, cols);
+      memcpy(q + (uint64_t)or_container2_row(b, &h, r0 + s) * h.cols + c0,
+             tile + (uint64_t)s * cols, cols);
   }
   free(tile);
   return worst;

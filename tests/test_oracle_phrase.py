@@ -343,3 +343,132 @@ def test_container2_int8_and_header_checks():
         oracle.container2_build(w, alpha, 96, 128)   # tile rows not 64/128/256
     with pytest.raises(ValueError):
         oracle.container2_build(w, alpha, 64, 126)   # tile columns not a multiple of 4
+
+
+# ---- row order (eq_phrase.c, item 4) ----
+
+def _row_costs(blob, q):
+    """Phrases of each matrix row's greedy parse, summed over its tile
+    segments: a plain loop over the container's dictionary (quads first,
+    then pairs, then the single code)."""
+    info = oracle.container2_info(blob)
+    codes, plen, _ = oracle.container2_phrases(blob)
+    quads = {tuple(int(v) for v in codes[k][:4]) for k in range(len(plen)) if plen[k] == 4}
+    pairs = {tuple(int(v) for v in codes[k][:2]) for k in range(len(plen)) if plen[k] == 2}
+    M, N = q.shape
+    TC = info.tile_cols
+    cost = []
+    for r in range(M):
+        n = 0
+        for c0 in range(0, N, TC):
+            u = [int(v) for v in q[r, c0:c0 + TC]]
+            j = 0
+            while j < len(u):
+                if j + 4 <= len(u) and tuple(u[j:j + 4]) in quads:
+                    j += 4
+                elif j + 2 <= len(u) and tuple(u[j:j + 2]) in pairs:
+                    j += 2
+                else:
+                    j += 1
+                n += 1
+        cost.append(n)
+    return np.array(cost)
+
+
+@pytest.mark.parametrize("M,N,TR,TC", SHAPES)
+def test_container2_row_order_round_trip(M, N, TR, TC):
+    """Tiles cut over the rows in their stored order: every tile's codes are
+    the stored rows' codes, and the whole decode is the quantised matrix."""
+    w = synth.weights(small_spec(M, N, seed=M * 31 + N))
+    alpha, _ = oracle.alpha_search(w, 2.5)
+    blob = oracle.container2_build(w, alpha, TR, TC, row_order=True)
+    info = oracle.container2_info(blob)
+    assert info.flags == 1
+    order = oracle.container2_row_order(blob)
+    assert sorted(order.tolist()) == list(range(M))
+    rc, q = oracle.container2_decode(blob)
+    assert rc == oracle.OK
+    assert np.array_equal(q, oracle.quantize(w, oracle.container_scales(blob)))
+    for c in range(info.n_chunks):
+        rc, t = oracle.container2_decode_chunk(blob, c)
+        r0, c0, rows, cols = oracle.tile_geometry(M, N, TR, TC, c)
+        assert rc == oracle.OK and np.array_equal(t, q[order[r0:r0 + rows], c0:c0 + cols])
+    rc, qp = oracle.container2_decode_par(blob)
+    assert rc == oracle.OK and np.array_equal(qp, q)
+
+
+def test_container2_row_order_sorts_by_phrase_count():
+    """The stored order is the rows by ascending phrase count, ties by lower
+    row index, with the counts from a plain greedy parse; rows of very
+    different code ranges (a few near-zero rows, a few with a large scale)
+    make the order far from the identity."""
+    M, N = 300, 1024
+    w = synth.weights(small_spec(M, N, seed=12)).copy()
+    w[::7] = 0                                      # all-zero rows: the cheapest
+    w[3::11, 5] = np.uint16(0x4480)                 # one large weight: codes near zero
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    blob = oracle.container2_build(w, alpha, 64, 256, row_order=True)
+    rc, q = oracle.container2_decode(blob)
+    assert rc == oracle.OK
+    cost = _row_costs(blob, q)
+    assert len(set(cost.tolist())) > 10
+    want = sorted(range(M), key=lambda r: (cost[r], r))
+    order = oracle.container2_row_order(blob)
+    assert order.tolist() == want
+    assert cost[order[0]] == N // 4                # an all-zero row: zero quads only
+
+
+def _sections(blob):
+    info = oracle.container2_info(blob)
+    n_st = 4 * info.n_chunks * info.lanes
+    return {
+        "phr": blob[info.off_phr:info.off_phr + 4 * info.n_syms].tobytes(),
+        "freq": blob[info.off_freq:info.off_freq + 2 * info.n_syms].tobytes(),
+        "off": blob[info.off_chunk_off:info.off_chunk_off + 4 * (info.n_chunks + 1)].tobytes(),
+        "state": blob[info.off_chunk_state:info.off_chunk_state + n_st].tobytes(),
+        "words": blob[info.off_words:info.off_words + 2 * info.total_words].tobytes(),
+        "tau": info.tau,
+    }
+
+
+def test_container2_row_order_is_the_row_permuted_container():
+    """With a row order, the container codes exactly the row-permuted
+    matrix: alphabet, chunk offsets, states and words equal those of the
+    matrix-order container of w[order] (with its scales permuted alike),
+    and the scales stay in matrix order."""
+    w = synth.weights(small_spec(200, 520, seed=21)).copy()
+    w[::5] = 0
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    blob = oracle.container2_build(w, alpha, 64, 128, row_order=True)
+    order = oracle.container2_row_order(blob)
+    scale = oracle.container_scales(blob)
+    assert np.array_equal(scale, oracle.row_scales(w, alpha))
+    ref = oracle.container2_build(w[order], 0.0, 64, 128, scale=scale[order])
+    assert oracle.container2_info(ref).flags == 0
+    assert _sections(blob) == _sections(ref)
+
+
+def test_container2_row_order_checks():
+    """A damaged order section (a repeated row, a row out of range), an
+    unknown flag, or an order offset without the flag is refused."""
+    w = synth.weights(small_spec(70, 256, seed=3))
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    blob = oracle.container2_build(w, alpha, 64, 128, row_order=True)
+    info = oracle.container2_info(blob)
+    o = info.off_order
+    for k, val in ((1, int(oracle.container2_row_order(blob)[0])), (5, 70)):
+        bad = blob.copy()
+        bad[o + 4 * k:o + 4 * k + 4] = np.frombuffer(np.uint32(val).tobytes(), dtype=np.uint8)
+        with pytest.raises(ValueError):
+            oracle.container2_info(bad)
+    bad = blob.copy()
+    bad[44:48] = np.frombuffer(np.uint32(3).tobytes(), dtype=np.uint8)
+    with pytest.raises(ValueError):
+        oracle.container2_info(bad)
+    bad = blob.copy()
+    bad[44:48] = 0                                  # offset present, flag clear
+    with pytest.raises(ValueError):
+        oracle.container2_info(bad)
+    plain = oracle.container2_build(w, alpha, 64, 128)
+    assert oracle.container2_info(plain).off_order == 0
+    assert np.array_equal(oracle.container2_row_order(plain), np.arange(70))

@@ -815,7 +815,8 @@ int or_container2_info(const uint8_t *b, uint64_t bytes, or_info2 *h) {
   /* item 4: the order section, a permutation of the rows */
   if (h->flags & ~(uint32_t)FLAG_ROW_ORDER) return OR_EFORMAT;
   if (!(h->flags & FLAG_ROW_ORDER)) return h->off_order == 0 ? OR_OK : OR_EFORMAT;
-  if (h->off_order < HEADER_BYTES || h->off_order + 4ull * h->rows > h->file_bytes)
+  if (h->off_order < HEADER_BYTES || h->off_order > h->file_bytes ||
+      4ull * h->rows > h->file_bytes - h->off_order)
     return OR_EFORMAT;
   uint8_t *seen = (uint8_t *)calloc(h->rows, 1);
   if (!seen) return OR_ENOMEM;

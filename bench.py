@@ -72,6 +72,9 @@ def parse():
     ap.add_argument("--tokens", type=int, default=2048, help="prefill batch (tokens)")
     ap.add_argument("--container", type=int, choices=(1, 2), default=1,
                     help="c5 workload: container version of the stack's layers")
+    ap.add_argument("--row-order", action="store_true",
+                    help="version-2 containers with the row order: tiles cut over the rows "
+                         "sorted by their phrase count")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="oracle threads for the all-cores sample (0: host CPUs, at most 16)")
     ap.add_argument("--base-format", choices=tuple(FORMATS), default="e4m3",
@@ -91,11 +94,11 @@ def v2_tile_rows(chunk_syms):
     return 256 if chunk_syms >= 65536 else 128
 
 
-def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0):
+def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0, row_order=False):
     """Encode each matrix (product encoder) and upload `copies` device copies;
     with v2_copies > 0 also the same codes (same alpha) in container version
     2, tiles of v2_tile_rows(C) rows x C / rows columns (the same C symbols
-    per chunk)."""
+    per chunk), with the row order if row_order."""
     out = []
     for spec in specs:
         t0 = time.time()
@@ -110,7 +113,7 @@ def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0):
             tr = v2_tile_rows(spec.chunk_syms)
             blob2 = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=spec.chunk_syms // tr,
                                    seed=spec.seed, target_bits=spec.target_bits,
-                                   base_format=fmt)
+                                   base_format=fmt, row_order=row_order)
             item["blob2"] = blob2
             item["layers2"] = [eq.Layer(blob2, dev) for _ in range(v2_copies)]
             msg += f", version 2 {blob2.size / 1e6:.1f} MB"
@@ -386,7 +389,8 @@ def run_stack(args):
             if args.container == 2:
                 tr = v2_tile_rows(spec.chunk_syms)
                 blob = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=spec.chunk_syms // tr,
-                                      seed=spec.seed, target_bits=spec.target_bits)
+                                      seed=spec.seed, target_bits=spec.target_bits,
+                                      row_order=args.row_order)
             else:
                 blob = eq.eqe_encode(w, alpha, chunk_syms=spec.chunk_syms, lanes=spec.lanes,
                                      seed=spec.seed, target_bits=spec.target_bits)
@@ -478,6 +482,7 @@ def run_stack(args):
                                "gate/up 28672x8192, down 8192x28672}, (2,3,4)[l mod 3] bits, "
                                "65536-symbol chunks; 3 distinct layers, 80 device copies",
                    "container": args.container,
+                   "v2_row_order": bool(args.row_order and args.container == 2),
                    "launch": "eager" if args.eager else "HIP graph of each 80-layer pass",
                    "params": params, "container_gb": round(cont_bytes / 1e9, 3),
                    "hbm_frac_compressed_block_gemv": round(
@@ -488,7 +493,7 @@ def run_stack(args):
 def run_small(args):
     """Configs 1-3 (1024x1024; the 4096x4096 Llama-2-7B attention projection;
     its 11008x4096 / 4096x11008 MLP matrices): for each matrix, decode to BF16
-    and the fused decode-GEMV at B = 1, each launch timed alone with HIP events
+    and the fused decode-GEMV at B = 1 and 8, each launch timed alone with HIP events
     over `--copies` rotated container copies.  Reports us per launch,
     Gparams/s and the fraction of the HBM peak on the algorithmic bytes."""
     import numpy as np
@@ -519,23 +524,27 @@ def run_small(args):
 
     for cfg in (1, 2, 3):
         specs = config_matrices(cfg)
-        for item in build_layers(eq, synth, specs, args.copies, dev, v2_copies=args.copies):
+        for item in build_layers(eq, synth, specs, args.copies, dev, v2_copies=args.copies,
+                                 row_order=args.row_order):
             spec = item["spec"]
             out = torch.empty(spec.params, dtype=torch.int16, device=dev)
             x = torch.from_numpy(synth.activations(spec, 1).view(np.int16)).to(dev)
             y = torch.empty(1, spec.rows, dtype=torch.float32, device=dev)
+            x8 = torch.from_numpy(synth.activations(spec, 8).view(np.int16)).to(dev)
+            y8 = torch.empty(8, spec.rows, dtype=torch.float32, device=dev)
             for version, blob, lays in ((1, item["blob"], item["layers"]),
                                         (2, item["blob2"], item["layers2"])):
                 info = blob_info(blob)
-                ws = lays[0].workspace(1)
+                ws = lays[0].workspace(8)
                 fns = {"bf16": lambda L: eq.eq_decode_bf16(L, out),
-                       "gemv1": lambda L, ws=ws: eq.eq_decode_gemv(L, x, 1, None, y, ws)}
+                       "gemv1": lambda L, ws=ws: eq.eq_decode_gemv(L, x, 1, None, y, ws),
+                       "gemv8": lambda L, ws=ws: eq.eq_decode_gemv(L, x8, 8, None, y8, ws)}
                 for op, fn in fns.items():
                     ts = time_op(fn, lays)
                     us_eager = sum(ts) / len(ts)
                     us = us_eager if args.eager else time_graph(
                         lambda i, fn=fn: fn(lays[i]), len(lays), 3)
-                    nbytes = algorithmic_bytes(info, op, 1)
+                    nbytes = algorithmic_bytes(info, op, 8 if op == "gemv8" else 1)
                     rows.append({"config": cfg, "matrix": spec.name,
                                  "shape": [spec.rows, spec.cols], "container": version,
                                  "chunk_syms": spec.chunk_syms, "lanes": spec.lanes,
@@ -570,6 +579,7 @@ def run_small(args):
         "config": {"workload": "config 1: 1024x1024, 2 bits, 4096-symbol chunks; config 2: "
                                "4096x4096, 3 bits, 16384-symbol chunks; config 3: 11008x4096 x2 "
                                "and 4096x11008 with 0.1% outliers, 2 bits, 16384-symbol chunks",
+                   "v2_row_order": bool(args.row_order),
                    "copies_rotated": args.copies},
         "matrices": rows, "env": run_env()}), flush=True)
 
@@ -768,7 +778,8 @@ def run_c4(args):
     specs = config_matrices(4)
     fmt = FORMATS[args.base_format]
     kernel_names = KERNEL if fmt == 1 else KERNEL_INT8
-    layers = build_layers(eq, synth, specs, args.copies, dev, fmt, v2_copies=args.copies)
+    layers = build_layers(eq, synth, specs, args.copies, dev, fmt, v2_copies=args.copies,
+                          row_order=args.row_order)
     ops = ["bf16", "gemv1", "gemv8"]
     copies = args.copies
 
@@ -1005,6 +1016,7 @@ def run_c4(args):
                    "entropy_bits": [round(i["entropy"], 4) for i in infos],
                    "container_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos],
                    "container_v2_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos2],
+                   "v2_row_order": bool(args.row_order),
                    "copies_rotated": copies,
                    "launch": "eager" if args.eager else "HIP graphs of the step"},
         "roofline": {"bound": "hbm", "kernel": kernel_names[dom], "op": dom,

@@ -58,7 +58,15 @@
  *   < 2^(16-R) (cum_k + f_k), x = F_k (x >> 16) + slot - 2^(16-R) cum_k with
  *   F_k = 2^(16-R) f_k, and appends its 4, 2 or 1 codes to the segment; then
  *   those states in ascending order take the next word when x < 2^16.
- *   Decoding a version-2 layer to codes or BF16 needs 2 * TR * N < 2^31.
+ *   Row order (44 flags bit 0; other bits 0): the tiles are cut over the rows
+ *   in a stored order, the section at byte offset 160 (u64; 0 without the
+ *   flag), u32[M], giving the matrix row of stored row k (a permutation).
+ *   Chunk c's rows are then stored rows [b TR, b TR + TR): state s codes a
+ *   segment of matrix row order[b TR + s].  Scales stay in matrix order, and
+ *   every output is in matrix order.  The encoder sorts rows by their phrase
+ *   count, so that a tile's states finish at nearly the same step.
+ *   Decoding a version-2 layer without a row order to codes or BF16 needs
+ *   2 * TR * N < 2^31.
  *
  * Conventions for every entry point below:
  *  - Device pointers are allocated and owned by the caller; the library never
@@ -114,6 +122,7 @@ typedef struct eq_layer {
   uint32_t version;          /* container version, 1 or 2                          */
   uint32_t tile_cols;        /* version 2: tile columns TC (tile rows = lanes)     */
   uint32_t n_quads, n_pairs, n_singles; /* version 2: alphabet parts (sum n_syms) */
+  const uint32_t *row_order; /* version 2, device: the order section, or null      */
 } eq_layer;
 
 /* Bytes of device scratch the decode tables of a layer need (either
@@ -129,7 +138,8 @@ size_t eq_lut_bytes(void);
  * and section bounds, 8 <= P <= 12 (the kernels multiply f by x >> P with
  * 24-bit operands), ascending symbols valid in the base format, frequencies
  * >= 1 summing to 2^P, monotone chunk offsets ending at total_words,
- * padding >= 1024 words, initial states in [2^16, 2^32), scales finite with
+ * padding >= 1024 words, initial states in [2^16, 2^32), a version-2 row
+ * order that is a permutation of the rows, scales finite with
  * magnitude in [2^-117, 2^120) (so every dequantised product s * v(q), an
  * 8-bit by at most 7-bit significand product, is exact in fp32).
  * Returns EQ_OK, EQ_EINVAL or EQ_EFORMAT. */

@@ -120,7 +120,12 @@ int eqe_rd_lambda_search(const uint16_t *w_bf16, uint32_t M, uint32_t N, double 
  *  - coder: interleaved rANS with the state arithmetic at 2^16 and
  *    frequencies F = f * 2^(16 - R); step t decodes the t-th symbol of every
  *    state whose segment is not yet complete, then those states take a word
- *    in ascending order when x < 2^16 (layout of the container: eq.h). */
+ *    in ascending order when x < 2^16 (layout of the container: eq.h);
+ *  - row order (optional): the tiles are cut over the rows taken by
+ *    ascending phrase count of their parse (summed over the row's segments;
+ *    ties: lower row).  A tile takes as many decode steps as its longest
+ *    segment has phrases, so alike rows in a tile shorten it.  The alphabet
+ *    does not depend on the order. */
 typedef struct eqe_params2 {
   uint32_t res_bits;    /* R: frequency resolution, 10..12 (12 recommended)          */
   uint32_t tile_rows;   /* TR: coder states per chunk, 64, 128 or 256                */
@@ -129,6 +134,9 @@ typedef struct eqe_params2 {
   uint64_t seed;        /* recorded in the header, not used                         */
   float target_bits;    /* recorded in the header, not used                         */
   uint32_t base_format; /* 1 = E4M3FN (0 is read as 1), 2 = Int8                    */
+  uint32_t row_order;   /* 1: tiles cut over the rows by ascending phrase count
+                           (ties: lower row), recorded in the order section; 0:
+                           matrix order                                          */
 } eqe_params2;
 
 /* Quantise w (M x N BF16, host) with scales bf16(alpha * absmax / Qmax), or

@@ -39,7 +39,7 @@ class eq_layer(ctypes.Structure):
                 ("chunk_state", _vp), ("words", _vp), ("lut", _vp), ("status", _vp),
                 ("version", ctypes.c_uint32), ("tile_cols", ctypes.c_uint32),
                 ("n_quads", ctypes.c_uint32), ("n_pairs", ctypes.c_uint32),
-                ("n_singles", ctypes.c_uint32)]
+                ("n_singles", ctypes.c_uint32), ("row_order", _vp)]
 
 
 class eqe_params(ctypes.Structure):
@@ -53,7 +53,7 @@ class eqe_params2(ctypes.Structure):
     _fields_ = [("res_bits", ctypes.c_uint32), ("tile_rows", ctypes.c_uint32),
                 ("tile_cols", ctypes.c_uint32), ("threads", ctypes.c_uint32),
                 ("seed", ctypes.c_uint64), ("target_bits", ctypes.c_float),
-                ("base_format", ctypes.c_uint32)]
+                ("base_format", ctypes.c_uint32), ("row_order", ctypes.c_uint32)]
 
 
 class eqe_rd_params(ctypes.Structure):
@@ -384,10 +384,13 @@ def eqe_encode(w: np.ndarray, alpha: float, *, prob_bits: int = 12, chunk_syms: 
 
 def eqe_encode2(w: np.ndarray, alpha: float, *, tile_rows: int, tile_cols: int,
                 res_bits: int = 12, threads: int = 0, seed: int = 0, target_bits: float = 0.0,
-                base_format: int = FMT_E4M3, scale_bf16: np.ndarray | None = None) -> np.ndarray:
-    """A version-2 container (tile-ordered chunks, phrase alphabet)."""
+                base_format: int = FMT_E4M3, scale_bf16: np.ndarray | None = None,
+                row_order: bool = False) -> np.ndarray:
+    """A version-2 container (tile-ordered chunks, phrase alphabet); with
+    row_order, the tiles are cut over the rows sorted by phrase count."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
-    prm = eqe_params2(res_bits, tile_rows, tile_cols, threads, seed, target_bits, base_format)
+    prm = eqe_params2(res_bits, tile_rows, tile_cols, threads, seed, target_bits, base_format,
+                      int(bool(row_order)))
     sc = None
     if scale_bf16 is not None:
         sc = np.ascontiguousarray(scale_bf16, dtype=np.uint16)

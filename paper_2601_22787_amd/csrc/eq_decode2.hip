@@ -33,6 +33,12 @@
 // Codes and BF16 output: each phrase's codes go to an LDS ring of its row,
 // and whole 32-code segments of rows leave the wavefront together, so that
 // stores write contiguous lines.
+//
+// Row order: a container may cut its tiles over the rows in a stored order
+// (row k of the tiling is matrix row order[k]; the encoder groups rows of
+// like phrase counts, so a tile's states finish at nearly the same step).
+// Only the outputs move: row sums (GEMV), scales and written rows go to the
+// matrix row, the partial sums of the column tiles stay in stored order.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -100,8 +106,20 @@ struct Args2 {
   uint32_t n_syms;           // phrases in the alphabet
   const uint16_t *bias;
   float *y;
-  float *ws;                 // partial row sums [batch][NT][rows] (NT > 1)
+  float *ws;                 // partial row sums [batch][NT][rows] (NT > 1), stored order
+  const uint32_t *order;     // matrix row of each stored row; null: the identity
 };
+
+// The matrix row of stored row k.  A damaged order section (a row out of
+// range; the host checked its own copy) marks the layer corrupt and keeps
+// the row in place, so no store leaves the output.
+__device__ inline uint32_t out_row(const Args2 &a, uint32_t k) {
+  if (!a.order) return k;
+  const uint32_t r = as_const(a.order)[k];
+  if (r < a.rows) return r;
+  atomicOr(a.status, 1);
+  return k;
+}
 
 // x' = x - ((2^16 - F) * (x >> 16) + cum): the 16-bit multiply takes the low
 // half of e.x and the high half of x.
@@ -127,6 +145,9 @@ __device__ inline uint32_t state_update_pk(uint32_t x, uint32_t w) {
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// the same at any byte address (outputs of an ordered layer: one store each)
+typedef uint32_t u32x2u __attribute__((ext_vector_type(2), aligned(1)));
+typedef uint32_t u32x4u __attribute__((ext_vector_type(4), aligned(1)));
 
 
 // LDS byte offset of the state half of the bucket of state x (the table
@@ -163,6 +184,8 @@ struct Tile {
                      // not yet written (pos mod 4 of them, low bytes first)
   bool cr[G];        // codes / BF16: the last phrase completed a segment
   uint32_t ring, list;  // codes / BF16: LDS addresses of the rings, the flush list
+  uint32_t rmap;        // codes / BF16 of an ordered layer: LDS address of each tile
+                        // row's matrix row times cols
   float acc[G][NB];
   // stream
   uint32_t p_end, wb, wa, ra, last8;
@@ -279,13 +302,17 @@ struct Tile {
     } else {
       ring = uniform(lds_addr(wave_lds + kWin2 * 2));
       list = ring + TR * kRing;
+      rmap = list + TR * 8;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
+        const uint32_t s = g * kWave + lane;
+        const uint32_t orow = valid[g] ? out_row(a, r0 + s) : r0;
         pos[g] = 0;
-        rr[g] = ring + (g * kWave + lane) * kRing;
+        rr[g] = ring + s * kRing;
         cr[g] = false;
         pend[g] = 0;
-        srow[g] = MODE == kBf16_2 && valid[g] ? bf16_at(a.scale, r0 + g * kWave + lane) : 0.0f;
+        srow[g] = MODE == kBf16_2 && valid[g] ? bf16_at(a.scale, orow) : 0.0f;
+        if (a.order) *lds_ptr<uint32_t>(rmap + 4 * s) = orow * a.cols;
       }
       end = cols;
       const uint32_t span = (rows - 1) * a.cols + cols;  // elements from the tile origin
@@ -456,8 +483,18 @@ struct Tile {
   __device__ __forceinline__ void store_piece(uint32_t row, uint32_t col0, u32x2 d, uint32_t n,
                                               float sc) {
     const uint32_t idx = row * a.cols + col0;  // < 2^31 (checked at launch)
+    // an ordered layer: the element offset of the piece in the whole matrix
+    // (< 2^32), written through a global address
+    const size_t at = a.order ? size_t(*lds_ptr<const uint32_t>(rmap + 4 * row)) + c0 + col0 : 0;
     if (MODE == kCodes2) {
-      if (n >= kCPL) {
+      if (a.order) {
+        uint8_t *dst = a.codes + at;
+        if (n >= kCPL) {
+          *reinterpret_cast<u32x2u *>(dst) = d;
+        } else {
+          for (uint32_t e = 0; e < n; ++e) dst[e] = static_cast<uint8_t>(d[e / 4] >> (8 * (e % 4)));
+        }
+      } else if (n >= kCPL) {
         __builtin_amdgcn_raw_buffer_store_b64(d, out_rsrc, idx, 0, 0);
       } else {
         for (uint32_t e = 0; e < n; ++e)
@@ -485,7 +522,14 @@ struct Tile {
       o[2 * w] = pack_bf16(sc * v0, sc * v1);
       o[2 * w + 1] = pack_bf16(sc * v2, sc * v3);
     }
-    if (n >= kCPL) {
+    if (a.order) {
+      uint16_t *dst = a.wout + at;
+      if (n >= kCPL) {
+        *reinterpret_cast<u32x4u *>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+      } else {
+        for (uint32_t e = 0; e < n; ++e) dst[e] = static_cast<uint16_t>(o[e / 2] >> (16 * (e % 2)));
+      }
+    } else if (n >= kCPL) {
       __builtin_amdgcn_raw_buffer_store_b128(u32x4{o[0], o[1], o[2], o[3]}, out_rsrc, 2 * idx, 0,
                                              0);
     } else {
@@ -808,8 +852,9 @@ struct Tile {
 
   // Batch-1 GEMV: the sum of tile row r (0 .. TR - 1) of this tile.
   __device__ __forceinline__ void write_sum(uint32_t r, float sum) {
-    const uint32_t row = r0 + r;
+    uint32_t row = r0 + r;
     if (a.NT == 1) {
+      row = out_row(a, row);
       const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
       a.y[row] = bf16_to_f32(a.scale[row]) * sum + bias;
     } else {
@@ -823,12 +868,13 @@ struct Tile {
       for (int g = 0; g < G; ++g) {
         if (!valid[g]) continue;
         const uint32_t row = r0 + g * kWave + lane;
+        const uint32_t orow = a.NT == 1 ? out_row(a, row) : row;
 #pragma unroll
         for (int bb = 0; bb < NB; ++bb) {
           if (bb >= nb) continue;
           if (a.NT == 1) {
-            const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
-            a.y[size_t(bb) * a.rows + row] = bf16_to_f32(a.scale[row]) * acc[g][bb] + bias;
+            const float bias = a.bias ? bf16_to_f32(a.bias[orow]) : 0.0f;
+            a.y[size_t(bb) * a.rows + orow] = bf16_to_f32(a.scale[orow]) * acc[g][bb] + bias;
           } else {
             a.ws[(size_t(bb) * a.NT + tcol) * a.rows + row] = acc[g][bb];
           }
@@ -932,7 +978,7 @@ __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_multi_ke
 }
 
 // Rows split over NT > 1 column tiles: y = s * (partials added in tile
-// order) + bias.  One block per 64 outputs (index i = batch row * rows +
+// order) + bias, the partials of stored row k going to matrix row order[k].  One block per 64 outputs (index i = batch row * rows +
 // row, one per lane), kMergeParts wavefronts: wavefront p sums tiles
 // [p NT / kMergeParts, (p + 1) NT / kMergeParts) in order (independent loads,
 // so their latencies overlap, each a contiguous 256 bytes of the workspace),
@@ -968,8 +1014,9 @@ __device__ __forceinline__ void merge2(const Args2 &a, uint32_t blk) {
     float total = part_sum[0][lane];
 #pragma unroll
     for (uint32_t q = 1; q < kMergeParts; ++q) total += part_sum[q][lane];
-    const float bias = a.bias ? bf16_to_f32(a.bias[row]) : 0.0f;
-    a.y[i] = bf16_to_f32(a.scale[row]) * total + bias;
+    const uint32_t orow = out_row(a, row);
+    const float bias = a.bias ? bf16_to_f32(a.bias[orow]) : 0.0f;
+    a.y[i - row + orow] = bf16_to_f32(a.scale[orow]) * total + bias;
   }
 }
 
@@ -1038,6 +1085,7 @@ Args2 make_args2(const eq_layer *L) {
   a.padded_words = static_cast<uint32_t>(L->padded_words);
   a.fmt = L->base_format;
   a.n_syms = L->n_syms;
+  a.order = L->row_order;
   return a;
 }
 
@@ -1070,10 +1118,10 @@ Facts2 facts2() {
 
 // LDS per wavefront: the stream window, then (GEMV) the tile's activations:
 // one 8-byte record per column at batch 1, else the rows; (codes, BF16) the
-// rows' rings and the flush list.
+// rows' rings, the flush list and, for an ordered layer, the rows' offsets.
 uint32_t wave_lds_bytes(int mode, const Args2 &a) {
   uint32_t b = kWin2 * 2;
-  if (mode != kGemv2) b += a.TR * (kRing + 8);
+  if (mode != kGemv2) b += a.TR * (kRing + 8 + (a.order ? 4 : 0));
   if (mode == kGemv2) {
     const uint32_t nbp = a.batch == 1 ? 1 : a.batch == 2 ? 2 : a.batch <= 4 ? 4 : 8;
     b += nbp == 1 ? rec_bytes(a.TC) + kWave * 16 : (a.TC + 8) * 4 * nbp;
@@ -1183,8 +1231,10 @@ int launch2_multi(MultiArgs2 m, hipStream_t s) {
 // the 8192 x 28672 matrix at batch 1).
 template <int MODE, int NB>
 int launch2(Args2 a, hipStream_t s) {
-  // output offsets from a tile's origin are 32-bit byte offsets
-  if (MODE != kGemv2 && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+  // output offsets from a tile's origin are 32-bit byte offsets (an ordered
+  // layer stores through 64-bit addresses)
+  if (MODE != kGemv2 && !a.order && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31))
+    return EQ_EINVAL;
   if constexpr (MODE != kGemv2) {
     if (a.n_syms > 1) return launch2_pk<MODE, NB, true>(a, s);
   }
@@ -1257,8 +1307,10 @@ int v2_decode_out_multi(const eq_layer *const *L, uint32_t n, void *const *out, 
   bool pk = true;
   for (uint32_t i = 0; i < n; ++i) {
     if (!out[i]) return EQ_EINVAL;
-    // output offsets from a tile's origin are 32-bit byte offsets
-    if (uint64_t(2) * L[i]->lanes * L[i]->cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+    // output offsets from a tile's origin are 32-bit byte offsets (an ordered
+    // layer stores through 64-bit addresses)
+    if (!L[i]->row_order && uint64_t(2) * L[i]->lanes * L[i]->cols >= (uint64_t(1) << 31))
+      return EQ_EINVAL;
     m.a[i] = make_args2(L[i]);
     if (MODE == kCodes2) m.a[i].codes = static_cast<uint8_t *>(out[i]);
     else m.a[i].wout = static_cast<uint16_t *>(out[i]);

@@ -758,7 +758,7 @@ int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const u
   const uint32_t fmt = p->base_format ? p->base_format : kFmtE4M3;
   if (n >= (uint64_t(1) << 32) || (TR != 64 && TR != 128 && TR != 256) || TC == 0 || TC % 4 ||
       uint64_t(TR) * TC >= (uint64_t(1) << 32) || R < 10 || R > 12 ||
-      (!given && !(alpha > 0.0f)) || (fmt != kFmtE4M3 && fmt != kFmtInt8))
+      (!given && !(alpha > 0.0f)) || (fmt != kFmtE4M3 && fmt != kFmtInt8) || p->row_order > 1)
     return -1;
   if (given)
     for (uint32_t i = 0; i < M; ++i)
@@ -800,6 +800,26 @@ int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const u
     // parse and encode every chunk
     const Lookup dq(best.quads), dp(best.pairs);
     const uint32_t nq_raw = uint32_t(best.quads.size()), np_raw = uint32_t(best.pairs.size());
+
+    // Row order: the rows by ascending phrase count over their segments
+    // (ties: lower row), so that a tile's rows, which it takes as many steps
+    // to decode as its longest one needs, are alike.  The alphabet does not
+    // depend on it.
+    std::vector<uint32_t> order(M);
+    for (uint32_t i = 0; i < M; ++i) order[i] = i;
+    if (p->row_order) {
+      std::vector<uint64_t> cost(M, 0);
+      parallel_for(M, nt, [&](uint64_t r) {
+        uint64_t k = 0;
+        for (uint32_t t = 0; t < g.NT; ++t) {
+          const uint32_t c0 = t * g.TC, w = std::min(g.TC, N - c0);
+          parse(codes.data() + r * N + c0, w, dq, dp, nq_raw, np_raw, [&](uint32_t) { ++k; });
+        }
+        cost[r] = k;
+      });
+      std::stable_sort(order.begin(), order.end(),
+                       [&](uint32_t a, uint32_t b) { return cost[a] < cost[b]; });
+    }
     std::vector<std::vector<uint16_t>> words(g.n_chunks);
     std::vector<uint32_t> states(uint64_t(g.n_chunks) * TR);
     parallel_for(g.n_chunks, nt, [&](uint64_t c) {
@@ -810,7 +830,7 @@ int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const u
       std::vector<uint32_t> off(TR, 0), len(TR, 0);
       for (uint32_t s = 0; s < rws; ++s) {
         off[s] = uint32_t(sym.size());
-        parse(codes.data() + uint64_t(r0 + s) * N + c0, cols, dq, dp, nq_raw, np_raw,
+        parse(codes.data() + uint64_t(order[r0 + s]) * N + c0, cols, dq, dp, nq_raw, np_raw,
               [&](uint32_t raw) { sym.push_back(static_cast<uint16_t>(best.map[raw])); });
         len[s] = uint32_t(sym.size()) - off[s];
       }
@@ -832,7 +852,9 @@ int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const u
     const uint64_t o_freq = round_up(o_phr + 4ull * n_sym, 256);
     const uint64_t o_off = round_up(o_freq + 2ull * n_sym, 256);
     const uint64_t o_state = round_up(o_off + 4ull * (g.n_chunks + 1), 256);
-    const uint64_t o_words = round_up(o_state + 4ull * g.n_chunks * TR, 256);
+    const uint64_t o_order = p->row_order ? round_up(o_state + 4ull * g.n_chunks * TR, 256) : 0;
+    const uint64_t o_words = p->row_order ? round_up(o_order + 4ull * M, 256)
+                                          : round_up(o_state + 4ull * g.n_chunks * TR, 256);
     const uint64_t bytes = round_up(o_words + 2 * padded, 256);
     uint8_t *b = static_cast<uint8_t *>(std::calloc(1, bytes));
     if (!b) return -5;
@@ -847,7 +869,7 @@ int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const u
     put<uint32_t>(b, 32, TR);
     put<uint32_t>(b, 36, R);
     put<uint32_t>(b, 40, n_sym);
-    put<uint32_t>(b, 44, 0);                 // flags
+    put<uint32_t>(b, 44, p->row_order ? 1u : 0u);  // flags: bit 0, row order
     put<uint64_t>(b, 48, total);
     put<uint64_t>(b, 56, padded);
     put<uint64_t>(b, 64, p->seed);
@@ -866,6 +888,8 @@ int encode2_impl(const uint16_t *w, uint32_t M, uint32_t N, float alpha, const u
     put<uint32_t>(b, 148, best.np);
     put<uint32_t>(b, 152, best.ns);
     put<uint32_t>(b, 156, best_tau);
+    put<uint64_t>(b, 160, o_order);
+    if (p->row_order) std::memcpy(b + o_order, order.data(), 4ull * M);
     std::memcpy(b + o_scale, scale.data(), 2ull * M);
     std::memcpy(b + o_phr, best.phr.data(), 4ull * n_sym);
     std::memcpy(b + o_freq, best.freq.data(), 2ull * n_sym);

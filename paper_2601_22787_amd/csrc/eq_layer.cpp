@@ -2,6 +2,7 @@
 // The container layout and the checks are documented in eq.h.
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "eq.h"
 #include "eq_internal.h"
@@ -86,6 +87,21 @@ int init_v2(eq_layer *L, const uint8_t *b, uint64_t bytes, const uint8_t *d) {
     if (rd<uint32_t>(b, o_state + 4 * s) < (1u << 16)) return EQ_EFORMAT;
   for (uint32_t i = 0; i < M; ++i)
     if (!scale_ok(rd<uint16_t>(b, o_scale + 2ull * i))) return EQ_EFORMAT;
+  // row order (flag bit 0): a permutation of the M rows
+  const uint32_t flags = rd<uint32_t>(b, 44);
+  const uint64_t o_order = rd<uint64_t>(b, 160);
+  if (flags & ~1u) return EQ_EFORMAT;
+  if (flags & 1u) {
+    if (!section_ok(o_order, 4ull * M, file_bytes)) return EQ_EFORMAT;
+    std::vector<uint8_t> seen(M, 0);
+    for (uint32_t k = 0; k < M; ++k) {
+      const uint32_t r = rd<uint32_t>(b, o_order + 4ull * k);
+      if (r >= M || seen[r]) return EQ_EFORMAT;
+      seen[r] = 1;
+    }
+  } else if (o_order != 0) {
+    return EQ_EFORMAT;
+  }
   L->rows = M;
   L->cols = N;
   L->chunk_syms = C;
@@ -107,6 +123,7 @@ int init_v2(eq_layer *L, const uint8_t *b, uint64_t bytes, const uint8_t *d) {
   L->n_quads = nq;
   L->n_pairs = np;
   L->n_singles = ns;
+  L->row_order = (flags & 1u) ? reinterpret_cast<const uint32_t *>(d + o_order) : nullptr;
   return EQ_OK;
 }
 

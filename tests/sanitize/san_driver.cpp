@@ -149,18 +149,21 @@ int main() {
       CHECK(or_container_build(w.data(), M, N, alpha, fmt, 11, 512, 64, 7, 2.5f, &raw, &n) == 0);
       const std::vector<uint8_t> o1 = take(raw, n, true);
       check_roundtrip(o1, w, M, N, fmt, false);
-      // version 2 at two tile shapes
-      for (const uint32_t tr : {64u, 256u}) {
-        eqe_params2 p2{12, tr, tr == 64 ? 64u : 32u, 2, 7, 2.5f, fmt};
-        CHECK(eqe_encode2(w.data(), M, N, alpha, nullptr, &p2, &raw, &n) == EQ_OK);
-        const std::vector<uint8_t> b2 = take(raw, n, false);
-        check_roundtrip(b2, w, M, N, fmt, true);
-        fuzz(b2, M, N, true, 150);
+      // version 2 at two tile shapes, in matrix order and with a row order
+      for (const uint32_t tr : {64u, 256u})
+        for (const uint32_t ro : {0u, 1u}) {
+          eqe_params2 p2{12, tr, tr == 64 ? 64u : 32u, 2, 7, 2.5f, fmt, ro};
+          CHECK(eqe_encode2(w.data(), M, N, alpha, nullptr, &p2, &raw, &n) == EQ_OK);
+          const std::vector<uint8_t> b2 = take(raw, n, false);
+          check_roundtrip(b2, w, M, N, fmt, true);
+          fuzz(b2, M, N, true, 150);
+        }
+      for (const uint32_t ro : {0u, 1u}) {
+        CHECK(or_container2_build(w.data(), M, N, alpha, nullptr, fmt, 11, 128, 16, ro, 7, 2.5f,
+                                  &raw, &n) == 0);
+        const std::vector<uint8_t> o2 = take(raw, n, true);
+        check_roundtrip(o2, w, M, N, fmt, true);
       }
-      CHECK(or_container2_build(w.data(), M, N, alpha, nullptr, fmt, 11, 128, 16, 7, 2.5f, &raw,
-                                &n) == 0);
-      const std::vector<uint8_t> o2 = take(raw, n, true);
-      check_roundtrip(o2, w, M, N, fmt, true);
       fuzz(b1, M, N, false, 150);
       fuzz(o1, M, N, false, 50);
     }

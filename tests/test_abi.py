@@ -216,3 +216,29 @@ def test_layer_init_version2():
     }
     for name, b in bad.items():
         assert _init(b)[0] == eq.EQ_EFORMAT, name
+
+
+def test_layer_init_version2_row_order():
+    """A version-2 container with a row order: the layer points at its order
+    section; a repeated or out-of-range row, an unknown flag, or an order
+    offset without the flag is rejected on the host."""
+    w = synth.weights(small_spec(70, 1000, seed=24))
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    b2 = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=256, row_order=True)
+    info = oracle.container2_info(b2)
+    rc, L = _init(b2)
+    assert rc == eq.EQ_OK and L.version == 2
+    assert L.row_order == _fake_ptr() + info.off_order
+    order = oracle.container2_row_order(b2)
+    bad = {
+        "repeated": _patch(b2, info.off_order + 4, int(order[0]), np.uint32),
+        "range": _patch(b2, info.off_order + 8, 70, np.uint32),
+        "flag": _patch(b2, 44, 3, np.uint32),
+        "offset_without_flag": _patch(b2, 44, 0, np.uint32),
+        "section": _patch(b2, 160, info.file_bytes - 16, np.uint64),
+    }
+    for name, b in bad.items():
+        assert _init(b)[0] == eq.EQ_EFORMAT, name
+    plain = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=256)
+    rc, L = _init(plain)
+    assert rc == eq.EQ_OK and not L.row_order

@@ -122,12 +122,28 @@ def test_c3_gate_full_size_matches_oracle_quantiser():
     (520, 2048, 256, 256, 4.0, 1, True),   # 4 bits: few quads pass
     (96, 4096, 128, 512, 3.0, 2, True),
 ])
-def test_v2_containers_identical_to_oracle(M, N, TR, TC, bits, fmt, outliers):
+@pytest.mark.parametrize("row_order", [False, True])
+def test_v2_containers_identical_to_oracle(M, N, TR, TC, bits, fmt, outliers, row_order):
     w = synth.weights(small_spec(M, N, seed=5 * M + N, outliers=outliers))
     alpha, _ = oracle.alpha_search(w, bits, fmt)
-    a = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, threads=3, base_format=fmt)
-    b = oracle.container2_build(w, alpha, TR, TC, fmt=fmt)
+    a = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, threads=3, base_format=fmt,
+                       row_order=row_order)
+    b = oracle.container2_build(w, alpha, TR, TC, fmt=fmt, row_order=row_order)
     assert a.size == b.size and (a == b).all()
+    assert oracle.container2_info(a).flags == int(row_order)
+
+
+def test_v2_row_order_identical_to_oracle_with_outlier_free_rows():
+    """Rows of two kinds (with and without a large weight) in one layer, the
+    case the row order is for: the product encoder's order, and the whole
+    container, equal the oracle's."""
+    w = synth.weights(small_spec(700, 1024, seed=91, outliers=True)).copy()
+    w[1::9] = synth.weights(small_spec(700, 1024, seed=92, outliers=False))[1::9]
+    alpha, _ = oracle.alpha_search(w, 2.0)
+    a = eq.eqe_encode2(w, alpha, tile_rows=128, tile_cols=128, threads=4, row_order=True)
+    b = oracle.container2_build(w, alpha, 128, 128, row_order=True)
+    assert a.size == b.size and (a == b).all()
+    assert not np.array_equal(oracle.container2_row_order(a), np.arange(700))
 
 
 def test_v2_given_scales_identical_to_oracle():
@@ -143,3 +159,6 @@ def test_v2_given_scales_identical_to_oracle():
         eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=130)
     with pytest.raises(eq.EqError):
         eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=128, res_bits=13)
+    a = eq.eqe_encode2(w, 0.0, tile_rows=64, tile_cols=128, scale_bf16=scale, row_order=True)
+    b = oracle.container2_build(w, 0.0, 64, 128, scale=scale, row_order=True)
+    assert (a == b).all()

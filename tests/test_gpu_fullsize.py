@@ -85,12 +85,12 @@ def v2_tiles(spec):
     return tr, spec.chunk_syms // tr
 
 
-def build2(eq, spec):
+def build2(eq, spec, row_order=False):
     w = synth.weights(spec)
     alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
     tr, tc = v2_tiles(spec)
     blob = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=tc, seed=spec.seed,
-                          target_bits=spec.target_bits)
+                          target_bits=spec.target_bits, row_order=row_order)
     assert oracle.container_version(blob) == 2
     return w, blob
 
@@ -229,14 +229,16 @@ def test_config5_layer_whole(eq, layer):
         del w_ref, q_ref
 
 
-def test_config4_whole_matrices_v2(eq):
+@pytest.mark.parametrize("row_order", [False, True])
+def test_config4_whole_matrices_v2(eq, row_order):
     """Version-2 containers of both config-4 matrices (256 x 256 tiles, the
-    target row's container), every tile and every row: codes and BF16 through
-    the single-layer entry points; the GEMV at B = 1 (the target row), 3 (the
-    pair table of 4 rows) and 8 (the pair table in two halves)."""
+    target row's container; with and without the row order), every tile and
+    every row: codes and BF16 through the single-layer entry points; the GEMV
+    at B = 1 (the target row), 3 (the pair table of 4 rows) and 8 (the pair
+    table in two halves)."""
     for spec in config_matrices(4):
-        say("config 4 version 2 build", spec.name, spec.rows, spec.cols)
-        w, blob = build2(eq, spec)
+        say("config 4 version 2 build", spec.name, spec.rows, spec.cols, row_order)
+        w, blob = build2(eq, spec, row_order)
         L = eq.Layer(blob, _dev())
         say("config 4 version 2 parity", spec.name)
         q_ref, w_ref = reference(w, blob)
@@ -253,18 +255,20 @@ def test_config4_whole_matrices_v2(eq):
         del w_ref, q_ref, L
 
 
-@pytest.mark.parametrize("layer", [0, 1, 2])
-def test_config5_layer_whole_v2(eq, layer):
-    """Version-2 containers of one config-5 layer of each entropy class, all
-    seven matrices whole: codes and BF16 through the single-layer entry points
-    and the block-wise calls; the GEMV at B = 1 through the joint launches the
-    benchmark times (q|k|v and gate|up in one launch each, o and down alone),
-    equal to the per-matrix launches and against the oracle."""
+@pytest.mark.parametrize("layer,row_order", [(0, False), (1, False), (2, False), (0, True)])
+def test_config5_layer_whole_v2(eq, layer, row_order):
+    """Version-2 containers of one config-5 layer of each entropy class (and
+    one with the row order), all seven matrices whole: codes and BF16 through
+    the single-layer entry points and the block-wise calls; the GEMV at B = 1
+    through the joint launches the benchmark times (q|k|v and gate|up in one
+    launch each, o and down alone), equal to the per-matrix launches and
+    against the oracle."""
     specs = {s.name.split(".")[-1]: s for s in config_matrices(5, layers=[layer])}
     built = {}
     for n, spec in specs.items():
-        say("config 5 version 2 build", layer, n, spec.rows, spec.cols, spec.target_bits)
-        w, blob = build2(eq, spec)
+        say("config 5 version 2 build", layer, n, spec.rows, spec.cols, spec.target_bits,
+            row_order)
+        w, blob = build2(eq, spec, row_order)
         built[n] = (w, blob, eq.Layer(blob, _dev()))
     names = list(specs)
     Ls = [built[n][2] for n in names]

@@ -96,10 +96,11 @@ def check_full(eq, blob, spec, batches=(1, 2, 3, 5, 8), with_bias=True, offsets=
     return L, q_ref, w_ref
 
 
-def build(eq, spec, TR, TC, bits, fmt=1):
+def build(eq, spec, TR, TC, bits, fmt=1, row_order=False):
     w = synth.weights(spec)
     alpha, _ = eq.eqe_alpha_search(w, bits, base_format=fmt)
-    return w, eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, base_format=fmt)
+    return w, eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, base_format=fmt,
+                             row_order=row_order)
 
 
 EDGE = [
@@ -240,16 +241,19 @@ def test_v2_corrupted_stream_flagged(eq):
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_v2_configs_1_to_3(eq, cfg):
+@pytest.mark.parametrize("TR,row_order", [(64, False), (128, False), (128, True)])
+def test_v2_configs_1_to_3(eq, cfg, TR, row_order):
+    """Whole matrices of configs 1-3 at 64-row tiles and at the benchmark's
+    128-row tiles (the same C symbols per tile), in matrix order and with the
+    row order (which moves config 3's outlier-free rows together)."""
     for spec in config_matrices(cfg):
-        TR = 64
         TC = spec.chunk_syms // TR
-        say("v2 config", cfg, spec.name, spec.rows, spec.cols, TR, TC)
+        say("v2 config", cfg, spec.name, spec.rows, spec.cols, TR, TC, row_order)
         w = synth.weights(spec)
         alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=1024)
         blob = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, seed=spec.seed,
-                              target_bits=spec.target_bits)
-        check_full(eq, blob, spec, batches=(1, 8) if cfg < 3 else (1,))
+                              target_bits=spec.target_bits, row_order=row_order)
+        check_full(eq, blob, spec, batches=(1, 8))
 
 
 @pytest.mark.parametrize("B", [1, 3, 8])
@@ -331,3 +335,107 @@ def test_v2_block_wise_codes_and_bf16(eq, single_phrase):
             assert np.array_equal(got[:k].reshape(w_ref.shape), w_ref), heights
             assert (got[k:] == 0xFFFF).all()
             assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+# ---- row order: tiles cut over the rows sorted by phrase count ----
+
+def _mixed_rows(spec):
+    """Weights whose rows are of two kinds, with and without outliers (the
+    rows the order groups), so that the stored order is far from the
+    identity."""
+    w = synth.weights(spec).copy()
+    plain = synth.weights(small_spec(spec.rows, spec.cols, seed=spec.seed + 1, outliers=False))
+    w[1::5] = plain[1::5]
+    return w
+
+
+@pytest.mark.parametrize("M,N,TR,TC,bits,outliers", EDGE)
+def test_v2_row_order_edge_shapes(eq, M, N, TR, TC, bits, outliers):
+    """Every entry point on ordered layers: codes and BF16 bit-exact in
+    matrix order, the GEMV (merged partials, and tiles of whole rows) within
+    the bar, at the edge shapes of the matrix-order case."""
+    say("v2 row order edge", M, N, TR, TC, bits)
+    spec = small_spec(M, N, bits=bits, seed=2000 + 7 * M + N, outliers=outliers)
+    _, blob = build(eq, spec, TR, TC, bits, row_order=True)
+    assert oracle.container2_info(blob).flags == 1
+    check_full(eq, blob, spec)
+
+
+@pytest.mark.parametrize("TR,TC", [(64, 256), (128, 128), (256, 256), (64, 1024)])
+def test_v2_row_order_mixed_rows_and_offsets(eq, TR, TC):
+    """Rows of two kinds in one layer: the order moves most rows; outputs
+    starting 0-3 elements into a buffer are bit-exact (stores at any byte
+    address) and nothing outside them is written."""
+    M, N = 700, 1024
+    spec = small_spec(M, N, bits=2.0, seed=2800 + TR + TC, outliers=True)
+    w = _mixed_rows(spec)
+    alpha, _ = eq.eqe_alpha_search(w, 2.0)
+    blob = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, row_order=True)
+    order = oracle.container2_row_order(blob)
+    say("v2 row order mixed", TR, TC, "rows moved", int((order != np.arange(M)).sum()))
+    assert (order != np.arange(M)).sum() > M // 2
+    check_full(eq, blob, spec, batches=(1, 2, 8), offsets=(0, 1, 2, 3))
+
+
+def test_v2_row_order_multi(eq):
+    """Joint launches over ordered and matrix-order layers together: the
+    GEMV of layers sharing an input equals the single-layer launches, and
+    block-wise codes and BF16 are bit-exact against the oracle."""
+    shapes = [(300, 1024, 256, True), (64, 1024, 128, False), (97, 1024, 256, True)]
+    layers = []
+    for i, (M, N, TC, ordered) in enumerate(shapes):
+        spec = small_spec(M, N, bits=2.0, seed=2950 + i, outliers=True)
+        w = _mixed_rows(spec)
+        alpha, _ = eq.eqe_alpha_search(w, 2.0)
+        blob = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=TC, row_order=ordered)
+        layers.append((spec, blob, eq.Layer(blob, _dev())))
+    Ls = [L for _, _, L in layers]
+    for B in (1, 8):
+        x_bits = synth.activations(layers[0][0], B)
+        x = torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(_dev())
+        ys = [torch.full((B, L.rows), float("nan"), dtype=torch.float32, device=_dev())
+              for L in Ls]
+        eq.eq_decode_gemv_multi(Ls, x, B, None, ys, eq.multi_workspace(Ls, B))
+        for L, y in zip(Ls, ys):
+            assert np.array_equal(y.cpu().numpy(), gpu_gemv(eq, L, x_bits)), B
+    n = [L.rows * L.cols for L in Ls]
+    codes = [torch.full((k + 8,), 0xA5, dtype=torch.uint8, device=_dev()) for k in n]
+    bufs = [torch.full((k + 8,), -1, dtype=torch.int16, device=_dev()) for k in n]
+    eq.eq_decode_codes_multi(Ls, [c[:k] for c, k in zip(codes, n)])
+    eq.eq_decode_bf16_multi(Ls, [b[:k] for b, k in zip(bufs, n)])
+    for (spec, blob, L), c, b, k in zip(layers, codes, bufs, n):
+        rc, q_ref = oracle.container2_decode(blob)
+        assert rc == oracle.OK
+        w_ref = oracle.dequant(q_ref, oracle.container_scales(blob))
+        got_c = c.cpu().numpy()
+        got_b = b.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got_c[:k].reshape(q_ref.shape), q_ref)
+        assert np.array_equal(got_b[:k].reshape(w_ref.shape), w_ref)
+        assert (got_c[k:] == 0xA5).all() and (got_b[k:] == 0xFFFF).all()
+        assert eq.eq_get_status(L) == eq.EQ_OK
+
+
+@pytest.mark.parametrize("TC", [256, 1024])
+def test_v2_row_order_damaged_on_device(eq, TC):
+    """An order entry out of range in the device copy only (the host checked
+    its own): every entry point marks the layer corrupt, keeps that row in
+    place and writes nothing outside its outputs."""
+    M, N = 70, 1024
+    spec = small_spec(M, N, bits=2.0, seed=2990)
+    _, blob = build(eq, spec, 64, TC, 2.0, row_order=True)
+    info = oracle.container2_info(blob)
+    L = eq.Layer(blob, _dev())
+    o = info.off_order + 4 * 3
+    L.dev_blob[o:o + 4] = torch.from_numpy(np.frombuffer(np.uint32(M + 5).tobytes(),
+                                                         dtype=np.uint8).copy()).to(_dev())
+    torch.cuda.synchronize()
+    for what in ("codes", "bf16", "gemv1", "gemv8"):
+        eq.eq_layer_prepare(L)
+        assert eq.eq_get_status(L) == eq.EQ_OK
+        if what == "codes":
+            gpu_codes(eq, L, 1)
+        elif what == "bf16":
+            gpu_bf16(eq, L, 1)
+        else:
+            gpu_gemv(eq, L, synth.activations(spec, 1 if what == "gemv1" else 8))
+        assert eq.eq_get_status(L) == eq.EQ_ECORRUPT, what

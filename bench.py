@@ -711,7 +711,8 @@ def time_graph(fn, calls, reps):
     in one HIP graph (the sequence repeated to about 40 calls, so that the
     gap between two replays is spread thin) and replayed reps times between
     two HIP events: the GPU time of the calls' kernels without the host's
-    launch and event gaps."""
+    launch and event gaps.  Replays for at least 20 ms first (at least two),
+    so that the timed ones run at the GPU's working clocks."""
     import torch
     rounds = max(1, -(-40 // calls))
     g = torch.cuda.CUDAGraph()
@@ -719,8 +720,12 @@ def time_graph(fn, calls, reps):
         for _ in range(rounds):
             for i in range(calls):
                 fn(i)
-    g.replay()
-    torch.cuda.synchronize()
+    t0 = time.time()
+    for k in range(1000):
+        g.replay()
+        torch.cuda.synchronize()
+        if k >= 1 and time.time() - t0 >= 0.02:
+            break
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()

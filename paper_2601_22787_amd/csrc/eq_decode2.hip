@@ -160,7 +160,10 @@ __device__ inline u32x2 value_half(uint32_t addr) { return *lds_ptr<const u32x2>
 // bytes, rounded to 16).
 __host__ __device__ constexpr uint32_t rec_bytes(uint32_t tc) { return ((tc + 4) * 8 + 15) / 16 * 16; }
 
-template <int G, int MODE, int NB, bool PK>
+// ORD (codes and BF16 only): outputs through the rows' offsets in LDS and
+// 64-bit addresses, for launches with an ordered layer; without it, buffer
+// stores from the tile's origin.
+template <int G, int MODE, int NB, bool PK, bool ORD>
 struct Tile {
   static constexpr uint32_t TR = G * kWave;
   // log2 of the position step per code (packed entries hold the length)
@@ -184,8 +187,8 @@ struct Tile {
                      // not yet written (pos mod 4 of them, low bytes first)
   bool cr[G];        // codes / BF16: the last phrase completed a segment
   uint32_t ring, list;  // codes / BF16: LDS addresses of the rings, the flush list
-  uint32_t rmap;        // codes / BF16 of an ordered layer: LDS address of each tile
-                        // row's matrix row times cols
+  uint32_t rmap;        // codes / BF16, ORD: LDS address of each tile row's matrix
+                        // row times cols
   float acc[G][NB];
   // stream
   uint32_t p_end, wb, wa, ra, last8;
@@ -306,13 +309,13 @@ struct Tile {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const uint32_t s = g * kWave + lane;
-        const uint32_t orow = valid[g] ? out_row(a, r0 + s) : r0;
+        const uint32_t orow = ORD && valid[g] ? out_row(a, r0 + s) : r0 + s;
         pos[g] = 0;
         rr[g] = ring + s * kRing;
         cr[g] = false;
         pend[g] = 0;
         srow[g] = MODE == kBf16_2 && valid[g] ? bf16_at(a.scale, orow) : 0.0f;
-        if (a.order) *lds_ptr<uint32_t>(rmap + 4 * s) = orow * a.cols;
+        if (ORD) *lds_ptr<uint32_t>(rmap + 4 * s) = valid[g] ? orow * a.cols : 0u;
       }
       end = cols;
       const uint32_t span = (rows - 1) * a.cols + cols;  // elements from the tile origin
@@ -483,11 +486,11 @@ struct Tile {
   __device__ __forceinline__ void store_piece(uint32_t row, uint32_t col0, u32x2 d, uint32_t n,
                                               float sc) {
     const uint32_t idx = row * a.cols + col0;  // < 2^31 (checked at launch)
-    // an ordered layer: the element offset of the piece in the whole matrix
-    // (< 2^32), written through a global address
-    const size_t at = a.order ? size_t(*lds_ptr<const uint32_t>(rmap + 4 * row)) + c0 + col0 : 0;
+    // ORD: the element offset of the piece in the whole matrix (< 2^32),
+    // written through a global address
+    const size_t at = ORD ? size_t(*lds_ptr<const uint32_t>(rmap + 4 * row)) + c0 + col0 : 0;
     if (MODE == kCodes2) {
-      if (a.order) {
+      if (ORD) {
         uint8_t *dst = a.codes + at;
         if (n >= kCPL) {
           *reinterpret_cast<u32x2u *>(dst) = d;
@@ -522,7 +525,7 @@ struct Tile {
       o[2 * w] = pack_bf16(sc * v0, sc * v1);
       o[2 * w + 1] = pack_bf16(sc * v2, sc * v3);
     }
-    if (a.order) {
+    if (ORD) {
       uint16_t *dst = a.wout + at;
       if (n >= kCPL) {
         *reinterpret_cast<u32x4u *>(dst) = u32x4{o[0], o[1], o[2], o[3]};
@@ -894,7 +897,7 @@ constexpr uint32_t table_bytes2(int mode, bool pk) {
 
 // The work of block `bid` of `nblocks` on layer a: stage the phrase table,
 // then each wavefront decodes its chunks (below).
-template <int G, int MODE, int NB, bool PK>
+template <int G, int MODE, int NB, bool PK, bool ORD>
 __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint32_t nblocks) {
   extern __shared__ uint4 dyn2[];
   // the phrase table at LDS address 0 (no static LDS in this kernel), the
@@ -950,14 +953,14 @@ __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint
   // or short together; spreading each block's tiles over all bands evens the
   // work of the compute units (batch-1 GEMV on 8192 x 28672: 67.0 -> 64.2 us)
   for (uint32_t c = uniform(wave * nblocks + bid); c < a.n_chunks; c += nblocks * nw) {
-    Tile<G, MODE, NB, PK> t(a, c, lane, mine);
+    Tile<G, MODE, NB, PK, ORD> t(a, c, lane, mine);
     t.run();
   }
 }
 
-template <int G, int MODE, int NB, bool PK>
+template <int G, int MODE, int NB, bool PK, bool ORD>
 __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_kernel(Args2 a) {
-  decode2_block<G, MODE, NB, PK>(a, blockIdx.x, gridDim.x);
+  decode2_block<G, MODE, NB, PK, ORD>(a, blockIdx.x, gridDim.x);
 }
 
 // Several layers in one launch (Sec. 2.2 block-wise decompression): blocks
@@ -970,11 +973,11 @@ struct MultiArgs2 {
   uint32_t n;
 };
 
-template <int G, int MODE, int NB, bool PK>
+template <int G, int MODE, int NB, bool PK, bool ORD>
 __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_multi_kernel(MultiArgs2 m) {
   uint32_t i = 0, b0 = 0;
   while (i + 1 < m.n && blockIdx.x >= m.blk_end[i]) b0 = m.blk_end[i++];
-  decode2_block<G, MODE, NB, PK>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0);
+  decode2_block<G, MODE, NB, PK, ORD>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0);
 }
 
 // Rows split over NT > 1 column tiles: y = s * (partials added in tile
@@ -1118,10 +1121,10 @@ Facts2 facts2() {
 
 // LDS per wavefront: the stream window, then (GEMV) the tile's activations:
 // one 8-byte record per column at batch 1, else the rows; (codes, BF16) the
-// rows' rings, the flush list and, for an ordered layer, the rows' offsets.
-uint32_t wave_lds_bytes(int mode, const Args2 &a) {
+// rows' rings, the flush list and, in an ORD launch, the rows' offsets.
+uint32_t wave_lds_bytes(int mode, const Args2 &a, bool ord) {
   uint32_t b = kWin2 * 2;
-  if (mode != kGemv2) b += a.TR * (kRing + 8 + (a.order ? 4 : 0));
+  if (mode != kGemv2) b += a.TR * (kRing + 8 + (ord ? 4 : 0));
   if (mode == kGemv2) {
     const uint32_t nbp = a.batch == 1 ? 1 : a.batch == 2 ? 2 : a.batch <= 4 ? 4 : 8;
     b += nbp == 1 ? rec_bytes(a.TC) + kWave * 16 : (a.TC + 8) * 4 * nbp;
@@ -1166,10 +1169,10 @@ uint32_t choose_waves(const uint32_t *n, uint32_t k, uint32_t wmax, size_t tb, s
   return w;
 }
 
-template <int MODE, int NB, bool PK>
+template <int MODE, int NB, bool PK, bool ORD>
 int launch2_pk(Args2 a, hipStream_t s) {
   const Facts2 f = facts2();
-  a.wave_lds = wave_lds_bytes(MODE, a);
+  a.wave_lds = wave_lds_bytes(MODE, a, ORD);
   const size_t tb = table_bytes2(MODE, PK);
   const uint32_t waves = choose_waves(&a.n_chunks, 1, max_waves2(MODE, NB), tb, a.wave_lds, f);
   if (waves == 0) return EQ_EINVAL;
@@ -1177,9 +1180,9 @@ int launch2_pk(Args2 a, hipStream_t s) {
   const size_t shm = tb + size_t(waves) * a.wave_lds;
   const dim3 grid(blocks), block(waves * kWave);
   switch (a.TR) {
-    case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB, PK>), grid, block, shm, s, a); break;
-    case 128: hipLaunchKernelGGL((decode2_kernel<2, MODE, NB, PK>), grid, block, shm, s, a); break;
-    default: hipLaunchKernelGGL((decode2_kernel<4, MODE, NB, PK>), grid, block, shm, s, a); break;
+    case 64: hipLaunchKernelGGL((decode2_kernel<1, MODE, NB, PK, ORD>), grid, block, shm, s, a); break;
+    case 128: hipLaunchKernelGGL((decode2_kernel<2, MODE, NB, PK, ORD>), grid, block, shm, s, a); break;
+    default: hipLaunchKernelGGL((decode2_kernel<4, MODE, NB, PK, ORD>), grid, block, shm, s, a); break;
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
@@ -1196,12 +1199,12 @@ __global__ __launch_bounds__(kMergeThreads) void merge2_multi_kernel(MultiArgs2 
 // Joint launch of m.n layers: one wavefront count for all (from the total
 // chunks, LDS for the largest per-wavefront need), each layer's blocks in
 // proportion to its chunks.
-template <int MODE, int NB, bool PK>
+template <int MODE, int NB, bool PK, bool ORD>
 int launch2_multi(MultiArgs2 m, hipStream_t s) {
   const Facts2 f = facts2();
   uint32_t wl = 0, n[kMaxLayers2];
   for (uint32_t i = 0; i < m.n; ++i) {
-    wl = max(wl, wave_lds_bytes(MODE, m.a[i]));
+    wl = max(wl, wave_lds_bytes(MODE, m.a[i], ORD));
     n[i] = m.a[i].n_chunks;
   }
   const size_t tb = table_bytes2(MODE, PK);
@@ -1216,9 +1219,9 @@ int launch2_multi(MultiArgs2 m, hipStream_t s) {
   const size_t shm = tb + size_t(waves) * wl;
   const dim3 grid(end), block(waves * kWave);
   switch (m.a[0].TR) {
-    case 64: hipLaunchKernelGGL((decode2_multi_kernel<1, MODE, NB, PK>), grid, block, shm, s, m); break;
-    case 128: hipLaunchKernelGGL((decode2_multi_kernel<2, MODE, NB, PK>), grid, block, shm, s, m); break;
-    default: hipLaunchKernelGGL((decode2_multi_kernel<4, MODE, NB, PK>), grid, block, shm, s, m); break;
+    case 64: hipLaunchKernelGGL((decode2_multi_kernel<1, MODE, NB, PK, ORD>), grid, block, shm, s, m); break;
+    case 128: hipLaunchKernelGGL((decode2_multi_kernel<2, MODE, NB, PK, ORD>), grid, block, shm, s, m); break;
+    default: hipLaunchKernelGGL((decode2_multi_kernel<4, MODE, NB, PK, ORD>), grid, block, shm, s, m); break;
   }
   return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
 }
@@ -1231,14 +1234,17 @@ int launch2_multi(MultiArgs2 m, hipStream_t s) {
 // the 8192 x 28672 matrix at batch 1).
 template <int MODE, int NB>
 int launch2(Args2 a, hipStream_t s) {
-  // output offsets from a tile's origin are 32-bit byte offsets (an ordered
-  // layer stores through 64-bit addresses)
-  if (MODE != kGemv2 && !a.order && uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31))
-    return EQ_EINVAL;
   if constexpr (MODE != kGemv2) {
-    if (a.n_syms > 1) return launch2_pk<MODE, NB, true>(a, s);
+    // an ordered layer stores through 64-bit addresses; otherwise output
+    // offsets from a tile's origin are 32-bit byte offsets
+    if (a.order) {
+      return a.n_syms > 1 ? launch2_pk<MODE, NB, true, true>(a, s)
+                          : launch2_pk<MODE, NB, false, true>(a, s);
+    }
+    if (uint64_t(2) * a.TR * a.cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
+    if (a.n_syms > 1) return launch2_pk<MODE, NB, true, false>(a, s);
   }
-  return launch2_pk<MODE, NB, false>(a, s);
+  return launch2_pk<MODE, NB, false, false>(a, s);
 }
 
 size_t round256(size_t v) { return (v + 255) / 256 * 256; }
@@ -1304,19 +1310,22 @@ int v2_decode_out_multi(const eq_layer *const *L, uint32_t n, void *const *out, 
   if (!v2_joint_out_ok(L, n)) return EQ_EINVAL;
   MultiArgs2 m{};
   m.n = n;
-  bool pk = true;
+  bool pk = true, ord = false;
+  for (uint32_t i = 0; i < n; ++i) ord |= L[i]->row_order != nullptr;
   for (uint32_t i = 0; i < n; ++i) {
     if (!out[i]) return EQ_EINVAL;
-    // output offsets from a tile's origin are 32-bit byte offsets (an ordered
-    // layer stores through 64-bit addresses)
-    if (!L[i]->row_order && uint64_t(2) * L[i]->lanes * L[i]->cols >= (uint64_t(1) << 31))
-      return EQ_EINVAL;
+    // with an ordered layer every layer of the launch stores through 64-bit
+    // addresses; otherwise output offsets from a tile's origin are 32-bit
+    // byte offsets
+    if (!ord && uint64_t(2) * L[i]->lanes * L[i]->cols >= (uint64_t(1) << 31)) return EQ_EINVAL;
     m.a[i] = make_args2(L[i]);
     if (MODE == kCodes2) m.a[i].codes = static_cast<uint8_t *>(out[i]);
     else m.a[i].wout = static_cast<uint16_t *>(out[i]);
     pk &= m.a[i].n_syms > 1;
   }
-  return pk ? launch2_multi<MODE, 1, true>(m, s) : launch2_multi<MODE, 1, false>(m, s);
+  if (ord)
+    return pk ? launch2_multi<MODE, 1, true, true>(m, s) : launch2_multi<MODE, 1, false, true>(m, s);
+  return pk ? launch2_multi<MODE, 1, true, false>(m, s) : launch2_multi<MODE, 1, false, false>(m, s);
 }
 
 int v2_decode_codes_multi(const eq_layer *const *L, uint8_t *const *codes, uint32_t n,
@@ -1355,10 +1364,10 @@ int v2_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x
     m.a[i].y = y[i];
     m.a[i].ws = static_cast<float *>(ws[i]);
   }
-  const int rc = B == 1   ? launch2_multi<kGemv2, 1, false>(m, s)
-                 : B == 2 ? launch2_multi<kGemv2, 2, false>(m, s)
-                 : B <= 4 ? launch2_multi<kGemv2, 4, false>(m, s)
-                          : launch2_multi<kGemv2, 8, false>(m, s);
+  const int rc = B == 1   ? launch2_multi<kGemv2, 1, false, false>(m, s)
+                 : B == 2 ? launch2_multi<kGemv2, 2, false, false>(m, s)
+                 : B <= 4 ? launch2_multi<kGemv2, 4, false, false>(m, s)
+                          : launch2_multi<kGemv2, 8, false, false>(m, s);
   if (rc != EQ_OK) return rc;
   uint32_t omax = 0;
   bool any = false;

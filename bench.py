@@ -683,8 +683,10 @@ def run_prefill(args):
 
 
 # (template arguments: tile rows / 64, op, batch, packed table entries)
-V2_KERNEL = {"gemv1": "decode2_kernel<4, 2, 1, false>", "gemv8": "decode2_kernel<4, 2, 8, false>",
-             "bf16": "decode2_kernel<4, 1, 1, true>", "codes": "decode2_kernel<4, 0, 1, true>"}
+V2_KERNEL = {"gemv1": "decode2_kernel<4, 2, 1, false, false>",
+             "gemv8": "decode2_kernel<4, 2, 8, false, false>",
+             "bf16": "decode2_kernel<4, 1, 1, true, false>",
+             "codes": "decode2_kernel<4, 0, 1, true, false>"}
 TARGET_FRAC = 0.60  # fused decode-GEMV B=1 on 8192x28672, compressed bytes / HBM peak
 
 

@@ -101,19 +101,22 @@ def test_graph_replays_match_eager(eq):
         assert eq.eq_get_status(L) == eq.EQ_OK
 
 
-def layer2(eq, M, N, TR, TC, seed):
-    spec = small_spec(M, N, bits=2.0, seed=seed)
+def layer2(eq, M, N, TR, TC, seed, row_order=False):
+    spec = small_spec(M, N, bits=2.0, seed=seed, outliers=row_order)
     w = synth.weights(spec)
     alpha, _ = eq.eqe_alpha_search(w, 2.0)
-    return eq.Layer(eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC), _dev()), spec
+    blob = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, row_order=row_order)
+    return eq.Layer(blob, _dev()), spec
 
 
-def test_graph_replays_match_eager_v2(eq):
-    """The same for container version 2: codes and BF16 (rings in LDS), the
-    GEMV at batch 1 and 8 with its column-tile merge, the joint GEMV of two
-    layers sharing an input, block-wise codes, and the no-alloc GEMV (its
-    static scratch address is taken on the eager call before capture)."""
-    La, sa = layer2(eq, 300, 1024, 256, 256, 6100)
+@pytest.mark.parametrize("row_order", [False, True])
+def test_graph_replays_match_eager_v2(eq, row_order):
+    """The same for container version 2 (in matrix order, and with the row
+    order): codes and BF16 (rings in LDS), the GEMV at batch 1 and 8 with its
+    column-tile merge, the joint GEMV of two layers sharing an input,
+    block-wise codes, and the no-alloc GEMV (its static scratch address is
+    taken on the eager call before capture)."""
+    La, sa = layer2(eq, 300, 1024, 256, 256, 6100, row_order)
     Lb, _ = layer2(eq, 70, 1024, 256, 256, 6101)
     x1, x8 = xs(sa, 1), xs(sa, 8)
     bias = torch.from_numpy(synth.bias(sa).view(np.int16)).to(_dev())

@@ -39,11 +39,11 @@ def _dev():
     return torch.device("cuda:0")
 
 
-def _v2(eq, M, N, TR, TC, seed):
-    spec = small_spec(M, N, bits=2.0, seed=seed)
+def _v2(eq, M, N, TR, TC, seed, row_order=False):
+    spec = small_spec(M, N, bits=2.0, seed=seed, outliers=row_order)
     w = synth.weights(spec)
     alpha, _ = eq.eqe_alpha_search(w, 2.0)
-    return spec, eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC)
+    return spec, eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, row_order=row_order)
 
 
 def _v1(eq, M, N, C, lanes, seed):
@@ -100,6 +100,14 @@ def test_noalloc_v2_partials(eq):
     big = _v2(eq, 1024, 4096, 256, 256, 3100)
     small = _v2(eq, 300, 1000, 64, 256, 3101)
     _run_pair(eq, [(*big, 8, True), (*small, 3, False)])
+
+
+def test_noalloc_v2_row_order(eq):
+    """Ordered layers (row sums merged into matrix rows, and tiles of whole
+    rows written in place) through the static scratch, then a smaller one."""
+    big = _v2(eq, 1024, 4096, 256, 256, 3102, row_order=True)
+    whole_rows = _v2(eq, 300, 1000, 64, 1024, 3103, row_order=True)
+    _run_pair(eq, [(*big, 1, True), (*whole_rows, 8, False)])
 
 
 def test_noalloc_v1_row_partials(eq):

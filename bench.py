@@ -72,6 +72,9 @@ def parse():
     ap.add_argument("--tokens", type=int, default=2048, help="prefill batch (tokens)")
     ap.add_argument("--container", type=int, choices=(1, 2), default=1,
                     help="c5 workload: container version of the stack's layers")
+    ap.add_argument("--v2-tile-rows", type=int, choices=(64, 128, 256), default=0,
+                    help="version-2 tile rows for every matrix (256 columns for 65536-symbol "
+                         "chunks, C / rows below) instead of the rule of v2_tiles")
     ap.add_argument("--row-order", action="store_true",
                     help="version-2 containers with the row order: tiles cut over the rows "
                          "sorted by their phrase count")
@@ -86,19 +89,30 @@ def parse():
     return ap.parse_args()
 
 
-def v2_tile_rows(chunk_syms):
-    """Tile rows of the version-2 containers for C-symbol chunks: 256 for
-    65536-symbol chunks (256 x 256 tiles), else 128 (two pipelined coder
-    states per lane; measured faster than 64 for the batch-1 GEMV on the
-    16384-symbol chunks of configs 2 and 3)."""
-    return 256 if chunk_syms >= 65536 else 128
+def v2_tiles(spec, rows=0):
+    """Tile rows and columns of the version-2 containers, C symbols a tile for
+    C-symbol chunks below 65536: 128 rows (two pipelined coder states per
+    lane; faster than 64 for the batch-1 GEMV on the 16384-symbol chunks of
+    configs 2 and 3) x C / 128 columns.  65536-symbol chunks: 256 columns,
+    and 256 rows when the matrix has at least 2048 such tiles (8 per compute
+    unit), else 128 rows: half the tile, the same state bytes per code (they
+    depend on the width alone), twice the tiles, and half the work per step
+    for each, which shortens launches that cannot fill the GPU (config-5
+    attention matrices, batch-1 GEMV: 43.5 -> 34 us).  rows > 0 sets the
+    tile rows instead (256 columns for 65536-symbol chunks, C / rows below)."""
+    if rows:
+        return rows, (256 if spec.chunk_syms >= 65536 else spec.chunk_syms // rows)
+    if spec.chunk_syms < 65536:
+        return 128, spec.chunk_syms // 128
+    tiles = -(-spec.rows // 256) * -(-spec.cols // 256)
+    return (256 if tiles >= 2048 else 128), 256
 
 
-def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0, row_order=False):
+def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0, row_order=False,
+                 v2_rows=0):
     """Encode each matrix (product encoder) and upload `copies` device copies;
     with v2_copies > 0 also the same codes (same alpha) in container version
-    2, tiles of v2_tile_rows(C) rows x C / rows columns (the same C symbols
-    per chunk), with the row order if row_order."""
+    2, tiles of v2_tiles(spec, v2_rows), with the row order if row_order."""
     out = []
     for spec in specs:
         t0 = time.time()
@@ -110,8 +124,8 @@ def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0, row_order=Fa
         item = {"spec": spec, "w": w, "blob": blob, "layers": layers}
         msg = f"container {blob.size / 1e6:.1f} MB"
         if v2_copies:
-            tr = v2_tile_rows(spec.chunk_syms)
-            blob2 = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=spec.chunk_syms // tr,
+            tr, tc = v2_tiles(spec, v2_rows)
+            blob2 = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=tc,
                                    seed=spec.seed, target_bits=spec.target_bits,
                                    base_format=fmt, row_order=row_order)
             item["blob2"] = blob2
@@ -131,7 +145,8 @@ def blob_info(blob):
     u64 = h.view(np.uint64)
     return dict(rows=int(u32[4]), cols=int(u32[5]), total_words=int(u64[6]),
                 padded_words=int(u64[7]), entropy=float(h[80:84].view(np.float32)[0]),
-                file_bytes=int(u64[17]))
+                file_bytes=int(u64[17]), lanes=int(u32[8]),
+                tile_cols=int(u32[21]) if int(u32[1]) == 2 else 0)
 
 
 def algorithmic_bytes(info, op, B):
@@ -387,8 +402,8 @@ def run_stack(args):
             w = synth.weights(spec)
             alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=512)
             if args.container == 2:
-                tr = v2_tile_rows(spec.chunk_syms)
-                blob = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=spec.chunk_syms // tr,
+                tr, tc = v2_tiles(spec, args.v2_tile_rows)
+                blob = eq.eqe_encode2(w, alpha, tile_rows=tr, tile_cols=tc,
                                       seed=spec.seed, target_bits=spec.target_bits,
                                       row_order=args.row_order)
             else:
@@ -480,7 +495,9 @@ def run_stack(args):
         "dtype": "u32", "data": "synthetic", "env": run_env(),
         "config": {"workload": "config 5: 80 layers x {q 8192x8192, k/v 1024x8192, o 8192x8192, "
                                "gate/up 28672x8192, down 8192x28672}, (2,3,4)[l mod 3] bits, "
-                               "65536-symbol chunks; 3 distinct layers, 80 device copies",
+                               "65536-symbol chunks (version 2: tiles of 256 columns, 128 rows "
+                               "for q/k/v/o, 256 for gate/up/down); 3 distinct layers, 80 device "
+                               "copies",
                    "container": args.container,
                    "v2_row_order": bool(args.row_order and args.container == 2),
                    "launch": "eager" if args.eager else "HIP graph of each 80-layer pass",
@@ -525,7 +542,7 @@ def run_small(args):
     for cfg in (1, 2, 3):
         specs = config_matrices(cfg)
         for item in build_layers(eq, synth, specs, args.copies, dev, v2_copies=args.copies,
-                                 row_order=args.row_order):
+                                 row_order=args.row_order, v2_rows=args.v2_tile_rows):
             spec = item["spec"]
             out = torch.empty(spec.params, dtype=torch.int16, device=dev)
             x = torch.from_numpy(synth.activations(spec, 1).view(np.int16)).to(dev)
@@ -547,6 +564,8 @@ def run_small(args):
                     nbytes = algorithmic_bytes(info, op, 8 if op == "gemv8" else 1)
                     rows.append({"config": cfg, "matrix": spec.name,
                                  "shape": [spec.rows, spec.cols], "container": version,
+                                 "tile": ([info["lanes"], info["tile_cols"]] if version == 2
+                                          else None),
                                  "chunk_syms": spec.chunk_syms, "lanes": spec.lanes,
                                  "entropy_bits": round(info["entropy"], 4),
                                  "container_mb": round(info["file_bytes"] / 1e6, 3), "op": op,
@@ -786,7 +805,7 @@ def run_c4(args):
     fmt = FORMATS[args.base_format]
     kernel_names = KERNEL if fmt == 1 else KERNEL_INT8
     layers = build_layers(eq, synth, specs, args.copies, dev, fmt, v2_copies=args.copies,
-                          row_order=args.row_order)
+                          row_order=args.row_order, v2_rows=args.v2_tile_rows)
     ops = ["bf16", "gemv1", "gemv8"]
     copies = args.copies
 
@@ -1023,6 +1042,7 @@ def run_c4(args):
                    "entropy_bits": [round(i["entropy"], 4) for i in infos],
                    "container_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos],
                    "container_v2_mb": [round(i["file_bytes"] / 1e6, 2) for i in infos2],
+                   "v2_tiles": [[i["lanes"], i["tile_cols"]] for i in infos2],
                    "v2_row_order": bool(args.row_order),
                    "copies_rotated": copies,
                    "launch": "eager" if args.eager else "HIP graphs of the step"},

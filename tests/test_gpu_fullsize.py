@@ -78,11 +78,14 @@ def build(eq, spec):
 
 
 def v2_tiles(spec):
-    """Tile shape of the version-2 containers the benchmark times: 256 rows
-    for 65536-symbol chunks (256 x 256 tiles), else 128 rows; C / rows
-    columns, so a tile holds the chunk's C symbols."""
-    tr = 256 if spec.chunk_syms >= 65536 else 128
-    return tr, spec.chunk_syms // tr
+    """Tile shape of the version-2 containers the benchmark times: for
+    65536-symbol chunks 256 columns, and 256 rows when the matrix has at
+    least 2048 such tiles, else 128 (the config-5 attention matrices); below,
+    128 rows x C / 128 columns."""
+    if spec.chunk_syms < 65536:
+        return 128, spec.chunk_syms // 128
+    tiles = -(-spec.rows // 256) * -(-spec.cols // 256)
+    return (256 if tiles >= 2048 else 128), 256
 
 
 def build2(eq, spec, row_order=False):

@@ -282,22 +282,25 @@ def test_block_codes_buffer_feeds_gemm(eq):
         assert eq.eq_get_status(L) == eq.EQ_OK
 
 
-@pytest.mark.parametrize("version", [1, 2])
+@pytest.mark.parametrize("version", [1, 2, "2-ordered"])
 @pytest.mark.parametrize("fmt", [1, 2])
 def test_small_batches_take_the_fused_gemv(eq, version, fmt):
     """Up to 8 tokens eq_decode_gemm runs the fused decode-GEMV: its outputs
     equal eq_decode_gemv's bit for bit (same workspace size rule), meet the
-    GEMV bar against the oracle, and 9 tokens go through the GEMM."""
+    GEMV bar against the oracle, and 9 tokens go through the GEMM (after a
+    decode to codes in matrix order, also for a layer with a row order)."""
     M, N = 96, 1024
-    spec = small_spec(M, N, bits=2.5, chunk=4096, lanes=64, seed=4321 + version + fmt)
+    seed = 4321 + (3 if version == "2-ordered" else version) + fmt
+    spec = small_spec(M, N, bits=2.5, chunk=4096, lanes=64, seed=seed)
     w = synth.weights(spec)
     alpha, _ = eq.eqe_alpha_search(w, 2.5, base_format=fmt)
     if version == 1:
         blob = eq.eqe_encode(w, alpha, chunk_syms=4096, lanes=64, base_format=fmt)
     else:
-        blob = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=64, base_format=fmt)
+        blob = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=64, base_format=fmt,
+                              row_order=version == "2-ordered")
     L = eq.Layer(blob, _dev())
-    rc, q = (oracle.container2_decode(blob) if version == 2 else oracle.container_decode(blob))
+    rc, q = (oracle.container_decode(blob) if version == 1 else oracle.container2_decode(blob))
     assert rc == oracle.OK
     w_ref = oracle.dequant(q, oracle.container_scales(blob), fmt)
     bias = synth.bias(spec)

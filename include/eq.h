@@ -194,11 +194,10 @@ int eq_decode_gemv_noalloc(const eq_layer *L, const uint16_t *x, uint32_t B,
  * together, ahead of the block's forward pass).  Decodes layers L[0..n-1]
  * (host array of n views, 1 <= n <= 8) to BF16: layer i to w[i] (device, its
  * M*N BF16 values), as eq_decode_bf16 does, with identical results.  One
- * launch decodes all layers when they share a container version and lane
- * count (version 1: rows that are whole steps, N a multiple of W; version 2:
- * the tile height), which keeps more chunks in flight per compute unit.
- * Version-2 layers of several tile heights get one launch per height (64,
- * 128, 256); otherwise each layer gets its own launch, in order. */
+ * launch decodes all layers when all are version 2 (any tile heights), or
+ * all version 1 with one lane count and rows that are whole steps (N a
+ * multiple of W), which keeps more chunks in flight per compute unit;
+ * otherwise each layer gets its own launch, in order. */
 int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
                          hipStream_t stream);
 
@@ -207,11 +206,10 @@ int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t 
  * Float8 buffer per device, which its W8A16 GEMM reads).  Decodes layers
  * L[0..n-1] (host array of n views, 1 <= n <= 8) to one-byte codes: layer i
  * to codes[i] (device, its M*N codes, as eq_decode_codes writes them), with
- * identical results.  One launch decodes all layers when they share a
- * container version and lane count (version 1: rows that are whole steps
- * and one base format; version 2: the tile height).  Version-2 layers of
- * several tile heights get one launch per height (64, 128, 256); otherwise
- * each layer gets its own launch, in order.  The codes feed eq_gemm_codes. */
+ * identical results.  One launch decodes all layers when all are version 2
+ * (any tile heights), or all version 1 with one lane count, one base format
+ * and rows that are whole steps; otherwise each layer gets its own launch,
+ * in order.  The codes feed eq_gemm_codes. */
 int eq_decode_codes_multi(const eq_layer *const *L, uint8_t *const *codes, uint32_t n,
                           hipStream_t stream);
 

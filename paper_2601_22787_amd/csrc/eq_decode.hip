@@ -1575,24 +1575,6 @@ extern "C" int eq_decode_gemv_noalloc(const eq_layer *L, const uint16_t *x, uint
   return eq_decode_gemv(L, x, B, bias, y, ws, EQ_NOALLOC_SCRATCH_BYTES, stream);
 }
 
-// Version-2 layers of several tile heights: one joint launch per height, in
-// the order 64, 128, 256 (a height held by one layer decodes alone).
-template <class T, class Single, class Joint>
-int v2_by_height(const eq_layer *const *L, T *const *out, uint32_t n, hipStream_t stream,
-                 Single single, Joint joint) {
-  for (const uint32_t tr : {64u, 128u, 256u}) {
-    const eq_layer *gl[kMaxLayers];
-    T *go[kMaxLayers];
-    uint32_t k = 0;
-    for (uint32_t i = 0; i < n; ++i)
-      if (L[i]->lanes == tr) gl[k] = L[i], go[k++] = out[i];
-    if (k == 0) continue;
-    const int rc = k == 1 ? single(gl[0], go[0], stream) : joint(gl, go, k, stream);
-    if (rc != EQ_OK) return rc;
-  }
-  return EQ_OK;
-}
-
 extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w, uint32_t n,
                                     hipStream_t stream) {
   if (!L || !w || n < 1 || n > kMaxLayers) return EQ_EINVAL;
@@ -1603,9 +1585,6 @@ extern "C" int eq_decode_bf16_multi(const eq_layer *const *L, uint16_t *const *w
     if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
   }
   if (v2 && v2_joint_out_ok(L, n)) return v2_decode_bf16_multi(L, w, n, stream);
-  bool all_v2 = true;
-  for (uint32_t i = 0; i < n; ++i) all_v2 &= L[i]->version == 2;
-  if (all_v2 && n > 1) return v2_by_height(L, w, n, stream, eq_decode_bf16, v2_decode_bf16_multi);
   if (n == 1 || v2 || !joint_ok(L, n)) {
     for (uint32_t i = 0; i < n; ++i) {
       const int rc = eq_decode_bf16(L[i], w[i], stream);
@@ -1632,10 +1611,6 @@ extern "C" int eq_decode_codes_multi(const eq_layer *const *L, uint8_t *const *c
     if (!(L[i]->version == 2 ? v2_layer_ok(L[i]) : layer_ok(L[i]))) return EQ_EINVAL;
   }
   if (v2 && v2_joint_out_ok(L, n)) return v2_decode_codes_multi(L, codes, n, stream);
-  bool all_v2 = true;
-  for (uint32_t i = 0; i < n; ++i) all_v2 &= L[i]->version == 2;
-  if (all_v2 && n > 1)
-    return v2_by_height(L, codes, n, stream, eq_decode_codes, v2_decode_codes_multi);
   if (n == 1 || v2 || !joint_ok(L, n)) {
     for (uint32_t i = 0; i < n; ++i) {
       const int rc = eq_decode_codes(L[i], codes[i], stream);

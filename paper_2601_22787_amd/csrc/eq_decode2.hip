@@ -897,8 +897,9 @@ constexpr uint32_t table_bytes2(int mode, bool pk) {
 
 // The work of block `bid` of `nblocks` on layer a: stage the phrase table,
 // then each wavefront decodes its chunks (below).
-template <int G, int MODE, int NB, bool PK, bool ORD>
-__device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint32_t nblocks) {
+// Stage the layer's phrase table in LDS (address 0); returns its base.
+template <int MODE, int NB, bool PK>
+__device__ __forceinline__ char *stage_table2(const Args2 &a) {
   extern __shared__ uint4 dyn2[];
   // the phrase table at LDS address 0 (no static LDS in this kernel), the
   // position step in this kernel's units: record bytes (GEMV at batch 1),
@@ -946,6 +947,13 @@ __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint
       *reinterpret_cast<uint32_t *>(tab + kCodesHalf + kIdentity2 / 2) = 0u;
   }
   __syncthreads();
+  return tab;
+}
+
+// Block bid of nblocks on layer a: its wavefronts decode their tiles.
+template <int G, int MODE, int NB, bool PK, bool ORD>
+__device__ __forceinline__ void run_tiles2(const Args2 &a, char *tab, uint32_t bid,
+                                           uint32_t nblocks) {
   const uint32_t nw = blockDim.x / kWave, wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   char *mine = tab + table_bytes2(MODE, PK) + size_t(wave) * a.wave_lds;
   // chunks strided over the layer (block bid, wave w: bid + w * nblocks, ...):
@@ -956,6 +964,11 @@ __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint
     Tile<G, MODE, NB, PK, ORD> t(a, c, lane, mine);
     t.run();
   }
+}
+
+template <int G, int MODE, int NB, bool PK, bool ORD>
+__device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint32_t nblocks) {
+  run_tiles2<G, MODE, NB, PK, ORD>(a, stage_table2<MODE, NB, PK>(a), bid, nblocks);
 }
 
 template <int G, int MODE, int NB, bool PK, bool ORD>
@@ -978,6 +991,21 @@ __global__ __launch_bounds__(kWave * max_waves2(MODE, NB)) void decode2_multi_ke
   uint32_t i = 0, b0 = 0;
   while (i + 1 < m.n && blockIdx.x >= m.blk_end[i]) b0 = m.blk_end[i++];
   decode2_block<G, MODE, NB, PK, ORD>(m.a[i], blockIdx.x - b0, m.blk_end[i] - b0);
+}
+
+// Codes or BF16 of layers of several tile heights in one launch: a block
+// runs its layer's tiles with the Tile of that height (the kernel holds all
+// three, so registers and LDS per wavefront are those of the largest).
+template <int MODE, bool PK, bool ORD>
+__global__ __launch_bounds__(kWave * max_waves2(MODE, 1)) void decode2_mixed_kernel(MultiArgs2 m) {
+  uint32_t i = 0, b0 = 0;
+  while (i + 1 < m.n && blockIdx.x >= m.blk_end[i]) b0 = m.blk_end[i++];
+  const Args2 &a = m.a[i];
+  char *tab = stage_table2<MODE, 1, PK>(a);
+  const uint32_t bid = blockIdx.x - b0, nb = m.blk_end[i] - b0;
+  if (a.TR == 64) run_tiles2<1, MODE, 1, PK, ORD>(a, tab, bid, nb);
+  else if (a.TR == 128) run_tiles2<2, MODE, 1, PK, ORD>(a, tab, bid, nb);
+  else run_tiles2<4, MODE, 1, PK, ORD>(a, tab, bid, nb);
 }
 
 // Rows split over NT > 1 column tiles: y = s * (partials added in tile
@@ -1199,7 +1227,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge2_multi_kernel(MultiArgs2 
 // Joint launch of m.n layers: one wavefront count for all (from the total
 // chunks, LDS for the largest per-wavefront need), each layer's blocks in
 // proportion to its chunks.
-template <int MODE, int NB, bool PK, bool ORD>
+template <int MODE, int NB, bool PK, bool ORD, bool MIX = false>
 int launch2_multi(MultiArgs2 m, hipStream_t s) {
   const Facts2 f = facts2();
   uint32_t wl = 0, n[kMaxLayers2];
@@ -1218,6 +1246,10 @@ int launch2_multi(MultiArgs2 m, hipStream_t s) {
   }
   const size_t shm = tb + size_t(waves) * wl;
   const dim3 grid(end), block(waves * kWave);
+  if constexpr (MIX) {
+    hipLaunchKernelGGL((decode2_mixed_kernel<MODE, PK, ORD>), grid, block, shm, s, m);
+    return hipGetLastError() == hipSuccess ? EQ_OK : EQ_EHIP;
+  }
   switch (m.a[0].TR) {
     case 64: hipLaunchKernelGGL((decode2_multi_kernel<1, MODE, NB, PK, ORD>), grid, block, shm, s, m); break;
     case 128: hipLaunchKernelGGL((decode2_multi_kernel<2, MODE, NB, PK, ORD>), grid, block, shm, s, m); break;
@@ -1293,15 +1325,16 @@ size_t v2_gemv_workspace_bytes(const eq_layer *L, uint32_t B) {
   return NT > 1 ? round256(size_t(B) * NT * L->rows * sizeof(float)) : 256;
 }
 
-// Block-wise decode of version-2 layers of one tile height to codes or BF16
-// (Sec. 2.2, block-wise decompression), each layer to its own output: one
-// launch, blocks per layer in proportion to its tiles, so that small layers
-// (the key and value projections of a block) run beside large ones instead
-// of leaving most compute units idle in launches of their own.  Packed table
+// Block-wise decode of version-2 layers to codes or BF16 (Sec. 2.2,
+// block-wise decompression), each layer to its own output: one launch,
+// blocks per layer in proportion to its tiles, so that small layers (the key
+// and value projections of a block) run beside large ones instead of leaving
+// most compute units idle in launches of their own.  Layers of several tile
+// heights share the launch through decode2_mixed_kernel.  Packed table
 // entries when every layer allows them.
 bool v2_joint_out_ok(const eq_layer *const *L, uint32_t n) {
   for (uint32_t i = 0; i < n; ++i)
-    if (!v2_layer_ok(L[i]) || L[i]->lanes != L[0]->lanes) return false;
+    if (!v2_layer_ok(L[i])) return false;
   return n >= 2 && n <= kMaxLayers2;
 }
 
@@ -1310,8 +1343,11 @@ int v2_decode_out_multi(const eq_layer *const *L, uint32_t n, void *const *out, 
   if (!v2_joint_out_ok(L, n)) return EQ_EINVAL;
   MultiArgs2 m{};
   m.n = n;
-  bool pk = true, ord = false;
-  for (uint32_t i = 0; i < n; ++i) ord |= L[i]->row_order != nullptr;
+  bool pk = true, ord = false, mix = false;
+  for (uint32_t i = 0; i < n; ++i) {
+    ord |= L[i]->row_order != nullptr;
+    mix |= L[i]->lanes != L[0]->lanes;
+  }
   for (uint32_t i = 0; i < n; ++i) {
     if (!out[i]) return EQ_EINVAL;
     // with an ordered layer every layer of the launch stores through 64-bit
@@ -1322,6 +1358,13 @@ int v2_decode_out_multi(const eq_layer *const *L, uint32_t n, void *const *out, 
     if (MODE == kCodes2) m.a[i].codes = static_cast<uint8_t *>(out[i]);
     else m.a[i].wout = static_cast<uint16_t *>(out[i]);
     pk &= m.a[i].n_syms > 1;
+  }
+  if (mix) {
+    if (ord)
+      return pk ? launch2_multi<MODE, 1, true, true, true>(m, s)
+                : launch2_multi<MODE, 1, false, true, true>(m, s);
+    return pk ? launch2_multi<MODE, 1, true, false, true>(m, s)
+              : launch2_multi<MODE, 1, false, false, true>(m, s);
   }
   if (ord)
     return pk ? launch2_multi<MODE, 1, true, true>(m, s) : launch2_multi<MODE, 1, false, true>(m, s);

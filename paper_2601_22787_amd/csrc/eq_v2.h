@@ -20,7 +20,7 @@ int v2_decode_gemv_multi(const eq_layer *const *L, uint32_t n, const uint16_t *x
                          const uint16_t *const *bias, float *const *y, void *const *ws,
                          hipStream_t s);
 // Layers that one version-2 launch can decode to codes or BF16 together:
-// 2..8 valid version-2 layers with one tile height.
+// 2..8 valid version-2 layers (of any tile heights).
 bool v2_joint_out_ok(const eq_layer *const *L, uint32_t n);
 // Codes or BF16 of n such layers, layer i to codes[i] / w[i], in one launch.
 int v2_decode_codes_multi(const eq_layer *const *L, uint8_t *const *codes, uint32_t n,

@@ -290,12 +290,12 @@ def test_v2_gemv_multi_joint(eq, B):
 
 @pytest.mark.parametrize("single_phrase", [False, True])
 def test_v2_block_wise_codes_and_bf16(eq, single_phrase):
-    """Block-wise decode of version-2 layers of one tile height (Sec. 2.2):
-    one launch over ragged layers of different widths, tile widths and base
-    formats (with a single-phrase layer: the split table for all), each
-    layer's codes and BF16 bit-exact against the oracle and nothing written
-    outside its output; layers of different tile heights fall back to one
-    launch each, with the same results."""
+    """Block-wise decode of version-2 layers (Sec. 2.2): one launch over
+    ragged layers of different widths, tile widths and base formats (with a
+    single-phrase layer: the split table for all), each layer's codes and
+    BF16 bit-exact against the oracle and nothing written outside its
+    output; with a layer of another tile height the launch runs each block's
+    tiles at its layer's height, with the same results."""
     shapes = [(130, 512, 64, 2.0, 1), (40, 640, 256, 3.0, 2), (5, 100, 32, 2.0, 1),
               (300, 1000, 256, 2.5, 1)]
     blobs, specs = [], []
@@ -380,14 +380,16 @@ def test_v2_row_order_mixed_rows_and_offsets(eq, TR, TC):
 def test_v2_row_order_multi(eq):
     """Joint launches over ordered and matrix-order layers together: the
     GEMV of layers sharing an input equals the single-layer launches, and
-    block-wise codes and BF16 are bit-exact against the oracle."""
-    shapes = [(300, 1024, 256, True), (64, 1024, 128, False), (97, 1024, 256, True)]
+    block-wise codes and BF16 (one launch over tile heights 64 and 128) are
+    bit-exact against the oracle."""
+    shapes = [(300, 1024, 64, 256, True), (64, 1024, 64, 128, False),
+              (97, 1024, 64, 256, True), (200, 1024, 128, 256, True)]
     layers = []
-    for i, (M, N, TC, ordered) in enumerate(shapes):
+    for i, (M, N, TR, TC, ordered) in enumerate(shapes):
         spec = small_spec(M, N, bits=2.0, seed=2950 + i, outliers=True)
         w = _mixed_rows(spec)
         alpha, _ = eq.eqe_alpha_search(w, 2.0)
-        blob = eq.eqe_encode2(w, alpha, tile_rows=64, tile_cols=TC, row_order=ordered)
+        blob = eq.eqe_encode2(w, alpha, tile_rows=TR, tile_cols=TC, row_order=ordered)
         layers.append((spec, blob, eq.Layer(blob, _dev())))
     Ls = [L for _, _, L in layers]
     for B in (1, 8):

@@ -895,8 +895,6 @@ constexpr uint32_t table_bytes2(int mode, bool pk) {
   return pk ? kTablePacked2 : (mode == kGemv2 ? kTableBytes2 : kTableCodes2);
 }
 
-// The work of block `bid` of `nblocks` on layer a: stage the phrase table,
-// then each wavefront decodes its chunks (below).
 // Stage the layer's phrase table in LDS (address 0); returns its base.
 template <int MODE, int NB, bool PK>
 __device__ __forceinline__ char *stage_table2(const Args2 &a) {
@@ -966,6 +964,8 @@ __device__ __forceinline__ void run_tiles2(const Args2 &a, char *tab, uint32_t b
   }
 }
 
+// The work of block `bid` of `nblocks` on layer a: stage the phrase table,
+// then each wavefront decodes its chunks.
 template <int G, int MODE, int NB, bool PK, bool ORD>
 __device__ __forceinline__ void decode2_block(const Args2 &a, uint32_t bid, uint32_t nblocks) {
   run_tiles2<G, MODE, NB, PK, ORD>(a, stage_table2<MODE, NB, PK>(a), bid, nblocks);
@@ -1009,14 +1009,15 @@ __global__ __launch_bounds__(kWave * max_waves2(MODE, 1)) void decode2_mixed_ker
 }
 
 // Rows split over NT > 1 column tiles: y = s * (partials added in tile
-// order) + bias, the partials of stored row k going to matrix row order[k].  One block per 64 outputs (index i = batch row * rows +
-// row, one per lane), kMergeParts wavefronts: wavefront p sums tiles
+// order) + bias, the partials of stored row k going to matrix row order[k].
+// One block per 64 outputs (index i = batch row * rows + row, one per
+// lane), kMergeParts wavefronts: wavefront p sums tiles
 // [p NT / kMergeParts, (p + 1) NT / kMergeParts) in order (independent loads,
 // so their latencies overlap, each a contiguous 256 bytes of the workspace),
 // then the parts are added in order 0, 1, ... through LDS (deterministic).
-// Sixteen threads per output inside one wavefront, as before, read 16 bytes
-// of each of 16 scattered segments per load (batch 8 on 8192 x 28672:
-// 167.5 -> 159 us).
+// Each load reads 256 contiguous bytes; sixteen threads per output inside
+// one wavefront read 16 bytes of each of 16 scattered segments per load and
+// were slower (batch 8 on 8192 x 28672: 167.5 against 159 us).
 constexpr uint32_t kMergeParts = 16;
 constexpr uint32_t kMergeThreads = kWave * kMergeParts;
 __device__ __forceinline__ void merge2(const Args2 &a, uint32_t blk) {

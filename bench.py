@@ -73,8 +73,8 @@ def parse():
     ap.add_argument("--container", type=int, choices=(1, 2), default=1,
                     help="c5 workload: container version of the stack's layers")
     ap.add_argument("--v2-tile-rows", type=int, choices=(64, 128, 256), default=0,
-                    help="version-2 tile rows for every matrix (256 columns for 65536-symbol "
-                         "chunks, C / rows below) instead of the rule of v2_tiles")
+                    help="version-2 tile rows for every matrix (columns as v2_tiles sets them) "
+                         "instead of the rule of v2_tiles")
     ap.add_argument("--row-order", action="store_true",
                     help="version-2 containers with the row order: tiles cut over the rows "
                          "sorted by their phrase count")
@@ -90,22 +90,20 @@ def parse():
 
 
 def v2_tiles(spec, rows=0):
-    """Tile rows and columns of the version-2 containers, C symbols a tile for
-    C-symbol chunks below 65536: 128 rows (two pipelined coder states per
-    lane; faster than 64 for the batch-1 GEMV on the 16384-symbol chunks of
-    configs 2 and 3) x C / 128 columns.  65536-symbol chunks: 256 columns,
-    and 256 rows when the matrix has at least 2048 such tiles (8 per compute
-    unit), else 128 rows: half the tile, the same state bytes per code (they
-    depend on the width alone), twice the tiles, and half the work per step
-    for each, which shortens launches that cannot fill the GPU (config-5
-    attention matrices, batch-1 GEMV: 43.5 -> 34 us).  rows > 0 sets the
-    tile rows instead (256 columns for 65536-symbol chunks, C / rows below)."""
+    """Tile rows and columns of the version-2 containers.  The width sets the
+    state bytes per code (32 bits per row segment), so it follows the chunk
+    size: 256 columns for 65536-symbol chunks, C / 128 below.  The height is
+    the taller of (256, 128), or of (128, 64) below 65536 symbols, when the
+    matrix has at least 2048 such tiles (8 per compute unit), else the
+    shorter: half the tile, the same bytes, twice the tiles and half the
+    work per step, which shortens launches that cannot fill the GPU
+    (batch-1 GEMV: config-5 attention matrices 43.5 -> 34 us, config 2
+    19.8 -> 17.6 us, config 1 12.7 -> 9.2 us).  rows > 0 sets the height."""
+    tall, tc = (256, 256) if spec.chunk_syms >= 65536 else (128, spec.chunk_syms // 128)
     if rows:
-        return rows, (256 if spec.chunk_syms >= 65536 else spec.chunk_syms // rows)
-    if spec.chunk_syms < 65536:
-        return 128, spec.chunk_syms // 128
-    tiles = -(-spec.rows // 256) * -(-spec.cols // 256)
-    return (256 if tiles >= 2048 else 128), 256
+        return rows, tc
+    tiles = -(-spec.rows // tall) * -(-spec.cols // tc)
+    return (tall if tiles >= 2048 else tall // 2), tc
 
 
 def build_layers(eq, synth, specs, copies, dev, fmt=1, v2_copies=0, row_order=False,

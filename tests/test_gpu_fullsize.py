@@ -78,14 +78,13 @@ def build(eq, spec):
 
 
 def v2_tiles(spec):
-    """Tile shape of the version-2 containers the benchmark times: for
-    65536-symbol chunks 256 columns, and 256 rows when the matrix has at
-    least 2048 such tiles, else 128 (the config-5 attention matrices); below,
-    128 rows x C / 128 columns."""
-    if spec.chunk_syms < 65536:
-        return 128, spec.chunk_syms // 128
-    tiles = -(-spec.rows // 256) * -(-spec.cols // 256)
-    return (256 if tiles >= 2048 else 128), 256
+    """Tile shape of the version-2 containers the benchmark times: 256
+    columns for 65536-symbol chunks, C / 128 below; the taller of (256, 128),
+    or (128, 64) below 65536 symbols, when the matrix has at least 2048 such
+    tiles, else the shorter."""
+    tall, tc = (256, 256) if spec.chunk_syms >= 65536 else (128, spec.chunk_syms // 128)
+    tiles = -(-spec.rows // tall) * -(-spec.cols // tc)
+    return (tall if tiles >= 2048 else tall // 2), tc
 
 
 def build2(eq, spec, row_order=False):

@@ -240,14 +240,23 @@ def test_v2_corrupted_stream_flagged(eq):
     assert flagged >= 1
 
 
+def bench_tiles(spec):
+    """The benchmark's version-2 tiles below 65536-symbol chunks: C / 128
+    columns, 128 rows when the matrix has at least 2048 such tiles, else 64."""
+    tc = spec.chunk_syms // 128
+    return (128 if -(-spec.rows // 128) * -(-spec.cols // tc) >= 2048 else 64), tc
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-@pytest.mark.parametrize("TR,row_order", [(64, False), (128, False), (128, True)])
-def test_v2_configs_1_to_3(eq, cfg, TR, row_order):
-    """Whole matrices of configs 1-3 at 64-row tiles and at the benchmark's
-    128-row tiles (the same C symbols per tile), in matrix order and with the
-    row order (which moves config 3's outlier-free rows together)."""
+@pytest.mark.parametrize("shape,row_order", [("C/64", False), ("bench", False),
+                                             ("bench", True)])
+def test_v2_configs_1_to_3(eq, cfg, shape, row_order):
+    """Whole matrices of configs 1-3 at 64-row tiles of C symbols and at the
+    benchmark's tiles (64 or 128 rows of C / 128 columns), in matrix order
+    and with the row order (which moves config 3's outlier-free rows
+    together)."""
     for spec in config_matrices(cfg):
-        TC = spec.chunk_syms // TR
+        TR, TC = (64, spec.chunk_syms // 64) if shape == "C/64" else bench_tiles(spec)
         say("v2 config", cfg, spec.name, spec.rows, spec.cols, TR, TC, row_order)
         w = synth.weights(spec)
         alpha, _ = eq.eqe_alpha_search(w, spec.target_bits, sample_rows=1024)

@@ -450,3 +450,23 @@ def test_v2_row_order_damaged_on_device(eq, TC):
         else:
             gpu_gemv(eq, L, synth.activations(spec, 1 if what == "gemv1" else 8))
         assert eq.eq_get_status(L) == eq.EQ_ECORRUPT, what
+
+
+def test_v2_row_order_int8_and_single_phrase(eq):
+    """Ordered layers through the other table and value paths: the Int8 base
+    format (its own BF16 conversion at write-out), and a single-phrase layer
+    (the split table; every row costs the same, so the order is the
+    identity, stored and used all the same)."""
+    spec = small_spec(300, 1000, bits=2.0, seed=2995, outliers=True)
+    w = _mixed_rows(spec)
+    alpha, _ = eq.eqe_alpha_search(w, 2.0, base_format=oracle.INT8)
+    blob = eq.eqe_encode2(w, alpha, tile_rows=128, tile_cols=256, base_format=oracle.INT8,
+                          row_order=True)
+    assert oracle.container2_info(blob).base_format == oracle.INT8
+    check_full(eq, blob, spec, batches=(1, 8), offsets=(0, 1))
+    z = np.zeros((70, 512), dtype=np.uint16)
+    blob = eq.eqe_encode2(z, 1.0, tile_rows=64, tile_cols=256, row_order=True)
+    info = oracle.container2_info(blob)
+    assert info.flags == 1 and info.n_syms == 1
+    assert np.array_equal(oracle.container2_row_order(blob), np.arange(70))
+    check_full(eq, blob, small_spec(70, 512, seed=2996), batches=(1, 3), offsets=(0, 3))
